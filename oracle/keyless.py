@@ -1,0 +1,338 @@
+"""CPU oracle for Keyless Attention (float64 NumPy). TEST INFRASTRUCTURE ONLY.
+
+This module defines what the GPU library must compute. It is plain, slow and
+written to be read against the paper; it shares no code with the HIP library
+and never imports it. Only the tests, the smoke check and the benchmark's CPU
+baseline may call it; the product path never does.
+
+Notation follows the paper: X [n, d] tokens, per-head projections
+W^Q_h, W^V_h in R^{d x d_k}, routing matrix W^R_h in R^{d_k x d_k},
+d_k = head dimension, tau = 1/sqrt(d_k).
+
+Readings of points the paper leaves open (each is also listed with the design
+notes):
+
+* The decode weight has a factor lambda in the exponent (Section 3, value-only
+  cache decode); it is never defined. We take lambda = 1, which makes decode
+  agree with Eq. 2 and with the per-head forms of Section 3. ``scale`` lets a
+  caller set lambda/sqrt(d_k) explicitly; the default is 1/sqrt(d_k).
+* Eq. 2 prints the scale as sqrt(d)_k; it is 1/sqrt(d_k) as in Eq. 1 and Eq. 4.
+* Causal self-attention includes the token itself (j <= i); decode at step n+1
+  attends over all n+1 cached values, the newest included (Section 3).
+* W^R is one d_k x d_k matrix per query head (Section 2.2 fixes W^Q W^R in
+  R^{d x d_k}; the GQA experiments make the second query matrix head specific,
+  Sections 5.4 and B.2).
+* Grouped heads: query head h reads value group g = h // (H // G) (Section 3,
+  GQA paragraph, leaves the assignment open; contiguous grouping is used).
+* No bias, no positional rotation and no output projection: Eq. 2 has none.
+* A cache of length 0 gives a zero output row (no value to average).
+"""
+
+from __future__ import annotations
+
+import math
+
+import numpy as np
+
+
+def _f64(a) -> np.ndarray:
+    return np.asarray(a, dtype=np.float64)
+
+
+def default_scale(d_head: int) -> float:
+    """tau = 1/sqrt(d_k) (Eq. 1, Eq. 4; lambda = 1 in the Section 3 decode)."""
+    return 1.0 / math.sqrt(d_head)
+
+
+def softmax_rows(S: np.ndarray) -> np.ndarray:
+    """Row softmax with the row maximum subtracted; -inf entries get weight 0."""
+    S = _f64(S)
+    m = np.max(S, axis=-1, keepdims=True)
+    E = np.exp(S - m)
+    return E / np.sum(E, axis=-1, keepdims=True)
+
+
+# ---------------------------------------------------------------------------
+# Section 2.1: weights
+# ---------------------------------------------------------------------------
+
+def fold_routing(W_Q, W_R, H: int, d_head: int) -> np.ndarray:
+    """Folded query weight W~^Q_h = W^Q_h W^R_h for every head (Section 2.1, the
+    inference-time composition; Section 5.5 fuses it before decoding).
+
+    W_Q: [d, H*d_k] (head h = columns h*d_k:(h+1)*d_k); W_R: [H, d_k, d_k].
+    Returns [d, H*d_k].
+    """
+    W_Q = _f64(W_Q)
+    W_R = _f64(W_R)
+    out = np.empty_like(W_Q)
+    for h in range(H):
+        cols = slice(h * d_head, (h + 1) * d_head)
+        out[:, cols] = W_Q[:, cols] @ W_R[h]
+    return out
+
+
+# ---------------------------------------------------------------------------
+# Eq. 2 / Eq. 4 and the Section 3 multi-head and grouped forms: prefill
+# ---------------------------------------------------------------------------
+
+def keyless_prefill(x, W_Q, W_R, W_V, H: int, G: int, d_head: int,
+                    causal: bool = True, scale: float | None = None):
+    """Keyless self-attention of Eq. 2, per head (Section 3 MHA/MQA/GQA forms).
+
+    For batch b and query head h with group g = h // (H // G):
+      Q_h  = X W^Q_h            (query projection)
+      Q~_h = Q_h W^R_h          (value-space routing, Section 2.1)
+      V_g  = X W^V_g            (the only cached projection)
+      S    = tau * Q~_h V_g^T   (routing scores, Eq. 4)
+      S_ij = -inf for j > i when causal
+      O_h  = softmax(S) V_g
+    If W_R is None, W_Q is taken as the already folded W~^Q.
+
+    x: [B, N, d]; W_Q: [d, H*d_k]; W_R: [H, d_k, d_k] or None; W_V: [d, G*d_k].
+    Returns (O [B, N, H, d_k], Q~ [B, N, H, d_k], V [B, N, G, d_k]).
+    """
+    x = _f64(x)
+    W_Q = _f64(W_Q)
+    W_V = _f64(W_V)
+    B, N, _ = x.shape
+    tau = default_scale(d_head) if scale is None else float(scale)
+    rep = H // G
+    O = np.zeros((B, N, H, d_head))
+    Qr = np.zeros((B, N, H, d_head))
+    V = np.zeros((B, N, G, d_head))
+    for b in range(B):
+        X = x[b]
+        for g in range(G):
+            V[b, :, g, :] = X @ W_V[:, g * d_head:(g + 1) * d_head]
+        for h in range(H):
+            Q_h = X @ W_Q[:, h * d_head:(h + 1) * d_head]
+            Qt_h = Q_h if W_R is None else Q_h @ _f64(W_R)[h]
+            Qr[b, :, h, :] = Qt_h
+            V_g = V[b, :, h // rep, :]
+            S = tau * (Qt_h @ V_g.T)
+            if causal:
+                S = np.where(np.tril(np.ones((N, N), dtype=bool)), S, -np.inf)
+            O[b, :, h, :] = softmax_rows(S) @ V_g
+    return O, Qr, V
+
+
+def keyless_prefill_rows(x, Wt_Q, W_V, rows, H: int, G: int, d_head: int,
+                         causal: bool = True, scale: float | None = None):
+    """Output rows ``rows`` of Eq. 2 for batch 0 only, given the folded W~^Q.
+
+    Used where the whole N x N problem is too large for the CPU: V is formed for
+    all tokens the requested rows can see, Q~ only for the requested rows.
+    Returns (O [len(rows), H, d_k], V [n_seen, G, d_k]).
+    """
+    X = _f64(x)[0]
+    Wt_Q = _f64(Wt_Q)
+    W_V = _f64(W_V)
+    tau = default_scale(d_head) if scale is None else float(scale)
+    rep = H // G
+    rows = [int(r) for r in rows]
+    n_seen = (max(rows) + 1) if causal else X.shape[0]
+    V = (X[:n_seen] @ W_V).reshape(n_seen, G, d_head)
+    Qt = (X[rows] @ Wt_Q).reshape(len(rows), H, d_head)
+    O = np.zeros((len(rows), H, d_head))
+    for k, i in enumerate(rows):
+        last = i + 1 if causal else n_seen
+        for h in range(H):
+            V_g = V[:last, h // rep, :]
+            s = tau * (V_g @ Qt[k, h])
+            p = softmax_rows(s[None, :])[0]
+            O[k, h] = p @ V_g
+    return O, V
+
+
+# ---------------------------------------------------------------------------
+# Section 3: value-only cache, append and decode
+# ---------------------------------------------------------------------------
+
+def cache_rows(cache, b: int, g: int, n: int, block_table=None, block_size: int = 16):
+    """The first n value rows of sequence b, group g, as an [n, d_k] array.
+
+    Contiguous cache: [B, G, L_max, d_k]. Paged cache: [num_blocks, G,
+    block_size, d_k] with row i of sequence b in block block_table[b][i //
+    block_size] at slot i % block_size.
+    """
+    cache = np.asarray(cache)
+    if block_table is None:
+        return _f64(cache[b, g, :n, :])
+    rows = []
+    for i in range(n):
+        blk = int(block_table[b][i // block_size])
+        rows.append(cache[blk, g, i % block_size, :])
+    if not rows:
+        return np.zeros((0, cache.shape[-1]))
+    return _f64(np.stack(rows))
+
+
+def decode_one(q, V_rows, scale: float | None = None, return_weights: bool = False):
+    """O_{n+1} = sum_i alpha_i v_i with alpha = softmax_i(lambda <q, v_i> / sqrt(d_k))
+    over all cached rows (Section 3 decode, lambda = 1 unless ``scale`` says
+    otherwise). An empty cache gives a zero row.
+    """
+    q = _f64(q)
+    V_rows = _f64(V_rows)
+    d = q.shape[-1]
+    tau = default_scale(d) if scale is None else float(scale)
+    if V_rows.shape[0] == 0:
+        out = np.zeros(d)
+        return (out, np.zeros(0)) if return_weights else out
+    s = tau * (V_rows @ q)
+    alpha = softmax_rows(s[None, :])[0]
+    out = alpha @ V_rows
+    return (out, alpha) if return_weights else out
+
+
+def keyless_decode(q_routed, cache, lengths, H: int, G: int, block_table=None,
+                   block_size: int = 16, scale: float | None = None, pairs=None):
+    """Decode for a batch (Section 3 MHA/MQA/GQA with the value-only cache).
+
+    q_routed: [B, H, d_k] routed queries q~ = x W^Q W^R of the current tokens.
+    lengths[b] counts every cached row, the current token's value included.
+    Returns [B, H, d_k]; with ``pairs`` (a list of (b, h)) only those rows are
+    computed and the rest stay zero.
+    """
+    q_routed = _f64(q_routed)
+    B = q_routed.shape[0]
+    rep = H // G
+    out = np.zeros(q_routed.shape)
+    todo = pairs if pairs is not None else [(b, h) for b in range(B) for h in range(H)]
+    cached = {}
+    for b, h in todo:
+        g = h // rep
+        key = (b, g)
+        if key not in cached:
+            cached = {key: cache_rows(cache, b, g, int(lengths[b]), block_table, block_size)}
+        out[b, h] = decode_one(q_routed[b, h], cached[key], scale)
+    return out
+
+
+def standard_decode(q, k_cache, v_cache, lengths, H: int, G: int, scale: float | None = None,
+                    pairs=None):
+    """Standard K+V decode of Eq. 1 for one new query per sequence (the
+    comparison baseline): o = softmax_i(<q, k_i>/sqrt(d_k)) weighted sum of v_i.
+    Caches are contiguous [B, G, L_max, d_k].
+    """
+    q = _f64(q)
+    B, _, d = q.shape
+    tau = default_scale(d) if scale is None else float(scale)
+    rep = H // G
+    out = np.zeros(q.shape)
+    todo = pairs if pairs is not None else [(b, h) for b in range(B) for h in range(H)]
+    for b, h in todo:
+        n = int(lengths[b])
+        if n == 0:
+            continue
+        K = _f64(np.asarray(k_cache)[b, h // rep, :n, :])
+        V = _f64(np.asarray(v_cache)[b, h // rep, :n, :])
+        s = tau * (K @ q[b, h])
+        out[b, h] = softmax_rows(s[None, :])[0] @ V
+    return out
+
+
+def value_cache_append(cache, values, lengths_before, block_table=None, block_size: int = 16):
+    """Returns a copy of ``cache`` with values[b, t, g, :] written at position
+    p = lengths_before[b] + t of sequence b, group g (the new v_{n+1} joins the
+    cache before the decode that reads it, Section 3).
+    """
+    out = np.array(cache, copy=True)
+    values = np.asarray(values)
+    B, T, G, _ = values.shape
+    for b in range(B):
+        for t in range(T):
+            p = int(lengths_before[b]) + t
+            for g in range(G):
+                if block_table is None:
+                    out[b, g, p, :] = values[b, t, g, :]
+                else:
+                    blk = int(block_table[b][p // block_size])
+                    out[blk, g, p % block_size, :] = values[b, t, g, :]
+    return out
+
+
+# ---------------------------------------------------------------------------
+# Eq. 1 and the equivalence constructions of Section 2.4 / Appendix A
+# ---------------------------------------------------------------------------
+
+def standard_attention(x, W_Q, W_K, W_V, H: int, d_head: int, causal: bool = True,
+                       scale: float | None = None):
+    """Standard multi-head attention of Eq. 1: softmax(Q K^T / sqrt(d_k)) V per head."""
+    x = _f64(x)
+    B, N, _ = x.shape
+    tau = default_scale(d_head) if scale is None else float(scale)
+    O = np.zeros((B, N, H, d_head))
+    for b in range(B):
+        X = x[b]
+        for h in range(H):
+            cols = slice(h * d_head, (h + 1) * d_head)
+            Q = X @ _f64(W_Q)[:, cols]
+            K = X @ _f64(W_K)[:, cols]
+            V = X @ _f64(W_V)[:, cols]
+            S = tau * (Q @ K.T)
+            if causal:
+                S = np.where(np.tril(np.ones((N, N), dtype=bool)), S, -np.inf)
+            O[b, :, h, :] = softmax_rows(S) @ V
+    return O
+
+
+def single_head_equivalent_query(W_Q, W_K, W_V) -> np.ndarray:
+    """Theorem 1: W~^Q = W^Q (W^K)^T (W^V)^{-T} for square, invertible W^V."""
+    W_Q, W_K, W_V = _f64(W_Q), _f64(W_K), _f64(W_V)
+    return W_Q @ W_K.T @ np.linalg.inv(W_V.T)
+
+
+def multi_head_equivalent_query(W_Q_h, W_K_h, W_V_h) -> np.ndarray:
+    """Theorem 2 construction: W~^Q_h = Omega_h B_h^+ with Omega_h = W^Q_h (W^K_h)^T,
+    B_h = (W^V_h)^T and the right pseudo-inverse B_h^+ = W^V_h ((W^V_h)^T W^V_h)^{-1}.
+    """
+    W_Q_h, W_K_h, W_V_h = _f64(W_Q_h), _f64(W_K_h), _f64(W_V_h)
+    Omega = W_Q_h @ W_K_h.T
+    B_plus = W_V_h @ np.linalg.inv(W_V_h.T @ W_V_h)
+    return Omega @ B_plus
+
+
+def keyless_attention_folded(x, Wt_Q, W_V, H: int, d_head: int, causal: bool = True,
+                             scale: float | None = None):
+    """Eq. 2 with an already folded W~^Q (W_R absent): the form the theorems use."""
+    O, _, _ = keyless_prefill(x, Wt_Q, None, W_V, H, H, d_head, causal, scale)
+    return O
+
+
+# ---------------------------------------------------------------------------
+# Brute force for tiny inputs: scalar loops straight from Eq. 4
+# ---------------------------------------------------------------------------
+
+def brute_force_keyless(X, Wt_Q, W_V, causal: bool = True, scale: float | None = None):
+    """Single head, pure Python loops: s_ij = (x_i W~^Q)(x_j W^V)^T * tau (Eq. 4),
+    softmax over j, output sum_j p_ij (x_j W^V). For n, d, d_k of a few units."""
+    X = [[float(v) for v in row] for row in np.asarray(X)]
+    Wq = [[float(v) for v in row] for row in np.asarray(Wt_Q)]
+    Wv = [[float(v) for v in row] for row in np.asarray(W_V)]
+    n, d, dk = len(X), len(Wq), len(Wq[0])
+    tau = 1.0 / math.sqrt(dk) if scale is None else float(scale)
+    q = [[sum(X[i][a] * Wq[a][c] for a in range(d)) for c in range(dk)] for i in range(n)]
+    v = [[sum(X[i][a] * Wv[a][c] for a in range(d)) for c in range(dk)] for i in range(n)]
+    out = []
+    for i in range(n):
+        js = range(i + 1) if causal else range(n)
+        s = {j: tau * sum(q[i][c] * v[j][c] for c in range(dk)) for j in js}
+        m = max(s.values())
+        e = {j: math.exp(s[j] - m) for j in js}
+        z = sum(e.values())
+        out.append([sum(e[j] / z * v[j][c] for j in js) for c in range(dk)])
+    return np.array(out)
+
+
+# ---------------------------------------------------------------------------
+# Byte accounting (Section 3, Section 5.5)
+# ---------------------------------------------------------------------------
+
+def cache_bytes(tokens: int, layers: int, kv_heads: int, d_head: int, elem_bytes: int,
+                keys: bool) -> int:
+    """Bytes held by a per-layer cache of ``tokens`` positions: values only
+    (keyless) or keys plus values (standard)."""
+    per = tokens * layers * kv_heads * d_head * elem_bytes
+    return 2 * per if keys else per

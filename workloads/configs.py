@@ -1,0 +1,117 @@
+"""The five synthetic workloads, by name, with their sizes and draw recipes.
+
+Each builder returns a dict of tensors on ``device``. Streams (the second key
+of every draw) are fixed per tensor so that one tensor's draw never depends
+on another tensor's size. Nothing here computes attention; the paged builder
+only lays the drawn value rows out in blocks and writes the block table.
+"""
+
+from __future__ import annotations
+
+import math
+
+import torch
+
+from .synth import normal, permutation, uniform_int
+
+NAMES = ("tiny_fp32", "decode_bf16", "prefill_bf16", "paged_gqa_bf16", "head_to_head_bf16")
+
+# Stream ids (one per drawn tensor).
+S_X, S_WQ, S_WR, S_WV, S_XNEXT, S_V, S_Q, S_K, S_LEN, S_PERM, S_VNEW = range(11)
+
+
+def tiny_fp32(device="cpu", seed=0, N=128, d_model=256, H=4, d_head=64):
+    """One fp32 attention layer: causal prefill of N tokens, then one decode step.
+
+    x ~ N(0,1); W_Q, W_V ~ N(0, 1/d_model) of shape [d_model, H*d_head];
+    W_R ~ N(0, 1/d_model) of shape [H, d_head, d_head] (one routing matrix per
+    query head). ``x_next`` is the token after the prefill, drawn from the same
+    seed on its own stream.
+    """
+    std_w = 1.0 / math.sqrt(d_model)
+    f = torch.float32
+    return dict(
+        x=normal((1, N, d_model), seed, S_X, 1.0, f, device),
+        W_Q=normal((d_model, H * d_head), seed, S_WQ, std_w, f, device),
+        W_R=normal((H, d_head, d_head), seed, S_WR, std_w, f, device),
+        W_V=normal((d_model, H * d_head), seed, S_WV, std_w, f, device),
+        x_next=normal((1, 1, d_model), seed, S_XNEXT, 1.0, f, device),
+        H=H, G=H, d_head=d_head,
+    )
+
+
+def decode_bf16(device="cpu", seed=1, B=8, H=32, L=4096, d_head=128, copies=1):
+    """Contiguous value-only cache [B, H, L, d_head] and routed queries [B, H, d_head].
+
+    ``copies`` > 1 draws extra independent caches (streams S_V + 100*c) so a
+    timing loop can rotate over a working set larger than the last-level cache.
+    The last cache row of each sequence is the step's new value: ``v_new``
+    holds it and ``lengths_before`` = L - 1, so appending it and decoding over
+    ``lengths`` = L reproduces the drawn cache exactly.
+    """
+    caches = [normal((B, H, L, d_head), seed, S_V + 100 * c, 1.0, torch.bfloat16, device)
+              for c in range(copies)]
+    q = normal((B, H, d_head), seed, S_Q, 1.0, torch.bfloat16, device)
+    v_new = caches[0][:, :, L - 1:L, :].permute(0, 2, 1, 3).contiguous()  # [B, 1, G, d]
+    lengths = torch.full((B,), L, dtype=torch.int32, device=device)
+    return dict(caches=caches, V=caches[0], q=q, v_new=v_new, lengths=lengths,
+                lengths_before=lengths - 1, B=B, H=H, G=H, L=L, d_head=d_head)
+
+
+def prefill_bf16(device="cpu", seed=2, B=1, N=8192, d_model=4096, H=32, G=32, d_head=128):
+    """Causal prefill: x ~ N(0,1), projection weights ~ N(0, 1/d_model), bf16."""
+    std_w = 1.0 / math.sqrt(d_model)
+    b = torch.bfloat16
+    return dict(
+        x=normal((B, N, d_model), seed, S_X, 1.0, b, device),
+        W_Q=normal((d_model, H * d_head), seed, S_WQ, std_w, b, device),
+        W_R=normal((H, d_head, d_head), seed, S_WR, std_w, b, device),
+        W_V=normal((d_model, G * d_head), seed, S_WV, std_w, b, device),
+        H=H, G=G, d_head=d_head,
+    )
+
+
+def paged_gqa_bf16(device="cpu", seed=3, B=64, H=32, G=8, d_head=128, block_size=16,
+                   L_lo=1024, L_hi=32768):
+    """Paged value-only cache with ragged lengths and a permuted block table.
+
+    lengths ~ U{L_lo..L_hi}; sequence b owns ceil(len_b / block_size) blocks,
+    taken in order from a random permutation of all blocks. One extra block,
+    the last, is never owned: every unused table entry points at it, and it is
+    filled with NaN, as are the padding slots past len_b in each last block.
+    Cache layout: [num_blocks, G, block_size, d_head].
+    """
+    lengths = uniform_int(B, L_lo, L_hi, seed, S_LEN)
+    nblk = (lengths + block_size - 1) // block_size
+    used = int(nblk.sum())
+    num_blocks = used + 1
+    poison = used
+    max_blocks = int(math.ceil(L_hi / block_size))
+    perm = permutation(used, seed, S_PERM)
+    table = torch.full((B, max_blocks), poison, dtype=torch.int32)
+    off = 0
+    for bi in range(B):
+        n = int(nblk[bi])
+        table[bi, :n] = perm[off:off + n].to(torch.int32)
+        off += n
+    data = normal((num_blocks, G, block_size, d_head), seed, S_V, 1.0, torch.bfloat16, device)
+    nan = torch.tensor(float("nan"), dtype=torch.bfloat16, device=device)
+    data[poison] = nan
+    for bi in range(B):
+        rem = int(lengths[bi]) % block_size
+        if rem:
+            last = int(table[bi, int(nblk[bi]) - 1])
+            data[last, :, rem:, :] = nan
+    q = normal((B, H, d_head), seed, S_Q, 1.0, torch.bfloat16, device)
+    return dict(data=data, block_table=table.to(device), lengths=lengths.to(torch.int32).to(device),
+                q=q, B=B, H=H, G=G, d_head=d_head, block_size=block_size,
+                num_blocks=num_blocks, max_blocks_per_seq=max_blocks, poison_block=poison)
+
+
+def head_to_head_bf16(device="cpu", seed=4, B=32, H=32, L=16384, d_head=128, with_keys=True):
+    """Contiguous caches [B, H, L, d_head]: values, and keys for the standard kernel."""
+    V = normal((B, H, L, d_head), seed, S_V, 1.0, torch.bfloat16, device)
+    K = normal((B, H, L, d_head), seed, S_K, 1.0, torch.bfloat16, device) if with_keys else None
+    q = normal((B, H, d_head), seed, S_Q, 1.0, torch.bfloat16, device)
+    lengths = torch.full((B,), L, dtype=torch.int32, device=device)
+    return dict(V=V, K=K, q=q, lengths=lengths, B=B, H=H, G=H, L=L, d_head=d_head)
