@@ -1,0 +1,191 @@
+/*
+ * keyless.h - C ABI of the keyless-attention library for MI355X (gfx950).
+ *
+ * Keyless attention scores each query against the cached VALUES through a
+ * value-space routing projection instead of separate keys: for one head,
+ *     out = softmax(tau * (x W^Q W^R) (X W^V)^T) (X W^V),   tau = 1/sqrt(d_head)
+ * (Eq. 2; the per-pair score is Eq. 4). Decoding therefore needs only a
+ * value-only cache (Section 3): o = sum_i alpha_i v_i with
+ * alpha_i proportional to exp(tau <q~, v_i>) over every cached row, the current
+ * token's value included.
+ *
+ * Conventions for every call below:
+ *  - All tensor arguments are DEVICE pointers to row-major, contiguous memory
+ *    owned by the caller. The library never allocates, frees or synchronises
+ *    inside these calls; every kernel is enqueued on `stream` (a hipStream_t;
+ *    NULL means the default stream) and the call returns without waiting.
+ *  - Weights right-multiply activations, as in the paper's X W.
+ *  - Grouped heads (Section 3, GQA): query head h reads value group
+ *    g = h / (H / G); H must be a multiple of G. G = H is multi-head, G = 1 is
+ *    multi-query.
+ *  - Errors: host-side validation returns a negative kl_status and sets a
+ *    thread-local message readable with keyless_last_error(). Nothing is
+ *    enqueued when validation fails. KL_ERR_HIP reports a failed launch.
+ *  - Device-resident integers (lengths, block tables) are not validated on
+ *    the host (that would need a synchronisation). The kernels clamp a length
+ *    to [0, capacity], treat block ids outside [0, num_blocks) as empty rows,
+ *    and drop appended rows that fall beyond capacity, so bad device data can
+ *    give wrong results but never an out-of-bounds access.
+ *  - Supported: d_head in {64, 128}; H / G in {1, 2, 4, 8}; element type bf16
+ *    (stored as raw 16-bit words) or fp32; arithmetic is fp32 in both cases.
+ */
+#ifndef KEYLESS_H_
+#define KEYLESS_H_
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  KL_OK = 0,
+  KL_ERR_INVALID_ARG = -1,  /* null pointer, bad size, inconsistent shapes      */
+  KL_ERR_UNSUPPORTED = -2,  /* valid request this build does not implement      */
+  KL_ERR_WORKSPACE = -3,    /* workspace missing or smaller than required       */
+  KL_ERR_HIP = -4           /* a HIP runtime call or kernel launch failed       */
+} kl_status;
+
+typedef enum { KL_F32 = 0, KL_BF16 = 1 } kl_dtype;
+
+typedef enum { KL_CONTIGUOUS = 0, KL_PAGED = 1 } kl_layout;
+
+/*
+ * Value-only cache descriptor (Section 3: each head or group keeps its own
+ * rows v_i in R^{d_head}). The descriptor itself lives in host memory; `data`
+ * and `block_table` are device pointers owned by the caller.
+ *
+ *  KL_CONTIGUOUS: data is [B, G, L_max, d_head]; row i of sequence b, group g
+ *                 is data[b][g][i]. Capacity per sequence = L_max.
+ *  KL_PAGED:      data is [num_blocks, G, block_size, d_head]; row i of
+ *                 sequence b lives in block block_table[b * max_blocks_per_seq
+ *                 + i / block_size] at slot i % block_size. block_size must be
+ *                 a power of two and a multiple of 16. Capacity per sequence =
+ *                 max_blocks_per_seq * block_size.
+ */
+typedef struct {
+  void* data;
+  kl_dtype dtype;
+  kl_layout layout;
+  int G;
+  int d_head;
+  int L_max;                  /* contiguous only                                */
+  int block_size;             /* paged only                                     */
+  int num_blocks;             /* paged only                                     */
+  int max_blocks_per_seq;     /* paged only                                     */
+  const int32_t* block_table; /* paged only: [B, max_blocks_per_seq], device    */
+} kl_value_cache;
+
+/*
+ * keyless_fold_routing - folded query weight W~^Q_h = W^Q_h W^R_h for every
+ * head h (Section 2.1: the two query matrices are composed once before
+ * inference; Section 5.5 uses the fused matrix for decoding).
+ *   W_Q   [d_model, H * d_head]   head h owns columns h*d_head .. h*d_head+d_head-1
+ *   W_R   [H, d_head, d_head]     one routing matrix per query head
+ *   Wt_Q  [d_model, H * d_head]   output, same dtype
+ * fp32 accumulation; a bf16 result is rounded to nearest even once.
+ */
+int keyless_fold_routing(const void* W_Q, const void* W_R, int d_model, int H, int d_head,
+                         kl_dtype dtype, void* Wt_Q, void* stream);
+
+/*
+ * keyless_prefill - keyless self-attention over N tokens (Eq. 2 with the
+ * score of Eq. 4; Section 3 multi-head/grouped forms).
+ *   x       [B, N, d_model]
+ *   W_Q     [d_model, H * d_head]; if W_R is NULL it is taken as the folded W~^Q
+ *   W_R     [H, d_head, d_head] or NULL
+ *   W_V     [d_model, G * d_head]
+ *   causal  nonzero: token i attends to tokens j <= i (itself included)
+ *   scale   softmax temperature; 0 selects 1/sqrt(d_head)
+ *   out     [B, N, H, d_head]
+ *   q_routed_out  [B, N, H, d_head] or NULL (the routed queries x W~^Q)
+ *   v_out         [B, N, G, d_head] or NULL (the values to append to the cache)
+ *   ws, ws_bytes  workspace of at least keyless_prefill_workspace_size(...) bytes
+ * There is no key projection. bf16 uses MFMA with fp32 accumulation; the
+ * routed queries and values are rounded to bf16 once, as they would be cached.
+ */
+int keyless_prefill(const void* x, const void* W_Q, const void* W_R, const void* W_V, int B,
+                    int N, int d_model, int H, int G, int d_head, int causal, float scale,
+                    kl_dtype dtype, void* out, void* q_routed_out, void* v_out, void* ws,
+                    size_t ws_bytes, void* stream);
+
+size_t keyless_prefill_workspace_size(int B, int N, int d_model, int H, int G, int d_head,
+                                      kl_dtype dtype, int has_W_R, int has_q_routed_out,
+                                      int has_v_out);
+
+/*
+ * keyless_decode - one decode step over a value-only cache (Section 3):
+ *   out[b,h] = sum_{i < lengths[b]} alpha_i v_i,
+ *   alpha_i = exp(scale <q_routed[b,h], v_i>) / sum_j exp(scale <q_routed[b,h], v_j>)
+ * with v_i the rows of group h / (H / G) of sequence b.
+ *   q_routed [B, H, d_head]  routed queries x W~^Q of the current tokens (cache dtype)
+ *   cache    value-only cache descriptor (host pointer)
+ *   lengths  [B] int32, device: rows per sequence, the current token's value
+ *            included (append it first with value_cache_append)
+ *   scale    0 selects 1/sqrt(d_head) (lambda = 1 in the Section 3 weight)
+ *   out      [B, H, d_head], cache dtype. lengths[b] == 0 gives a zero row.
+ *   ws       at least keyless_decode_workspace_size(...) bytes
+ * Each cached value tile is read from HBM once and used both for the scores
+ * and for the weighted sum. Work is split over the cache length; the split
+ * results are merged in a fixed order, so results are reproducible.
+ */
+int keyless_decode(const void* q_routed, const kl_value_cache* cache, const int32_t* lengths,
+                   int B, int H, float scale, void* out, void* ws, size_t ws_bytes, void* stream);
+
+/* As keyless_decode, with the number of cache rows per split fixed by the
+ * caller (a multiple of 64; 0 selects the built-in choice). */
+int keyless_decode_chunked(const void* q_routed, const kl_value_cache* cache,
+                           const int32_t* lengths, int B, int H, float scale, void* out,
+                           void* ws, size_t ws_bytes, int chunk_rows, void* stream);
+
+size_t keyless_decode_workspace_size(const kl_value_cache* cache, int B, int H, int chunk_rows);
+
+/*
+ * value_cache_append - write T new value rows per sequence into the cache
+ * (Section 3: the new value v_{n+1} joins the cache before the decode step
+ * that reads it).
+ *   values          [B, T, G, d_head], cache dtype
+ *   lengths_before  [B] int32, device: rows already cached; row t of sequence
+ *                   b goes to position lengths_before[b] + t
+ * Positions at or beyond the capacity are dropped. `lengths` is not updated:
+ * the caller owns it.
+ */
+int value_cache_append(const kl_value_cache* cache, const void* values,
+                       const int32_t* lengths_before, int B, int T, void* stream);
+
+/*
+ * standard_decode - the comparison baseline: standard attention of Eq. 1 for
+ * one new query per sequence over a key cache and a value cache with the same
+ * layout as `v_cache` (scores <q, k_i>, weights applied to v_i). Same tiling,
+ * split and merge as keyless_decode; it reads twice the bytes.
+ */
+int standard_decode(const void* q, const kl_value_cache* k_cache, const kl_value_cache* v_cache,
+                    const int32_t* lengths, int B, int H, float scale, void* out, void* ws,
+                    size_t ws_bytes, void* stream);
+
+int standard_decode_chunked(const void* q, const kl_value_cache* k_cache,
+                            const kl_value_cache* v_cache, const int32_t* lengths, int B, int H,
+                            float scale, void* out, void* ws, size_t ws_bytes, int chunk_rows,
+                            void* stream);
+
+/*
+ * keyless_set_kernel_timer - instrumentation for benchmarks. When both handles
+ * are non-NULL (hipEvent_t created by the caller), every later decode or
+ * standard_decode call made on this thread records `start` on its stream just
+ * before its split kernel (the kernel that reads the cache) and `stop` just
+ * after it, so that kernel can be timed alone. NULL, NULL turns it off.
+ */
+void keyless_set_kernel_timer(void* start_event, void* stop_event);
+
+/* Thread-local text describing the last non-OK status returned on this thread. */
+const char* keyless_last_error(void);
+
+/* Library version string. */
+const char* keyless_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* KEYLESS_H_ */

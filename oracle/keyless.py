@@ -133,12 +133,13 @@ def keyless_prefill_rows(x, Wt_Q, W_V, rows, H: int, G: int, d_head: int,
     rows = [int(r) for r in rows]
     n_seen = (max(rows) + 1) if causal else X.shape[0]
     V = (X[:n_seen] @ W_V).reshape(n_seen, G, d_head)
+    Vg = np.ascontiguousarray(V.transpose(1, 0, 2))  # [G, n_seen, d_k], rows of each group
     Qt = (X[rows] @ Wt_Q).reshape(len(rows), H, d_head)
     O = np.zeros((len(rows), H, d_head))
     for k, i in enumerate(rows):
         last = i + 1 if causal else n_seen
         for h in range(H):
-            V_g = V[:last, h // rep, :]
+            V_g = Vg[h // rep, :last, :]
             s = tau * (V_g @ Qt[k, h])
             p = softmax_rows(s[None, :])[0]
             O[k, h] = p @ V_g

@@ -1,0 +1,236 @@
+"""Thin ctypes binding of libkeyless.so (the C ABI in include/keyless.h).
+
+Argument marshalling only: torch supplies device memory and the current HIP
+stream; every step of the computation runs in the library's HIP kernels.
+There is no fallback: if the library is not built, every call raises.
+"""
+
+from __future__ import annotations
+
+import ctypes
+import os
+
+import torch
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libkeyless.so")
+
+KL_OK, KL_ERR_INVALID_ARG, KL_ERR_UNSUPPORTED, KL_ERR_WORKSPACE, KL_ERR_HIP = 0, -1, -2, -3, -4
+KL_F32, KL_BF16 = 0, 1
+KL_CONTIGUOUS, KL_PAGED = 0, 1
+
+# Every symbol include/keyless.h declares.
+EXPORTS = (
+    "keyless_fold_routing", "keyless_prefill", "keyless_prefill_workspace_size",
+    "keyless_decode", "keyless_decode_chunked", "keyless_decode_workspace_size",
+    "value_cache_append", "standard_decode", "standard_decode_chunked",
+    "keyless_set_kernel_timer", "keyless_last_error", "keyless_version",
+)
+
+
+class KeylessError(RuntimeError):
+    def __init__(self, status: int, message: str):
+        super().__init__(f"status {status}: {message}")
+        self.status = status
+
+
+class KLValueCache(ctypes.Structure):
+    _fields_ = [
+        ("data", ctypes.c_void_p), ("dtype", ctypes.c_int), ("layout", ctypes.c_int),
+        ("G", ctypes.c_int), ("d_head", ctypes.c_int), ("L_max", ctypes.c_int),
+        ("block_size", ctypes.c_int), ("num_blocks", ctypes.c_int),
+        ("max_blocks_per_seq", ctypes.c_int), ("block_table", ctypes.c_void_p),
+    ]
+
+
+_lib = None
+
+
+def load(path: str = LIB_PATH):
+    """Load the shared library (once). Raises if it has not been built."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(path):
+        raise RuntimeError(f"{path} is missing: build it with `python -m paper_2606_21848_amd.build`")
+    # torch's HIP runtime must be loaded first so the library binds to it.
+    import torch.cuda  # noqa: F401
+    lib = ctypes.CDLL(path)
+    vp, i, f, sz = ctypes.c_void_p, ctypes.c_int, ctypes.c_float, ctypes.c_size_t
+    cp = ctypes.POINTER(KLValueCache)
+    sig = {
+        "keyless_fold_routing": (i, [vp, vp, i, i, i, i, vp, vp]),
+        "keyless_prefill": (i, [vp, vp, vp, vp, i, i, i, i, i, i, i, f, i, vp, vp, vp, vp, sz, vp]),
+        "keyless_prefill_workspace_size": (sz, [i, i, i, i, i, i, i, i, i, i]),
+        "keyless_decode": (i, [vp, cp, vp, i, i, f, vp, vp, sz, vp]),
+        "keyless_decode_chunked": (i, [vp, cp, vp, i, i, f, vp, vp, sz, i, vp]),
+        "keyless_decode_workspace_size": (sz, [cp, i, i, i]),
+        "value_cache_append": (i, [cp, vp, vp, i, i, vp]),
+        "standard_decode": (i, [vp, cp, cp, vp, i, i, f, vp, vp, sz, vp]),
+        "standard_decode_chunked": (i, [vp, cp, cp, vp, i, i, f, vp, vp, sz, i, vp]),
+        "keyless_set_kernel_timer": (None, [vp, vp]),
+        "keyless_last_error": (ctypes.c_char_p, []),
+        "keyless_version": (ctypes.c_char_p, []),
+    }
+    for name, (res, args) in sig.items():
+        fn = getattr(lib, name)
+        fn.restype = res
+        fn.argtypes = args
+    _lib = lib
+    return lib
+
+
+def _check(status: int):
+    if status != KL_OK:
+        raise KeylessError(status, _lib.keyless_last_error().decode())
+
+
+def _dt(t: torch.Tensor) -> int:
+    if t.dtype == torch.bfloat16:
+        return KL_BF16
+    if t.dtype == torch.float32:
+        return KL_F32
+    raise TypeError(f"unsupported dtype {t.dtype} (bf16 or fp32)")
+
+
+def _ptr(t):
+    if t is None:
+        return None
+    if not t.is_cuda:
+        raise ValueError("tensors must be on the GPU")
+    if not t.is_contiguous():
+        raise ValueError("tensors must be contiguous")
+    return ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(t: torch.Tensor):
+    return ctypes.c_void_p(torch.cuda.current_stream(t.device).cuda_stream)
+
+
+class ValueCache:
+    """A value-only cache: contiguous [B, G, L_max, d] or paged [num_blocks, G, bs, d]."""
+
+    def __init__(self, data: torch.Tensor, block_table: torch.Tensor | None = None):
+        self.data = data
+        self.block_table = block_table
+        d = KLValueCache()
+        d.data = data.data_ptr()
+        d.dtype = _dt(data)
+        d.G = data.shape[1]
+        d.d_head = data.shape[3]
+        if block_table is None:
+            d.layout = KL_CONTIGUOUS
+            d.L_max = data.shape[2]
+        else:
+            if block_table.dtype != torch.int32:
+                raise TypeError("block_table must be int32")
+            _ptr(block_table)
+            d.layout = KL_PAGED
+            d.block_size = data.shape[2]
+            d.num_blocks = data.shape[0]
+            d.max_blocks_per_seq = block_table.shape[1]
+            d.block_table = block_table.data_ptr()
+        _ptr(data)
+        self.desc = d
+
+    @property
+    def ref(self):
+        return ctypes.byref(self.desc)
+
+
+def decode_workspace_bytes(cache: ValueCache, B: int, H: int, chunk_rows: int = 0) -> int:
+    load()
+    return int(_lib.keyless_decode_workspace_size(cache.ref, B, H, chunk_rows))
+
+
+def keyless_decode(q_routed: torch.Tensor, cache: ValueCache, lengths: torch.Tensor,
+                   scale: float = 0.0, out: torch.Tensor | None = None,
+                   workspace: torch.Tensor | None = None, chunk_rows: int = 0) -> torch.Tensor:
+    """out[b, h] = softmax over the cached values of <q~, v> * scale, applied to the values."""
+    load()
+    B, H, _ = q_routed.shape
+    if lengths.dtype != torch.int32:
+        raise TypeError("lengths must be int32")
+    if out is None:
+        out = torch.empty_like(q_routed)
+    if workspace is None:
+        workspace = torch.empty(max(decode_workspace_bytes(cache, B, H, chunk_rows), 256),
+                                dtype=torch.uint8, device=q_routed.device)
+    _check(_lib.keyless_decode_chunked(_ptr(q_routed), cache.ref, _ptr(lengths), B, H, scale,
+                                       _ptr(out), _ptr(workspace), workspace.numel(), chunk_rows,
+                                       _stream(q_routed)))
+    return out
+
+
+def standard_decode(q: torch.Tensor, k_cache: ValueCache, v_cache: ValueCache,
+                    lengths: torch.Tensor, scale: float = 0.0, out: torch.Tensor | None = None,
+                    workspace: torch.Tensor | None = None, chunk_rows: int = 0) -> torch.Tensor:
+    load()
+    B, H, _ = q.shape
+    if out is None:
+        out = torch.empty_like(q)
+    if workspace is None:
+        workspace = torch.empty(max(decode_workspace_bytes(v_cache, B, H, chunk_rows), 256),
+                                dtype=torch.uint8, device=q.device)
+    _check(_lib.standard_decode_chunked(_ptr(q), k_cache.ref, v_cache.ref, _ptr(lengths), B, H,
+                                        scale, _ptr(out), _ptr(workspace), workspace.numel(),
+                                        chunk_rows, _stream(q)))
+    return out
+
+
+def value_cache_append(cache: ValueCache, values: torch.Tensor, lengths_before: torch.Tensor):
+    """Write values[b, t, g, :] at position lengths_before[b] + t of sequence b."""
+    load()
+    B, T = values.shape[0], values.shape[1]
+    _check(_lib.value_cache_append(cache.ref, _ptr(values), _ptr(lengths_before), B, T,
+                                   _stream(values)))
+
+
+def keyless_fold_routing(W_Q: torch.Tensor, W_R: torch.Tensor) -> torch.Tensor:
+    """W~^Q_h = W^Q_h W^R_h for every head; W_Q [d, H*d_k], W_R [H, d_k, d_k]."""
+    load()
+    H, dk, _ = W_R.shape
+    out = torch.empty_like(W_Q)
+    _check(_lib.keyless_fold_routing(_ptr(W_Q), _ptr(W_R), W_Q.shape[0], H, dk, _dt(W_Q),
+                                     _ptr(out), _stream(W_Q)))
+    return out
+
+
+def keyless_prefill(x: torch.Tensor, W_Q: torch.Tensor, W_R: torch.Tensor | None,
+                    W_V: torch.Tensor, H: int, G: int, causal: bool = True, scale: float = 0.0,
+                    return_qv: bool = False, out=None, q_routed_out=None, v_out=None,
+                    workspace=None):
+    """Keyless self-attention; returns out [B, N, H, d] (and Q~, V if return_qv)."""
+    load()
+    B, N, d_model = x.shape
+    dk = W_Q.shape[1] // H
+    if out is None:
+        out = torch.empty((B, N, H, dk), dtype=x.dtype, device=x.device)
+    if return_qv:
+        if q_routed_out is None:
+            q_routed_out = torch.empty((B, N, H, dk), dtype=x.dtype, device=x.device)
+        if v_out is None:
+            v_out = torch.empty((B, N, G, dk), dtype=x.dtype, device=x.device)
+    need = int(_lib.keyless_prefill_workspace_size(B, N, d_model, H, G, dk, _dt(x),
+                                                   int(W_R is not None), int(q_routed_out is not None),
+                                                   int(v_out is not None)))
+    if workspace is None:
+        workspace = torch.empty(max(need, 256), dtype=torch.uint8, device=x.device)
+    _check(_lib.keyless_prefill(_ptr(x), _ptr(W_Q), _ptr(W_R), _ptr(W_V), B, N, d_model, H, G, dk,
+                                int(causal), scale, _dt(x), _ptr(out), _ptr(q_routed_out),
+                                _ptr(v_out), _ptr(workspace), workspace.numel(), _stream(x)))
+    if return_qv:
+        return out, q_routed_out, v_out
+    return out
+
+
+def set_kernel_timer(start: "torch.cuda.Event | None", stop: "torch.cuda.Event | None"):
+    """Record ``start``/``stop`` around the split kernel of later decode calls on
+    this thread (both events must already have been recorded once, so that
+    torch has created them); ``None, None`` turns it off."""
+    load()
+    if start is None or stop is None:
+        _lib.keyless_set_kernel_timer(None, None)
+    else:
+        _lib.keyless_set_kernel_timer(ctypes.c_void_p(start.cuda_event),
+                                      ctypes.c_void_p(stop.cuda_event))

@@ -1,0 +1,363 @@
+// C ABI of the keyless-attention library: argument validation, workspace
+// sizing, split selection and kernel launches on the caller's stream.
+// Nothing here allocates, frees or synchronises.
+
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <string>
+
+#include "keyless.h"
+#include "kl_internal.h"
+
+namespace kl {
+hipError_t launch_prefill_attention_simple(const AttnParams& p, hipStream_t stream);
+}
+
+namespace {
+
+thread_local std::string g_err;
+thread_local hipEvent_t g_timer_start = nullptr;
+thread_local hipEvent_t g_timer_stop = nullptr;
+
+int fail(int code, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof(buf), fmt, ap);
+  va_end(ap);
+  g_err = buf;
+  return code;
+}
+
+int hip_status(hipError_t e, const char* what) {
+  if (e == hipSuccess) return KL_OK;
+  return fail(KL_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+size_t elem_bytes(kl_dtype dt) { return dt == KL_BF16 ? 2 : 4; }
+
+bool dtype_ok(kl_dtype dt) { return dt == KL_BF16 || dt == KL_F32; }
+
+size_t align256(size_t n) { return (n + 255) & ~size_t(255); }
+
+int log2_exact(int v) {
+  if (v <= 0 || (v & (v - 1))) return -1;
+  int s = 0;
+  while ((1 << s) < v) ++s;
+  return s;
+}
+
+float scale_or_default(float scale, int d_head) {
+  return scale != 0.f ? scale : 1.f / std::sqrt((float)d_head);
+}
+
+constexpr float kLog2e = 1.4426950408889634f;
+
+// Validates a cache descriptor. Returns KL_OK or an error code (message set).
+int check_cache(const kl_value_cache* c, const char* name) {
+  if (!c) return fail(KL_ERR_INVALID_ARG, "%s: descriptor is NULL", name);
+  if (!c->data) return fail(KL_ERR_INVALID_ARG, "%s: data is NULL", name);
+  if (!aligned16(c->data)) return fail(KL_ERR_INVALID_ARG, "%s: data is not 16-byte aligned", name);
+  if (!dtype_ok(c->dtype)) return fail(KL_ERR_UNSUPPORTED, "%s: unknown dtype %d", name, (int)c->dtype);
+  if (c->d_head != 64 && c->d_head != 128)
+    return fail(KL_ERR_UNSUPPORTED, "%s: d_head %d not supported (64 or 128)", name, c->d_head);
+  if (c->G <= 0) return fail(KL_ERR_INVALID_ARG, "%s: G must be positive (got %d)", name, c->G);
+  if (c->layout == KL_CONTIGUOUS) {
+    if (c->L_max < 0) return fail(KL_ERR_INVALID_ARG, "%s: L_max is negative", name);
+  } else if (c->layout == KL_PAGED) {
+    if (log2_exact(c->block_size) < 4)
+      return fail(KL_ERR_UNSUPPORTED, "%s: block_size %d must be a power of two >= 16", name,
+                  c->block_size);
+    if (c->num_blocks <= 0 || c->max_blocks_per_seq <= 0)
+      return fail(KL_ERR_INVALID_ARG, "%s: num_blocks and max_blocks_per_seq must be positive", name);
+    if (!c->block_table) return fail(KL_ERR_INVALID_ARG, "%s: block_table is NULL", name);
+    if ((long)c->max_blocks_per_seq * c->block_size > (1L << 30))
+      return fail(KL_ERR_UNSUPPORTED, "%s: capacity per sequence too large", name);
+  } else {
+    return fail(KL_ERR_INVALID_ARG, "%s: unknown layout %d", name, (int)c->layout);
+  }
+  return KL_OK;
+}
+
+int cache_capacity(const kl_value_cache* c) {
+  return c->layout == KL_PAGED ? c->max_blocks_per_seq * c->block_size : c->L_max;
+}
+
+// Rows per split: enough splits that the grid holds several workgroups per
+// compute unit, but at least 256 rows per split so each wave walks several tiles.
+int auto_chunk(int B, int G, int cap) {
+  const long pairs = (long)B * G;
+  const long target_groups = 4096;
+  long chunk = (pairs * cap + target_groups - 1) / target_groups;
+  long c = 256;
+  while (c < chunk && c < 8192) c <<= 1;
+  return (int)c;
+}
+
+int decode_common(const void* q, const kl_value_cache* k_cache, const kl_value_cache* v_cache,
+                  const int32_t* lengths, int B, int H, float scale, void* out, void* ws,
+                  size_t ws_bytes, int chunk_rows, void* stream, const char* who) {
+  int st = check_cache(v_cache, who);
+  if (st != KL_OK) return st;
+  if (k_cache) {
+    st = check_cache(k_cache, "k_cache");
+    if (st != KL_OK) return st;
+    if (k_cache->layout != KL_CONTIGUOUS || v_cache->layout != KL_CONTIGUOUS)
+      return fail(KL_ERR_UNSUPPORTED, "%s: only contiguous key/value caches", who);
+    if (k_cache->dtype != v_cache->dtype || k_cache->G != v_cache->G ||
+        k_cache->d_head != v_cache->d_head || k_cache->L_max != v_cache->L_max)
+      return fail(KL_ERR_INVALID_ARG, "%s: key and value caches differ in shape or dtype", who);
+  }
+  if (!q || !lengths || !out)
+    return fail(KL_ERR_INVALID_ARG, "%s: q, lengths and out must be non-NULL", who);
+  if (!aligned16(q) || !aligned16(out))
+    return fail(KL_ERR_INVALID_ARG, "%s: q and out must be 16-byte aligned", who);
+  if (B < 0 || H <= 0) return fail(KL_ERR_INVALID_ARG, "%s: bad B=%d or H=%d", who, B, H);
+  const int G = v_cache->G;
+  if (H % G != 0) return fail(KL_ERR_INVALID_ARG, "%s: H=%d is not a multiple of G=%d", who, H, G);
+  const int R = H / G;
+  if (R != 1 && R != 2 && R != 4 && R != 8)
+    return fail(KL_ERR_UNSUPPORTED, "%s: H/G=%d not supported (1, 2, 4 or 8)", who, R);
+  if (chunk_rows < 0 || chunk_rows % 64 != 0)
+    return fail(KL_ERR_INVALID_ARG, "%s: chunk_rows=%d must be a multiple of 64", who, chunk_rows);
+  if (B == 0) return KL_OK;
+  const int cap = cache_capacity(v_cache);
+  const int chunk = chunk_rows ? chunk_rows : auto_chunk(B, G, cap);
+  const size_t need = keyless_decode_workspace_size(v_cache, B, H, chunk);
+  if (!ws || ws_bytes < need)
+    return fail(KL_ERR_WORKSPACE, "%s: workspace of %zu bytes needed, %zu given", who, need, ws_bytes);
+  if (!aligned16(ws)) return fail(KL_ERR_INVALID_ARG, "%s: workspace must be 16-byte aligned", who);
+
+  kl::DecodeParams p{};
+  p.q = q;
+  p.vdata = v_cache->data;
+  p.kdata = k_cache ? k_cache->data : nullptr;
+  p.table = v_cache->layout == KL_PAGED ? v_cache->block_table : nullptr;
+  p.lengths = lengths;
+  p.out = out;
+  p.part = static_cast<float*>(ws);
+  p.B = B;
+  p.H = H;
+  p.G = G;
+  p.D = v_cache->d_head;
+  p.R = R;
+  p.dtype = v_cache->dtype;
+  p.paged = v_cache->layout == KL_PAGED;
+  p.L_max = v_cache->L_max;
+  p.block_shift = p.paged ? log2_exact(v_cache->block_size) : 0;
+  p.num_blocks = v_cache->num_blocks;
+  p.max_blocks = v_cache->max_blocks_per_seq;
+  p.chunk = chunk;
+  p.S = cap > 0 ? (cap + chunk - 1) / chunk : 1;
+  p.scale_log2 = scale_or_default(scale, p.D) * kLog2e;
+  p.ev_start = g_timer_start;
+  p.ev_stop = g_timer_stop;
+  if (p.S > 65535) return fail(KL_ERR_UNSUPPORTED, "%s: too many splits (%d)", who, p.S);
+  return hip_status(kl::launch_decode(p, static_cast<hipStream_t>(stream)), who);
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* keyless_last_error(void) { return g_err.c_str(); }
+
+const char* keyless_version(void) { return "keyless-gfx950 0.1"; }
+
+void keyless_set_kernel_timer(void* start_event, void* stop_event) {
+  const bool on = start_event && stop_event;
+  g_timer_start = on ? static_cast<hipEvent_t>(start_event) : nullptr;
+  g_timer_stop = on ? static_cast<hipEvent_t>(stop_event) : nullptr;
+}
+
+size_t keyless_decode_workspace_size(const kl_value_cache* cache, int B, int H, int chunk_rows) {
+  if (!cache || B <= 0 || H <= 0 || cache->G <= 0 || chunk_rows < 0) return 0;
+  const int cap = cache->layout == KL_PAGED ? cache->max_blocks_per_seq * cache->block_size
+                                            : cache->L_max;
+  const int chunk = chunk_rows ? chunk_rows : auto_chunk(B, cache->G, cap);
+  const size_t S = cap > 0 ? (size_t)(cap + chunk - 1) / chunk : 1;
+  return align256((size_t)B * H * S * (cache->d_head + 2) * sizeof(float));
+}
+
+int keyless_decode(const void* q_routed, const kl_value_cache* cache, const int32_t* lengths,
+                   int B, int H, float scale, void* out, void* ws, size_t ws_bytes, void* stream) {
+  return decode_common(q_routed, nullptr, cache, lengths, B, H, scale, out, ws, ws_bytes, 0,
+                       stream, "keyless_decode");
+}
+
+int keyless_decode_chunked(const void* q_routed, const kl_value_cache* cache,
+                           const int32_t* lengths, int B, int H, float scale, void* out, void* ws,
+                           size_t ws_bytes, int chunk_rows, void* stream) {
+  return decode_common(q_routed, nullptr, cache, lengths, B, H, scale, out, ws, ws_bytes,
+                       chunk_rows, stream, "keyless_decode_chunked");
+}
+
+int standard_decode(const void* q, const kl_value_cache* k_cache, const kl_value_cache* v_cache,
+                    const int32_t* lengths, int B, int H, float scale, void* out, void* ws,
+                    size_t ws_bytes, void* stream) {
+  if (!k_cache) return fail(KL_ERR_INVALID_ARG, "standard_decode: k_cache is NULL");
+  return decode_common(q, k_cache, v_cache, lengths, B, H, scale, out, ws, ws_bytes, 0, stream,
+                       "standard_decode");
+}
+
+int standard_decode_chunked(const void* q, const kl_value_cache* k_cache,
+                            const kl_value_cache* v_cache, const int32_t* lengths, int B, int H,
+                            float scale, void* out, void* ws, size_t ws_bytes, int chunk_rows,
+                            void* stream) {
+  if (!k_cache) return fail(KL_ERR_INVALID_ARG, "standard_decode_chunked: k_cache is NULL");
+  return decode_common(q, k_cache, v_cache, lengths, B, H, scale, out, ws, ws_bytes, chunk_rows,
+                       stream, "standard_decode_chunked");
+}
+
+int value_cache_append(const kl_value_cache* cache, const void* values,
+                       const int32_t* lengths_before, int B, int T, void* stream) {
+  int st = check_cache(cache, "value_cache_append");
+  if (st != KL_OK) return st;
+  if (!values || !lengths_before)
+    return fail(KL_ERR_INVALID_ARG, "value_cache_append: values and lengths_before must be non-NULL");
+  if (!aligned16(values)) return fail(KL_ERR_INVALID_ARG, "value_cache_append: values not 16-byte aligned");
+  if (B < 0 || T < 0) return fail(KL_ERR_INVALID_ARG, "value_cache_append: bad B=%d or T=%d", B, T);
+  if (B == 0 || T == 0) return KL_OK;
+  kl::AppendParams p{};
+  p.data = cache->data;
+  p.values = values;
+  p.lengths_before = lengths_before;
+  p.table = cache->layout == KL_PAGED ? cache->block_table : nullptr;
+  p.B = B;
+  p.T = T;
+  p.G = cache->G;
+  p.D = cache->d_head;
+  p.dtype = cache->dtype;
+  p.paged = cache->layout == KL_PAGED;
+  p.L_max = cache->L_max;
+  p.block_shift = p.paged ? log2_exact(cache->block_size) : 0;
+  p.num_blocks = cache->num_blocks;
+  p.max_blocks = cache->max_blocks_per_seq;
+  return hip_status(kl::launch_append(p, static_cast<hipStream_t>(stream)), "value_cache_append");
+}
+
+int keyless_fold_routing(const void* W_Q, const void* W_R, int d_model, int H, int d_head,
+                         kl_dtype dtype, void* Wt_Q, void* stream) {
+  if (!W_Q || !W_R || !Wt_Q)
+    return fail(KL_ERR_INVALID_ARG, "keyless_fold_routing: W_Q, W_R and Wt_Q must be non-NULL");
+  if (!dtype_ok(dtype)) return fail(KL_ERR_UNSUPPORTED, "keyless_fold_routing: unknown dtype");
+  if (d_model <= 0 || H <= 0 || d_head <= 0)
+    return fail(KL_ERR_INVALID_ARG, "keyless_fold_routing: sizes must be positive");
+  kl::GemmParams g{};
+  g.A = W_Q;
+  g.Bm = W_R;
+  g.C = Wt_Q;
+  g.M = d_model;
+  g.N = d_head;
+  g.K = d_head;
+  g.lda = (long)H * d_head;
+  g.ldb = d_head;
+  g.ldc = (long)H * d_head;
+  g.strideA = d_head;
+  g.strideB = (long)d_head * d_head;
+  g.strideC = d_head;
+  g.batch = H;
+  g.dtype = dtype;
+  return hip_status(kl::launch_gemm_simple(g, static_cast<hipStream_t>(stream)),
+                    "keyless_fold_routing");
+}
+
+size_t keyless_prefill_workspace_size(int B, int N, int d_model, int H, int G, int d_head,
+                                      kl_dtype dtype, int has_W_R, int has_q_routed_out,
+                                      int has_v_out) {
+  if (B < 0 || N < 0 || d_model <= 0 || H <= 0 || G <= 0 || d_head <= 0) return 0;
+  const size_t e = elem_bytes(dtype);
+  size_t n = 0;
+  if (has_W_R) n += align256((size_t)d_model * H * d_head * e);
+  if (!has_q_routed_out) n += align256((size_t)B * N * H * d_head * e);
+  if (!has_v_out) n += align256((size_t)B * N * G * d_head * e);
+  return n;
+}
+
+int keyless_prefill(const void* x, const void* W_Q, const void* W_R, const void* W_V, int B,
+                    int N, int d_model, int H, int G, int d_head, int causal, float scale,
+                    kl_dtype dtype, void* out, void* q_routed_out, void* v_out, void* ws,
+                    size_t ws_bytes, void* stream) {
+  const char* who = "keyless_prefill";
+  if (!x || !W_Q || !W_V || !out)
+    return fail(KL_ERR_INVALID_ARG, "%s: x, W_Q, W_V and out must be non-NULL", who);
+  if (!dtype_ok(dtype)) return fail(KL_ERR_UNSUPPORTED, "%s: unknown dtype", who);
+  if (B < 0 || N < 0 || d_model <= 0 || H <= 0 || G <= 0)
+    return fail(KL_ERR_INVALID_ARG, "%s: bad sizes B=%d N=%d d_model=%d H=%d G=%d", who, B, N,
+                d_model, H, G);
+  if (d_head != 64 && d_head != 128)
+    return fail(KL_ERR_UNSUPPORTED, "%s: d_head %d not supported (64 or 128)", who, d_head);
+  if (H % G != 0) return fail(KL_ERR_INVALID_ARG, "%s: H=%d is not a multiple of G=%d", who, H, G);
+  const size_t need = keyless_prefill_workspace_size(B, N, d_model, H, G, d_head, dtype,
+                                                     W_R != nullptr, q_routed_out != nullptr,
+                                                     v_out != nullptr);
+  if (need && (!ws || ws_bytes < need))
+    return fail(KL_ERR_WORKSPACE, "%s: workspace of %zu bytes needed, %zu given", who, need, ws_bytes);
+  if (B == 0 || N == 0) return KL_OK;
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  const size_t e = elem_bytes(dtype);
+  char* w = static_cast<char*>(ws);
+  const void* Wt = W_Q;
+  if (W_R) {
+    void* fold = w;
+    w += align256((size_t)d_model * H * d_head * e);
+    const int s = keyless_fold_routing(W_Q, W_R, d_model, H, d_head, dtype, fold, stream);
+    if (s != KL_OK) return s;
+    Wt = fold;
+  }
+  void* qr = q_routed_out;
+  if (!qr) {
+    qr = w;
+    w += align256((size_t)B * N * H * d_head * e);
+  }
+  void* vv = v_out;
+  if (!vv) {
+    vv = w;
+    w += align256((size_t)B * N * G * d_head * e);
+  }
+  const long M = (long)B * N;
+  if (M > (1L << 30)) return fail(KL_ERR_UNSUPPORTED, "%s: B*N too large", who);
+  kl::GemmParams g{};
+  g.A = x;
+  g.M = (int)M;
+  g.K = d_model;
+  g.lda = d_model;
+  g.batch = 1;
+  g.dtype = dtype;
+  // Routed queries Q~ = X W~^Q and values V = X W^V; no key projection.
+  g.Bm = Wt;
+  g.C = qr;
+  g.N = H * d_head;
+  g.ldb = g.ldc = (long)H * d_head;
+  int s = hip_status(kl::launch_gemm_simple(g, st), who);
+  if (s != KL_OK) return s;
+  g.Bm = W_V;
+  g.C = vv;
+  g.N = G * d_head;
+  g.ldb = g.ldc = (long)G * d_head;
+  s = hip_status(kl::launch_gemm_simple(g, st), who);
+  if (s != KL_OK) return s;
+  kl::AttnParams a{};
+  a.q = qr;
+  a.v = vv;
+  a.out = out;
+  a.q_stride = (long)H * d_head;
+  a.v_stride = (long)G * d_head;
+  a.o_stride = (long)H * d_head;
+  a.B = B;
+  a.N = N;
+  a.H = H;
+  a.G = G;
+  a.D = d_head;
+  a.causal = causal ? 1 : 0;
+  a.scale_log2 = scale_or_default(scale, d_head) * kLog2e;
+  a.dtype = dtype;
+  return hip_status(kl::launch_prefill_attention_simple(a, st), who);
+}
+
+}  // extern "C"

@@ -1,0 +1,78 @@
+// Internal launch interface between the C-ABI host code and the kernels.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "keyless.h"
+
+namespace kl {
+
+struct DecodeParams {
+  const void* q;          // [B, H, D]
+  const void* vdata;      // value cache data
+  const void* kdata;      // key cache data (standard decode) or nullptr
+  const int32_t* table;   // paged block table or nullptr
+  const int32_t* lengths; // [B]
+  void* out;              // [B, H, D]
+  float* part;            // [B * H, S, D + 2] split partials
+  int B, H, G, D, R;
+  kl_dtype dtype;
+  bool paged;
+  int L_max;              // contiguous capacity
+  int block_shift;        // log2(block_size), paged
+  int num_blocks, max_blocks;
+  int chunk;              // rows per split (multiple of 64)
+  int S;                  // splits per sequence
+  float scale_log2;       // scale * log2(e)
+  hipEvent_t ev_start;    // optional: recorded around the split kernel
+  hipEvent_t ev_stop;
+};
+
+hipError_t launch_decode(const DecodeParams& p, hipStream_t stream);
+
+struct AppendParams {
+  void* data;
+  const void* values;     // [B, T, G, D]
+  const int32_t* lengths_before;
+  const int32_t* table;
+  int B, T, G, D;
+  kl_dtype dtype;
+  bool paged;
+  int L_max, block_shift, num_blocks, max_blocks;
+};
+
+hipError_t launch_append(const AppendParams& p, hipStream_t stream);
+
+// C[b] (M x N) = A[b] (M x K) * B[b] (K x N), row-major with leading
+// dimensions, fp32 accumulation; batched by pointer strides. Generic tiled
+// kernel for the small products (routing fold, fp32 prefill projections).
+struct GemmParams {
+  const void* A; const void* Bm; void* C;
+  int M, N, K;
+  long lda, ldb, ldc;
+  long strideA, strideB, strideC;  // elements between batch items
+  int batch;
+  kl_dtype dtype;
+};
+
+hipError_t launch_gemm_simple(const GemmParams& p, hipStream_t stream);
+
+// bf16 MFMA GEMM: C (M x N, bf16) = A (M x K, bf16) * B (K x N, bf16).
+hipError_t launch_gemm_bf16(const void* A, const void* Bm, void* C, int M, int N, int K, long lda,
+                            long ldb, long ldc, hipStream_t stream);
+
+struct AttnParams {
+  const void* q;   // routed queries, [B, N, H, D] with row stride q_stride (elements per token)
+  const void* v;   // values, [B, N, G, D] with row stride v_stride
+  void* out;       // [B, N, H, D]
+  long q_stride, v_stride, o_stride;
+  int B, N, H, G, D;
+  int causal;
+  float scale_log2;
+  kl_dtype dtype;
+};
+
+hipError_t launch_prefill_attention(const AttnParams& p, hipStream_t stream);
+
+}  // namespace kl

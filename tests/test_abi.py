@@ -1,0 +1,114 @@
+"""The C ABI without a GPU: the library loads, exports what include/keyless.h
+declares, sizes workspaces, and rejects bad arguments before touching the
+device (every call below fails host-side validation, so nothing is launched)."""
+
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2606_21848_amd import binding as kb
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+FAKE = ctypes.c_void_p(0x100000)  # never dereferenced: validation fails first
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(kb.LIB_PATH):
+        pytest.fail("libkeyless.so is not built (run __graft_entry__.build())")
+    return kb.load()
+
+
+def declared_functions():
+    text = open(os.path.join(ROOT, "include", "keyless.h")).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"^\s*(?:const\s+)?\w+\*?\s+\*?(\w+)\s*\(", text, flags=re.M)))
+
+
+def test_exports_every_declared_symbol(lib):
+    names = declared_functions()
+    assert set(names) == set(kb.EXPORTS), names
+    for n in names:
+        assert hasattr(lib, n), n
+    assert lib.keyless_version().decode().startswith("keyless")
+
+
+def cache(G=8, d=128, layout=kb.KL_CONTIGUOUS, L_max=4096, bs=16, nb=10, mb=4, dtype=kb.KL_BF16,
+          table=FAKE):
+    c = kb.KLValueCache()
+    c.data = FAKE.value
+    c.dtype, c.layout, c.G, c.d_head, c.L_max = dtype, layout, G, d, L_max
+    c.block_size, c.num_blocks, c.max_blocks_per_seq = bs, nb, mb
+    c.block_table = table.value if table else None
+    return c
+
+
+def decode(lib, c, B=2, H=8, ws_bytes=1 << 30, chunk=0, q=FAKE, lengths=FAKE, out=FAKE, ws=FAKE):
+    return lib.keyless_decode_chunked(q, ctypes.byref(c), lengths, B, H, 0.0, out, ws, ws_bytes,
+                                      chunk, None)
+
+
+def expect(lib, status, code, fragment):
+    assert status == code, (status, lib.keyless_last_error())
+    assert fragment in lib.keyless_last_error().decode()
+
+
+def test_workspace_sizes(lib):
+    c = cache(G=32, L_max=4096)
+    # B*H*splits*(d+2)*4 bytes, rounded to 256; 512 rows per split here.
+    assert lib.keyless_decode_workspace_size(ctypes.byref(c), 8, 32, 512) == 8 * 32 * 8 * 130 * 4
+    assert lib.keyless_decode_workspace_size(ctypes.byref(c), 8, 32, 0) > 0
+    n = lib.keyless_prefill_workspace_size(1, 128, 256, 4, 4, 64, kb.KL_F32, 1, 0, 0)
+    assert n == 256 * 256 * 4 + 128 * 256 * 4 * 2
+
+
+def test_decode_rejects_bad_arguments(lib):
+    expect(lib, decode(lib, cache(), q=None), kb.KL_ERR_INVALID_ARG, "non-NULL")
+    expect(lib, decode(lib, cache(d=96)), kb.KL_ERR_UNSUPPORTED, "d_head 96")
+    expect(lib, decode(lib, cache(G=3), H=8), kb.KL_ERR_INVALID_ARG, "multiple")
+    expect(lib, decode(lib, cache(G=1), H=16), kb.KL_ERR_UNSUPPORTED, "H/G=16")
+    expect(lib, decode(lib, cache(), ws_bytes=1000), kb.KL_ERR_WORKSPACE, "workspace")
+    expect(lib, decode(lib, cache(), chunk=100), kb.KL_ERR_INVALID_ARG, "multiple of 64")
+    expect(lib, decode(lib, cache(dtype=7)), kb.KL_ERR_UNSUPPORTED, "dtype")
+    expect(lib, decode(lib, cache(layout=kb.KL_PAGED, bs=8)), kb.KL_ERR_UNSUPPORTED, "block_size")
+    expect(lib, decode(lib, cache(layout=kb.KL_PAGED, table=None)), kb.KL_ERR_INVALID_ARG,
+           "block_table")
+    misaligned = ctypes.c_void_p(0x100008)
+    expect(lib, decode(lib, cache(), q=misaligned), kb.KL_ERR_INVALID_ARG, "aligned")
+    assert lib.keyless_decode(FAKE, None, FAKE, 1, 1, 0.0, FAKE, FAKE, 1 << 20, None) == \
+        kb.KL_ERR_INVALID_ARG
+
+
+def test_standard_decode_rejects_mismatched_caches(lib):
+    k, v = cache(L_max=100), cache(L_max=200)
+    st = lib.standard_decode(FAKE, ctypes.byref(k), ctypes.byref(v), FAKE, 2, 8, 0.0, FAKE, FAKE,
+                             1 << 30, None)
+    expect(lib, st, kb.KL_ERR_INVALID_ARG, "differ")
+    st = lib.standard_decode(FAKE, None, ctypes.byref(v), FAKE, 2, 8, 0.0, FAKE, FAKE, 1 << 30, None)
+    expect(lib, st, kb.KL_ERR_INVALID_ARG, "k_cache")
+
+
+def test_append_and_prefill_reject_bad_arguments(lib):
+    c = cache()
+    expect(lib, lib.value_cache_append(ctypes.byref(c), None, FAKE, 1, 1, None),
+           kb.KL_ERR_INVALID_ARG, "non-NULL")
+    expect(lib, lib.value_cache_append(ctypes.byref(c), FAKE, FAKE, -1, 1, None),
+           kb.KL_ERR_INVALID_ARG, "bad B")
+    st = lib.keyless_prefill(FAKE, FAKE, None, FAKE, 1, 16, 64, 4, 3, 64, 1, 0.0, kb.KL_BF16,
+                             FAKE, None, None, FAKE, 1 << 30, None)
+    expect(lib, st, kb.KL_ERR_INVALID_ARG, "multiple")
+    st = lib.keyless_prefill(FAKE, FAKE, None, FAKE, 1, 16, 64, 4, 4, 32, 1, 0.0, kb.KL_BF16,
+                             FAKE, None, None, FAKE, 1 << 30, None)
+    expect(lib, st, kb.KL_ERR_UNSUPPORTED, "d_head 32")
+    st = lib.keyless_prefill(FAKE, FAKE, None, FAKE, 1, 16, 64, 4, 4, 64, 1, 0.0, kb.KL_BF16,
+                             FAKE, None, None, FAKE, 10, None)
+    expect(lib, st, kb.KL_ERR_WORKSPACE, "workspace")
+    st = lib.keyless_fold_routing(None, FAKE, 64, 4, 64, kb.KL_BF16, FAKE, None)
+    expect(lib, st, kb.KL_ERR_INVALID_ARG, "non-NULL")
+
+
+def test_zero_batch_is_a_no_op(lib):
+    assert decode(lib, cache(), B=0, ws_bytes=0, ws=None) == kb.KL_OK
+    assert lib.value_cache_append(ctypes.byref(cache()), FAKE, FAKE, 0, 1, None) == kb.KL_OK

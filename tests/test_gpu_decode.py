@@ -1,0 +1,247 @@
+"""GPU parity of the value-only-cache decode, the cache append and the standard
+K+V comparison decode against the CPU oracle (same seeded inputs)."""
+
+import math
+
+import numpy as np
+import pytest
+import torch
+
+from oracle import keyless as K
+from paper_2606_21848_amd import binding as kb
+from tests.parity import assert_parity, rowwise_rel, say, to64
+from workloads import configs, synth
+
+pytestmark = pytest.mark.gpu
+DEV = "cuda"
+
+
+def _lengths(B, L, seed):
+    """Ragged lengths covering the edge cases: 0, 1, tile +-1, split +-1, full."""
+    special = [0, 1, 15, 16, 17, 63, 64, 65, 255, 256, 257, L - 1, L]
+    vals = [v for v in special if v <= L]
+    extra = synth.uniform_int(max(B - len(vals), 0), 0, L, seed, 77).tolist()
+    return torch.tensor((vals + extra)[:B], dtype=torch.int32)
+
+
+def _paged(cache_cpu, lengths, bs, seed):
+    """Lay a contiguous [B, G, L, d] cache out in permuted blocks; padding and
+    unused table entries hold NaN."""
+    B, G, L, d = cache_cpu.shape
+    nb = [math.ceil(int(n) / bs) for n in lengths]
+    used = sum(nb)
+    perm = synth.permutation(used, seed, 5).tolist()
+    poison = used
+    maxb = max(1, math.ceil(L / bs))
+    data = torch.full((used + 1, G, bs, d), float("nan"), dtype=cache_cpu.dtype)
+    table = torch.full((B, maxb), poison, dtype=torch.int32)
+    k = 0
+    for b in range(B):
+        for j in range(nb[b]):
+            blk = perm[k]
+            k += 1
+            table[b, j] = blk
+            lo, hi = j * bs, min((j + 1) * bs, int(lengths[b]))
+            data[blk, :, :hi - lo, :] = cache_cpu[b, :, lo:hi, :]
+    return data, table
+
+
+CASES = [
+    # dtype, d_head, H, G
+    (torch.bfloat16, 128, 8, 8),
+    (torch.bfloat16, 128, 8, 2),
+    (torch.bfloat16, 128, 8, 1),
+    (torch.bfloat16, 128, 16, 2),
+    (torch.bfloat16, 64, 4, 4),
+    (torch.bfloat16, 64, 8, 2),
+    (torch.float32, 64, 4, 4),
+    (torch.float32, 128, 4, 2),
+    (torch.float32, 64, 8, 1),
+]
+
+
+@pytest.mark.parametrize("dtype,d,H,G", CASES)
+@pytest.mark.parametrize("paged", [False, True])
+def test_decode_matches_oracle(lib, dtype, d, H, G, paged):
+    B, L = 14, 600
+    say(f"decode dtype={dtype} d={d} H={H} G={G} paged={paged}")
+    cache = synth.normal((B, G, L, d), 11, 1, 1.0, dtype)
+    q = synth.normal((B, H, d), 11, 2, 1.0, dtype)
+    lengths = _lengths(B, L, 3)
+    if paged:
+        data, table = _paged(cache, lengths, 16, 9)
+        vc = kb.ValueCache(data.to(DEV), table.to(DEV))
+        ref = K.keyless_decode(to64(q), to64(data), lengths.numpy(), H, G,
+                               block_table=table.numpy(), block_size=16)
+    else:
+        vc = kb.ValueCache(cache.to(DEV))
+        ref = K.keyless_decode(to64(q), to64(cache), lengths.numpy(), H, G)
+    for chunk in (0, 64, 192):
+        out = kb.keyless_decode(q.to(DEV), vc, lengths.to(DEV), chunk_rows=chunk)
+        torch.cuda.synchronize()
+        assert_parity(out, ref, dtype, f"chunk={chunk}")
+        zero = lengths == 0
+        assert torch.all(out.cpu()[zero] == 0)
+
+
+def test_paged_equals_contiguous_bitwise(lib):
+    B, G, H, L, d = 6, 4, 8, 333, 128
+    say("paged vs contiguous bitwise")
+    cache = synth.normal((B, G, L, d), 12, 1)
+    q = synth.normal((B, H, d), 12, 2)
+    lengths = torch.tensor([333, 1, 16, 17, 200, 0], dtype=torch.int32)
+    data, table = _paged(cache, lengths, 16, 4)
+    a = kb.keyless_decode(q.to(DEV), kb.ValueCache(cache.to(DEV)), lengths.to(DEV), chunk_rows=128)
+    b = kb.keyless_decode(q.to(DEV), kb.ValueCache(data.to(DEV), table.to(DEV)), lengths.to(DEV),
+                          chunk_rows=128)
+    torch.cuda.synchronize()
+    assert torch.equal(a, b)
+
+
+def test_grouped_equals_mha_over_repeated_values(lib):
+    B, G, H, L, d = 4, 2, 8, 500, 128
+    say("gqa vs repeated mha")
+    cache = synth.normal((B, G, L, d), 13, 1)
+    q = synth.normal((B, H, d), 13, 2)
+    lengths = torch.tensor([500, 77, 1, 256], dtype=torch.int32, device=DEV)
+    gqa = kb.keyless_decode(q.to(DEV), kb.ValueCache(cache.to(DEV)), lengths)
+    rep = cache.repeat_interleave(H // G, dim=1).contiguous()
+    mha = kb.keyless_decode(q.to(DEV), kb.ValueCache(rep.to(DEV)), lengths)
+    torch.cuda.synchronize()
+    assert rowwise_rel(gqa, to64(mha)) < 1e-6
+
+
+def test_lengths_beyond_capacity_are_clamped(lib):
+    B, G, H, L, d = 2, 2, 2, 100, 64
+    say("length clamp")
+    cache = synth.normal((B, G, L, d), 14, 1)
+    q = synth.normal((B, H, d), 14, 2)
+    vc = kb.ValueCache(cache.to(DEV))
+    big = kb.keyless_decode(q.to(DEV), vc, torch.tensor([5000, -3], dtype=torch.int32, device=DEV))
+    ref = kb.keyless_decode(q.to(DEV), vc, torch.tensor([100, 0], dtype=torch.int32, device=DEV))
+    torch.cuda.synchronize()
+    assert torch.equal(big, ref)
+
+
+@pytest.mark.parametrize("dtype", [torch.bfloat16, torch.float32])
+@pytest.mark.parametrize("paged", [False, True])
+def test_append_matches_oracle(lib, dtype, paged):
+    B, G, L, d, T = 5, 4, 96, 128, 7
+    say(f"append dtype={dtype} paged={paged}")
+    base = synth.normal((B, G, L, d), 15, 1, 1.0, dtype)
+    vals = synth.normal((B, T, G, d), 15, 2, 1.0, dtype)
+    before = torch.tensor([0, 10, 89, 50, 40], dtype=torch.int32)  # all rows land in range
+    if paged:
+        data, table = _paged(base, torch.full((B,), L, dtype=torch.int32), 16, 2)
+        data = torch.nan_to_num(data)
+        vc = kb.ValueCache(data.to(DEV), table.to(DEV))
+        ref = K.value_cache_append(to64(data), to64(vals), before.numpy(), table.numpy(), 16)
+    else:
+        vc = kb.ValueCache(base.to(DEV))
+        ref = K.value_cache_append(to64(base), to64(vals), before.numpy())
+    kb.value_cache_append(vc, vals.to(DEV), before.to(DEV))
+    torch.cuda.synchronize()
+    np.testing.assert_array_equal(to64(vc.data), ref)
+
+
+@pytest.mark.parametrize("paged", [False, True])
+def test_append_past_capacity_is_dropped(lib, paged):
+    B, G, L, d, T = 2, 2, 32, 64, 5
+    say(f"append past capacity paged={paged}")
+    base = synth.normal((B, G, L, d), 17, 1)
+    vals = synth.normal((B, T, G, d), 17, 2)
+    before = torch.tensor([30, 40], dtype=torch.int32)  # rows 30, 31 fit; the rest do not
+    if paged:
+        data, table = _paged(base, torch.full((B,), L, dtype=torch.int32), 16, 3)
+        data = torch.nan_to_num(data)
+        vc = kb.ValueCache(data.to(DEV), table.to(DEV))
+        ref = K.value_cache_append(to64(data), to64(vals[:1, :2]), before[:1].numpy(),
+                                   table[:1].numpy(), 16)
+    else:
+        vc = kb.ValueCache(base.to(DEV))
+        ref = K.value_cache_append(to64(base), to64(vals[:1, :2]), before[:1].numpy())
+    kb.value_cache_append(vc, vals.to(DEV), before.to(DEV))
+    torch.cuda.synchronize()
+    np.testing.assert_array_equal(to64(vc.data), ref)
+
+
+@pytest.mark.parametrize("dtype,d,H,G", [(torch.bfloat16, 128, 8, 8), (torch.bfloat16, 128, 8, 2),
+                                         (torch.float32, 64, 4, 4)])
+def test_standard_decode_matches_oracle(lib, dtype, d, H, G):
+    B, L = 6, 700
+    say(f"standard dtype={dtype} d={d} H={H} G={G}")
+    kc = synth.normal((B, G, L, d), 16, 1, 1.0, dtype)
+    vcache = synth.normal((B, G, L, d), 16, 2, 1.0, dtype)
+    q = synth.normal((B, H, d), 16, 3, 1.0, dtype)
+    lengths = torch.tensor([700, 1, 0, 17, 256, 333], dtype=torch.int32)
+    out = kb.standard_decode(q.to(DEV), kb.ValueCache(kc.to(DEV)), kb.ValueCache(vcache.to(DEV)),
+                             lengths.to(DEV), chunk_rows=128)
+    torch.cuda.synchronize()
+    ref = K.standard_decode(to64(q), to64(kc), to64(vcache), lengths.numpy(), H, G)
+    assert_parity(out, ref, dtype, "standard")
+
+
+def test_decode_bf16_full_size_with_append(lib):
+    """B=8, 32 heads x 128, cache length 4096 (contiguous), the launch the bench times:
+    append the step's new value, then decode over all 4096 rows; every output row
+    is compared with the oracle."""
+    say("decode_bf16 full size")
+    c = configs.decode_bf16(device=DEV)
+    V = c["V"]
+    work = V.clone()
+    work[:, :, -1, :] = 0
+    vc = kb.ValueCache(work)
+    kb.value_cache_append(vc, c["v_new"], c["lengths_before"])
+    out = kb.keyless_decode(c["q"], vc, c["lengths"])
+    torch.cuda.synchronize()
+    assert torch.equal(work, V)
+    Vh = to64(V)
+    ref = K.keyless_decode(to64(c["q"]), Vh, c["lengths"].cpu().numpy(), 32, 32)
+    err = assert_parity(out, ref, torch.bfloat16, "decode_bf16")
+    print(f"decode_bf16 row-wise rel err {err:.3e}")
+
+
+def test_paged_gqa_full_size_sampled(lib):
+    """B=64, 32 query heads on 8 value heads, lengths U[1024, 32768], 16-row blocks in
+    permuted order, NaN padding. All outputs must be finite; 8 sequences (every
+    head) are checked against the oracle."""
+    say("paged_gqa_bf16 full size")
+    c = configs.paged_gqa_bf16(device=DEV)
+    vc = kb.ValueCache(c["data"], c["block_table"])
+    out = kb.keyless_decode(c["q"], vc, c["lengths"])
+    torch.cuda.synchronize()
+    assert torch.isfinite(out.float()).all()
+    lengths = c["lengths"].cpu().numpy()
+    order = np.argsort(lengths)
+    picks = [int(order[0]), int(order[-1])] + [int(x) for x in order[8::9][:6]]
+    for b in picks:
+        n = int(lengths[b])
+        nblk = math.ceil(n / 16)
+        blocks = c["data"][c["block_table"][b, :nblk].long()]  # this sequence's blocks, in order
+        ref = K.keyless_decode(to64(c["q"][b:b + 1]), to64(blocks), [n], 32, 8,
+                               block_table=[list(range(nblk))], block_size=16)
+        assert_parity(out[b:b + 1], ref, torch.bfloat16, f"paged b={b} len={n}")
+
+
+def test_head_to_head_full_size_sampled(lib):
+    """B=32, 32 heads x 128, L=16384: keyless and standard decode on 128 sampled
+    (b, h) pairs each."""
+    say("head_to_head_bf16 full size")
+    c = configs.head_to_head_bf16(device=DEV)
+    vcache, kcache = kb.ValueCache(c["V"]), kb.ValueCache(c["K"])
+    out = kb.keyless_decode(c["q"], vcache, c["lengths"])
+    std = kb.standard_decode(c["q"], kcache, vcache, c["lengths"])
+    torch.cuda.synchronize()
+    idx = synth.uniform_int(128, 0, 32 * 32 - 1, 4, 99).tolist()
+    pairs = [(i // 32, i % 32) for i in idx]
+    g_k, r_k, g_s, r_s = [], [], [], []
+    for b, h in pairs:
+        q = to64(c["q"][b, h])[None, None]
+        V = to64(c["V"][b, h])[None, None]
+        Kc = to64(c["K"][b, h])[None, None]
+        r_k.append(K.keyless_decode(q, V, [16384], 1, 1)[0, 0])
+        r_s.append(K.standard_decode(q, Kc, V, [16384], 1, 1)[0, 0])
+        g_k.append(out[b, h])
+        g_s.append(std[b, h])
+    assert_parity(torch.stack(g_k), np.stack(r_k), torch.bfloat16, "keyless sampled")
+    assert_parity(torch.stack(g_s), np.stack(r_s), torch.bfloat16, "standard sampled")

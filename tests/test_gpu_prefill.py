@@ -1,0 +1,94 @@
+"""GPU parity of the routing fold and the keyless prefill against the CPU oracle,
+and the prefill -> append -> decode consistency of one attention layer."""
+
+import numpy as np
+import pytest
+import torch
+
+from oracle import keyless as K
+from paper_2606_21848_amd import binding as kb
+from tests.parity import assert_parity, say, to64
+from workloads import configs, synth
+
+pytestmark = pytest.mark.gpu
+DEV = "cuda"
+
+
+@pytest.mark.parametrize("dtype", [torch.float32, torch.bfloat16])
+def test_fold_routing(lib, dtype):
+    d, H, dk = 256, 4, 64
+    say(f"fold dtype={dtype}")
+    W_Q = synth.normal((d, H * dk), 21, 1, 1 / 16, dtype)
+    W_R = synth.normal((H, dk, dk), 21, 2, 1 / 16, dtype)
+    got = kb.keyless_fold_routing(W_Q.to(DEV), W_R.to(DEV))
+    torch.cuda.synchronize()
+    ref = K.fold_routing(to64(W_Q), to64(W_R), H, dk)
+    assert_parity(got.reshape(d, H, dk), ref.reshape(d, H, dk), dtype, "fold")
+
+
+@pytest.mark.parametrize("dtype", [torch.float32, torch.bfloat16])
+@pytest.mark.parametrize("causal", [True, False])
+@pytest.mark.parametrize("N,d,H,G,dk", [(200, 128, 4, 2, 64), (77, 256, 2, 2, 128), (1, 64, 2, 1, 64)])
+def test_prefill_matches_oracle(lib, dtype, causal, N, d, H, G, dk):
+    say(f"prefill dtype={dtype} causal={causal} N={N} d={d} H={H} G={G} dk={dk}")
+    B = 2
+    x = synth.normal((B, N, d), 22, 1, 1.0, dtype)
+    W_Q = synth.normal((d, H * dk), 22, 2, d ** -0.5, dtype)
+    W_R = synth.normal((H, dk, dk), 22, 3, dk ** -0.5, dtype)
+    W_V = synth.normal((d, G * dk), 22, 4, d ** -0.5, dtype)
+    out, qr, v = kb.keyless_prefill(x.to(DEV), W_Q.to(DEV), W_R.to(DEV), W_V.to(DEV), H, G,
+                                    causal=causal, return_qv=True)
+    torch.cuda.synchronize()
+    O, Qr, V = K.keyless_prefill(to64(x), to64(W_Q), to64(W_R), to64(W_V), H, G, dk, causal=causal)
+    assert_parity(qr, Qr, dtype, "routed queries")
+    assert_parity(v, V, dtype, "values")
+    assert_parity(out, O, dtype, "output")
+
+
+def test_tiny_fp32_layer_prefill_append_decode(lib):
+    """One fp32 attention layer (d_model 256, 4 heads x 64): causal prefill of 128
+    tokens, append the 128 values, decode with the last routed query over the
+    128-row cache: equal to prefill row 127. Then token 129: prefill of the
+    129-token sequence gives its routed query and value; decode over 129 rows
+    equals prefill row 128."""
+    say("tiny_fp32 layer")
+    c = configs.tiny_fp32()
+    x, W_Q, W_R, W_V = (c[k] for k in ("x", "W_Q", "W_R", "W_V"))
+    H, dk = c["H"], c["d_head"]
+    O, Qr, V = K.keyless_prefill(to64(x), to64(W_Q), to64(W_R), to64(W_V), H, H, dk)
+    out, qr, v = kb.keyless_prefill(x.to(DEV), W_Q.to(DEV), W_R.to(DEV), W_V.to(DEV), H, H,
+                                    return_qv=True)
+    cache = kb.ValueCache(torch.zeros((1, H, 256, dk), dtype=torch.float32, device=DEV))
+    kb.value_cache_append(cache, v, torch.zeros(1, dtype=torch.int32, device=DEV))
+    dec = kb.keyless_decode(qr[:, 127].contiguous(), cache,
+                            torch.full((1,), 128, dtype=torch.int32, device=DEV))
+    torch.cuda.synchronize()
+    assert_parity(out, O, torch.float32, "prefill")
+    assert_parity(dec, O[:, 127], torch.float32, "decode over 128")
+    x129 = torch.cat([x, c["x_next"]], dim=1)
+    O2, _, _ = K.keyless_prefill(to64(x129), to64(W_Q), to64(W_R), to64(W_V), H, H, dk)
+    out2, qr2, v2 = kb.keyless_prefill(x129.to(DEV), W_Q.to(DEV), W_R.to(DEV), W_V.to(DEV), H, H,
+                                       return_qv=True)
+    kb.value_cache_append(cache, v2[:, 128:].contiguous(),
+                          torch.full((1,), 128, dtype=torch.int32, device=DEV))
+    dec2 = kb.keyless_decode(qr2[:, 128].contiguous(), cache,
+                             torch.full((1,), 129, dtype=torch.int32, device=DEV))
+    torch.cuda.synchronize()
+    assert_parity(dec2, O2[:, 128], torch.float32, "decode over 129")
+
+
+def test_prefill_bf16_full_size_sampled(lib):
+    """Batch 1, 8192 tokens, d_model 4096, 32 heads x 128, causal, with W_R folded
+    first (as at inference): 510 sampled rows plus rows 0 and 8191 against the
+    oracle; all of V against the oracle."""
+    say("prefill_bf16 full size")
+    c = configs.prefill_bf16(device=DEV)
+    Wt = kb.keyless_fold_routing(c["W_Q"], c["W_R"])
+    out, qr, v = kb.keyless_prefill(c["x"], Wt, None, c["W_V"], 32, 32, return_qv=True)
+    torch.cuda.synchronize()
+    rows = sorted(set([0, 8191] + synth.uniform_int(510, 1, 8190, 2, 50).tolist()))
+    Wt_ref = K.fold_routing(to64(c["W_Q"]), to64(c["W_R"]), 32, 128)
+    Orows, Vref = K.keyless_prefill_rows(to64(c["x"]), Wt_ref, to64(c["W_V"]), rows, 32, 32, 128)
+    assert_parity(v[0], Vref, torch.bfloat16, "values")
+    assert_parity(out[0, rows], Orows, torch.bfloat16, "sampled rows")
+    assert torch.isfinite(out.float()).all()
