@@ -153,7 +153,7 @@ def main():
     B, H, L, d = c["B"], c["H"], c["L"], c["d_head"]
     caches = [kb.ValueCache(x) for x in c["caches"]]
     out = torch.empty_like(c["q"])
-    ws = torch.empty(kb.decode_workspace_bytes(caches[0], B, H, args.chunk), dtype=torch.uint8,
+    ws = torch.zeros(kb.decode_workspace_bytes(caches[0], B, H, args.chunk), dtype=torch.uint8,
                      device=dev)
     q, v_new, lengths, before = c["q"], c["v_new"], c["lengths"], c["lengths_before"]
 
@@ -230,7 +230,7 @@ def extra_measurements(torch, kb, configs, dev):
     # Paged grouped-head decode.
     g = configs.paged_gqa_bf16(device=dev)
     vc = kb.ValueCache(g["data"], g["block_table"])
-    ws = torch.empty(kb.decode_workspace_bytes(vc, g["B"], g["H"]), dtype=torch.uint8, device=dev)
+    ws = torch.zeros(kb.decode_workspace_bytes(vc, g["B"], g["H"]), dtype=torch.uint8, device=dev)
     out = torch.empty_like(g["q"])
 
     def gstep(i):
@@ -246,7 +246,7 @@ def extra_measurements(torch, kb, configs, dev):
     # Head-to-head: keyless value-only vs standard K+V, same structure.
     hh = configs.head_to_head_bf16(device=dev)
     vcache, kcache = kb.ValueCache(hh["V"]), kb.ValueCache(hh["K"])
-    ws = torch.empty(kb.decode_workspace_bytes(vcache, 32, 32), dtype=torch.uint8, device=dev)
+    ws = torch.zeros(kb.decode_workspace_bytes(vcache, 32, 32), dtype=torch.uint8, device=dev)
     out = torch.empty_like(hh["q"])
     ms_k = timed_steps(lambda i: kb.keyless_decode(hh["q"], vcache, hh["lengths"], out=out,
                                                    workspace=ws), 10, 2, torch)

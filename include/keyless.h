@@ -125,16 +125,20 @@ size_t keyless_prefill_workspace_size(int B, int N, int d_model, int H, int G, i
  *            included (append it first with value_cache_append)
  *   scale    0 selects 1/sqrt(d_head) (lambda = 1 in the Section 3 weight)
  *   out      [B, H, d_head], cache dtype. lengths[b] == 0 gives a zero row.
- *   ws       at least keyless_decode_workspace_size(...) bytes
+ *   ws       at least keyless_decode_workspace_size(...) bytes (may be 0, then
+ *            ws may be NULL). Calls that run at the same time must not share it.
  * Each cached value tile is read from HBM once and used both for the scores
- * and for the weighted sum. Work is split over the cache length; the split
- * results are merged in a fixed order, so results are reproducible.
+ * and for the weighted sum. When the cache length is split, a second kernel
+ * merges the splits of each (b, h) in split order, so results are
+ * reproducible.
  */
 int keyless_decode(const void* q_routed, const kl_value_cache* cache, const int32_t* lengths,
                    int B, int H, float scale, void* out, void* ws, size_t ws_bytes, void* stream);
 
 /* As keyless_decode, with the number of cache rows per split fixed by the
- * caller (a multiple of 64; 0 selects the built-in choice). */
+ * caller (a multiple of 64; 0 selects the built-in choice). A chunk at least
+ * as long as the capacity gives one split and no merge kernel. At most 1024
+ * splits per sequence. */
 int keyless_decode_chunked(const void* q_routed, const kl_value_cache* cache,
                            const int32_t* lengths, int B, int H, float scale, void* out,
                            void* ws, size_t ws_bytes, int chunk_rows, void* stream);

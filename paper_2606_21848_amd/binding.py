@@ -154,7 +154,7 @@ def keyless_decode(q_routed: torch.Tensor, cache: ValueCache, lengths: torch.Ten
     if out is None:
         out = torch.empty_like(q_routed)
     if workspace is None:
-        workspace = torch.empty(max(decode_workspace_bytes(cache, B, H, chunk_rows), 256),
+        workspace = torch.zeros(max(decode_workspace_bytes(cache, B, H, chunk_rows), 256),
                                 dtype=torch.uint8, device=q_routed.device)
     _check(_lib.keyless_decode_chunked(_ptr(q_routed), cache.ref, _ptr(lengths), B, H, scale,
                                        _ptr(out), _ptr(workspace), workspace.numel(), chunk_rows,
@@ -170,7 +170,7 @@ def standard_decode(q: torch.Tensor, k_cache: ValueCache, v_cache: ValueCache,
     if out is None:
         out = torch.empty_like(q)
     if workspace is None:
-        workspace = torch.empty(max(decode_workspace_bytes(v_cache, B, H, chunk_rows), 256),
+        workspace = torch.zeros(max(decode_workspace_bytes(v_cache, B, H, chunk_rows), 256),
                                 dtype=torch.uint8, device=q.device)
     _check(_lib.standard_decode_chunked(_ptr(q), k_cache.ref, v_cache.ref, _ptr(lengths), B, H,
                                         scale, _ptr(out), _ptr(workspace), workspace.numel(),

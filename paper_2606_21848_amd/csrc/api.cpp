@@ -7,6 +7,7 @@
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
+#include <cstdlib>
 #include <string>
 
 #include "keyless.h"
@@ -88,15 +89,44 @@ int cache_capacity(const kl_value_cache* c) {
   return c->layout == KL_PAGED ? c->max_blocks_per_seq * c->block_size : c->L_max;
 }
 
-// Rows per split: enough splits that the grid holds several workgroups per
-// compute unit, but at least 256 rows per split so each wave walks several tiles.
-int auto_chunk(int B, int G, int cap) {
-  const long pairs = (long)B * G;
-  const long target_groups = 4096;
-  long chunk = (pairs * cap + target_groups - 1) / target_groups;
-  long c = 256;
-  while (c < chunk && c < 8192) c <<= 1;
-  return (int)c;
+// Work split of a decode call. With at least one (b, g) pair per compute unit
+// and a contiguous cache, one wide workgroup (8 waves) per pair streams the
+// whole cache and writes the output directly. Otherwise the cache length is
+// split so the grid holds several workgroups per compute unit, with at least
+// 256 rows per split so each wave walks several tiles, and a merge kernel
+// combines the splits.
+struct DecodePlan {
+  int chunk, S, waves;
+};
+
+constexpr int kComputeUnits = 256;
+
+DecodePlan plan_decode(const kl_value_cache* c, int B, int chunk_rows) {
+  const int cap = c->layout == KL_PAGED ? c->max_blocks_per_seq * c->block_size : c->L_max;
+  const long pairs = (long)B * c->G;
+  DecodePlan pl{};
+  if (chunk_rows > 0) {
+    pl.chunk = chunk_rows;
+  } else if (c->layout == KL_CONTIGUOUS && pairs >= kComputeUnits) {
+    pl.chunk = ((cap > 0 ? cap : 1) + 63) / 64 * 64;
+  } else {
+    const long want = (pairs * cap + 2047) / 2048;
+    long ch = 256;
+    while (ch < want && ch < 8192) ch <<= 1;
+    pl.chunk = (int)ch;
+  }
+  pl.S = cap > 0 ? (cap + pl.chunk - 1) / pl.chunk : 1;
+  pl.waves = pl.S == 1 ? 8 : 4;
+  if (const char* w = getenv("KL_DECODE_WAVES")) {
+    const int v = atoi(w);
+    if (v == 4 || v == 8) pl.waves = v;
+  }
+  return pl;
+}
+
+// Split partials (acc[d], m, l) per (b, h, split); none with a single split.
+size_t partials_bytes(int B, int H, int d_head, int S) {
+  return S > 1 ? align256((size_t)B * H * S * (d_head + 2) * sizeof(float)) : 0;
 }
 
 int decode_common(const void* q, const kl_value_cache* k_cache, const kl_value_cache* v_cache,
@@ -126,12 +156,15 @@ int decode_common(const void* q, const kl_value_cache* k_cache, const kl_value_c
   if (chunk_rows < 0 || chunk_rows % 64 != 0)
     return fail(KL_ERR_INVALID_ARG, "%s: chunk_rows=%d must be a multiple of 64", who, chunk_rows);
   if (B == 0) return KL_OK;
-  const int cap = cache_capacity(v_cache);
-  const int chunk = chunk_rows ? chunk_rows : auto_chunk(B, G, cap);
-  const size_t need = keyless_decode_workspace_size(v_cache, B, H, chunk);
-  if (!ws || ws_bytes < need)
+  const DecodePlan pl = plan_decode(v_cache, B, chunk_rows);
+  if (pl.S > kl::kMaxSplits)
+    return fail(KL_ERR_UNSUPPORTED, "%s: %d splits exceed the maximum of %d (use larger chunks)",
+                who, pl.S, kl::kMaxSplits);
+  const size_t need = partials_bytes(B, H, v_cache->d_head, pl.S);
+  if (need && (!ws || ws_bytes < need))
     return fail(KL_ERR_WORKSPACE, "%s: workspace of %zu bytes needed, %zu given", who, need, ws_bytes);
-  if (!aligned16(ws)) return fail(KL_ERR_INVALID_ARG, "%s: workspace must be 16-byte aligned", who);
+  if (need && !aligned16(ws))
+    return fail(KL_ERR_INVALID_ARG, "%s: workspace must be 16-byte aligned", who);
 
   kl::DecodeParams p{};
   p.q = q;
@@ -152,12 +185,12 @@ int decode_common(const void* q, const kl_value_cache* k_cache, const kl_value_c
   p.block_shift = p.paged ? log2_exact(v_cache->block_size) : 0;
   p.num_blocks = v_cache->num_blocks;
   p.max_blocks = v_cache->max_blocks_per_seq;
-  p.chunk = chunk;
-  p.S = cap > 0 ? (cap + chunk - 1) / chunk : 1;
+  p.chunk = pl.chunk;
+  p.S = pl.S;
+  p.waves = pl.waves;
   p.scale_log2 = scale_or_default(scale, p.D) * kLog2e;
   p.ev_start = g_timer_start;
   p.ev_stop = g_timer_stop;
-  if (p.S > 65535) return fail(KL_ERR_UNSUPPORTED, "%s: too many splits (%d)", who, p.S);
   return hip_status(kl::launch_decode(p, static_cast<hipStream_t>(stream)), who);
 }
 
@@ -177,11 +210,8 @@ void keyless_set_kernel_timer(void* start_event, void* stop_event) {
 
 size_t keyless_decode_workspace_size(const kl_value_cache* cache, int B, int H, int chunk_rows) {
   if (!cache || B <= 0 || H <= 0 || cache->G <= 0 || chunk_rows < 0) return 0;
-  const int cap = cache->layout == KL_PAGED ? cache->max_blocks_per_seq * cache->block_size
-                                            : cache->L_max;
-  const int chunk = chunk_rows ? chunk_rows : auto_chunk(B, cache->G, cap);
-  const size_t S = cap > 0 ? (size_t)(cap + chunk - 1) / chunk : 1;
-  return align256((size_t)B * H * S * (cache->d_head + 2) * sizeof(float));
+  const DecodePlan pl = plan_decode(cache, B, chunk_rows);
+  return partials_bytes(B, H, cache->d_head, pl.S);
 }
 
 int keyless_decode(const void* q_routed, const kl_value_cache* cache, const int32_t* lengths,

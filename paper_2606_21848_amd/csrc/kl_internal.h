@@ -8,6 +8,8 @@
 
 namespace kl {
 
+constexpr int kMaxSplits = 1024;
+
 struct DecodeParams {
   const void* q;          // [B, H, D]
   const void* vdata;      // value cache data
@@ -15,7 +17,7 @@ struct DecodeParams {
   const int32_t* table;   // paged block table or nullptr
   const int32_t* lengths; // [B]
   void* out;              // [B, H, D]
-  float* part;            // [B * H, S, D + 2] split partials
+  float* part;            // [B * H, S, D + 2] split partials (S > 1 only)
   int B, H, G, D, R;
   kl_dtype dtype;
   bool paged;
@@ -23,7 +25,8 @@ struct DecodeParams {
   int block_shift;        // log2(block_size), paged
   int num_blocks, max_blocks;
   int chunk;              // rows per split (multiple of 64)
-  int S;                  // splits per sequence
+  int S;                  // splits per sequence (at most kMaxSplits)
+  int waves;              // waves per workgroup of the split kernel: 4 or 8
   float scale_log2;       // scale * log2(e)
   hipEvent_t ev_start;    // optional: recorded around the split kernel
   hipEvent_t ev_stop;

@@ -57,9 +57,12 @@ def expect(lib, status, code, fragment):
 
 def test_workspace_sizes(lib):
     c = cache(G=32, L_max=4096)
-    # B*H*splits*(d+2)*4 bytes, rounded to 256; 512 rows per split here.
+    # Partials B*H*splits*(d+2)*4 bytes (512 rows per split here), rounded to 256.
     assert lib.keyless_decode_workspace_size(ctypes.byref(c), 8, 32, 512) == 8 * 32 * 8 * 130 * 4
-    assert lib.keyless_decode_workspace_size(ctypes.byref(c), 8, 32, 0) > 0
+    # One split per sequence (chunk >= capacity) needs no workspace.
+    assert lib.keyless_decode_workspace_size(ctypes.byref(c), 8, 32, 4096) == 0
+    p = cache(G=8, layout=kb.KL_PAGED, mb=2048)
+    assert lib.keyless_decode_workspace_size(ctypes.byref(p), 64, 32, 0) > 0
     n = lib.keyless_prefill_workspace_size(1, 128, 256, 4, 4, 64, kb.KL_F32, 1, 0, 0)
     assert n == 256 * 256 * 4 + 128 * 256 * 4 * 2
 
@@ -71,6 +74,7 @@ def test_decode_rejects_bad_arguments(lib):
     expect(lib, decode(lib, cache(G=1), H=16), kb.KL_ERR_UNSUPPORTED, "H/G=16")
     expect(lib, decode(lib, cache(), ws_bytes=1000), kb.KL_ERR_WORKSPACE, "workspace")
     expect(lib, decode(lib, cache(), chunk=100), kb.KL_ERR_INVALID_ARG, "multiple of 64")
+    expect(lib, decode(lib, cache(L_max=1 << 20), chunk=64), kb.KL_ERR_UNSUPPORTED, "splits")
     expect(lib, decode(lib, cache(dtype=7)), kb.KL_ERR_UNSUPPORTED, "dtype")
     expect(lib, decode(lib, cache(layout=kb.KL_PAGED, bs=8)), kb.KL_ERR_UNSUPPORTED, "block_size")
     expect(lib, decode(lib, cache(layout=kb.KL_PAGED, table=None)), kb.KL_ERR_INVALID_ARG,

@@ -76,7 +76,7 @@ def test_decode_matches_oracle(lib, dtype, d, H, G, paged):
     else:
         vc = kb.ValueCache(cache.to(DEV))
         ref = K.keyless_decode(to64(q), to64(cache), lengths.numpy(), H, G)
-    for chunk in (0, 64, 192):
+    for chunk in (0, 64, 192, 640):  # 640 >= capacity: one split, no merge kernel
         out = kb.keyless_decode(q.to(DEV), vc, lengths.to(DEV), chunk_rows=chunk)
         torch.cuda.synchronize()
         assert_parity(out, ref, dtype, f"chunk={chunk}")
