@@ -13,10 +13,6 @@
 #include "keyless.h"
 #include "kl_internal.h"
 
-namespace kl {
-hipError_t launch_prefill_attention_simple(const AttnParams& p, hipStream_t stream);
-}
-
 namespace {
 
 thread_local std::string g_err;
@@ -352,26 +348,36 @@ int keyless_prefill(const void* x, const void* W_Q, const void* W_R, const void*
   }
   const long M = (long)B * N;
   if (M > (1L << 30)) return fail(KL_ERR_UNSUPPORTED, "%s: B*N too large", who);
-  kl::GemmParams g{};
-  g.A = x;
-  g.M = (int)M;
-  g.K = d_model;
-  g.lda = d_model;
-  g.batch = 1;
-  g.dtype = dtype;
   // Routed queries Q~ = X W~^Q and values V = X W^V; no key projection.
-  g.Bm = Wt;
-  g.C = qr;
-  g.N = H * d_head;
-  g.ldb = g.ldc = (long)H * d_head;
-  int s = hip_status(kl::launch_gemm_simple(g, st), who);
-  if (s != KL_OK) return s;
-  g.Bm = W_V;
-  g.C = vv;
-  g.N = G * d_head;
-  g.ldb = g.ldc = (long)G * d_head;
-  s = hip_status(kl::launch_gemm_simple(g, st), who);
-  if (s != KL_OK) return s;
+  const int NQ = H * d_head, NV = G * d_head;
+  int s;
+  if (dtype == KL_BF16 && kl::gemm_bf16_supported((int)M, NQ, d_model, d_model, NQ, NQ) &&
+      kl::gemm_bf16_supported((int)M, NV, d_model, d_model, NV, NV)) {
+    s = hip_status(kl::launch_gemm_bf16_pair(x, (int)M, d_model, d_model, Wt, qr, NQ, NQ, NQ, W_V,
+                                             vv, NV, NV, NV, st),
+                   who);
+    if (s != KL_OK) return s;
+  } else {
+    kl::GemmParams g{};
+    g.A = x;
+    g.M = (int)M;
+    g.K = d_model;
+    g.lda = d_model;
+    g.batch = 1;
+    g.dtype = dtype;
+    g.Bm = Wt;
+    g.C = qr;
+    g.N = NQ;
+    g.ldb = g.ldc = NQ;
+    s = hip_status(kl::launch_gemm_simple(g, st), who);
+    if (s != KL_OK) return s;
+    g.Bm = W_V;
+    g.C = vv;
+    g.N = NV;
+    g.ldb = g.ldc = NV;
+    s = hip_status(kl::launch_gemm_simple(g, st), who);
+    if (s != KL_OK) return s;
+  }
   kl::AttnParams a{};
   a.q = qr;
   a.v = vv;
@@ -387,6 +393,7 @@ int keyless_prefill(const void* x, const void* W_Q, const void* W_R, const void*
   a.causal = causal ? 1 : 0;
   a.scale_log2 = scale_or_default(scale, d_head) * kLog2e;
   a.dtype = dtype;
+  if (kl::attn_bf16_supported(a)) return hip_status(kl::launch_prefill_attention(a, st), who);
   return hip_status(kl::launch_prefill_attention_simple(a, st), who);
 }
 

@@ -61,9 +61,12 @@ struct GemmParams {
 
 hipError_t launch_gemm_simple(const GemmParams& p, hipStream_t stream);
 
-// bf16 MFMA GEMM: C (M x N, bf16) = A (M x K, bf16) * B (K x N, bf16).
-hipError_t launch_gemm_bf16(const void* A, const void* Bm, void* C, int M, int N, int K, long lda,
-                            long ldb, long ldc, hipStream_t stream);
+// bf16 MFMA GEMM: C_i (M x N_i) = A (M x K) * B_i (K x N_i) for one or two
+// problems sharing A (B1 == nullptr: one problem). All bf16, row-major.
+bool gemm_bf16_supported(int M, int N, int K, long lda, long ldb, long ldc);
+hipError_t launch_gemm_bf16_pair(const void* A, int M, int K, long lda, const void* B0, void* C0,
+                                 int N0, long ldb0, long ldc0, const void* B1, void* C1, int N1,
+                                 long ldb1, long ldc1, hipStream_t stream);
 
 struct AttnParams {
   const void* q;   // routed queries, [B, N, H, D] with row stride q_stride (elements per token)
@@ -76,6 +79,10 @@ struct AttnParams {
   kl_dtype dtype;
 };
 
+// bf16 MFMA flash-style keyless attention (d_head 64 or 128).
+bool attn_bf16_supported(const AttnParams& p);
 hipError_t launch_prefill_attention(const AttnParams& p, hipStream_t stream);
+// fp32 (or fallback) VALU attention.
+hipError_t launch_prefill_attention_simple(const AttnParams& p, hipStream_t stream);
 
 }  // namespace kl

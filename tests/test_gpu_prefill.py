@@ -28,7 +28,8 @@ def test_fold_routing(lib, dtype):
 
 @pytest.mark.parametrize("dtype", [torch.float32, torch.bfloat16])
 @pytest.mark.parametrize("causal", [True, False])
-@pytest.mark.parametrize("N,d,H,G,dk", [(200, 128, 4, 2, 64), (77, 256, 2, 2, 128), (1, 64, 2, 1, 64)])
+@pytest.mark.parametrize("N,d,H,G,dk", [(200, 128, 4, 2, 64), (77, 256, 2, 2, 128), (1, 64, 2, 1, 64),
+                                        (700, 512, 8, 2, 128), (333, 256, 3, 1, 64)])
 def test_prefill_matches_oracle(lib, dtype, causal, N, d, H, G, dk):
     say(f"prefill dtype={dtype} causal={causal} N={N} d={d} H={H} G={G} dk={dk}")
     B = 2
