@@ -212,21 +212,21 @@ def extra_measurements(torch, kb, configs, dev):
     res = {}
     # Causal prefill, bf16, with the routing matrix folded beforehand (as at inference).
     p = configs.prefill_bf16(device=dev)
-    Wt = kb.keyless_fold_routing(p["W_Q"], p["W_R"])
-    x, W_V = p["x"], p["W_V"]
+    x = p["x"]
     N, dm, H, G, dk = x.shape[1], x.shape[2], p["H"], p["G"], p["d_head"]
-    outs = kb.keyless_prefill(x, Wt, None, W_V, H, G, return_qv=True)
+    packed = kb.keyless_pack_weights(p["W_Q"], p["W_R"], p["W_V"], H, G)  # once, before inference
+    outs = kb.keyless_prefill_packed(x, packed, H, G, return_qv=True)
 
     def pstep(i):
-        kb.keyless_prefill(x, Wt, None, W_V, H, G, out=outs[0], q_routed_out=outs[1],
-                           v_out=outs[2])
-    ms = timed_steps(pstep, 5, 2, torch)
+        kb.keyless_prefill_packed(x, packed, H, G, out=outs[0], q_routed_out=outs[1],
+                                  v_out=outs[2])
+    ms = timed_steps(pstep, 10, 3, torch)
     flops = 2 * N * dm * (H + G) * dk + 2 * H * dk * N * (N + 1)
     res["prefill_bf16"] = {"workload": "batch 1, 8192 tokens, d_model 4096, 32 heads x 128, causal",
                            "ms": round(ms, 3), "tflops": round(flops / (ms * 1e-3) / 1e12, 2),
                            "frac_of_bf16_mfma_peak": round(flops / (ms * 1e-3) / 1e12 /
                                                           BF16_MFMA_PEAK_TFLOPS, 4)}
-    del p, Wt, x, W_V, outs
+    del p, packed, x, outs
     # Paged grouped-head decode.
     g = configs.paged_gqa_bf16(device=dev)
     vc = kb.ValueCache(g["data"], g["block_table"])

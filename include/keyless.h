@@ -104,6 +104,9 @@ int keyless_fold_routing(const void* W_Q, const void* W_R, int d_model, int H, i
  *   ws, ws_bytes  workspace of at least keyless_prefill_workspace_size(...) bytes
  * There is no key projection. bf16 uses MFMA with fp32 accumulation; the
  * routed queries and values are rounded to bf16 once, as they would be cached.
+ * For bf16 the weights are folded and packed into the workspace on every call
+ * (d_model must be a multiple of 64); callers that keep weights resident
+ * should pack once with keyless_pack_weights and call keyless_prefill_packed.
  */
 int keyless_prefill(const void* x, const void* W_Q, const void* W_R, const void* W_V, int B,
                     int N, int d_model, int H, int G, int d_head, int causal, float scale,
@@ -113,6 +116,33 @@ int keyless_prefill(const void* x, const void* W_Q, const void* W_R, const void*
 size_t keyless_prefill_workspace_size(int B, int N, int d_model, int H, int G, int d_head,
                                       kl_dtype dtype, int has_W_R, int has_q_routed_out,
                                       int has_v_out);
+
+/*
+ * keyless_pack_weights - the one-time weight preparation before inference
+ * (Section 2.1: W^Q and W^R are composed into W~^Q once; Section 5.5 does the
+ * same before decoding). Writes, for the bf16 path, the packed matrix
+ *   packed [(H + G) * d_head, d_model]:  row n < H*d_head is column n of
+ *   W~^Q = W^Q W^R (per head; W^Q itself when W_R is NULL), row H*d_head + n
+ *   is column n of W^V,
+ * i.e. the projection weights transposed so that d_model is contiguous, the
+ * layout the MFMA projection reads. fp32 accumulation for the fold, one
+ * rounding to bf16. packed holds keyless_packed_weights_size(...) bytes.
+ * bf16 only (KL_ERR_UNSUPPORTED otherwise).
+ */
+size_t keyless_packed_weights_size(int d_model, int H, int G, int d_head, kl_dtype dtype);
+int keyless_pack_weights(const void* W_Q, const void* W_R, const void* W_V, int d_model, int H,
+                         int G, int d_head, kl_dtype dtype, void* packed, void* stream);
+
+/*
+ * keyless_prefill_packed - keyless_prefill with weights prepared by
+ * keyless_pack_weights (bf16 only; d_model a multiple of 64). The workspace is
+ * needed only for q_routed / v when those outputs are NULL:
+ * B*N*H*d_head*2 and B*N*G*d_head*2 bytes, each rounded up to 256.
+ */
+int keyless_prefill_packed(const void* x, const void* packed, int B, int N, int d_model, int H,
+                           int G, int d_head, int causal, float scale, kl_dtype dtype, void* out,
+                           void* q_routed_out, void* v_out, void* ws, size_t ws_bytes,
+                           void* stream);
 
 /*
  * keyless_decode - one decode step over a value-only cache (Section 3):

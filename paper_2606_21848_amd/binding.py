@@ -22,6 +22,7 @@ KL_CONTIGUOUS, KL_PAGED = 0, 1
 # Every symbol include/keyless.h declares.
 EXPORTS = (
     "keyless_fold_routing", "keyless_prefill", "keyless_prefill_workspace_size",
+    "keyless_packed_weights_size", "keyless_pack_weights", "keyless_prefill_packed",
     "keyless_decode", "keyless_decode_chunked", "keyless_decode_workspace_size",
     "value_cache_append", "standard_decode", "standard_decode_chunked",
     "keyless_set_kernel_timer", "keyless_last_error", "keyless_version",
@@ -62,6 +63,9 @@ def load(path: str = LIB_PATH):
         "keyless_fold_routing": (i, [vp, vp, i, i, i, i, vp, vp]),
         "keyless_prefill": (i, [vp, vp, vp, vp, i, i, i, i, i, i, i, f, i, vp, vp, vp, vp, sz, vp]),
         "keyless_prefill_workspace_size": (sz, [i, i, i, i, i, i, i, i, i, i]),
+        "keyless_packed_weights_size": (sz, [i, i, i, i, i]),
+        "keyless_pack_weights": (i, [vp, vp, vp, i, i, i, i, i, vp, vp]),
+        "keyless_prefill_packed": (i, [vp, vp, i, i, i, i, i, i, i, f, i, vp, vp, vp, vp, sz, vp]),
         "keyless_decode": (i, [vp, cp, vp, i, i, f, vp, vp, sz, vp]),
         "keyless_decode_chunked": (i, [vp, cp, vp, i, i, f, vp, vp, sz, i, vp]),
         "keyless_decode_workspace_size": (sz, [cp, i, i, i]),
@@ -234,3 +238,48 @@ def set_kernel_timer(start: "torch.cuda.Event | None", stop: "torch.cuda.Event |
     else:
         _lib.keyless_set_kernel_timer(ctypes.c_void_p(start.cuda_event),
                                       ctypes.c_void_p(stop.cuda_event))
+
+
+def keyless_pack_weights(W_Q: torch.Tensor, W_R: torch.Tensor | None, W_V: torch.Tensor, H: int,
+                         G: int) -> torch.Tensor:
+    """Packed [(H+G)*d, d_model] bf16 weights: (W^Q W^R)^T over W^V^T, d_model contiguous."""
+    load()
+    d_model = W_Q.shape[0]
+    dk = W_Q.shape[1] // H
+    n = int(_lib.keyless_packed_weights_size(d_model, H, G, dk, _dt(W_Q)))
+    if n == 0:
+        raise KeylessError(KL_ERR_UNSUPPORTED, "packed weights are bf16 only")
+    packed = torch.empty(((H + G) * dk, d_model), dtype=W_Q.dtype, device=W_Q.device)
+    _check(_lib.keyless_pack_weights(_ptr(W_Q), _ptr(W_R), _ptr(W_V), d_model, H, G, dk, _dt(W_Q),
+                                     _ptr(packed), _stream(W_Q)))
+    return packed
+
+
+def keyless_prefill_packed(x: torch.Tensor, packed: torch.Tensor, H: int, G: int,
+                           causal: bool = True, scale: float = 0.0, return_qv: bool = False,
+                           out=None, q_routed_out=None, v_out=None, workspace=None):
+    """keyless_prefill with weights from keyless_pack_weights."""
+    load()
+    B, N, d_model = x.shape
+    dk = packed.shape[0] // (H + G)
+    if out is None:
+        out = torch.empty((B, N, H, dk), dtype=x.dtype, device=x.device)
+    if return_qv:
+        if q_routed_out is None:
+            q_routed_out = torch.empty((B, N, H, dk), dtype=x.dtype, device=x.device)
+        if v_out is None:
+            v_out = torch.empty((B, N, G, dk), dtype=x.dtype, device=x.device)
+    need = 0
+    if q_routed_out is None:
+        need += -(-B * N * H * dk * 2 // 256) * 256
+    if v_out is None:
+        need += -(-B * N * G * dk * 2 // 256) * 256
+    if workspace is None and need:
+        workspace = torch.empty(need, dtype=torch.uint8, device=x.device)
+    _check(_lib.keyless_prefill_packed(_ptr(x), _ptr(packed), B, N, d_model, H, G, dk, int(causal),
+                                       scale, _dt(x), _ptr(out), _ptr(q_routed_out), _ptr(v_out),
+                                       _ptr(workspace), 0 if workspace is None else workspace.numel(),
+                                       _stream(x)))
+    if return_qv:
+        return out, q_routed_out, v_out
+    return out

@@ -293,25 +293,55 @@ int keyless_fold_routing(const void* W_Q, const void* W_R, int d_model, int H, i
                     "keyless_fold_routing");
 }
 
+size_t keyless_packed_weights_size(int d_model, int H, int G, int d_head, kl_dtype dtype) {
+  if (d_model <= 0 || H <= 0 || G <= 0 || d_head <= 0 || dtype != KL_BF16) return 0;
+  return align256((size_t)(H + G) * d_head * d_model * 2);
+}
+
+int keyless_pack_weights(const void* W_Q, const void* W_R, const void* W_V, int d_model, int H,
+                         int G, int d_head, kl_dtype dtype, void* packed, void* stream) {
+  const char* who = "keyless_pack_weights";
+  if (!W_Q || !W_V || !packed)
+    return fail(KL_ERR_INVALID_ARG, "%s: W_Q, W_V and packed must be non-NULL", who);
+  if (dtype != KL_BF16) return fail(KL_ERR_UNSUPPORTED, "%s: packed weights are bf16 only", who);
+  if (d_model <= 0 || H <= 0 || G <= 0 || d_head <= 0 || H % G != 0)
+    return fail(KL_ERR_INVALID_ARG, "%s: bad sizes d_model=%d H=%d G=%d d_head=%d", who, d_model,
+                H, G, d_head);
+  kl::PackParams pp{};
+  pp.W_Q = W_Q;
+  pp.W_R = W_R;
+  pp.W_V = W_V;
+  pp.packed = packed;
+  pp.d_model = d_model;
+  pp.H = H;
+  pp.G = G;
+  pp.d_head = d_head;
+  pp.N = (H + G) * d_head;
+  return hip_status(kl::launch_pack_weights(pp, static_cast<hipStream_t>(stream)), who);
+}
+
 size_t keyless_prefill_workspace_size(int B, int N, int d_model, int H, int G, int d_head,
                                       kl_dtype dtype, int has_W_R, int has_q_routed_out,
                                       int has_v_out) {
   if (B < 0 || N < 0 || d_model <= 0 || H <= 0 || G <= 0 || d_head <= 0) return 0;
   const size_t e = elem_bytes(dtype);
   size_t n = 0;
-  if (has_W_R) n += align256((size_t)d_model * H * d_head * e);
+  if (dtype == KL_BF16)
+    n += keyless_packed_weights_size(d_model, H, G, d_head, dtype);
+  else if (has_W_R)
+    n += align256((size_t)d_model * H * d_head * e);
   if (!has_q_routed_out) n += align256((size_t)B * N * H * d_head * e);
   if (!has_v_out) n += align256((size_t)B * N * G * d_head * e);
   return n;
 }
 
-int keyless_prefill(const void* x, const void* W_Q, const void* W_R, const void* W_V, int B,
-                    int N, int d_model, int H, int G, int d_head, int causal, float scale,
-                    kl_dtype dtype, void* out, void* q_routed_out, void* v_out, void* ws,
-                    size_t ws_bytes, void* stream) {
-  const char* who = "keyless_prefill";
-  if (!x || !W_Q || !W_V || !out)
-    return fail(KL_ERR_INVALID_ARG, "%s: x, W_Q, W_V and out must be non-NULL", who);
+}  // extern "C"
+
+namespace {
+
+int check_prefill_args(const char* who, const void* x, const void* W, const void* out, int B,
+                       int N, int d_model, int H, int G, int d_head, kl_dtype dtype) {
+  if (!x || !W || !out) return fail(KL_ERR_INVALID_ARG, "%s: inputs and out must be non-NULL", who);
   if (!dtype_ok(dtype)) return fail(KL_ERR_UNSUPPORTED, "%s: unknown dtype", who);
   if (B < 0 || N < 0 || d_model <= 0 || H <= 0 || G <= 0)
     return fail(KL_ERR_INVALID_ARG, "%s: bad sizes B=%d N=%d d_model=%d H=%d G=%d", who, B, N,
@@ -319,71 +349,20 @@ int keyless_prefill(const void* x, const void* W_Q, const void* W_R, const void*
   if (d_head != 64 && d_head != 128)
     return fail(KL_ERR_UNSUPPORTED, "%s: d_head %d not supported (64 or 128)", who, d_head);
   if (H % G != 0) return fail(KL_ERR_INVALID_ARG, "%s: H=%d is not a multiple of G=%d", who, H, G);
-  const size_t need = keyless_prefill_workspace_size(B, N, d_model, H, G, d_head, dtype,
-                                                     W_R != nullptr, q_routed_out != nullptr,
-                                                     v_out != nullptr);
-  if (need && (!ws || ws_bytes < need))
-    return fail(KL_ERR_WORKSPACE, "%s: workspace of %zu bytes needed, %zu given", who, need, ws_bytes);
-  if (B == 0 || N == 0) return KL_OK;
-  hipStream_t st = static_cast<hipStream_t>(stream);
-  const size_t e = elem_bytes(dtype);
-  char* w = static_cast<char*>(ws);
-  const void* Wt = W_Q;
-  if (W_R) {
-    void* fold = w;
-    w += align256((size_t)d_model * H * d_head * e);
-    const int s = keyless_fold_routing(W_Q, W_R, d_model, H, d_head, dtype, fold, stream);
-    if (s != KL_OK) return s;
-    Wt = fold;
-  }
-  void* qr = q_routed_out;
-  if (!qr) {
-    qr = w;
-    w += align256((size_t)B * N * H * d_head * e);
-  }
-  void* vv = v_out;
-  if (!vv) {
-    vv = w;
-    w += align256((size_t)B * N * G * d_head * e);
-  }
-  const long M = (long)B * N;
-  if (M > (1L << 30)) return fail(KL_ERR_UNSUPPORTED, "%s: B*N too large", who);
-  // Routed queries Q~ = X W~^Q and values V = X W^V; no key projection.
-  const int NQ = H * d_head, NV = G * d_head;
-  int s;
-  if (dtype == KL_BF16 && kl::gemm_bf16_supported((int)M, NQ, d_model, d_model, NQ, NQ) &&
-      kl::gemm_bf16_supported((int)M, NV, d_model, d_model, NV, NV)) {
-    s = hip_status(kl::launch_gemm_bf16_pair(x, (int)M, d_model, d_model, Wt, qr, NQ, NQ, NQ, W_V,
-                                             vv, NV, NV, NV, st),
-                   who);
-    if (s != KL_OK) return s;
-  } else {
-    kl::GemmParams g{};
-    g.A = x;
-    g.M = (int)M;
-    g.K = d_model;
-    g.lda = d_model;
-    g.batch = 1;
-    g.dtype = dtype;
-    g.Bm = Wt;
-    g.C = qr;
-    g.N = NQ;
-    g.ldb = g.ldc = NQ;
-    s = hip_status(kl::launch_gemm_simple(g, st), who);
-    if (s != KL_OK) return s;
-    g.Bm = W_V;
-    g.C = vv;
-    g.N = NV;
-    g.ldb = g.ldc = NV;
-    s = hip_status(kl::launch_gemm_simple(g, st), who);
-    if (s != KL_OK) return s;
-  }
+  if ((long)B * N > (1L << 30)) return fail(KL_ERR_UNSUPPORTED, "%s: B*N too large", who);
+  return KL_OK;
+}
+
+// Attention over the routed queries and values (Eq. 2 with the Eq. 4 score).
+int run_attention(const char* who, const void* qr, long q_stride, const void* vv, long v_stride,
+                  void* out, int B, int N, int H, int G, int d_head, int causal, float scale,
+                  kl_dtype dtype, hipStream_t st) {
   kl::AttnParams a{};
   a.q = qr;
   a.v = vv;
   a.out = out;
-  a.q_stride = (long)H * d_head;
-  a.v_stride = (long)G * d_head;
+  a.q_stride = q_stride;
+  a.v_stride = v_stride;
   a.o_stride = (long)H * d_head;
   a.B = B;
   a.N = N;
@@ -395,6 +374,121 @@ int keyless_prefill(const void* x, const void* W_Q, const void* W_R, const void*
   a.dtype = dtype;
   if (kl::attn_bf16_supported(a)) return hip_status(kl::launch_prefill_attention(a, st), who);
   return hip_status(kl::launch_prefill_attention_simple(a, st), who);
+}
+
+// bf16 prefill against packed weights; qr / vv are where the routed queries and
+// values go (caller outputs or workspace).
+int prefill_packed_core(const char* who, const void* x, const void* packed, int B, int N,
+                        int d_model, int H, int G, int d_head, int causal, float scale, void* out,
+                        void* qr, void* vv, hipStream_t st) {
+  const int M = B * N, NQ = H * d_head, NV = G * d_head;
+  if (!kl::gemm_bf16_supported(M, NQ + NV, d_model, d_model, NQ, NV))
+    return fail(KL_ERR_UNSUPPORTED, "%s: d_model=%d must be a multiple of 64 for bf16", who,
+                d_model);
+  int s = hip_status(kl::launch_gemm_bf16_packed(x, M, d_model, d_model, packed, NQ + NV, NQ, qr,
+                                                 NQ, vv, NV, st),
+                     who);
+  if (s != KL_OK) return s;
+  return run_attention(who, qr, NQ, vv, NV, out, B, N, H, G, d_head, causal, scale, KL_BF16, st);
+}
+
+}  // namespace
+
+extern "C" {
+
+int keyless_prefill_packed(const void* x, const void* packed, int B, int N, int d_model, int H,
+                           int G, int d_head, int causal, float scale, kl_dtype dtype, void* out,
+                           void* q_routed_out, void* v_out, void* ws, size_t ws_bytes,
+                           void* stream) {
+  const char* who = "keyless_prefill_packed";
+  int s = check_prefill_args(who, x, packed, out, B, N, d_model, H, G, d_head, dtype);
+  if (s != KL_OK) return s;
+  if (dtype != KL_BF16) return fail(KL_ERR_UNSUPPORTED, "%s: packed weights are bf16 only", who);
+  const size_t e = 2;
+  const size_t qbytes = q_routed_out ? 0 : align256((size_t)B * N * H * d_head * e);
+  const size_t vbytes = v_out ? 0 : align256((size_t)B * N * G * d_head * e);
+  if (qbytes + vbytes && (!ws || ws_bytes < qbytes + vbytes))
+    return fail(KL_ERR_WORKSPACE, "%s: workspace of %zu bytes needed, %zu given", who,
+                qbytes + vbytes, ws_bytes);
+  if (B == 0 || N == 0) return KL_OK;
+  char* w = static_cast<char*>(ws);
+  void* qr = q_routed_out ? q_routed_out : w;
+  void* vv = v_out ? v_out : w + qbytes;
+  return prefill_packed_core(who, x, packed, B, N, d_model, H, G, d_head, causal, scale, out, qr,
+                             vv, static_cast<hipStream_t>(stream));
+}
+
+int keyless_prefill(const void* x, const void* W_Q, const void* W_R, const void* W_V, int B,
+                    int N, int d_model, int H, int G, int d_head, int causal, float scale,
+                    kl_dtype dtype, void* out, void* q_routed_out, void* v_out, void* ws,
+                    size_t ws_bytes, void* stream) {
+  const char* who = "keyless_prefill";
+  int s = check_prefill_args(who, x, W_Q, out, B, N, d_model, H, G, d_head, dtype);
+  if (s != KL_OK) return s;
+  if (!W_V) return fail(KL_ERR_INVALID_ARG, "%s: W_V must be non-NULL", who);
+  const size_t need = keyless_prefill_workspace_size(B, N, d_model, H, G, d_head, dtype,
+                                                     W_R != nullptr, q_routed_out != nullptr,
+                                                     v_out != nullptr);
+  if (need && (!ws || ws_bytes < need))
+    return fail(KL_ERR_WORKSPACE, "%s: workspace of %zu bytes needed, %zu given", who, need, ws_bytes);
+  if (B == 0 || N == 0) return KL_OK;
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  const size_t e = elem_bytes(dtype);
+  char* w = static_cast<char*>(ws);
+  if (dtype == KL_BF16) {
+    // Fold and pack the weights into the workspace, then the packed path.
+    if (d_model % 64 != 0)
+      return fail(KL_ERR_UNSUPPORTED, "%s: d_model=%d must be a multiple of 64 for bf16", who,
+                  d_model);
+    void* packed = w;
+    w += keyless_packed_weights_size(d_model, H, G, d_head, dtype);
+    s = keyless_pack_weights(W_Q, W_R, W_V, d_model, H, G, d_head, dtype, packed, stream);
+    if (s != KL_OK) return s;
+    void* qr = q_routed_out;
+    if (!qr) {
+      qr = w;
+      w += align256((size_t)B * N * H * d_head * e);
+    }
+    void* vv = v_out ? v_out : w;
+    return prefill_packed_core(who, x, packed, B, N, d_model, H, G, d_head, causal, scale, out,
+                               qr, vv, st);
+  }
+  // fp32: VALU kernels on the weights as given.
+  const void* Wt = W_Q;
+  if (W_R) {
+    void* fold = w;
+    w += align256((size_t)d_model * H * d_head * e);
+    s = keyless_fold_routing(W_Q, W_R, d_model, H, d_head, dtype, fold, stream);
+    if (s != KL_OK) return s;
+    Wt = fold;
+  }
+  void* qr = q_routed_out;
+  if (!qr) {
+    qr = w;
+    w += align256((size_t)B * N * H * d_head * e);
+  }
+  void* vv = v_out ? v_out : w;
+  const int NQ = H * d_head, NV = G * d_head;
+  kl::GemmParams g{};
+  g.A = x;
+  g.M = B * N;
+  g.K = d_model;
+  g.lda = d_model;
+  g.batch = 1;
+  g.dtype = dtype;
+  g.Bm = Wt;
+  g.C = qr;
+  g.N = NQ;
+  g.ldb = g.ldc = NQ;
+  s = hip_status(kl::launch_gemm_simple(g, st), who);
+  if (s != KL_OK) return s;
+  g.Bm = W_V;
+  g.C = vv;
+  g.N = NV;
+  g.ldb = g.ldc = NV;
+  s = hip_status(kl::launch_gemm_simple(g, st), who);
+  if (s != KL_OK) return s;
+  return run_attention(who, qr, NQ, vv, NV, out, B, N, H, G, d_head, causal, scale, dtype, st);
 }
 
 }  // extern "C"

@@ -1,17 +1,22 @@
 // bf16 MFMA GEMM for the prefill projections [Q~ | V] = X [W~^Q | W^V]
-// (Eq. 2: no key projection). Two problems that share A run in one launch.
+// (Eq. 2: no key projection), against weights packed once before inference.
 //
-// C (M x N, bf16) = A (M x K, bf16, row-major) * B (K x N, bf16, row-major),
+// C (M x N) = A (M x K) * Wp^T, where A = X is row-major [M, K] and Wp is the
+// packed weight [N, K] (row n = output column n, K contiguous): both operands
+// are K-major, which is the layout the MFMA fragments want. Columns below
+// n_split go to C0 (the routed queries), the rest to C1 (the values).
 // fp32 accumulation in v_mfma_f32_16x16x32_bf16, one rounding to bf16 on store.
 //
-// Tile 256 x 256 x 64, 8 waves (2 x 4), each wave 128 x 64 of C. Both operands
-// are staged in LDS K-major (64 k values of one row or column contiguous, rows
-// padded by 16 bytes): A is copied as is; B arrives n-major from memory and is
-// transposed in registers (4 x 8 blocks, v_perm) on its way into LDS. Global
-// loads of tile k+1 are in flight while tile k is multiplied (two LDS buffers,
-// 144 KiB). Workgroup ids are remapped so each XCD owns a band of 4 tile rows
-// walked column-major, which keeps the A and B tiles of concurrently running
-// workgroups in that XCD's L2.
+// Tile 256 x 256 x 64, 8 waves (2 x 4), each wave 128 x 64 of C (128 fp32
+// accumulators per lane, two waves per SIMD). Each operand tile is 256 rows of
+// 128 bytes in LDS with the 16-byte chunks of row r XOR-swizzled by
+// (r >> 1) & 7, so the fragment reads (16 rows per access) are free of bank
+// conflicts. Tiles move from memory straight into LDS (global_load_lds, 16
+// bytes per lane, no register staging); the swizzle is applied to the global
+// addresses. Two LDS stages (128 KiB): the next tile is in flight while the
+// current one is multiplied.
+// Workgroup ids are remapped so each XCD owns a band of tile rows walked
+// column-major, which keeps concurrently running tiles in that XCD's L2.
 
 #include "kl_device.h"
 #include "kl_internal.h"
@@ -21,103 +26,84 @@ namespace {
 
 typedef __attribute__((__vector_size__(8 * sizeof(__bf16)))) __bf16 bf16x8_t;
 typedef __attribute__((__vector_size__(4 * sizeof(float)))) float f32x4_t;
-typedef unsigned int u32x2 __attribute__((ext_vector_type(2)));
+typedef __attribute__((address_space(3))) unsigned char lds_u8;
 
 constexpr int BM = 256, BN = 256, BK = 64;
-constexpr int LDK = BK + 8;  // padded row length (elements) of an LDS tile
 constexpr int kThreads = 512;
+constexpr int TILE_BYTES = 256 * BK * 2;  // one operand tile, 32 KiB
 
-struct GemmBf16Params {
-  const uint16_t* A;
-  const uint16_t* B[2];
-  uint16_t* C[2];
-  int M, K;
-  int N[2];
-  long lda, ldb[2], ldc[2];
+struct GemmParams2 {
+  const uint16_t* A;   // [M, K]
+  const uint16_t* W;   // [N, K] packed
+  uint16_t* C0;        // columns [0, n_split)
+  uint16_t* C1;        // columns [n_split, N)
+  int M, N, K, n_split;
+  long lda;            // A row stride (elements)
+  long ldc0, ldc1;
 };
 
-// Low halves of a and b -> (a.lo, b.lo); high halves -> (a.hi, b.hi).
-__device__ __forceinline__ uint32_t lo_pair(uint32_t a, uint32_t b) {
-  return __builtin_amdgcn_perm(b, a, 0x05040100u);
-}
-__device__ __forceinline__ uint32_t hi_pair(uint32_t a, uint32_t b) {
-  return __builtin_amdgcn_perm(b, a, 0x07060302u);
+// One 16-byte-per-lane copy from global memory into LDS: lane L's bytes land at
+// lds + 16 L. Issued as inline assembly so the compiler does not order every copy
+// behind the previous one (it cannot see that the copies target disjoint LDS
+// rows); the caller waits with s_waitcnt vmcnt before the tile is read.
+__device__ __forceinline__ void copy_to_lds(const void* gbase, uint32_t voff, uint32_t lds) {
+  asm volatile("s_mov_b32 m0, %2\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, %1"
+               :
+               : "v"(voff), "s"(gbase), "s"(lds)
+               : "memory", "m0");
 }
 
-__global__ __launch_bounds__(kThreads) void gemm_bf16_kernel(GemmBf16Params p) {
-  const int prob = blockIdx.y;
-  const int N = p.N[prob];
-  const int tilesM = (p.M + BM - 1) / BM, tilesN = (N + BN - 1) / BN;
+// Byte offset of (row, 16-byte chunk) inside a swizzled operand tile.
+__device__ __forceinline__ int swz(int row, int chunk) {
+  return row * (BK * 2) + ((chunk ^ ((row >> 1) & 7)) << 4);
+}
+
+__global__ __launch_bounds__(kThreads) void gemm_bf16_kernel(GemmParams2 p) {
+  const int tilesM = (p.M + BM - 1) / BM, tilesN = (p.N + BN - 1) / BN;
   const int ntiles = tilesM * tilesN;
   int wg = blockIdx.x;
-  if (wg >= ntiles) return;
   // XCD-aware order: hardware places workgroup i on XCD i % 8.
-  if (gridDim.x == (unsigned)ntiles && (ntiles & 7) == 0) wg = (wg & 7) * (ntiles >> 3) + (wg >> 3);
+  if ((ntiles & 7) == 0) wg = (wg & 7) * (ntiles >> 3) + (wg >> 3);
   constexpr int GM = 4;
   const int group = wg / (GM * tilesN);
   const int first_m = group * GM;
   const int gsize = min(tilesM - first_m, GM);
   const int in_group = wg % (GM * tilesN);
-  const int tm = first_m + in_group % gsize;
-  const int tn = in_group / gsize;
-  const int m0 = tm * BM, n0 = tn * BN;
+  const int m0 = (first_m + in_group % gsize) * BM;
+  const int n0 = (in_group / gsize) * BN;
 
-  const uint16_t* __restrict__ A = p.A;
-  const uint16_t* __restrict__ Bm = p.B[prob];
-  const long lda = p.lda, ldb = p.ldb[prob];
+  // Two pipeline stages, each an A tile and a W tile: [stage][A | W].
+  extern __shared__ __attribute__((aligned(1024))) unsigned char smem[];
 
-  extern __shared__ __attribute__((aligned(16))) uint16_t smem[];
-  uint16_t* As = smem;                    // [2][BM][LDK]
-  uint16_t* Bs = smem + 2 * BM * LDK;     // [2][BN][LDK]
+  const int t = threadIdx.x, lane = t & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(t >> 6);
+  const int wm = wave >> 2, wn = wave & 3;  // wave tile: rows 128 wm.., columns 64 wn..
 
-  const int t = threadIdx.x;
-  const int lane = t & 63;
-  const int wave = t >> 6;
-  const int wm = wave >> 2, wn = wave & 3;
-
-  // Global -> register staging assignments.
-  const int a_chunk = t & 7, a_row = t >> 3;          // rows a_row + 64 i, 16 B chunk a_chunk
-  const int b_nchunk = t & 31, b_kgroup = t >> 5;     // 4 k rows x 8 n columns
-  u32x4 ra[4];
-  u32x4 rb[4];
-
-  auto load_global = [&](int k0) {
+  // Direct-to-LDS copies: one wave instruction fills 8 rows (1 KiB) of a tile,
+  // lane L landing at byte 16 L, i.e. row L / 8, physical chunk L % 8, which
+  // holds logical chunk (L % 8) ^ ((row >> 1) & 7). Each wave fills 4 row groups
+  // of each operand. Rows past the end are clamped: they only feed output rows
+  // or columns that are never stored.
+  uint32_t offA[4], offW[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int r = (i * 8 + wave) * 8 + (lane >> 3);
+    const int lc = (lane & 7) ^ ((r >> 1) & 7);
+    const int ra = min(m0 + r, p.M - 1), rw = min(n0 + r, p.N - 1);
+    offA[i] = (uint32_t)(((size_t)ra * p.lda + lc * 8) * 2);
+    offW[i] = (uint32_t)(((size_t)rw * p.K + lc * 8) * 2);
+  }
+  const unsigned char* gA = reinterpret_cast<const unsigned char*>(p.A);
+  const unsigned char* gW = reinterpret_cast<const unsigned char*>(p.W);
+  auto issue = [&](lds_u8* sa, lds_u8* sw, int k0) {
+    const unsigned char* ga = gA + (size_t)k0 * 2;
+    const unsigned char* gw = gW + (size_t)k0 * 2;
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-      const int row = m0 + a_row + 64 * i;
-      const int rr = min(row, p.M - 1);
-      ra[i] = *reinterpret_cast<const u32x4*>(A + (size_t)rr * lda + k0 + a_chunk * 8);
-      if (row >= p.M) ra[i] = u32x4{0u, 0u, 0u, 0u};
+      const uint32_t grp_off = (uint32_t)((i * 8 + wave) * 1024);
+      copy_to_lds(ga, offA[i], (uint32_t)(uintptr_t)sa + grp_off);
+      copy_to_lds(gw, offW[i], (uint32_t)(uintptr_t)sw + grp_off);
     }
-    const int col = n0 + b_nchunk * 8;
-    const int cc = min(col, N - 8);
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int k = k0 + b_kgroup * 4 + i;
-      rb[i] = *reinterpret_cast<const u32x4*>(Bm + (size_t)k * ldb + cc);
-      if (col >= N) rb[i] = u32x4{0u, 0u, 0u, 0u};
-    }
-  };
-
-  auto store_lds = [&](int buf) {
-    uint16_t* as = As + buf * BM * LDK;
-#pragma unroll
-    for (int i = 0; i < 4; ++i)
-      *reinterpret_cast<u32x4*>(as + (a_row + 64 * i) * LDK + a_chunk * 8) = ra[i];
-    // Transpose the 4 (k) x 8 (n) block: column n gets its 4 k values (8 bytes).
-    uint16_t* bs = Bs + buf * BN * LDK;
-    uint32_t w01[8], w23[8];  // (k0,k1) and (k2,k3) pairs per n
-#pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const uint32_t a0 = rb[0][j], a1 = rb[1][j], a2 = rb[2][j], a3 = rb[3][j];
-      w01[2 * j] = lo_pair(a0, a1);
-      w01[2 * j + 1] = hi_pair(a0, a1);
-      w23[2 * j] = lo_pair(a2, a3);
-      w23[2 * j + 1] = hi_pair(a2, a3);
-    }
-#pragma unroll
-    for (int n = 0; n < 8; ++n)
-      *reinterpret_cast<u32x2*>(bs + (b_nchunk * 8 + n) * LDK + b_kgroup * 4) = u32x2{w01[n], w23[n]};
   };
 
   f32x4_t acc[8][4];
@@ -126,95 +112,161 @@ __global__ __launch_bounds__(kThreads) void gemm_bf16_kernel(GemmBf16Params p) {
 #pragma unroll
     for (int j = 0; j < 4; ++j) acc[i][j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 
-  const int nk = p.K / BK;
-  load_global(0);
-  store_lds(0);
-  __syncthreads();
-  const int fr = lane & 15;          // fragment row (A) or column (B)
-  const int fk = (lane >> 4) * 8;    // fragment k offset
-  for (int kt = 0; kt < nk; ++kt) {
-    const int buf = kt & 1;
-    if (kt + 1 < nk) load_global((kt + 1) * BK);
-    const uint16_t* as = As + buf * BM * LDK + (wm * 128 + fr) * LDK + fk;
-    const uint16_t* bs = Bs + buf * BN * LDK + (wn * 64 + fr) * LDK + fk;
+  const int fr = lane & 15, grp = lane >> 4;
+  auto compute = [&](const lds_u8* a, const lds_u8* w) {
 #pragma unroll
     for (int ks = 0; ks < BK / 32; ++ks) {
+      const int chunk = ks * 4 + grp;
       bf16x8_t af[8], bf[4];
 #pragma unroll
       for (int i = 0; i < 8; ++i)
-        af[i] = *reinterpret_cast<const bf16x8_t*>(as + i * 16 * LDK + ks * 32);
+        af[i] = *reinterpret_cast<const __attribute__((address_space(3))) bf16x8_t*>(
+            a + swz(wm * 128 + i * 16 + fr, chunk));
 #pragma unroll
       for (int j = 0; j < 4; ++j)
-        bf[j] = *reinterpret_cast<const bf16x8_t*>(bs + j * 16 * LDK + ks * 32);
+        bf[j] = *reinterpret_cast<const __attribute__((address_space(3))) bf16x8_t*>(
+            w + swz(wn * 64 + j * 16 + fr, chunk));
 #pragma unroll
       for (int i = 0; i < 8; ++i)
 #pragma unroll
         for (int j = 0; j < 4; ++j)
           acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[i], bf[j], acc[i][j], 0, 0, 0);
     }
-    if (kt + 1 < nk) store_lds(buf ^ 1);
+  };
+
+  lds_u8* const base = (lds_u8*)smem;
+  auto stageA = [&](int st) { return base + st * 2 * TILE_BYTES; };
+  auto stageW = [&](int st) { return base + st * 2 * TILE_BYTES + TILE_BYTES; };
+  const int nk = p.K / BK;
+  issue(stageA(0), stageW(0), 0);
+  // Each wave issues 8 copies per tile; waiting until at most 8 are outstanding
+  // means the current tile has landed while the next one is still in flight.
+  for (int kt = 0; kt < nk; ++kt) {
+    const int cur = kt & 1;
+    if (kt + 1 < nk) {
+      issue(stageA(cur ^ 1), stageW(cur ^ 1), (kt + 1) * BK);
+      __builtin_amdgcn_s_waitcnt(0x3F78);  // vmcnt(8)
+    } else {
+      __builtin_amdgcn_s_waitcnt(0x3F70);  // vmcnt(0)
+    }
+    __syncthreads();
+    compute(stageA(cur), stageW(cur));
     __syncthreads();
   }
 
-  uint16_t* __restrict__ C = p.C[prob];
-  const long ldc = p.ldc[prob];
+  // Lane holds C[row 16 i + 4 grp + r][col 16 j + fr] of the wave's 128 x 64 block.
 #pragma unroll
-  for (int i = 0; i < 8; ++i) {
+  for (int j = 0; j < 4; ++j) {
+    const int col = n0 + wn * 64 + j * 16 + fr;
+    if (col >= p.N) continue;
+    uint16_t* dst;
+    long ldc;
+    if (col < p.n_split) {
+      dst = p.C0 + col;
+      ldc = p.ldc0;
+    } else {
+      dst = p.C1 + (col - p.n_split);
+      ldc = p.ldc1;
+    }
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const int col = n0 + wn * 64 + j * 16 + fr;
+    for (int i = 0; i < 8; ++i)
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
-        const int row = m0 + wm * 128 + i * 16 + (lane >> 4) * 4 + r;
-        if (row < p.M && col < N)
-          C[(size_t)row * ldc + col] = __builtin_bit_cast(uint16_t, (__bf16)acc[i][j][r]);
+        const int row = m0 + wm * 128 + i * 16 + grp * 4 + r;
+        if (row < p.M) dst[(size_t)row * ldc] = __builtin_bit_cast(uint16_t, (__bf16)acc[i][j][r]);
+      }
+  }
+}
+
+// Packing: Wp[n][k] = W~^Q[k][n] for n < H d (W~^Q = W^Q W^R per head, or W^Q
+// itself), Wp[H d + n][k] = W^V[k][n]. One thread per output element of a
+// 64 x 64 tile, through LDS so both the reads and the writes are coalesced.
+template <bool FOLD>
+__global__ __launch_bounds__(256) void pack_weights_kernel(PackParams p) {
+  __shared__ float tile[64][65];
+  const int n_tile = blockIdx.x, k_tile = blockIdx.y;  // 64 x 64 output tile of Wp
+  const int NQ = p.H * p.d_head;
+  const int n0 = n_tile * 64, k0 = k_tile * 64;
+  const uint16_t* Wq = reinterpret_cast<const uint16_t*>(p.W_Q);
+  const uint16_t* Wr = reinterpret_cast<const uint16_t*>(p.W_R);
+  const uint16_t* Wv = reinterpret_cast<const uint16_t*>(p.W_V);
+  // Phase 1: tile[kk][nn] = source value at (k0 + kk, n0 + nn), fp32.
+  for (int e = threadIdx.x; e < 64 * 64; e += 256) {
+    const int kk = e / 64, nn = e % 64;
+    const int k = k0 + kk, n = n0 + nn;
+    float v = 0.f;
+    if (k < p.d_model && n < p.N) {
+      if (n < NQ) {
+        if (FOLD) {
+          const int h = n / p.d_head, j = n % p.d_head;
+          const uint16_t* qrow = Wq + (size_t)k * NQ + (size_t)h * p.d_head;
+          const uint16_t* rcol = Wr + (size_t)h * p.d_head * p.d_head + j;
+          for (int i = 0; i < p.d_head; ++i)
+            v = fmaf(__uint_as_float((uint32_t)qrow[i] << 16),
+                     __uint_as_float((uint32_t)rcol[(size_t)i * p.d_head] << 16), v);
+        } else {
+          v = __uint_as_float((uint32_t)Wq[(size_t)k * NQ + n] << 16);
+        }
+      } else {
+        v = __uint_as_float((uint32_t)Wv[(size_t)k * (p.N - NQ) + (n - NQ)] << 16);
       }
     }
+    tile[kk][nn] = v;
+  }
+  __syncthreads();
+  uint16_t* out = reinterpret_cast<uint16_t*>(p.packed);
+  for (int e = threadIdx.x; e < 64 * 64; e += 256) {
+    const int nn = e / 64, kk = e % 64;
+    const int k = k0 + kk, n = n0 + nn;
+    if (k < p.d_model && n < p.N)
+      out[(size_t)n * p.d_model + k] = __builtin_bit_cast(uint16_t, (__bf16)tile[kk][nn]);
   }
 }
 
 }  // namespace
 
-size_t gemm_bf16_lds_bytes() { return (size_t)2 * (BM + BN) * LDK * sizeof(uint16_t); }
-
-// Validates shapes the kernel supports: K a multiple of 64, N and leading
-// dimensions multiples of 8, N >= 8.
-bool gemm_bf16_supported(int M, int N, int K, long lda, long ldb, long ldc) {
-  return M > 0 && N >= 8 && K >= BK && K % BK == 0 && N % 8 == 0 && lda % 8 == 0 &&
-         ldb % 8 == 0 && ldc % 8 == 0;
+bool gemm_bf16_supported(int M, int N, int K, long lda, long ldc0, long ldc1) {
+  // Operand offsets are 32-bit byte offsets.
+  const bool fits = (size_t)M * lda * 2 < (1ull << 32) && (size_t)N * K * 2 < (1ull << 32);
+  return M > 0 && N > 0 && K >= BK && K % BK == 0 && lda % 8 == 0 && lda >= K && ldc0 > 0 &&
+         ldc1 > 0 && fits;
 }
 
-hipError_t launch_gemm_bf16_pair(const void* A, int M, int K, long lda, const void* B0,
-                                 void* C0, int N0, long ldb0, long ldc0, const void* B1, void* C1,
-                                 int N1, long ldb1, long ldc1, hipStream_t st) {
+constexpr size_t kGemmLds = 4 * TILE_BYTES;
+
+hipError_t launch_gemm_bf16_packed(const void* A, int M, int K, long lda, const void* Wp, int N,
+                                   int n_split, void* C0, long ldc0, void* C1, long ldc1,
+                                   hipStream_t st) {
   static bool attr_set = false;
   if (!attr_set) {
     hipError_t e = hipFuncSetAttribute((const void*)gemm_bf16_kernel,
-                                       hipFuncAttributeMaxDynamicSharedMemorySize,
-                                       (int)gemm_bf16_lds_bytes());
+                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)kGemmLds);
     if (e != hipSuccess) return e;
     attr_set = true;
   }
-  GemmBf16Params p{};
+  GemmParams2 p{};
   p.A = static_cast<const uint16_t*>(A);
+  p.W = static_cast<const uint16_t*>(Wp);
+  p.C0 = static_cast<uint16_t*>(C0);
+  p.C1 = static_cast<uint16_t*>(C1);
   p.M = M;
+  p.N = N;
   p.K = K;
+  p.n_split = n_split;
   p.lda = lda;
-  p.B[0] = static_cast<const uint16_t*>(B0);
-  p.C[0] = static_cast<uint16_t*>(C0);
-  p.N[0] = N0;
-  p.ldb[0] = ldb0;
-  p.ldc[0] = ldc0;
-  const int nprob = B1 ? 2 : 1;
-  p.B[1] = static_cast<const uint16_t*>(B1 ? B1 : B0);
-  p.C[1] = static_cast<uint16_t*>(B1 ? C1 : C0);
-  p.N[1] = B1 ? N1 : N0;
-  p.ldb[1] = B1 ? ldb1 : ldb0;
-  p.ldc[1] = B1 ? ldc1 : ldc0;
-  const int tilesM = (M + BM - 1) / BM;
-  const int t0 = tilesM * ((p.N[0] + BN - 1) / BN), t1 = tilesM * ((p.N[1] + BN - 1) / BN);
-  dim3 grid(t0 > t1 ? t0 : t1, nprob);
-  hipLaunchKernelGGL(gemm_bf16_kernel, grid, dim3(kThreads), gemm_bf16_lds_bytes(), st, p);
+  p.ldc0 = ldc0;
+  p.ldc1 = ldc1;
+  const int tiles = ((M + BM - 1) / BM) * ((N + BN - 1) / BN);
+  hipLaunchKernelGGL(gemm_bf16_kernel, dim3(tiles), dim3(kThreads), kGemmLds, st, p);
+  return hipGetLastError();
+}
+
+hipError_t launch_pack_weights(const PackParams& p, hipStream_t st) {
+  dim3 grid((p.N + 63) / 64, (p.d_model + 63) / 64);
+  if (p.W_R)
+    hipLaunchKernelGGL(pack_weights_kernel<true>, grid, dim3(256), 0, st, p);
+  else
+    hipLaunchKernelGGL(pack_weights_kernel<false>, grid, dim3(256), 0, st, p);
   return hipGetLastError();
 }
 

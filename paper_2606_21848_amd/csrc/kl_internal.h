@@ -61,12 +61,23 @@ struct GemmParams {
 
 hipError_t launch_gemm_simple(const GemmParams& p, hipStream_t stream);
 
-// bf16 MFMA GEMM: C_i (M x N_i) = A (M x K) * B_i (K x N_i) for one or two
-// problems sharing A (B1 == nullptr: one problem). All bf16, row-major.
-bool gemm_bf16_supported(int M, int N, int K, long lda, long ldb, long ldc);
-hipError_t launch_gemm_bf16_pair(const void* A, int M, int K, long lda, const void* B0, void* C0,
-                                 int N0, long ldb0, long ldc0, const void* B1, void* C1, int N1,
-                                 long ldb1, long ldc1, hipStream_t stream);
+// bf16 MFMA GEMM against packed weights: C = A (M x K, row-major) * Wp^T with
+// Wp [N, K] (K contiguous). Columns < n_split go to C0, the rest to C1.
+bool gemm_bf16_supported(int M, int N, int K, long lda, long ldc0, long ldc1);
+hipError_t launch_gemm_bf16_packed(const void* A, int M, int K, long lda, const void* Wp, int N,
+                                   int n_split, void* C0, long ldc0, void* C1, long ldc1,
+                                   hipStream_t stream);
+
+// Packed projection weights: rows [0, H d) = (W^Q W^R per head)^T (or W^Q^T
+// when W_R is null), rows [H d, (H+G) d) = W^V^T; each row has d_model entries.
+struct PackParams {
+  const void* W_Q;
+  const void* W_R;
+  const void* W_V;
+  void* packed;
+  int d_model, H, G, d_head, N;
+};
+hipError_t launch_pack_weights(const PackParams& p, hipStream_t stream);
 
 struct AttnParams {
   const void* q;   // routed queries, [B, N, H, D] with row stride q_stride (elements per token)

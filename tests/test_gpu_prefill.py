@@ -26,6 +26,48 @@ def test_fold_routing(lib, dtype):
     assert_parity(got.reshape(d, H, dk), ref.reshape(d, H, dk), dtype, "fold")
 
 
+@pytest.mark.parametrize("with_wr", [True, False])
+def test_pack_weights(lib, with_wr):
+    """Packed rows: (W^Q W^R)^T per head over W^V^T, d_model contiguous. Without a
+    routing matrix the pack is a pure transpose and must be bit-exact."""
+    d, H, G, dk = 320, 4, 2, 64
+    say(f"pack weights with_wr={with_wr}")
+    W_Q = synth.normal((d, H * dk), 23, 1, d ** -0.5)
+    W_R = synth.normal((H, dk, dk), 23, 2, dk ** -0.5)
+    W_V = synth.normal((d, G * dk), 23, 3, d ** -0.5)
+    packed = kb.keyless_pack_weights(W_Q.to(DEV), W_R.to(DEV) if with_wr else None, W_V.to(DEV),
+                                     H, G)
+    torch.cuda.synchronize()
+    got = to64(packed)
+    assert got.shape == ((H + G) * dk, d)
+    if with_wr:
+        ref_q = K.fold_routing(to64(W_Q), to64(W_R), H, dk).T
+        assert_parity(got[:H * dk].reshape(H, dk, d), ref_q.reshape(H, dk, d), torch.bfloat16,
+                      "folded rows")
+    else:
+        np.testing.assert_array_equal(got[:H * dk], to64(W_Q).T)
+    np.testing.assert_array_equal(got[H * dk:], to64(W_V).T)
+
+
+@pytest.mark.parametrize("N,d,H,G,dk", [(300, 256, 4, 2, 128), (64, 128, 2, 1, 64)])
+def test_prefill_packed_matches_oracle(lib, N, d, H, G, dk):
+    say(f"prefill packed N={N} d={d} H={H} G={G} dk={dk}")
+    B = 2
+    x = synth.normal((B, N, d), 24, 1)
+    W_Q = synth.normal((d, H * dk), 24, 2, d ** -0.5)
+    W_R = synth.normal((H, dk, dk), 24, 3, dk ** -0.5)
+    W_V = synth.normal((d, G * dk), 24, 4, d ** -0.5)
+    packed = kb.keyless_pack_weights(W_Q.to(DEV), W_R.to(DEV), W_V.to(DEV), H, G)
+    out, qr, v = kb.keyless_prefill_packed(x.to(DEV), packed, H, G, return_qv=True)
+    out_only = kb.keyless_prefill_packed(x.to(DEV), packed, H, G)  # Q~ and V in the workspace
+    torch.cuda.synchronize()
+    O, Qr, V = K.keyless_prefill(to64(x), to64(W_Q), to64(W_R), to64(W_V), H, G, dk)
+    assert_parity(qr, Qr, torch.bfloat16, "routed queries")
+    assert_parity(v, V, torch.bfloat16, "values")
+    assert_parity(out, O, torch.bfloat16, "output")
+    assert torch.equal(out, out_only)
+
+
 @pytest.mark.parametrize("dtype", [torch.float32, torch.bfloat16])
 @pytest.mark.parametrize("causal", [True, False])
 @pytest.mark.parametrize("N,d,H,G,dk", [(200, 128, 4, 2, 64), (77, 256, 2, 2, 128), (1, 64, 2, 1, 64),
@@ -79,13 +121,13 @@ def test_tiny_fp32_layer_prefill_append_decode(lib):
 
 
 def test_prefill_bf16_full_size_sampled(lib):
-    """Batch 1, 8192 tokens, d_model 4096, 32 heads x 128, causal, with W_R folded
-    first (as at inference): 510 sampled rows plus rows 0 and 8191 against the
-    oracle; all of V against the oracle."""
+    """Batch 1, 8192 tokens, d_model 4096, 32 heads x 128, causal, with the weights
+    folded and packed once first (as at inference) and the launch the bench times:
+    510 sampled rows plus rows 0 and 8191 against the oracle; all of V too."""
     say("prefill_bf16 full size")
     c = configs.prefill_bf16(device=DEV)
-    Wt = kb.keyless_fold_routing(c["W_Q"], c["W_R"])
-    out, qr, v = kb.keyless_prefill(c["x"], Wt, None, c["W_V"], 32, 32, return_qv=True)
+    packed = kb.keyless_pack_weights(c["W_Q"], c["W_R"], c["W_V"], 32, 32)
+    out, qr, v = kb.keyless_prefill_packed(c["x"], packed, 32, 32, return_qv=True)
     torch.cuda.synchronize()
     rows = sorted(set([0, 8191] + synth.uniform_int(510, 1, 8190, 2, 50).tolist()))
     Wt_ref = K.fold_routing(to64(c["W_Q"]), to64(c["W_R"]), 32, 128)
