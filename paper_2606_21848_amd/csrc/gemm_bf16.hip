@@ -42,17 +42,6 @@ struct GemmParams2 {
   long ldc0, ldc1;
 };
 
-// One 16-byte-per-lane copy from global memory into LDS: lane L's bytes land at
-// lds + 16 L. Issued as inline assembly so the compiler does not order every copy
-// behind the previous one (it cannot see that the copies target disjoint LDS
-// rows); the caller waits with s_waitcnt vmcnt before the tile is read.
-__device__ __forceinline__ void copy_to_lds(const void* gbase, uint32_t voff, uint32_t lds) {
-  asm volatile("s_mov_b32 m0, %2\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, %1"
-               :
-               : "v"(voff), "s"(gbase), "s"(lds)
-               : "memory", "m0");
-}
-
 // Byte offset of (row, 16-byte chunk) inside a swizzled operand tile.
 __device__ __forceinline__ int swz(int row, int chunk) {
   return row * (BK * 2) + ((chunk ^ ((row >> 1) & 7)) << 4);
@@ -145,9 +134,9 @@ __global__ __launch_bounds__(kThreads) void gemm_bf16_kernel(GemmParams2 p) {
     const int cur = kt & 1;
     if (kt + 1 < nk) {
       issue(stageA(cur ^ 1), stageW(cur ^ 1), (kt + 1) * BK);
-      __builtin_amdgcn_s_waitcnt(0x3F78);  // vmcnt(8)
+      KL_WAIT_VMCNT(8);
     } else {
-      __builtin_amdgcn_s_waitcnt(0x3F70);  // vmcnt(0)
+      KL_WAIT_VMCNT(0);
     }
     __syncthreads();
     compute(stageA(cur), stageW(cur));

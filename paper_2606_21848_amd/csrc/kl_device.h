@@ -53,6 +53,23 @@ __device__ __forceinline__ float group_sum(float x) {
 
 __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
 
+// One 16-byte-per-lane copy from global memory straight into LDS
+// (global_load_lds_dwordx4): lane L's bytes land at lds + 16 L, where lds is a
+// wave-uniform LDS byte address and gbase + voff the lane's source. Issued as
+// inline assembly so the compiler does not serialise consecutive copies (it
+// cannot tell they fill disjoint LDS rows). The copy counts against vmcnt:
+// callers wait with s_waitcnt vmcnt and a barrier before the rows are read.
+__device__ __forceinline__ void copy_to_lds(const void* gbase, uint32_t voff, uint32_t lds) {
+  asm volatile("s_mov_b32 m0, %2\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, %1"
+               :
+               : "v"(voff), "s"(gbase), "s"(lds)
+               : "memory", "m0");
+}
+
+// s_waitcnt with only the vector-memory counter constrained (0..63).
+#define KL_WAIT_VMCNT(n) \
+  __builtin_amdgcn_s_waitcnt((((n) & 15) | (((n) >> 4) << 14)) | (0x7 << 4) | (0xF << 8))
+
 // Merge two online-softmax states (m: running max in log2 units, l: sum of
 // weights, a: weighted sum) into the first. An empty state has m = -inf, l = 0.
 __device__ __forceinline__ void merge_scale(float m1, float m2, float& f1, float& f2, float& m) {

@@ -2,20 +2,23 @@
 // of Eq. 4): O_h = softmax(tau * Q~_h V_g^T) V_g, where the value tile is both
 // the "key" of the score and the value of the weighted sum.
 //
-// A workgroup (4 waves) owns 128 query rows of one head; each wave owns 32 rows.
-// The routed-query fragments stay in registers. For every 64-row value tile,
-// read from memory once, two LDS copies are written: row-major (rows of d_head
-// contiguous) and transposed (64 rows of one column contiguous, built in
-// registers with v_perm). Then, with v_mfma_f32_16x16x32_bf16:
-//   S^T = V Q~^T     A operand = value rows (row-major copy), B = routed queries
-//   O^T += V^T P^T   A operand = value columns (transposed copy), B = P in bf16
-// Computing S^T leaves each lane holding scores of a single query row, so the
-// online softmax needs only two cross-lane steps per row, and the score
-// registers become the B operand of the second product without a transpose
-// (the MFMA reduction order over a 32-row step is free as long as both operands
-// agree; here a lane group g covers rows 4g..4g+3 and 16+4g..16+4g+3).
-// The next value tile is loaded from memory while the current one is used.
-// Causal work grows with the query tile, so the last tiles are scheduled first.
+// A workgroup (4 waves) owns 128 query rows of one head; each wave owns 32 rows
+// and keeps their routed-query fragments in registers. Value tiles of 64 rows
+// move from memory straight into LDS (global_load_lds, 16 bytes per lane), one
+// copy per tile, three tiles in flight. With v_mfma_f32_16x16x32_bf16:
+//   S^T = V Q~^T     A operand = value rows (ds_read_b128 of the row-major tile)
+//   O^T += V^T P^T   A operand = value columns, read from the same row-major tile
+//                    with ds_read_b64_tr_b16 (each 16-lane group transposes a
+//                    4-row x 16-column block into 4 rows of one column per lane)
+// Computing S^T leaves each lane holding scores of one query row, so the online
+// softmax needs two cross-lane steps per row, and the score registers become the
+// B operand of the second product directly. The MFMA reduction order over a
+// 32-row step is free as long as both operands agree; here lane group g covers
+// rows 4g..4g+3 and 16+4g..16+4g+3 of the step.
+// The tile's 16-byte chunks are XOR-swizzled per row so that both the score
+// reads (16 rows, one chunk) and the transposed reads (8 rows, two chunks per
+// pass) hit distinct LDS banks. Causal work grows with the query tile, so the
+// last tiles are scheduled first.
 
 #include "kl_device.h"
 #include "kl_internal.h"
@@ -25,18 +28,15 @@ namespace {
 
 typedef __attribute__((__vector_size__(8 * sizeof(__bf16)))) __bf16 bf16x8_t;
 typedef __attribute__((__vector_size__(4 * sizeof(float)))) float f32x4_t;
+typedef short s16x4 __attribute__((ext_vector_type(4)));
 typedef unsigned int u32x2 __attribute__((ext_vector_type(2)));
+typedef __attribute__((address_space(3))) unsigned char lds_u8;
 
-constexpr int BQ = 128;   // query rows per workgroup
-constexpr int BKV = 64;   // value rows per tile
+constexpr int BQ = 128;     // query rows per workgroup
+constexpr int BKV = 64;     // value rows per tile
+constexpr int NSTAGE = 3;   // value tiles in flight
 constexpr int kThreads = 256;
 
-__device__ __forceinline__ uint32_t lo_pair(uint32_t a, uint32_t b) {
-  return __builtin_amdgcn_perm(b, a, 0x05040100u);
-}
-__device__ __forceinline__ uint32_t hi_pair(uint32_t a, uint32_t b) {
-  return __builtin_amdgcn_perm(b, a, 0x07060302u);
-}
 __device__ __forceinline__ uint32_t pack2(float lo, float hi) {
   typedef __attribute__((__vector_size__(2 * sizeof(__bf16)))) __bf16 b2;
   b2 v = {(__bf16)lo, (__bf16)hi};
@@ -44,50 +44,47 @@ __device__ __forceinline__ uint32_t pack2(float lo, float hi) {
 }
 
 template <int D>
-struct AttnLds {
-  static constexpr int VS_LD = D + 8;     // row-major copy: [BKV][D + 8]
-  static constexpr int VT_LD = BKV + 8;   // transposed copy: [D][BKV + 8]
-  static constexpr int VS = BKV * VS_LD;  // elements
-  static constexpr int VT = D * VT_LD;
-  static constexpr int BUF = VS + VT;
-  static constexpr size_t BYTES = 2 * BUF * sizeof(uint16_t);
+struct Tile {
+  static constexpr int ROW = D * 2;              // bytes per value row
+  static constexpr int CHUNKS = D / 8;           // 16-byte chunks per row
+  static constexpr int BYTES = BKV * ROW;        // one tile
+  static constexpr int COPIES = BYTES / 1024 / 4;  // wave copies per wave per tile
+  // Physical chunk of logical chunk c in row r.
+  static __device__ __forceinline__ int swz(int r, int c) {
+    if constexpr (D == 128) return c ^ (((r & 7) << 1) | ((r >> 3) & 1));
+    else return c ^ ((r >> 1) & 7);
+  }
+  static __device__ __forceinline__ int off(int r, int c) { return r * ROW + (swz(r, c) << 4); }
 };
 
 template <int D>
-__global__ __launch_bounds__(kThreads) void attn_bf16_kernel(AttnParams p) {
-  using L = AttnLds<D>;
-  constexpr int KS = D / 32;       // MFMA k-steps over d_head for S^T
-  constexpr int DB = D / 16;       // 16-wide column blocks of the output
-  constexpr int DCH = D / 8;       // 16-byte chunks per value row
-  constexpr int LOADERS = (BKV / 4) * DCH;  // threads that load a 4 x 8 block each
+__global__ __launch_bounds__(kThreads, 2) void attn_bf16_kernel(AttnParams p) {
+  using T = Tile<D>;
+  constexpr int KS = D / 32;  // MFMA k-steps over d_head for S^T
+  constexpr int DB = D / 16;  // 16-wide column blocks of the output
+  extern __shared__ __attribute__((aligned(1024))) unsigned char smem[];  // NSTAGE tiles
 
   const int ntq = (p.N + BQ - 1) / BQ;
   const int qt = p.causal ? (ntq - 1 - (int)blockIdx.x) : (int)blockIdx.x;
   const int h = blockIdx.y, b = blockIdx.z;
   const int g = h / (p.H / p.G);
-  const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
+  const int t = threadIdx.x, lane = t & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(t >> 6);
   const int fr = lane & 15, grp = lane >> 4;
   const int q0 = qt * BQ + wave * 32;  // this wave's first query row
 
   const uint16_t* __restrict__ Q = reinterpret_cast<const uint16_t*>(p.q);
-  const uint16_t* __restrict__ V = reinterpret_cast<const uint16_t*>(p.v);
-
-  extern __shared__ __attribute__((aligned(16))) uint16_t smem[];
 
   // Routed-query fragments (B operand of S^T): query row q0 + 16 qb + fr,
-  // columns 32 ks + 8 grp .. + 7.
+  // columns 32 ks + 8 grp .. + 7. Rows past the end are clamped (never stored).
   bf16x8_t qf[2][KS];
 #pragma unroll
   for (int qb = 0; qb < 2; ++qb) {
-    const int q = q0 + qb * 16 + fr;
-    const int qq = min(q, p.N - 1);
+    const int qq = min(q0 + qb * 16 + fr, p.N - 1);
     const uint16_t* src = Q + ((size_t)b * p.N + qq) * p.q_stride + (size_t)h * D + grp * 8;
 #pragma unroll
-    for (int ks = 0; ks < KS; ++ks) {
-      u32x4 w = *reinterpret_cast<const u32x4*>(src + ks * 32);
-      if (q >= p.N) w = u32x4{0u, 0u, 0u, 0u};
-      qf[qb][ks] = __builtin_bit_cast(bf16x8_t, w);
-    }
+    for (int ks = 0; ks < KS; ++ks)
+      qf[qb][ks] = *reinterpret_cast<const bf16x8_t*>(src + ks * 32);
   }
 
   f32x4_t o[DB][2];
@@ -96,135 +93,142 @@ __global__ __launch_bounds__(kThreads) void attn_bf16_kernel(AttnParams p) {
   float m[2] = {-INFINITY, -INFINITY};
   float lsum[2] = {0.f, 0.f};  // per-lane partial sums; reduced at the end
 
-  // Value-tile loader: thread t < LOADERS moves a 4-row x 8-column block.
-  const bool loader = t < LOADERS;
-  const int ld_ch = t % DCH, ld_grp = t / DCH;
-  u32x4 rv[4];
-  const size_t vrow0 = (size_t)b * p.N;
-  auto load_tile = [&](int j0) {
-    if (!loader) return;
+  // Tile copies: wave copy c of this wave fills tile rows 4 (c * 4 + wave) ..
+  // + 3; lane L lands at row + L / CHUNKS, physical chunk L % CHUNKS. Rows past
+  // the end are clamped: their scores are masked, so they carry no weight.
+  const unsigned char* gV = reinterpret_cast<const unsigned char*>(p.v);
+  constexpr int ROWS_PER_COPY = 1024 / T::ROW;
+  // The copy's source is a wave-uniform base (first row of the group, clamped)
+  // plus a per-lane offset (row within the group, clamped, and chunk).
+  uint32_t col_off[T::COPIES];  // bytes: group g's columns plus the logical chunk
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int row = j0 + ld_grp * 4 + i;
-      const int rr = min(row, p.N - 1);
-      rv[i] = *reinterpret_cast<const u32x4*>(V + (vrow0 + rr) * p.v_stride + (size_t)g * D + ld_ch * 8);
-      if (row >= p.N) rv[i] = u32x4{0u, 0u, 0u, 0u};
+  for (int c = 0; c < T::COPIES; ++c) {
+    const int r = (c * 4 + wave) * ROWS_PER_COPY + lane / T::CHUNKS;
+    const int pc = lane % T::CHUNKS;
+    int lc = pc;
+    // invert the swizzle: logical chunk whose physical position is pc
+#pragma unroll
+    for (int x = 0; x < T::CHUNKS; ++x)
+      if (T::swz(r, x) == pc) lc = x;
+    col_off[c] = (uint32_t)(((size_t)g * D + lc * 8) * 2);
+  }
+  const uint32_t lds0 = (uint32_t)(uintptr_t)(lds_u8*)smem;
+  const size_t row_bytes = (size_t)p.v_stride * 2;
+  auto issue = [&](int jt) {
+    const int stage = jt % NSTAGE;
+#pragma unroll
+    for (int c = 0; c < T::COPIES; ++c) {
+      const int r0 = jt * BKV + (c * 4 + wave) * ROWS_PER_COPY;  // uniform
+      const int r0c = min(r0, p.N - 1);
+      const int rl = min(r0 + lane / T::CHUNKS, p.N - 1) - r0c;  // 0 .. ROWS_PER_COPY - 1
+      const unsigned char* base = gV + ((size_t)b * p.N + r0c) * row_bytes;
+      copy_to_lds(base, (uint32_t)(rl * row_bytes) + col_off[c],
+                  lds0 + stage * T::BYTES + (c * 4 + wave) * 1024);
     }
-  };
-  auto store_tile = [&](int buf) {
-    if (!loader) return;
-    uint16_t* vs = smem + buf * L::BUF;
-    uint16_t* vt = vs + L::VS;
-#pragma unroll
-    for (int i = 0; i < 4; ++i)
-      *reinterpret_cast<u32x4*>(vs + (ld_grp * 4 + i) * L::VS_LD + ld_ch * 8) = rv[i];
-    uint32_t w01[8], w23[8];
-#pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      w01[2 * j] = lo_pair(rv[0][j], rv[1][j]);
-      w01[2 * j + 1] = hi_pair(rv[0][j], rv[1][j]);
-      w23[2 * j] = lo_pair(rv[2][j], rv[3][j]);
-      w23[2 * j + 1] = hi_pair(rv[2][j], rv[3][j]);
-    }
-#pragma unroll
-    for (int c = 0; c < 8; ++c)
-      *reinterpret_cast<u32x2*>(vt + (ld_ch * 8 + c) * L::VT_LD + ld_grp * 4) = u32x2{w01[c], w23[c]};
   };
 
-  // Value tiles this workgroup needs.
   const int last_row = p.causal ? min(qt * BQ + BQ, p.N) : p.N;
   const int ntiles = (last_row + BKV - 1) / BKV;
-  load_tile(0);
-  store_tile(0);
-  __syncthreads();
+#pragma unroll
+  for (int s = 0; s < NSTAGE - 1; ++s)
+    if (s < ntiles) issue(s);
+
   for (int jt = 0; jt < ntiles; ++jt) {
-    const int buf = jt & 1;
+    // Tile jt has landed once at most the copies of the later issued tiles remain.
+    const int later = min(ntiles - 1 - jt, NSTAGE - 2);
+    if (later >= 1) KL_WAIT_VMCNT(T::COPIES);
+    else KL_WAIT_VMCNT(0);
+    __syncthreads();
+    if (jt + NSTAGE - 1 < ntiles) issue(jt + NSTAGE - 1);
+    const lds_u8* tile = (const lds_u8*)smem + (jt % NSTAGE) * T::BYTES;
     const int j0 = jt * BKV;
-    if (jt + 1 < ntiles) load_tile(j0 + BKV);
-    const uint16_t* vs = smem + buf * L::BUF;
-    const uint16_t* vt = vs + L::VS;
     // Skip tiles entirely above the diagonal for this wave.
-    const bool live = !p.causal || j0 <= q0 + 31;
-    if (live) {
-      // S^T[kv][q] for kv blocks kb (16 rows) and query blocks qb.
-      f32x4_t s[4][2];
+    if (p.causal && j0 > q0 + 31) continue;
+
+    // S^T[kv][q] for kv blocks kb (16 rows) and query blocks qb.
+    f32x4_t s[4][2];
 #pragma unroll
-      for (int kb = 0; kb < 4; ++kb) {
-        s[kb][0] = s[kb][1] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+    for (int kb = 0; kb < 4; ++kb) {
+      s[kb][0] = s[kb][1] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-        for (int ks = 0; ks < KS; ++ks) {
-          const bf16x8_t a = *reinterpret_cast<const bf16x8_t*>(
-              vs + (kb * 16 + fr) * L::VS_LD + ks * 32 + grp * 8);
-          s[kb][0] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, qf[0][ks], s[kb][0], 0, 0, 0);
-          s[kb][1] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, qf[1][ks], s[kb][1], 0, 0, 0);
-        }
-      }
-      // Lane holds scores of query q0 + 16 qb + fr against rows j0 + 16 kb + 4 grp + r.
-      const bool need_mask = (p.causal && j0 + BKV - 1 > q0) || (j0 + BKV > p.N);
-#pragma unroll
-      for (int qb = 0; qb < 2; ++qb) {
-        const int q = q0 + qb * 16 + fr;
-        float mx = -INFINITY;
-#pragma unroll
-        for (int kb = 0; kb < 4; ++kb)
-#pragma unroll
-          for (int r = 0; r < 4; ++r) {
-            float x = s[kb][qb][r] * p.scale_log2;
-            if (need_mask) {
-              const int kv = j0 + kb * 16 + grp * 4 + r;
-              if (kv >= p.N || (p.causal && kv > q)) x = -INFINITY;
-            }
-            s[kb][qb][r] = x;
-            mx = fmaxf(mx, x);
-          }
-        mx = fmaxf(mx, __shfl_xor(mx, 16));
-        mx = fmaxf(mx, __shfl_xor(mx, 32));
-        const float mn = fmaxf(m[qb], mx);
-        const float ms = (mn == -INFINITY) ? 0.f : mn;
-        const float alpha = fast_exp2(m[qb] - ms);
-        m[qb] = mn;
-        float ps = 0.f;
-#pragma unroll
-        for (int kb = 0; kb < 4; ++kb)
-#pragma unroll
-          for (int r = 0; r < 4; ++r) {
-            const float w = fast_exp2(s[kb][qb][r] - ms);
-            s[kb][qb][r] = w;
-            ps += w;
-          }
-        lsum[qb] = lsum[qb] * alpha + ps;
-#pragma unroll
-        for (int i = 0; i < DB; ++i) o[i][qb] *= alpha;
-      }
-      // P^T fragments: k-step ks covers rows 32 ks + {4 grp .. 4 grp + 3, 16 + 4 grp ..}.
-      bf16x8_t pf[2][2];
-#pragma unroll
-      for (int qb = 0; qb < 2; ++qb)
-#pragma unroll
-        for (int ks = 0; ks < 2; ++ks) {
-          u32x4 w;
-          w[0] = pack2(s[2 * ks][qb][0], s[2 * ks][qb][1]);
-          w[1] = pack2(s[2 * ks][qb][2], s[2 * ks][qb][3]);
-          w[2] = pack2(s[2 * ks + 1][qb][0], s[2 * ks + 1][qb][1]);
-          w[3] = pack2(s[2 * ks + 1][qb][2], s[2 * ks + 1][qb][3]);
-          pf[qb][ks] = __builtin_bit_cast(bf16x8_t, w);
-        }
-      // O^T[d][q] += V^T P^T: A = value column d = 16 db + fr over the same rows.
-#pragma unroll
-      for (int db = 0; db < DB; ++db) {
-#pragma unroll
-        for (int ks = 0; ks < 2; ++ks) {
-          const uint16_t* col = vt + (db * 16 + fr) * L::VT_LD + ks * 32 + grp * 4;
-          const u32x2 lo = *reinterpret_cast<const u32x2*>(col);
-          const u32x2 hi = *reinterpret_cast<const u32x2*>(col + 16);
-          const bf16x8_t a = __builtin_bit_cast(bf16x8_t, u32x4{lo[0], lo[1], hi[0], hi[1]});
-          o[db][0] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, pf[0][ks], o[db][0], 0, 0, 0);
-          o[db][1] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, pf[1][ks], o[db][1], 0, 0, 0);
-        }
+      for (int ks = 0; ks < KS; ++ks) {
+        const bf16x8_t a = *reinterpret_cast<const __attribute__((address_space(3))) bf16x8_t*>(
+            tile + T::off(kb * 16 + fr, ks * 4 + grp));
+        s[kb][0] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, qf[0][ks], s[kb][0], 0, 0, 0);
+        s[kb][1] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, qf[1][ks], s[kb][1], 0, 0, 0);
       }
     }
-    if (jt + 1 < ntiles) store_tile(buf ^ 1);
-    __syncthreads();
+    // Lane holds scores of query q0 + 16 qb + fr against rows j0 + 16 kb + 4 grp + r.
+    const bool need_mask = (p.causal && j0 + BKV - 1 > q0) || (j0 + BKV > p.N);
+#pragma unroll
+    for (int qb = 0; qb < 2; ++qb) {
+      const int q = q0 + qb * 16 + fr;
+      float mx = -INFINITY;
+#pragma unroll
+      for (int kb = 0; kb < 4; ++kb)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          float x = s[kb][qb][r] * p.scale_log2;
+          if (need_mask) {
+            const int kv = j0 + kb * 16 + grp * 4 + r;
+            if (kv >= p.N || (p.causal && kv > q)) x = -INFINITY;
+          }
+          s[kb][qb][r] = x;
+          mx = fmaxf(mx, x);
+        }
+      mx = fmaxf(mx, __shfl_xor(mx, 16));
+      mx = fmaxf(mx, __shfl_xor(mx, 32));
+      const float mn = fmaxf(m[qb], mx);
+      const float ms = (mn == -INFINITY) ? 0.f : mn;
+      const float alpha = fast_exp2(m[qb] - ms);
+      m[qb] = mn;
+      float ps = 0.f;
+#pragma unroll
+      for (int kb = 0; kb < 4; ++kb)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const float w = fast_exp2(s[kb][qb][r] - ms);
+          s[kb][qb][r] = w;
+          ps += w;
+        }
+      lsum[qb] = lsum[qb] * alpha + ps;
+#pragma unroll
+      for (int i = 0; i < DB; ++i) o[i][qb] *= alpha;
+    }
+    // P^T fragments: k-step ks covers rows 32 ks + {4 grp .. 4 grp + 3, 16 + 4 grp ..}.
+    bf16x8_t pf[2][2];
+#pragma unroll
+    for (int qb = 0; qb < 2; ++qb)
+#pragma unroll
+      for (int ks = 0; ks < 2; ++ks) {
+        u32x4 w;
+        w[0] = pack2(s[2 * ks][qb][0], s[2 * ks][qb][1]);
+        w[1] = pack2(s[2 * ks][qb][2], s[2 * ks][qb][3]);
+        w[2] = pack2(s[2 * ks + 1][qb][0], s[2 * ks + 1][qb][1]);
+        w[3] = pack2(s[2 * ks + 1][qb][2], s[2 * ks + 1][qb][3]);
+        pf[qb][ks] = __builtin_bit_cast(bf16x8_t, w);
+      }
+    // O^T[d][q] += V^T P^T. For column block db and step ks, lane (grp, fr = l)
+    // addresses row 32 ks + 4 grp + l / 4 (and + 16), columns 16 db + 4 (l % 4);
+    // the transposed read hands lane l the 4 rows of column 16 db + l.
+#pragma unroll
+    for (int db = 0; db < DB; ++db) {
+#pragma unroll
+      for (int ks = 0; ks < 2; ++ks) {
+        const int r0 = ks * 32 + grp * 4 + (fr >> 2);
+        const int col = db * 16 + (fr & 3) * 4;  // element column of this lane's 8 bytes
+        const int c16 = col >> 3, half = (col & 7) * 2;
+        const s16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+            (__attribute__((address_space(3))) s16x4*)(tile + T::off(r0, c16) + half));
+        const s16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+            (__attribute__((address_space(3))) s16x4*)(tile + T::off(r0 + 16, c16) + half));
+        const bf16x8_t a = __builtin_bit_cast(
+            bf16x8_t, u32x4{__builtin_bit_cast(u32x2, lo)[0], __builtin_bit_cast(u32x2, lo)[1],
+                            __builtin_bit_cast(u32x2, hi)[0], __builtin_bit_cast(u32x2, hi)[1]});
+        o[db][0] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, pf[0][ks], o[db][0], 0, 0, 0);
+        o[db][1] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, pf[1][ks], o[db][1], 0, 0, 0);
+      }
+    }
   }
 
   // Normalise and store: lane holds O[q][16 db + 4 grp + r] for its query rows.
@@ -250,24 +254,18 @@ __global__ __launch_bounds__(kThreads) void attn_bf16_kernel(AttnParams p) {
 
 template <int D>
 hipError_t launch_attn(const AttnParams& p, hipStream_t st) {
-  static bool attr_set = false;
-  if (!attr_set) {
-    hipError_t e = hipFuncSetAttribute((const void*)attn_bf16_kernel<D>,
-                                       hipFuncAttributeMaxDynamicSharedMemorySize,
-                                       (int)AttnLds<D>::BYTES);
-    if (e != hipSuccess) return e;
-    attr_set = true;
-  }
   dim3 grid((p.N + BQ - 1) / BQ, p.H, p.B);
-  hipLaunchKernelGGL(attn_bf16_kernel<D>, grid, dim3(kThreads), AttnLds<D>::BYTES, st, p);
+  hipLaunchKernelGGL(attn_bf16_kernel<D>, grid, dim3(kThreads), NSTAGE * Tile<D>::BYTES, st, p);
   return hipGetLastError();
 }
 
 }  // namespace
 
 bool attn_bf16_supported(const AttnParams& p) {
+  // Strides keep 16-byte alignment; a copy's per-lane offset spans at most 8
+  // value rows and must fit in 32 bits.
   return p.dtype == KL_BF16 && (p.D == 64 || p.D == 128) && p.q_stride % 8 == 0 &&
-         p.v_stride % 8 == 0 && p.o_stride % 8 == 0;
+         p.v_stride % 8 == 0 && p.o_stride % 8 == 0 && (size_t)p.v_stride * 2 * 8 < (1u << 31);
 }
 
 hipError_t launch_prefill_attention(const AttnParams& p, hipStream_t st) {
