@@ -97,7 +97,7 @@ int keyless_fold_routing(const void* W_Q, const void* W_R, int d_model, int H, i
  *   W_R     [H, d_head, d_head] or NULL
  *   W_V     [d_model, G * d_head]
  *   causal  nonzero: token i attends to tokens j <= i (itself included)
- *   scale   softmax temperature; 0 selects 1/sqrt(d_head)
+ *   scale   softmax temperature, >= 0; 0 selects 1/sqrt(d_head)
  *   out     [B, N, H, d_head]
  *   q_routed_out  [B, N, H, d_head] or NULL (the routed queries x W~^Q)
  *   v_out         [B, N, G, d_head] or NULL (the values to append to the cache)

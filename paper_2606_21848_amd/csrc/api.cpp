@@ -340,7 +340,7 @@ size_t keyless_prefill_workspace_size(int B, int N, int d_model, int H, int G, i
 namespace {
 
 int check_prefill_args(const char* who, const void* x, const void* W, const void* out, int B,
-                       int N, int d_model, int H, int G, int d_head, kl_dtype dtype) {
+                       int N, int d_model, int H, int G, int d_head, kl_dtype dtype, float scale) {
   if (!x || !W || !out) return fail(KL_ERR_INVALID_ARG, "%s: inputs and out must be non-NULL", who);
   if (!dtype_ok(dtype)) return fail(KL_ERR_UNSUPPORTED, "%s: unknown dtype", who);
   if (B < 0 || N < 0 || d_model <= 0 || H <= 0 || G <= 0)
@@ -350,6 +350,7 @@ int check_prefill_args(const char* who, const void* x, const void* W, const void
     return fail(KL_ERR_UNSUPPORTED, "%s: d_head %d not supported (64 or 128)", who, d_head);
   if (H % G != 0) return fail(KL_ERR_INVALID_ARG, "%s: H=%d is not a multiple of G=%d", who, H, G);
   if ((long)B * N > (1L << 30)) return fail(KL_ERR_UNSUPPORTED, "%s: B*N too large", who);
+  if (!(scale >= 0.f)) return fail(KL_ERR_INVALID_ARG, "%s: scale must be >= 0 (0 = 1/sqrt(d_head))", who);
   return KL_OK;
 }
 
@@ -401,7 +402,7 @@ int keyless_prefill_packed(const void* x, const void* packed, int B, int N, int 
                            void* q_routed_out, void* v_out, void* ws, size_t ws_bytes,
                            void* stream) {
   const char* who = "keyless_prefill_packed";
-  int s = check_prefill_args(who, x, packed, out, B, N, d_model, H, G, d_head, dtype);
+  int s = check_prefill_args(who, x, packed, out, B, N, d_model, H, G, d_head, dtype, scale);
   if (s != KL_OK) return s;
   if (dtype != KL_BF16) return fail(KL_ERR_UNSUPPORTED, "%s: packed weights are bf16 only", who);
   const size_t e = 2;
@@ -423,7 +424,7 @@ int keyless_prefill(const void* x, const void* W_Q, const void* W_R, const void*
                     kl_dtype dtype, void* out, void* q_routed_out, void* v_out, void* ws,
                     size_t ws_bytes, void* stream) {
   const char* who = "keyless_prefill";
-  int s = check_prefill_args(who, x, W_Q, out, B, N, d_model, H, G, d_head, dtype);
+  int s = check_prefill_args(who, x, W_Q, out, B, N, d_model, H, G, d_head, dtype, scale);
   if (s != KL_OK) return s;
   if (!W_V) return fail(KL_ERR_INVALID_ARG, "%s: W_V must be non-NULL", who);
   const size_t need = keyless_prefill_workspace_size(B, N, d_model, H, G, d_head, dtype,

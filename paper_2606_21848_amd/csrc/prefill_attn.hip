@@ -20,6 +20,8 @@
 // pass) hit distinct LDS banks. Causal work grows with the query tile, so the
 // last tiles are scheduled first.
 
+#include <type_traits>
+
 #include "kl_device.h"
 #include "kl_internal.h"
 
@@ -90,7 +92,7 @@ __global__ __launch_bounds__(kThreads, 2) void attn_bf16_kernel(AttnParams p) {
   f32x4_t o[DB][2];
 #pragma unroll
   for (int i = 0; i < DB; ++i) o[i][0] = o[i][1] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-  float m[2] = {-INFINITY, -INFINITY};
+  float m[2] = {-INFINITY, -INFINITY};  // reference exponent (log2 units) per query block
   float lsum[2] = {0.f, 0.f};  // per-lane partial sums; reduced at the end
 
   // Tile copies: wave copy c of this wave fills tile rows 4 (c * 4 + wave) ..
@@ -114,8 +116,7 @@ __global__ __launch_bounds__(kThreads, 2) void attn_bf16_kernel(AttnParams p) {
   }
   const uint32_t lds0 = (uint32_t)(uintptr_t)(lds_u8*)smem;
   const size_t row_bytes = (size_t)p.v_stride * 2;
-  auto issue = [&](int jt) {
-    const int stage = jt % NSTAGE;
+  auto issue = [&](int jt, const int stage) {
 #pragma unroll
     for (int c = 0; c < T::COPIES; ++c) {
       const int r0 = jt * BKV + (c * 4 + wave) * ROWS_PER_COPY;  // uniform
@@ -127,108 +128,141 @@ __global__ __launch_bounds__(kThreads, 2) void attn_bf16_kernel(AttnParams p) {
     }
   };
 
+  // Per-lane LDS byte offsets inside a tile. The swizzle of a row depends only
+  // on the lane here, so the block, step and stage offsets are immediates.
+  int offS[KS];  // score operand: row fr, chunk 4 ks + grp (+ 16 kb rows)
+#pragma unroll
+  for (int ks = 0; ks < KS; ++ks) offS[ks] = T::off(fr, ks * 4 + grp);
+  int offT[DB];  // transposed operand: row 4 grp + fr / 4, columns 16 db + 4 (fr % 4)
+#pragma unroll
+  for (int db = 0; db < DB; ++db) {
+    const int col = db * 16 + (fr & 3) * 4;
+    offT[db] = T::off(grp * 4 + (fr >> 2), col >> 3) + (col & 7) * 2;
+  }
+
+  const float c = p.scale_log2;  // scores are kept raw; c folds into the exponent
   const int last_row = p.causal ? min(qt * BQ + BQ, p.N) : p.N;
   const int ntiles = (last_row + BKV - 1) / BKV;
 #pragma unroll
   for (int s = 0; s < NSTAGE - 1; ++s)
-    if (s < ntiles) issue(s);
+    if (s < ntiles) issue(s, s);
 
-  for (int jt = 0; jt < ntiles; ++jt) {
-    // Tile jt has landed once at most the copies of the later issued tiles remain.
-    const int later = min(ntiles - 1 - jt, NSTAGE - 2);
-    if (later >= 1) KL_WAIT_VMCNT(T::COPIES);
+  auto process = [&](const int jt, auto stage_tag) {
+    constexpr int STAGE = decltype(stage_tag)::value;
+    // Tile jt has landed once at most the copies of the later issued tile remain.
+    if (jt + 1 < ntiles) KL_WAIT_VMCNT(T::COPIES);
     else KL_WAIT_VMCNT(0);
     __syncthreads();
-    if (jt + NSTAGE - 1 < ntiles) issue(jt + NSTAGE - 1);
-    const lds_u8* tile = (const lds_u8*)smem + (jt % NSTAGE) * T::BYTES;
+    if (jt + NSTAGE - 1 < ntiles) issue(jt + NSTAGE - 1, (STAGE + NSTAGE - 1) % NSTAGE);
     const int j0 = jt * BKV;
     // Skip tiles entirely above the diagonal for this wave.
-    if (p.causal && j0 > q0 + 31) continue;
+    if (p.causal && j0 > q0 + 31) return;
+    const lds_u8* tile = (const lds_u8*)smem + STAGE * T::BYTES;
 
-    // S^T[kv][q] for kv blocks kb (16 rows) and query blocks qb.
-    f32x4_t s[4][2];
+    // S^T[kv][q] for kv blocks kb (16 rows) and query blocks qb, raw (unscaled).
+    f32x4_t sc[4][2];
 #pragma unroll
     for (int kb = 0; kb < 4; ++kb) {
-      s[kb][0] = s[kb][1] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
       for (int ks = 0; ks < KS; ++ks) {
         const bf16x8_t a = *reinterpret_cast<const __attribute__((address_space(3))) bf16x8_t*>(
-            tile + T::off(kb * 16 + fr, ks * 4 + grp));
-        s[kb][0] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, qf[0][ks], s[kb][0], 0, 0, 0);
-        s[kb][1] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, qf[1][ks], s[kb][1], 0, 0, 0);
+            tile + offS[ks] + kb * 16 * T::ROW);
+        if (ks == 0) {
+          sc[kb][0] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, qf[0][0], f32x4_t{0.f, 0.f, 0.f, 0.f}, 0, 0, 0);
+          sc[kb][1] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, qf[1][0], f32x4_t{0.f, 0.f, 0.f, 0.f}, 0, 0, 0);
+        } else {
+          sc[kb][0] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, qf[0][ks], sc[kb][0], 0, 0, 0);
+          sc[kb][1] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, qf[1][ks], sc[kb][1], 0, 0, 0);
+        }
       }
     }
     // Lane holds scores of query q0 + 16 qb + fr against rows j0 + 16 kb + 4 grp + r.
-    const bool need_mask = (p.causal && j0 + BKV - 1 > q0) || (j0 + BKV > p.N);
+    if ((p.causal && j0 + BKV - 1 > q0) || (j0 + BKV > p.N)) {
+#pragma unroll
+      for (int qb = 0; qb < 2; ++qb) {
+        const int q = q0 + qb * 16 + fr;
+#pragma unroll
+        for (int kb = 0; kb < 4; ++kb)
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            const int kv = j0 + kb * 16 + grp * 4 + r;
+            if (kv >= p.N || (p.causal && kv > q)) sc[kb][qb][r] = -INFINITY;
+          }
+      }
+    }
+    // Online softmax with a lazily moved reference: weights are 2^(c s - m) with
+    // m only raised when a score exceeds it by more than 2^8, which keeps every
+    // weight below 256 and skips the rescale of O on most tiles.
+    float mx[2];
 #pragma unroll
     for (int qb = 0; qb < 2; ++qb) {
-      const int q = q0 + qb * 16 + fr;
-      float mx = -INFINITY;
+      float v = -INFINITY;
 #pragma unroll
       for (int kb = 0; kb < 4; ++kb)
+        v = fmaxf(v, fmaxf(fmaxf(sc[kb][qb][0], sc[kb][qb][1]), fmaxf(sc[kb][qb][2], sc[kb][qb][3])));
+      v = fmaxf(v, __shfl_xor(v, 16));
+      v = fmaxf(v, __shfl_xor(v, 32));
+      mx[qb] = v * c;
+    }
+    const bool grow = (mx[0] > m[0] + 8.f) || (mx[1] > m[1] + 8.f);
+    if (__builtin_amdgcn_ballot_w64(grow)) {
 #pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          float x = s[kb][qb][r] * p.scale_log2;
-          if (need_mask) {
-            const int kv = j0 + kb * 16 + grp * 4 + r;
-            if (kv >= p.N || (p.causal && kv > q)) x = -INFINITY;
-          }
-          s[kb][qb][r] = x;
-          mx = fmaxf(mx, x);
-        }
-      mx = fmaxf(mx, __shfl_xor(mx, 16));
-      mx = fmaxf(mx, __shfl_xor(mx, 32));
-      const float mn = fmaxf(m[qb], mx);
-      const float ms = (mn == -INFINITY) ? 0.f : mn;
-      const float alpha = fast_exp2(m[qb] - ms);
-      m[qb] = mn;
+      for (int qb = 0; qb < 2; ++qb) {
+        const float mn = (mx[qb] > m[qb] + 8.f) ? mx[qb] : m[qb];
+        const float alpha = (m[qb] == -INFINITY) ? 0.f : fast_exp2(m[qb] - mn);
+        m[qb] = mn;
+        lsum[qb] *= alpha;
+#pragma unroll
+        for (int i = 0; i < DB; ++i) o[i][qb] *= alpha;
+      }
+    }
+    bf16x8_t pf[2][2];
+#pragma unroll
+    for (int qb = 0; qb < 2; ++qb) {
+      const float nm = (m[qb] == -INFINITY) ? 0.f : -m[qb];
       float ps = 0.f;
 #pragma unroll
       for (int kb = 0; kb < 4; ++kb)
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
-          const float w = fast_exp2(s[kb][qb][r] - ms);
-          s[kb][qb][r] = w;
+          const float w = fast_exp2(fmaf(sc[kb][qb][r], c, nm));
+          sc[kb][qb][r] = w;
           ps += w;
         }
-      lsum[qb] = lsum[qb] * alpha + ps;
-#pragma unroll
-      for (int i = 0; i < DB; ++i) o[i][qb] *= alpha;
-    }
-    // P^T fragments: k-step ks covers rows 32 ks + {4 grp .. 4 grp + 3, 16 + 4 grp ..}.
-    bf16x8_t pf[2][2];
-#pragma unroll
-    for (int qb = 0; qb < 2; ++qb)
+      lsum[qb] += ps;
+      // P^T fragments: k-step ks covers rows 32 ks + {4 grp .. 4 grp + 3, 16 + 4 grp ..}.
 #pragma unroll
       for (int ks = 0; ks < 2; ++ks) {
         u32x4 w;
-        w[0] = pack2(s[2 * ks][qb][0], s[2 * ks][qb][1]);
-        w[1] = pack2(s[2 * ks][qb][2], s[2 * ks][qb][3]);
-        w[2] = pack2(s[2 * ks + 1][qb][0], s[2 * ks + 1][qb][1]);
-        w[3] = pack2(s[2 * ks + 1][qb][2], s[2 * ks + 1][qb][3]);
+        w[0] = pack2(sc[2 * ks][qb][0], sc[2 * ks][qb][1]);
+        w[1] = pack2(sc[2 * ks][qb][2], sc[2 * ks][qb][3]);
+        w[2] = pack2(sc[2 * ks + 1][qb][0], sc[2 * ks + 1][qb][1]);
+        w[3] = pack2(sc[2 * ks + 1][qb][2], sc[2 * ks + 1][qb][3]);
         pf[qb][ks] = __builtin_bit_cast(bf16x8_t, w);
       }
-    // O^T[d][q] += V^T P^T. For column block db and step ks, lane (grp, fr = l)
-    // addresses row 32 ks + 4 grp + l / 4 (and + 16), columns 16 db + 4 (l % 4);
-    // the transposed read hands lane l the 4 rows of column 16 db + l.
+    }
+    // O^T[d][q] += V^T P^T: the transposed read hands lane fr the 4 rows of
+    // column 16 db + fr (rows 32 ks + 4 grp .., and 16 further for the high half).
 #pragma unroll
     for (int db = 0; db < DB; ++db) {
 #pragma unroll
       for (int ks = 0; ks < 2; ++ks) {
-        const int r0 = ks * 32 + grp * 4 + (fr >> 2);
-        const int col = db * 16 + (fr & 3) * 4;  // element column of this lane's 8 bytes
-        const int c16 = col >> 3, half = (col & 7) * 2;
+        const lds_u8* src = tile + offT[db] + ks * 32 * T::ROW;
         const s16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-            (__attribute__((address_space(3))) s16x4*)(tile + T::off(r0, c16) + half));
+            (__attribute__((address_space(3))) s16x4*)(src));
         const s16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-            (__attribute__((address_space(3))) s16x4*)(tile + T::off(r0 + 16, c16) + half));
-        const bf16x8_t a = __builtin_bit_cast(
-            bf16x8_t, u32x4{__builtin_bit_cast(u32x2, lo)[0], __builtin_bit_cast(u32x2, lo)[1],
-                            __builtin_bit_cast(u32x2, hi)[0], __builtin_bit_cast(u32x2, hi)[1]});
+            (__attribute__((address_space(3))) s16x4*)(src + 16 * T::ROW));
+        const bf16x8_t a = __builtin_bit_cast(bf16x8_t, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
         o[db][0] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, pf[0][ks], o[db][0], 0, 0, 0);
         o[db][1] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, pf[1][ks], o[db][1], 0, 0, 0);
       }
     }
+  };
+
+  for (int jt = 0; jt < ntiles; jt += NSTAGE) {
+    process(jt, std::integral_constant<int, 0>{});
+    if (jt + 1 < ntiles) process(jt + 1, std::integral_constant<int, 1>{});
+    if (jt + 2 < ntiles) process(jt + 2, std::integral_constant<int, 2>{});
   }
 
   // Normalise and store: lane holds O[q][16 db + 4 grp + r] for its query rows.

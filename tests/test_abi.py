@@ -109,6 +109,9 @@ def test_append_and_prefill_reject_bad_arguments(lib):
     st = lib.keyless_prefill(FAKE, FAKE, None, FAKE, 1, 16, 64, 4, 4, 64, 1, 0.0, kb.KL_BF16,
                              FAKE, None, None, FAKE, 10, None)
     expect(lib, st, kb.KL_ERR_WORKSPACE, "workspace")
+    st = lib.keyless_prefill(FAKE, FAKE, None, FAKE, 1, 16, 64, 4, 4, 64, 1, -1.0, kb.KL_BF16,
+                             FAKE, None, None, FAKE, 1 << 30, None)
+    expect(lib, st, kb.KL_ERR_INVALID_ARG, "scale")
     st = lib.keyless_fold_routing(None, FAKE, 64, 4, 64, kb.KL_BF16, FAKE, None)
     expect(lib, st, kb.KL_ERR_INVALID_ARG, "non-NULL")
 
