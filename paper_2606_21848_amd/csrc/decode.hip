@@ -58,6 +58,12 @@ __device__ __forceinline__ void slice_to_f32(const u32x4& x, float* f, float) {
   f[2] = __uint_as_float(x.z); f[3] = __uint_as_float(x.w);
 }
 
+__device__ __forceinline__ uint32_t pack_bf16_rne(float lo, float hi) {
+  typedef __attribute__((__vector_size__(2 * sizeof(__bf16)))) __bf16 b2;
+  b2 x = {(__bf16)lo, (__bf16)hi};
+  return __builtin_bit_cast(uint32_t, x);
+}
+
 template <typename T>
 __device__ __forceinline__ void store_out(void* out, size_t i, float v) {
   if constexpr (sizeof(T) == 2)
@@ -66,169 +72,132 @@ __device__ __forceinline__ void store_out(void* out, size_t i, float v) {
     reinterpret_cast<float*>(out)[i] = v;
 }
 
-__device__ __forceinline__ u32x4 load16(const void* p) {
-  return __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(p));
+typedef __attribute__((address_space(3))) unsigned char lds_u8;
+typedef __attribute__((__vector_size__(8 * sizeof(__bf16)))) __bf16 bf16x8_t;
+typedef __attribute__((__vector_size__(4 * sizeof(float)))) float f32x4_t;
+typedef short s16x4 __attribute__((ext_vector_type(4)));
+typedef unsigned int u32x2 __attribute__((ext_vector_type(2)));
+
+// Stages of the per-wave LDS ring: as many as fit in 64 KiB per 4-wave
+// workgroup (two per CU) or 96 KiB per 8-wave one, at least 2 and at most 4.
+constexpr int stage_count(int stage_bytes, int waves) {
+  const int n = (waves >= 8 ? 98304 : 65536) / (stage_bytes * waves);
+  return n < 2 ? 2 : (n > 4 ? 4 : n);
 }
 
-template <typename T, int D, int R, bool PAGED, bool KEYS, int NW>
-__global__ __launch_bounds__(NW * 64) void decode_partial_kernel(DecodeParams p) {
-  constexpr int E = Elem<T>::E;
-  constexpr int LPR = D / E;     // lanes per cache row
-  constexpr int RPL = 64 / LPR;  // rows per wave-wide load
-  constexpr int U = kTile / RPL; // loads per tile
-  static_assert(RPL * U == kTile, "tile shape");
+// Shape of the per-wave staging ring: NBUF stages of one 16-row tile (V, then
+// K when present), each moved by NI direct-to-LDS copy instructions of 1 KiB.
+template <typename T, int D, bool KEYS, int NW>
+struct Ring {
+  static constexpr int ROWB = D * (int)sizeof(T);  // bytes per cache row
+  static constexpr int TB = kTile * ROWB;          // bytes per tile
+  static constexpr int NI = TB / 1024;             // copy instructions per tile
+  static constexpr int KV = KEYS ? 2 : 1;
+  static constexpr int SB = TB * KV;               // bytes per stage
+  static constexpr int NBUF = stage_count(SB, NW);
+  static constexpr int PER_TILE = NI * KV;         // copies per tile
+  static constexpr int BYTES = NBUF * SB * NW;     // whole workgroup
+};
 
-  const int s = blockIdx.x, g = blockIdx.y, b = blockIdx.z;
-  const int lane = threadIdx.x & 63;
-  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-  const int cap = PAGED ? (p.max_blocks << p.block_shift) : p.L_max;
-  const int len = min(max(p.lengths[b], 0), cap);
-  const int start = s * p.chunk;
-  const size_t bh0 = (size_t)b * p.H + g * R;  // first query head of this group
-  if (start >= len) {  // uniform over the workgroup
-    if (s == 0 && p.S == 1) {  // empty cache: zero output rows (the merge does this when S > 1)
-      for (int i = threadIdx.x; i < R * D; i += NW * 64) store_out<T>(p.out, bh0 * D + i, 0.f);
-    }
-    return;
+// Streams the tiles of rows [t_first + j * step, +16) for j = 0, 1, ... below
+// `end` through this wave's LDS ring and hands each landed tile to
+// consume(stage, t0, blk_ok). Copy instruction i of a tile moves its bytes
+// [1024 i, 1024 i + 1024): lane L lands at byte 1024 i + 16 L, i.e. row rr,
+// slot sl, and fetches logical chunk sl ^ swz(rr) of that row, so the consumer
+// finds chunk c of row rr at slot c ^ swz(rr). Rows past `end` are clamped to
+// the last row; a block id outside the cache reads block 0 and is reported as
+// blk_ok = false. `ready` runs once after the first copies are issued.
+template <typename T, int D, bool PAGED, bool KEYS, int NW, class Swz, class Ready, class Consume>
+__device__ __forceinline__ void stream_tiles(const DecodeParams& p, int b, int g, int lane,
+                                             lds_u8* ring, int t_first, int end, Swz swz,
+                                             Ready ready, Consume consume) {
+  using RS = Ring<T, D, KEYS, NW>;
+  constexpr int ROWB = RS::ROWB, TB = RS::TB, NI = RS::NI, SB = RS::SB, NBUF = RS::NBUF;
+  constexpr int PER_TILE = RS::PER_TILE;
+  const int step = NW * kTile;
+  const int ntiles = (t_first < end) ? (end - t_first + step - 1) / step : 0;  // uniform
+  if (ntiles == 0) return;
+  const uint32_t ring_addr = (uint32_t)(uintptr_t)ring;
+
+  int cp_row[NI];       // tile row this lane copies, per instruction
+  uint32_t cp_col[NI];  // byte offset of the fetched chunk within the row
+#pragma unroll
+  for (int i = 0; i < NI; ++i) {
+    const int pos = i * 1024 + 16 * lane;
+    cp_row[i] = pos / ROWB;
+    cp_col[i] = (uint32_t)((((pos % ROWB) / 16) ^ swz(pos / ROWB)) * 16);
   }
-  const int end = min(start + p.chunk, len);
-
-  const int rslot = lane / LPR;        // which row of a load this lane reads
-  const int col = (lane % LPR) * E;    // first element of this lane's slice
-
-  const T* __restrict__ qp = reinterpret_cast<const T*>(p.q);
-  u32x4 qv[R];
-#pragma unroll
-  for (int r = 0; r < R; ++r)
-    qv[r] = *reinterpret_cast<const u32x4*>(qp + ((bh0 + r) * D + col));
-
-  float m[R], l[R], acc[R][E];
-#pragma unroll
-  for (int r = 0; r < R; ++r) {
-    m[r] = -INFINITY;
-    l[r] = 0.f;
-#pragma unroll
-    for (int e = 0; e < E; ++e) acc[r][e] = 0.f;
-  }
-
-  const T* __restrict__ vbase = reinterpret_cast<const T*>(p.vdata);
-  const T* __restrict__ kbase = reinterpret_cast<const T*>(p.kdata);
+  const unsigned char* __restrict__ vbytes = reinterpret_cast<const unsigned char*>(p.vdata);
+  const unsigned char* __restrict__ kbytes = reinterpret_cast<const unsigned char*>(p.kdata);
   const int bs_mask = (1 << p.block_shift) - 1;
-
-  // Tile loader: this lane's U rows of the 16-row tile starting at row t0. Rows
-  // past `end` (or in a block outside the cache) are clamped for the load and
-  // flagged invalid; `full` says every row is valid.
-  auto load_tile = [&](int t0, u32x4* v, u32x4* k, bool* valid, bool& full) {
-    bool blk_ok = true;
-    size_t tile_base;
-    if constexpr (PAGED) {
-      // The tile lies inside one block: t0 is a multiple of 16 and so is the block size.
-      const int blk = p.table[(size_t)b * p.max_blocks + (t0 >> p.block_shift)];
-      blk_ok = (blk >= 0) && (blk < p.num_blocks);
-      tile_base = ((size_t)(blk_ok ? blk : 0) * p.G + g) << p.block_shift;
-    } else {
-      tile_base = (size_t)(b * p.G + g) * p.L_max;
-    }
-    full = blk_ok && (t0 + kTile <= end);
+  // The table is read through the constant address space so the uniform
+  // lookups stay scalar loads (the copies' memory clobbers would otherwise turn
+  // them into vector loads whose waits drain the copy pipeline).
+  const __attribute__((address_space(4))) int* table =
+      (const __attribute__((address_space(4))) int*)p.table;
+  auto block_of = [&](int t) -> int {
+    if constexpr (PAGED) return table[(size_t)b * p.max_blocks + (t >> p.block_shift)];
+    return 0;
+  };
+  auto block_ok = [&](int blk) { return !PAGED || (blk >= 0 && blk < p.num_blocks); };
+  auto issue = [&](int j, int blk) {
+    const int t = t_first + j * step;
+    size_t row0;
+    if constexpr (PAGED)  // the tile lies inside one block (both are multiples of 16 rows)
+      row0 = (((size_t)(block_ok(blk) ? blk : 0) * p.G + g) << p.block_shift) + (t & bs_mask);
+    else
+      row0 = (size_t)(b * p.G + g) * p.L_max + t;
+    const int last = end - 1 - t;
+    const uint32_t st = ring_addr + (uint32_t)((j % NBUF) * SB);
 #pragma unroll
-    for (int u = 0; u < U; ++u) {
-      int tok = t0 + u * RPL + rslot;
-      valid[u] = blk_ok && (tok < end);
-      if (!full) tok = min(tok, end - 1);
-      const int in_blk = PAGED ? (tok & bs_mask) : tok;
-      const size_t off = (tile_base + in_blk) * D + col;
-      v[u] = load16(vbase + off);
-      if constexpr (KEYS) k[u] = load16(kbase + off);
+    for (int i = 0; i < NI; ++i) {
+      const uint32_t off = (uint32_t)(min(cp_row[i], last) * ROWB) + cp_col[i];
+      copy_to_lds_nt(vbytes + row0 * ROWB, off, st + i * 1024);
+      if constexpr (KEYS) copy_to_lds_nt(kbytes + row0 * ROWB, off, st + TB + i * 1024);
     }
   };
 
-  // Two tiles in flight per wave: the next tile's loads are issued before the
-  // current tile is consumed.
-  u32x4 v[U], k[U], vn[U], kn[U];
-  bool valid[U], validn[U];
-  bool full = true, fulln = true;
-  int t0 = start + wave * kTile;
-  if (t0 < end) load_tile(t0, v, k, valid, full);
-  for (; t0 < end; t0 += NW * kTile) {
-    const int t1 = t0 + NW * kTile;
-    if (t1 < end) load_tile(t1, vn, kn, validn, fulln);
-    if (!full) {
+  int bq[NBUF];  // block ids of tiles j .. j + NBUF - 1 (constant indices: scalar registers)
 #pragma unroll
-      for (int u = 0; u < U; ++u)
-        if (!valid[u]) v[u] = u32x4{0u, 0u, 0u, 0u};  // padding may hold NaN
-    }
-    float vf[U][E];
+  for (int i = 0; i < NBUF; ++i) bq[i] = 0;
 #pragma unroll
-    for (int u = 0; u < U; ++u) slice_to_f32(v[u], vf[u], T());
-
-#pragma unroll
-    for (int r = 0; r < R; ++r) {
-      float sc[U];
-      float mt = m[r];
-#pragma unroll
-      for (int u = 0; u < U; ++u) {
-        const float part = slice_dot(qv[r], KEYS ? k[u] : v[u], T());
-        float x = group_sum<LPR>(part) * p.scale_log2;
-        if (!full && !valid[u]) x = -INFINITY;
-        sc[u] = x;
-        mt = fmaxf(mt, x);
-      }
-      const float ms = (mt == -INFINITY) ? 0.f : mt;
-      const float alpha = fast_exp2(m[r] - ms);
-      float lsum = l[r] * alpha;
-#pragma unroll
-      for (int e = 0; e < E; ++e) acc[r][e] *= alpha;
-#pragma unroll
-      for (int u = 0; u < U; ++u) {
-        const float w = fast_exp2(sc[u] - ms);
-        lsum += w;
-#pragma unroll
-        for (int e = 0; e < E; ++e) acc[r][e] = fmaf(w, vf[u][e], acc[r][e]);
-      }
-      l[r] = lsum;
-      m[r] = mt;
-    }
-#pragma unroll
-    for (int u = 0; u < U; ++u) {
-      v[u] = vn[u];
-      if constexpr (KEYS) k[u] = kn[u];
-      valid[u] = validn[u];
-    }
-    full = fulln;
-  }
-
-  // Merge the RPL row slots of the wave (lanes LPR apart), then the waves.
-#pragma unroll
-  for (int sh = LPR; sh < 64; sh <<= 1) {
-#pragma unroll
-    for (int r = 0; r < R; ++r) {
-      const float m2 = __shfl_xor(m[r], sh);
-      const float l2 = __shfl_xor(l[r], sh);
-      float f1, f2, mm;
-      merge_scale(m[r], m2, f1, f2, mm);
-      l[r] = l[r] * f1 + l2 * f2;
-#pragma unroll
-      for (int e = 0; e < E; ++e) {
-        const float a2 = __shfl_xor(acc[r][e], sh);
-        acc[r][e] = acc[r][e] * f1 + a2 * f2;
-      }
-      m[r] = mm;
+  for (int i = 0; i < NBUF - 1; ++i) {
+    if (i < ntiles) {
+      bq[i] = block_of(t_first + i * step);
+      issue(i, bq[i]);
     }
   }
-
-  __shared__ float s_acc[NW][R][D];
-  __shared__ float s_ml[NW][R][2];
-  if (lane < LPR) {
-#pragma unroll
-    for (int r = 0; r < R; ++r) {
-#pragma unroll
-      for (int e = 0; e < E; ++e) s_acc[wave][r][col + e] = acc[r][e];
-      if (lane == 0) {
-        s_ml[wave][r][0] = m[r];
-        s_ml[wave][r][1] = l[r];
-      }
+  ready();
+  // Tiles j+1 .. j+NBUF-1 stay in flight while tile j is consumed. The wait
+  // before tile j allows only the copies issued after it to be outstanding;
+  // the vector memory counter retires in issue order, so tile j has landed.
+  for (int j = 0; j < ntiles; ++j) {
+    const int jn = j + NBUF - 1;
+    const int ahead = min(NBUF - 1, ntiles - 1 - j);  // tiles issued after tile j
+    if (jn < ntiles) {
+      // The stage being refilled was consumed in the previous iteration: its
+      // LDS reads have completed before the copies may overwrite it.
+      asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+      bq[NBUF - 1] = block_of(t_first + jn * step);
+      issue(jn, bq[NBUF - 1]);
     }
+    switch (ahead) {
+      case 0: asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); break;
+      case 1: asm volatile("s_waitcnt vmcnt(%0)" ::"n"(PER_TILE) : "memory"); break;
+      case 2: asm volatile("s_waitcnt vmcnt(%0)" ::"n"(2 * PER_TILE) : "memory"); break;
+      default: asm volatile("s_waitcnt vmcnt(%0)" ::"n"(3 * PER_TILE) : "memory"); break;
+    }
+    consume(ring + (j % NBUF) * SB, t_first + j * step, block_ok(bq[0]));
+#pragma unroll
+    for (int i = 0; i < NBUF - 1; ++i) bq[i] = bq[i + 1];
   }
+}
+
+// Merge the per-wave states (acc[R][D], m, l in LDS) of the workgroup and
+// store either the normalised output rows (one split) or the split partials.
+template <typename T, int D, int R, int NW>
+__device__ __forceinline__ void merge_waves(const DecodeParams& p, const float (*s_acc)[R][D],
+                                            const float (*s_ml)[R][2], size_t bh0, int s) {
   __syncthreads();
   for (int i = threadIdx.x; i < R * (D + 2); i += NW * 64) {
     const int r = i / (D + 2);
@@ -254,6 +223,360 @@ __global__ __launch_bounds__(NW * 64) void decode_partial_kernel(DecodeParams p)
       p.part[((bh0 + r) * p.S + s) * (D + 2) + c] = val;
     }
   }
+}
+
+// Work item of a workgroup: split s of (sequence b, value group g). Returns
+// false (after writing zero rows where this is the only split) when the split
+// holds no cached rows.
+template <typename T, int D, int R, bool PAGED, int NW>
+__device__ __forceinline__ bool work_item(const DecodeParams& p, int& start, int& end,
+                                          size_t& bh0) {
+  const int s = blockIdx.x, g = blockIdx.y, b = blockIdx.z;
+  const int cap = PAGED ? (p.max_blocks << p.block_shift) : p.L_max;
+  const int len = min(max(p.lengths[b], 0), cap);
+  start = s * p.chunk;
+  bh0 = (size_t)b * p.H + g * R;  // first query head of this group
+  if (start >= len) {  // uniform over the workgroup
+    if (s == 0 && p.S == 1) {  // empty cache: zero output rows (the merge does this when S > 1)
+      for (int i = threadIdx.x; i < R * D; i += NW * 64) store_out<T>(p.out, bh0 * D + i, 0.f);
+    }
+    return false;
+  }
+  end = min(start + p.chunk, len);
+  return true;
+}
+
+// Vector-ALU consumer. A lane group of LPR lanes holds one cache row per
+// 16-byte chunk, so one wave-wide LDS read covers RPL rows and a tile is U
+// reads. The tile is used twice: for the scores s = <q~, v> (dot products
+// reduced over the lane group with DPP) and for acc += 2^(s - m) v.
+template <typename T, int D, int R, bool PAGED, bool KEYS, int NW>
+__global__ __launch_bounds__(NW * 64) void decode_partial_kernel(DecodeParams p) {
+  constexpr int EC = Elem<T>::E;  // elements per 16-byte chunk
+  constexpr int NC = D / EC;      // chunks per cache row
+  constexpr int LPR = NC;         // lanes per cache row
+  constexpr int RPL = 64 / LPR;   // rows per wave-wide read
+  constexpr int U = kTile / RPL;  // rows per lane per tile
+  constexpr int E = EC;           // elements per lane per row
+  static_assert(RPL * U == kTile, "tile shape");
+  using RS = Ring<T, D, KEYS, NW>;
+  constexpr int ROWB = RS::ROWB, TB = RS::TB, NBUF = RS::NBUF, SB = RS::SB;
+  // Grouped heads over a bf16 cache take the lazy-reference / bf16-dot path.
+  constexpr bool kGroupedBf16 = (R >= 2) && (sizeof(T) == 2) && (U % 2 == 0);
+  constexpr float kLazy = 8.f;  // log2 headroom before the reference moves
+
+  int start, end;
+  size_t bh0;
+  if (!work_item<T, D, R, PAGED, NW>(p, start, end, bh0)) return;
+  const int g = blockIdx.y, b = blockIdx.z;
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int rslot = lane / LPR;  // which row of a read this lane takes
+  const int lc = lane % LPR;     // this lane's chunk
+
+  const T* __restrict__ qp = reinterpret_cast<const T*>(p.q);
+  u32x4 qv[R];
+#pragma unroll
+  for (int r = 0; r < R; ++r) qv[r] = *reinterpret_cast<const u32x4*>(qp + ((bh0 + r) * D + lc * EC));
+
+  float m[R], l[R], acc[R][E];
+#pragma unroll
+  for (int r = 0; r < R; ++r) {
+    m[r] = -INFINITY;
+    l[r] = 0.f;
+#pragma unroll
+    for (int e = 0; e < E; ++e) acc[r][e] = 0.f;
+  }
+
+  extern __shared__ __attribute__((aligned(1024))) unsigned char dyn_lds[];
+  lds_u8* const ring = (lds_u8*)dyn_lds + wave * (NBUF * SB);
+  auto swz = [](int) { return 0; };  // one row per 16-lane pass: no conflicts
+  // Take the query loads' wait once, outside the tile loop.
+  auto ready = [&]() {
+#pragma unroll
+    for (int r = 0; r < R; ++r) asm volatile("" ::"v"(qv[r]));
+  };
+
+  auto consume = [&](const lds_u8* stage, int t0, bool blk_ok) {
+    const bool full = blk_ok && (t0 + kTile <= end);
+    u32x4 v[U], k[U];
+    bool valid[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int rr = u * RPL + rslot;
+      valid[u] = blk_ok && (t0 + rr < end);
+      const int off = rr * ROWB + lc * 16;
+      v[u] = *reinterpret_cast<const __attribute__((address_space(3))) u32x4*>(stage + off);
+      if constexpr (KEYS)
+        k[u] = *reinterpret_cast<const __attribute__((address_space(3))) u32x4*>(stage + TB + off);
+    }
+    if (!full) {
+#pragma unroll
+      for (int u = 0; u < U; ++u)
+        if (!valid[u]) v[u] = u32x4{0u, 0u, 0u, 0u};  // clamped rows, or a block outside the cache
+    }
+    // Scores: dot products over the lane's elements, summed over the LPR lanes
+    // of the row (DPP), scaled to log2 units; invalid rows get -inf.
+    float sc[R][U];
+#pragma unroll
+    for (int r = 0; r < R; ++r)
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        float x = group_sum<LPR>(slice_dot(qv[r], KEYS ? k[u] : v[u], T())) * p.scale_log2;
+        if (!full && !valid[u]) x = -INFINITY;
+        sc[r][u] = x;
+      }
+    if constexpr (kGroupedBf16) {
+      // A lazily moved reference exponent per head (raised only when a score
+      // exceeds it by 2^8, so the rescale of acc is rare and weights stay below
+      // 256), and the weighted sum as bf16 dot products over row pairs:
+      // (w_u0, w_u1) . (v_u0[e], v_u1[e]).
+      float tmax[R];
+      bool grow = false;
+#pragma unroll
+      for (int r = 0; r < R; ++r) {
+        tmax[r] = sc[r][0];
+#pragma unroll
+        for (int u = 1; u < U; ++u) tmax[r] = fmaxf(tmax[r], sc[r][u]);
+        grow |= tmax[r] > m[r] + kLazy;
+      }
+      if (__builtin_amdgcn_ballot_w64(grow)) {
+#pragma unroll
+        for (int r = 0; r < R; ++r) {
+          const float mn = (tmax[r] > m[r] + kLazy) ? tmax[r] : m[r];
+          const float alpha = (m[r] == -INFINITY) ? 0.f : fast_exp2(m[r] - mn);
+          l[r] *= alpha;
+#pragma unroll
+          for (int e = 0; e < E; ++e) acc[r][e] *= alpha;
+          m[r] = mn;
+        }
+      }
+      uint32_t lo[U / 2][4], hi[U / 2][4];
+#pragma unroll
+      for (int pr = 0; pr < U / 2; ++pr)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          lo[pr][j] = __builtin_amdgcn_perm(v[2 * pr + 1][j], v[2 * pr][j], 0x05040100u);
+          hi[pr][j] = __builtin_amdgcn_perm(v[2 * pr + 1][j], v[2 * pr][j], 0x07060302u);
+        }
+#pragma unroll
+      for (int r = 0; r < R; ++r) {
+        const float nm = (m[r] == -INFINITY) ? 0.f : -m[r];
+        float w[U];
+        float ls = 0.f;
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+          w[u] = fast_exp2(sc[r][u] + nm);
+          ls += w[u];
+        }
+        l[r] += ls;
+#pragma unroll
+        for (int pr = 0; pr < U / 2; ++pr) {
+          const uint32_t wp = pack_bf16_rne(w[2 * pr], w[2 * pr + 1]);
+#pragma unroll
+          for (int j = 0; j < 4; ++j) {
+            acc[r][2 * j] = dot2_bf16(wp, lo[pr][j], acc[r][2 * j]);
+            acc[r][2 * j + 1] = dot2_bf16(wp, hi[pr][j], acc[r][2 * j + 1]);
+          }
+        }
+      }
+    } else {
+      float vf[U][E];
+#pragma unroll
+      for (int u = 0; u < U; ++u) slice_to_f32(v[u], vf[u], T());
+#pragma unroll
+      for (int r = 0; r < R; ++r) {
+        float mt = m[r];
+#pragma unroll
+        for (int u = 0; u < U; ++u) mt = fmaxf(mt, sc[r][u]);
+        const float ms = (mt == -INFINITY) ? 0.f : mt;
+        const float alpha = fast_exp2(m[r] - ms);
+        float lsum = l[r] * alpha;
+#pragma unroll
+        for (int e = 0; e < E; ++e) acc[r][e] *= alpha;
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+          const float w = fast_exp2(sc[r][u] - ms);
+          lsum += w;
+#pragma unroll
+          for (int e = 0; e < E; ++e) acc[r][e] = fmaf(w, vf[u][e], acc[r][e]);
+        }
+        l[r] = lsum;
+        m[r] = mt;
+      }
+    }
+  };
+
+  stream_tiles<T, D, PAGED, KEYS, NW>(p, b, g, lane, ring, start + wave * kTile, end, swz, ready,
+                                      consume);
+
+  // Merge the RPL row slots of the wave (lanes LPR apart), then the waves.
+#pragma unroll
+  for (int sh = LPR; sh < 64; sh <<= 1) {
+#pragma unroll
+    for (int r = 0; r < R; ++r) {
+      const float m2 = __shfl_xor(m[r], sh);
+      const float l2 = __shfl_xor(l[r], sh);
+      float f1, f2, mm;
+      merge_scale(m[r], m2, f1, f2, mm);
+      l[r] = l[r] * f1 + l2 * f2;
+#pragma unroll
+      for (int e = 0; e < E; ++e) {
+        const float a2 = __shfl_xor(acc[r][e], sh);
+        acc[r][e] = acc[r][e] * f1 + a2 * f2;
+      }
+      m[r] = mm;
+    }
+  }
+  __shared__ float s_acc[NW][R][D];
+  __shared__ float s_ml[NW][R][2];
+  if (lane < LPR) {
+#pragma unroll
+    for (int r = 0; r < R; ++r) {
+#pragma unroll
+      for (int j = 0; j < EC; ++j) s_acc[wave][r][lc * EC + j] = acc[r][j];
+      if (lane == 0) {
+        s_ml[wave][r][0] = m[r];
+        s_ml[wave][r][1] = l[r];
+      }
+    }
+  }
+  merge_waves<T, D, R, NW>(p, s_acc, s_ml, bh0, blockIdx.x);
+}
+
+// Matrix-core consumer for grouped heads over a 128-wide bf16 cache (R >= 2).
+// Per 16-row tile, with the R heads of the group as the N = 16 columns (the
+// rest zero):
+//   scores   S[row][h]  = sum_d V[row][d] q~[h][d]       4 x MFMA 16x16x32,
+//   weights  P[row][h]  = 2^(S - m_h)  (lazy reference m_h, as above),
+//   output   O^T[d][h] += sum_row V^T[d][row] P[row][h]  8 x MFMA 16x16x16.
+// The score result already has the layout of the second product's B operand
+// (lane l: rows 4 (l/16) + i, head l % 16), and V^T comes from transposing LDS
+// reads of the same staged tile, so every value row is still read from HBM
+// once. Tile rows are XOR-swizzled by f(r) = ((r & 7) << 1) | (r >> 3) over
+// the 16 chunks of a row: the score reads (16 rows, one chunk) and the
+// transposing reads (8 rows, two chunks per pass) hit disjoint banks.
+template <int R, bool PAGED, bool KEYS, int NW>
+__global__ __launch_bounds__(NW * 64) void decode_mfma_kernel(DecodeParams p) {
+  using T = uint16_t;
+  constexpr int D = 128;
+  using RS = Ring<T, D, KEYS, NW>;
+  constexpr int TB = RS::TB, NBUF = RS::NBUF, SB = RS::SB;
+  constexpr float kLazy = 8.f;
+  static_assert(R >= 2 && R <= 16, "heads per group");
+
+  int start, end;
+  size_t bh0;
+  if (!work_item<T, D, R, PAGED, NW>(p, start, end, bh0)) return;
+  const int g = blockIdx.y, b = blockIdx.z;
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int grp = lane >> 4;  // lane group: rows 4 grp .. 4 grp + 3 of a score tile
+  const int hl = lane & 15;   // head (column) of this lane in the score / output tiles
+  auto fsw = [](int r) { return ((r & 7) << 1) | ((r >> 3) & 1); };
+
+  // Score B operand: q~[h][32 kk + 8 grp .. +7] for h = hl < R, zero otherwise.
+  bf16x8_t qf[4];
+  const T* __restrict__ qp = reinterpret_cast<const T*>(p.q);
+#pragma unroll
+  for (int kk = 0; kk < 4; ++kk) {
+    u32x4 x = u32x4{0u, 0u, 0u, 0u};
+    if (hl < R) x = *reinterpret_cast<const u32x4*>(qp + ((bh0 + hl) * D + 32 * kk + 8 * grp));
+    qf[kk] = __builtin_bit_cast(bf16x8_t, x);
+  }
+  // LDS byte offsets within a stage. Score A operand: row hl, chunk 4 kk + grp.
+  uint32_t offS[4];
+#pragma unroll
+  for (int kk = 0; kk < 4; ++kk) offS[kk] = hl * 256 + (((4 * kk + grp) ^ fsw(hl)) << 4);
+  // Transposing reads for O^T: lane (grp, i = hl) supplies row 4 grp + i / 4,
+  // columns 16 dd + 4 (i % 4) .. +3 (chunk 2 dd + (i % 4) / 2, half i % 2).
+  uint32_t offT[8];
+  {
+    const int row = 4 * grp + (hl >> 2);
+#pragma unroll
+    for (int dd = 0; dd < 8; ++dd)
+      offT[dd] = row * 256 + (((2 * dd + ((hl & 3) >> 1)) ^ fsw(row)) << 4) + ((hl & 1) << 3);
+  }
+
+  float m = -INFINITY, lsum = 0.f;
+  f32x4_t acc[8];
+#pragma unroll
+  for (int dd = 0; dd < 8; ++dd) acc[dd] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+
+  extern __shared__ __attribute__((aligned(1024))) unsigned char dyn_lds[];
+  lds_u8* const ring = (lds_u8*)dyn_lds + wave * (NBUF * SB);
+  auto ready = [&]() {
+#pragma unroll
+    for (int kk = 0; kk < 4; ++kk) asm volatile("" ::"v"(qf[kk]));
+  };
+
+  auto consume = [&](const lds_u8* stage, int t0, bool blk_ok) {
+    if (!blk_ok) return;  // uniform: a block outside the cache contributes nothing
+    const lds_u8* ks = KEYS ? stage + TB : stage;
+    f32x4_t sc = f32x4_t{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int kk = 0; kk < 4; ++kk) {
+      const bf16x8_t a =
+          *reinterpret_cast<const __attribute__((address_space(3))) bf16x8_t*>(ks + offS[kk]);
+      sc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, qf[kk], sc, 0, 0, 0);
+    }
+    float s4[4];
+    float tmax = -INFINITY;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      float x = sc[i] * p.scale_log2;
+      if (t0 + 4 * grp + i >= end) x = -INFINITY;
+      s4[i] = x;
+      tmax = fmaxf(tmax, x);
+    }
+    if (__builtin_amdgcn_ballot_w64(tmax > m + kLazy)) {
+      // New reference for each head: the tile maximum over its four lane
+      // groups, so the reference stays identical across them.
+      float tm = fmaxf(tmax, __shfl_xor(tmax, 16));
+      tm = fmaxf(tm, __shfl_xor(tm, 32));
+      const float mn = (tm > m + kLazy) ? tm : m;
+      const float alpha = (m == -INFINITY) ? 0.f : fast_exp2(m - mn);
+      lsum *= alpha;
+#pragma unroll
+      for (int dd = 0; dd < 8; ++dd) acc[dd] *= alpha;
+      m = mn;
+    }
+    const float nm = (m == -INFINITY) ? 0.f : -m;
+    float w[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      w[i] = fast_exp2(s4[i] + nm);
+      lsum += w[i];
+    }
+    const s16x4 pf = __builtin_bit_cast(
+        s16x4, u32x2{pack_bf16_rne(w[0], w[1]), pack_bf16_rne(w[2], w[3])});
+#pragma unroll
+    for (int dd = 0; dd < 8; ++dd) {
+      const s16x4 a = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+          (__attribute__((address_space(3))) s16x4*)(stage + offT[dd]));
+      acc[dd] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(a, pf, acc[dd], 0, 0, 0);
+    }
+  };
+
+  stream_tiles<T, D, PAGED, KEYS, NW>(p, b, g, lane, ring, start + wave * kTile, end, fsw, ready,
+                                      consume);
+
+  // Row sums of each head over the four lane groups (the reference is shared).
+  lsum += __shfl_xor(lsum, 16);
+  lsum += __shfl_xor(lsum, 32);
+  __shared__ float s_acc[NW][R][D];
+  __shared__ float s_ml[NW][R][2];
+  if (hl < R) {
+#pragma unroll
+    for (int dd = 0; dd < 8; ++dd)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) s_acc[wave][hl][16 * dd + 4 * grp + i] = acc[dd][i];
+    if (grp == 0) {
+      s_ml[wave][hl][0] = m;
+      s_ml[wave][hl][1] = lsum;
+    }
+  }
+  merge_waves<T, D, R, NW>(p, s_acc, s_ml, bh0, blockIdx.x);
 }
 
 // Merge the splits of one (b, h): weights 2^(m_s - M) / L per split, then the
@@ -314,8 +637,25 @@ hipError_t launch_t(const DecodeParams& p, hipStream_t st) {
     hipError_t e = hipEventRecord(p.ev_start, st);
     if (e != hipSuccess) return e;
   }
-  hipLaunchKernelGGL((decode_partial_kernel<T, D, R, PAGED, KEYS, NW>), grid, dim3(NW * 64), 0,
-                     st, p);
+  // Grouped heads over a 128-wide bf16 cache run on the matrix cores.
+  constexpr bool kMfma = sizeof(T) == 2 && D == 128 && R >= 2;
+  constexpr int lds = Ring<T, D, KEYS, NW>::BYTES;
+  static_assert(lds + NW * R * (D + 2) * 4 <= 160 * 1024, "LDS budget");
+  const void* kern;
+  if constexpr (kMfma)
+    kern = reinterpret_cast<const void*>(decode_mfma_kernel<R, PAGED, KEYS, NW>);
+  else
+    kern = reinterpret_cast<const void*>(decode_partial_kernel<T, D, R, PAGED, KEYS, NW>);
+  if (lds > 65536) {
+    static std::atomic<uint32_t> done{0};
+    hipError_t a = set_max_lds(kern, lds, done);
+    if (a != hipSuccess) return a;
+  }
+  if constexpr (kMfma)
+    hipLaunchKernelGGL((decode_mfma_kernel<R, PAGED, KEYS, NW>), grid, dim3(NW * 64), lds, st, p);
+  else
+    hipLaunchKernelGGL((decode_partial_kernel<T, D, R, PAGED, KEYS, NW>), grid, dim3(NW * 64), lds,
+                       st, p);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   if (p.ev_stop) {
@@ -333,7 +673,10 @@ template <typename T, int D, int R, bool PAGED, bool KEYS>
 hipError_t pick_waves(const DecodeParams& p, hipStream_t st) {
   switch (p.waves) {
     case 4: return launch_t<T, D, R, PAGED, KEYS, 4>(p, st);
-    case 8: return launch_t<T, D, R, PAGED, KEYS, 8>(p, st);
+    case 8:
+      // Fall back to 4 waves where an 8-wave ring would not fit in LDS.
+      if constexpr (Ring<T, D, KEYS, 8>::BYTES > 98304) return launch_t<T, D, R, PAGED, KEYS, 4>(p, st);
+      else return launch_t<T, D, R, PAGED, KEYS, 8>(p, st);
     default: return hipErrorInvalidValue;
   }
 }

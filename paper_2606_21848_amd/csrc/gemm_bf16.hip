@@ -226,12 +226,10 @@ constexpr size_t kGemmLds = 4 * TILE_BYTES;
 hipError_t launch_gemm_bf16_packed(const void* A, int M, int K, long lda, const void* Wp, int N,
                                    int n_split, void* C0, long ldc0, void* C1, long ldc1,
                                    hipStream_t st) {
-  static bool attr_set = false;
-  if (!attr_set) {
-    hipError_t e = hipFuncSetAttribute((const void*)gemm_bf16_kernel,
-                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)kGemmLds);
+  static std::atomic<uint32_t> attr_done{0};
+  {
+    hipError_t e = set_max_lds((const void*)gemm_bf16_kernel, (int)kGemmLds, attr_done);
     if (e != hipSuccess) return e;
-    attr_set = true;
   }
   GemmParams2 p{};
   p.A = static_cast<const uint16_t*>(A);

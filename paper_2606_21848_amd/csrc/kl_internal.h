@@ -4,11 +4,26 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <atomic>
+
 #include "keyless.h"
 
 namespace kl {
 
 constexpr int kMaxSplits = 1024;
+
+// Raise a kernel's dynamic-LDS limit to `bytes`, once per device (devices
+// 0..31 are remembered in `done`; others set it on every call).
+inline hipError_t set_max_lds(const void* fn, int bytes, std::atomic<uint32_t>& done) {
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  const uint32_t bit = (dev >= 0 && dev < 32) ? (1u << dev) : 0u;
+  if (bit && (done.load(std::memory_order_acquire) & bit)) return hipSuccess;
+  e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, bytes);
+  if (e == hipSuccess && bit) done.fetch_or(bit, std::memory_order_release);
+  return e;
+}
 
 struct DecodeParams {
   const void* q;          // [B, H, D]
