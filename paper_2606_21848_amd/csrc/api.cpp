@@ -85,34 +85,41 @@ int cache_capacity(const kl_value_cache* c) {
   return c->layout == KL_PAGED ? c->max_blocks_per_seq * c->block_size : c->L_max;
 }
 
-// Work split of a decode call. With at least one (b, g) pair per compute unit
-// and a contiguous cache, one wide workgroup (8 waves) per pair streams the
-// whole cache and writes the output directly. Otherwise the cache length is
-// split so the grid holds several workgroups per compute unit, with at least
-// 256 rows per split so each wave walks several tiles, and a merge kernel
-// combines the splits.
+// Work split of a decode call.
+//  - chunk_rows > 0: split mode with that many rows per split (grid S x G x B).
+//  - A contiguous cache with at least one (b, g) pair per compute unit: one
+//    workgroup per pair streams its whole cache and writes the output directly.
+//  - Otherwise balanced mode: kBalancedWorkgroups workgroups (two per compute
+//    unit) take equal shares of the 16-row tiles of all pairs, whatever the
+//    spread of lengths, and a merge kernel combines pairs that were shared.
+//    Used while the tile count fits comfortably in 32 bits; beyond that the
+//    cache is split into chunks of 8192 rows.
 struct DecodePlan {
   int chunk, S, waves;
+  bool balanced;
 };
 
 constexpr int kComputeUnits = 256;
+constexpr int kBalancedWorkgroups = 2 * kComputeUnits;
 
 DecodePlan plan_decode(const kl_value_cache* c, int B, int chunk_rows) {
-  const int cap = c->layout == KL_PAGED ? c->max_blocks_per_seq * c->block_size : c->L_max;
+  const int cap = cache_capacity(c);
   const long pairs = (long)B * c->G;
   DecodePlan pl{};
+  pl.waves = 4;
   if (chunk_rows > 0) {
     pl.chunk = chunk_rows;
   } else if (c->layout == KL_CONTIGUOUS && pairs >= kComputeUnits) {
     pl.chunk = ((cap > 0 ? cap : 1) + 63) / 64 * 64;
+  } else if (pairs * ((long)cap + 15) / 16 < (1L << 30)) {
+    pl.balanced = true;
+    pl.chunk = 0;
+    pl.S = 0;
+    return pl;
   } else {
-    const long want = (pairs * cap + 2047) / 2048;
-    long ch = 256;
-    while (ch < want && ch < 8192) ch <<= 1;
-    pl.chunk = (int)ch;
+    pl.chunk = 8192;
   }
   pl.S = cap > 0 ? (cap + pl.chunk - 1) / pl.chunk : 1;
-  pl.waves = pl.S == 1 ? 8 : 4;
   if (const char* w = getenv("KL_DECODE_WAVES")) {
     const int v = atoi(w);
     if (v == 4 || v == 8) pl.waves = v;
@@ -120,9 +127,15 @@ DecodePlan plan_decode(const kl_value_cache* c, int B, int chunk_rows) {
   return pl;
 }
 
-// Split partials (acc[d], m, l) per (b, h, split); none with a single split.
-size_t partials_bytes(int B, int H, int d_head, int S) {
-  return S > 1 ? align256((size_t)B * H * S * (d_head + 2) * sizeof(float)) : 0;
+// Workspace: split partials (acc[d], m, l) per (b, h, split), none with a
+// single split; in balanced mode the plan (B + 3 ints) and then one partial row
+// per head for each of B * G + kBalancedWorkgroups segment slots.
+size_t plan_bytes(int B) { return align256((size_t)(B + 3) * sizeof(int)); }
+size_t partials_bytes(const DecodePlan& pl, int B, int H, int G, int d_head) {
+  if (pl.balanced)
+    return plan_bytes(B) + align256(((size_t)B * G + kBalancedWorkgroups) * (H / G) *
+                                    (d_head + 2) * sizeof(float));
+  return pl.S > 1 ? align256((size_t)B * H * pl.S * (d_head + 2) * sizeof(float)) : 0;
 }
 
 int decode_common(const void* q, const kl_value_cache* k_cache, const kl_value_cache* v_cache,
@@ -156,7 +169,7 @@ int decode_common(const void* q, const kl_value_cache* k_cache, const kl_value_c
   if (pl.S > kl::kMaxSplits)
     return fail(KL_ERR_UNSUPPORTED, "%s: %d splits exceed the maximum of %d (use larger chunks)",
                 who, pl.S, kl::kMaxSplits);
-  const size_t need = partials_bytes(B, H, v_cache->d_head, pl.S);
+  const size_t need = partials_bytes(pl, B, H, G, v_cache->d_head);
   if (need && (!ws || ws_bytes < need))
     return fail(KL_ERR_WORKSPACE, "%s: workspace of %zu bytes needed, %zu given", who, need, ws_bytes);
   if (need && !aligned16(ws))
@@ -169,7 +182,14 @@ int decode_common(const void* q, const kl_value_cache* k_cache, const kl_value_c
   p.table = v_cache->layout == KL_PAGED ? v_cache->block_table : nullptr;
   p.lengths = lengths;
   p.out = out;
-  p.part = static_cast<float*>(ws);
+  p.balanced = pl.balanced;
+  p.nwg = kBalancedWorkgroups;
+  if (pl.balanced) {
+    p.plan = static_cast<int*>(ws);
+    p.part = reinterpret_cast<float*>(static_cast<char*>(ws) + plan_bytes(B));
+  } else {
+    p.part = static_cast<float*>(ws);
+  }
   p.B = B;
   p.H = H;
   p.G = G;
@@ -207,7 +227,7 @@ void keyless_set_kernel_timer(void* start_event, void* stop_event) {
 size_t keyless_decode_workspace_size(const kl_value_cache* cache, int B, int H, int chunk_rows) {
   if (!cache || B <= 0 || H <= 0 || cache->G <= 0 || chunk_rows < 0) return 0;
   const DecodePlan pl = plan_decode(cache, B, chunk_rows);
-  return partials_bytes(B, H, cache->d_head, pl.S);
+  return partials_bytes(pl, B, H, cache->G, cache->d_head);
 }
 
 int keyless_decode(const void* q_routed, const kl_value_cache* cache, const int32_t* lengths,

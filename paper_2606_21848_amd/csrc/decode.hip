@@ -193,11 +193,19 @@ __device__ __forceinline__ void stream_tiles(const DecodeParams& p, int b, int g
   }
 }
 
+// Where a finished segment goes: the normalised output rows of its heads
+// (part == nullptr), or one partial row (acc[D], m, l) per head, `stride`
+// floats apart.
+struct SegOut {
+  float* part;
+  int stride;
+};
+
 // Merge the per-wave states (acc[R][D], m, l in LDS) of the workgroup and
-// store either the normalised output rows (one split) or the split partials.
+// store them to `o`. Ends with a barrier, so the LDS can be refilled.
 template <typename T, int D, int R, int NW>
 __device__ __forceinline__ void merge_waves(const DecodeParams& p, const float (*s_acc)[R][D],
-                                            const float (*s_ml)[R][2], size_t bh0, int s) {
+                                            const float (*s_ml)[R][2], size_t bh0, SegOut o) {
   __syncthreads();
   for (int i = threadIdx.x; i < R * (D + 2); i += NW * 64) {
     const int r = i / (D + 2);
@@ -217,33 +225,86 @@ __device__ __forceinline__ void merge_waves(const DecodeParams& p, const float (
     } else {
       val = (c == D) ? mm : lsum;
     }
-    if (p.S == 1) {
+    if (o.part == nullptr) {
       if (c < D) store_out<T>(p.out, (bh0 + r) * D + c, lsum > 0.f ? val / lsum : 0.f);
     } else {
-      p.part[((bh0 + r) * p.S + s) * (D + 2) + c] = val;
+      o.part[(size_t)r * o.stride + c] = val;
     }
   }
+  __syncthreads();
 }
 
-// Work item of a workgroup: split s of (sequence b, value group g). Returns
-// false (after writing zero rows where this is the only split) when the split
-// holds no cached rows.
-template <typename T, int D, int R, bool PAGED, int NW>
-__device__ __forceinline__ bool work_item(const DecodeParams& p, int& start, int& end,
-                                          size_t& bh0) {
-  const int s = blockIdx.x, g = blockIdx.y, b = blockIdx.z;
+// Cached rows of sequence b, clamped to the cache capacity.
+template <bool PAGED>
+__device__ __forceinline__ int seq_len(const DecodeParams& p, int b) {
   const int cap = PAGED ? (p.max_blocks << p.block_shift) : p.L_max;
-  const int len = min(max(p.lengths[b], 0), cap);
-  start = s * p.chunk;
-  bh0 = (size_t)b * p.H + g * R;  // first query head of this group
-  if (start >= len) {  // uniform over the workgroup
-    if (s == 0 && p.S == 1) {  // empty cache: zero output rows (the merge does this when S > 1)
-      for (int i = threadIdx.x; i < R * D; i += NW * 64) store_out<T>(p.out, bh0 * D + i, 0.f);
+  return min(max(p.lengths[b], 0), cap);
+}
+
+// Runs seg(b, g, row_begin, row_end, out) for every segment this workgroup owns.
+//
+// Split mode: the grid is (S, G, B) and workgroup (s, g, b) owns rows
+// [s chunk, (s+1) chunk) of pair (b, g); with one split it stores the output
+// rows, otherwise partial s of each head.
+//
+// Balanced mode: the 16-row tiles of all pairs, pair (b, g) after (b, g-1) and
+// sequence b after b-1, form one sequence of T tiles, and workgroup w owns
+// tiles [w per, (w+1) per) with per = ceil(T / workgroups), which may cross
+// pairs. A pair that lies inside one workgroup stores its output rows;
+// otherwise each workgroup on it stores a partial at index pair + w, which is
+// unique (along the tile sequence both the pair and the workgroup index are
+// non-decreasing and at least one grows from one segment to the next).
+template <typename T, int D, int R, bool PAGED, int NW, class Seg>
+__device__ __forceinline__ void for_each_segment(const DecodeParams& p, Seg seg) {
+  if (!p.balanced) {
+    const int s = blockIdx.x, g = blockIdx.y, b = blockIdx.z;
+    const int len = seq_len<PAGED>(p, b);
+    const int start = s * p.chunk;
+    const size_t bh0 = (size_t)b * p.H + g * R;
+    if (start >= len) {  // uniform over the workgroup
+      if (s == 0 && p.S == 1) {  // empty cache: zero output rows (the merge does this when S > 1)
+        for (int i = threadIdx.x; i < R * D; i += NW * 64) store_out<T>(p.out, bh0 * D + i, 0.f);
+      }
+      return;
     }
-    return false;
+    const SegOut o = p.S == 1 ? SegOut{nullptr, 0}
+                              : SegOut{p.part + (bh0 * p.S + s) * (D + 2), p.S * (D + 2)};
+    seg(b, g, start, min(start + p.chunk, len), o);
+    return;
   }
-  end = min(start + p.chunk, len);
-  return true;
+  const int* __restrict__ plan = p.plan;
+  const int total = plan[0], per = plan[1];
+  const int* __restrict__ pre = plan + 2;  // exclusive prefix sums of tiles per sequence, [B + 1]
+  const int w = blockIdx.x;
+  int t = w * per;
+  const int t_end = min(total, t + per);
+  if (t >= t_end) return;
+  // Sequence holding tile t: the last b with G * pre[b] <= t (empty sequences
+  // share their start with the next one and are skipped by taking the last).
+  int lo = 0, hi = p.B - 1;
+  while (lo < hi) {
+    const int mid = (lo + hi + 1) >> 1;
+    if (p.G * pre[mid] <= t) lo = mid; else hi = mid - 1;
+  }
+  int b = lo;
+  while (t < t_end) {
+    const int n = pre[b + 1] - pre[b];  // tiles per pair of sequence b (> 0 here)
+    const int base = p.G * pre[b];
+    const int g = (t - base) / n;
+    const int tp = base + g * n;  // first tile of pair (b, g)
+    const int seg_end = min(t_end, tp + n);
+    const int len = seq_len<PAGED>(p, b);
+    const bool whole = (tp / per) == ((tp + n - 1) / per);
+    const int pair = b * p.G + g;
+    const SegOut o = whole ? SegOut{nullptr, 0}
+                           : SegOut{p.part + (size_t)(pair + w) * R * (D + 2), D + 2};
+    seg(b, g, (t - tp) * kTile, min((seg_end - tp) * kTile, len), o);
+    t = seg_end;
+    if (t >= base + p.G * n) {  // past the last pair of b: next non-empty sequence
+      ++b;
+      while (b < p.B && pre[b + 1] == pre[b]) ++b;
+    }
+  }
 }
 
 // Vector-ALU consumer. A lane group of LPR lanes holds one cache row per
@@ -265,15 +326,17 @@ __global__ __launch_bounds__(NW * 64) void decode_partial_kernel(DecodeParams p)
   constexpr bool kGroupedBf16 = (R >= 2) && (sizeof(T) == 2) && (U % 2 == 0);
   constexpr float kLazy = 8.f;  // log2 headroom before the reference moves
 
-  int start, end;
-  size_t bh0;
-  if (!work_item<T, D, R, PAGED, NW>(p, start, end, bh0)) return;
-  const int g = blockIdx.y, b = blockIdx.z;
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int rslot = lane / LPR;  // which row of a read this lane takes
   const int lc = lane % LPR;     // this lane's chunk
+  extern __shared__ __attribute__((aligned(1024))) unsigned char dyn_lds[];
+  lds_u8* const ring = (lds_u8*)dyn_lds + wave * (NBUF * SB);
+  __shared__ float s_acc[NW][R][D];
+  __shared__ float s_ml[NW][R][2];
 
+  auto segment = [&](int b, int g, int start, int end, SegOut so) {
+  const size_t bh0 = (size_t)b * p.H + g * R;
   const T* __restrict__ qp = reinterpret_cast<const T*>(p.q);
   u32x4 qv[R];
 #pragma unroll
@@ -288,8 +351,6 @@ __global__ __launch_bounds__(NW * 64) void decode_partial_kernel(DecodeParams p)
     for (int e = 0; e < E; ++e) acc[r][e] = 0.f;
   }
 
-  extern __shared__ __attribute__((aligned(1024))) unsigned char dyn_lds[];
-  lds_u8* const ring = (lds_u8*)dyn_lds + wave * (NBUF * SB);
   auto swz = [](int) { return 0; };  // one row per 16-lane pass: no conflicts
   // Take the query loads' wait once, outside the tile loop.
   auto ready = [&]() {
@@ -428,8 +489,6 @@ __global__ __launch_bounds__(NW * 64) void decode_partial_kernel(DecodeParams p)
       m[r] = mm;
     }
   }
-  __shared__ float s_acc[NW][R][D];
-  __shared__ float s_ml[NW][R][2];
   if (lane < LPR) {
 #pragma unroll
     for (int r = 0; r < R; ++r) {
@@ -441,7 +500,9 @@ __global__ __launch_bounds__(NW * 64) void decode_partial_kernel(DecodeParams p)
       }
     }
   }
-  merge_waves<T, D, R, NW>(p, s_acc, s_ml, bh0, blockIdx.x);
+  merge_waves<T, D, R, NW>(p, s_acc, s_ml, bh0, so);
+  };
+  for_each_segment<T, D, R, PAGED, NW>(p, segment);
 }
 
 // Matrix-core consumer for grouped heads over a 128-wide bf16 cache (R >= 2).
@@ -465,25 +526,16 @@ __global__ __launch_bounds__(NW * 64) void decode_mfma_kernel(DecodeParams p) {
   constexpr float kLazy = 8.f;
   static_assert(R >= 2 && R <= 16, "heads per group");
 
-  int start, end;
-  size_t bh0;
-  if (!work_item<T, D, R, PAGED, NW>(p, start, end, bh0)) return;
-  const int g = blockIdx.y, b = blockIdx.z;
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int grp = lane >> 4;  // lane group: rows 4 grp .. 4 grp + 3 of a score tile
   const int hl = lane & 15;   // head (column) of this lane in the score / output tiles
   auto fsw = [](int r) { return ((r & 7) << 1) | ((r >> 3) & 1); };
+  extern __shared__ __attribute__((aligned(1024))) unsigned char dyn_lds[];
+  lds_u8* const ring = (lds_u8*)dyn_lds + wave * (NBUF * SB);
+  __shared__ float s_acc[NW][R][D];
+  __shared__ float s_ml[NW][R][2];
 
-  // Score B operand: q~[h][32 kk + 8 grp .. +7] for h = hl < R, zero otherwise.
-  bf16x8_t qf[4];
-  const T* __restrict__ qp = reinterpret_cast<const T*>(p.q);
-#pragma unroll
-  for (int kk = 0; kk < 4; ++kk) {
-    u32x4 x = u32x4{0u, 0u, 0u, 0u};
-    if (hl < R) x = *reinterpret_cast<const u32x4*>(qp + ((bh0 + hl) * D + 32 * kk + 8 * grp));
-    qf[kk] = __builtin_bit_cast(bf16x8_t, x);
-  }
   // LDS byte offsets within a stage. Score A operand: row hl, chunk 4 kk + grp.
   uint32_t offS[4];
 #pragma unroll
@@ -498,13 +550,23 @@ __global__ __launch_bounds__(NW * 64) void decode_mfma_kernel(DecodeParams p) {
       offT[dd] = row * 256 + (((2 * dd + ((hl & 3) >> 1)) ^ fsw(row)) << 4) + ((hl & 1) << 3);
   }
 
+  auto segment = [&](int b, int g, int start, int end, SegOut so) {
+  const size_t bh0 = (size_t)b * p.H + g * R;
+
+  // Score B operand: q~[h][32 kk + 8 grp .. +7] for h = hl < R, zero otherwise.
+  bf16x8_t qf[4];
+  const T* __restrict__ qp = reinterpret_cast<const T*>(p.q);
+#pragma unroll
+  for (int kk = 0; kk < 4; ++kk) {
+    u32x4 x = u32x4{0u, 0u, 0u, 0u};
+    if (hl < R) x = *reinterpret_cast<const u32x4*>(qp + ((bh0 + hl) * D + 32 * kk + 8 * grp));
+    qf[kk] = __builtin_bit_cast(bf16x8_t, x);
+  }
   float m = -INFINITY, lsum = 0.f;
   f32x4_t acc[8];
 #pragma unroll
   for (int dd = 0; dd < 8; ++dd) acc[dd] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 
-  extern __shared__ __attribute__((aligned(1024))) unsigned char dyn_lds[];
-  lds_u8* const ring = (lds_u8*)dyn_lds + wave * (NBUF * SB);
   auto ready = [&]() {
 #pragma unroll
     for (int kk = 0; kk < 4; ++kk) asm volatile("" ::"v"(qf[kk]));
@@ -564,8 +626,6 @@ __global__ __launch_bounds__(NW * 64) void decode_mfma_kernel(DecodeParams p) {
   // Row sums of each head over the four lane groups (the reference is shared).
   lsum += __shfl_xor(lsum, 16);
   lsum += __shfl_xor(lsum, 32);
-  __shared__ float s_acc[NW][R][D];
-  __shared__ float s_ml[NW][R][2];
   if (hl < R) {
 #pragma unroll
     for (int dd = 0; dd < 8; ++dd)
@@ -576,7 +636,46 @@ __global__ __launch_bounds__(NW * 64) void decode_mfma_kernel(DecodeParams p) {
       s_ml[wave][hl][1] = lsum;
     }
   }
-  merge_waves<T, D, R, NW>(p, s_acc, s_ml, bh0, blockIdx.x);
+  merge_waves<T, D, R, NW>(p, s_acc, s_ml, bh0, so);
+  };
+  for_each_segment<T, D, R, PAGED, NW>(p, segment);
+}
+
+// Balanced-mode plan: tiles per sequence n_b = ceil(len_b / 16), their
+// exclusive prefix sums pre[0..B], the total T = G pre[B] over all pairs and
+// the tiles per workgroup ceil(T / nwg). One workgroup scans the sequences in
+// blocks of 1024.
+__global__ __launch_bounds__(1024) void decode_plan_kernel(DecodeParams p) {
+  __shared__ int s_scan[1024];
+  __shared__ int s_carry;
+  const int t = threadIdx.x;
+  int* pre = p.plan + 2;
+  const int cap = p.paged ? (p.max_blocks << p.block_shift) : p.L_max;
+  if (t == 0) s_carry = 0;
+  __syncthreads();
+  for (int b0 = 0; b0 < p.B; b0 += 1024) {
+    const int b = b0 + t;
+    const int n = b < p.B ? (min(max(p.lengths[b], 0), cap) + kTile - 1) / kTile : 0;
+    s_scan[t] = n;
+    __syncthreads();
+    for (int off = 1; off < 1024; off <<= 1) {
+      const int v = t >= off ? s_scan[t - off] : 0;
+      __syncthreads();
+      s_scan[t] += v;
+      __syncthreads();
+    }
+    const int carry = s_carry;
+    if (b < p.B) pre[b] = carry + s_scan[t] - n;
+    __syncthreads();
+    if (t == 1023) s_carry = carry + s_scan[1023];
+    __syncthreads();
+  }
+  if (t == 0) {
+    const int total = p.G * s_carry;  // the host bounds this below 2^30
+    pre[p.B] = s_carry;
+    p.plan[0] = total;
+    p.plan[1] = total > 0 ? (total + p.nwg - 1) / p.nwg : 1;
+  }
 }
 
 // Merge the splits of one (b, h): weights 2^(m_s - M) / L per split, then the
@@ -592,14 +691,33 @@ __global__ __launch_bounds__(256) void decode_combine_kernel(DecodeParams p) {
   const int t = threadIdx.x;
   const int cap = p.paged ? (p.max_blocks << p.block_shift) : p.L_max;
   const int len = min(max(p.lengths[b], 0), cap);
-  const int ns = (len + p.chunk - 1) / p.chunk;
-  const float* __restrict__ part = p.part + (size_t)bh * p.S * (D + 2);
+  int ns;                      // partials of this head
+  const float* part;           // its first partial row
+  size_t stride = D + 2;       // floats between consecutive partial rows
+  if (!p.balanced) {
+    ns = (len + p.chunk - 1) / p.chunk;
+    part = p.part + (size_t)bh * p.S * (D + 2);
+  } else {
+    // The workgroups that covered pair (b, g) wrote partials pair + w for w in
+    // [first, last]; a pair inside one workgroup was stored directly.
+    const int* pre = p.plan + 2;
+    const int per = p.plan[1];
+    const int n = pre[b + 1] - pre[b];
+    const int h = bh % p.H, g = h / p.R, r = h % p.R;
+    const int tp = p.G * pre[b] + g * n;
+    const int first = n > 0 ? tp / per : 0;
+    const int last = n > 0 ? (tp + n - 1) / per : -1;
+    if (n > 0 && first == last) return;
+    ns = last - first + 1;
+    part = p.part + ((size_t)(b * p.G + g + first) * p.R + r) * (D + 2);
+    stride = (size_t)p.R * (D + 2);
+  }
   if (ns == 0) {
     if (t < D) store_out<T>(p.out, (size_t)bh * D + t, 0.f);
     return;
   }
   float mloc = -INFINITY;
-  for (int k = t; k < ns; k += 256) mloc = fmaxf(mloc, part[k * (D + 2) + D]);
+  for (int k = t; k < ns; k += 256) mloc = fmaxf(mloc, part[k * stride + D]);
   for (int sh = 32; sh > 0; sh >>= 1) mloc = fmaxf(mloc, __shfl_xor(mloc, sh));
   if ((t & 63) == 0) s_red[t >> 6] = mloc;
   __syncthreads();
@@ -608,9 +726,9 @@ __global__ __launch_bounds__(256) void decode_combine_kernel(DecodeParams p) {
   __syncthreads();
   float lloc = 0.f;
   for (int k = t; k < ns; k += 256) {
-    const float w = fast_exp2(part[k * (D + 2) + D] - Ms);
+    const float w = fast_exp2(part[k * stride + D] - Ms);
     s_w[k] = w;
-    lloc = fmaf(part[k * (D + 2) + D + 1], w, lloc);
+    lloc = fmaf(part[k * stride + D + 1], w, lloc);
   }
   for (int sh = 32; sh > 0; sh >>= 1) lloc += __shfl_xor(lloc, sh);
   if ((t & 63) == 0) s_red[t >> 6] = lloc;
@@ -619,7 +737,7 @@ __global__ __launch_bounds__(256) void decode_combine_kernel(DecodeParams p) {
   const int c = t % D, sub = t / D;
   float a = 0.f;
 #pragma unroll 4
-  for (int k = sub; k < ns; k += SUB) a = fmaf(part[k * (D + 2) + c], s_w[k], a);
+  for (int k = sub; k < ns; k += SUB) a = fmaf(part[k * stride + c], s_w[k], a);
   s_acc[sub][c] = a;
   __syncthreads();
   if (t < D) {
@@ -632,7 +750,12 @@ __global__ __launch_bounds__(256) void decode_combine_kernel(DecodeParams p) {
 
 template <typename T, int D, int R, bool PAGED, bool KEYS, int NW>
 hipError_t launch_t(const DecodeParams& p, hipStream_t st) {
-  dim3 grid(p.S, p.G, p.B);
+  const dim3 grid = p.balanced ? dim3(p.nwg) : dim3(p.S, p.G, p.B);
+  if (p.balanced) {
+    hipLaunchKernelGGL(decode_plan_kernel, dim3(1), dim3(1024), 0, st, p);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
   if (p.ev_start) {
     hipError_t e = hipEventRecord(p.ev_start, st);
     if (e != hipSuccess) return e;
@@ -662,7 +785,7 @@ hipError_t launch_t(const DecodeParams& p, hipStream_t st) {
     e = hipEventRecord(p.ev_stop, st);
     if (e != hipSuccess) return e;
   }
-  if (p.S > 1) {
+  if (p.balanced || p.S > 1) {
     hipLaunchKernelGGL((decode_combine_kernel<T, D>), dim3(p.B * p.H), dim3(256), 0, st, p);
     e = hipGetLastError();
   }
@@ -703,7 +826,8 @@ hipError_t pick_r(const DecodeParams& p, hipStream_t st) {
 }  // namespace
 
 hipError_t launch_decode(const DecodeParams& p, hipStream_t st) {
-  if (p.S > kMaxSplits) return hipErrorInvalidValue;
+  if (!p.balanced && p.S > kMaxSplits) return hipErrorInvalidValue;
+  if (p.balanced && (p.nwg < 1 || p.nwg > kMaxSplits || p.plan == nullptr)) return hipErrorInvalidValue;
   if (p.dtype == KL_BF16) {
     if (p.D == 128) return pick_r<uint16_t, 128>(p, st);
     if (p.D == 64) return pick_r<uint16_t, 64>(p, st);

@@ -32,7 +32,9 @@ struct DecodeParams {
   const int32_t* table;   // paged block table or nullptr
   const int32_t* lengths; // [B]
   void* out;              // [B, H, D]
-  float* part;            // [B * H, S, D + 2] split partials (S > 1 only)
+  float* part;            // split partials: [B * H, S, D + 2] (split mode, S > 1) or
+                          // [B * G + nwg, R, D + 2] (balanced mode)
+  int* plan;              // balanced mode: [total tiles, tiles per workgroup, prefix[B + 1]]
   int B, H, G, D, R;
   kl_dtype dtype;
   bool paged;
@@ -42,6 +44,8 @@ struct DecodeParams {
   int chunk;              // rows per split (multiple of 64)
   int S;                  // splits per sequence (at most kMaxSplits)
   int waves;              // waves per workgroup of the split kernel: 4 or 8
+  bool balanced;          // balanced mode: nwg workgroups share the tiles of all pairs evenly
+  int nwg;                // workgroups in balanced mode (at most kMaxSplits)
   float scale_log2;       // scale * log2(e)
   hipEvent_t ev_start;    // optional: recorded around the split kernel
   hipEvent_t ev_stop;

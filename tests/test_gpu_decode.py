@@ -118,6 +118,30 @@ def test_grouped_equals_mha_over_repeated_values(lib):
     assert_parity(mha, ref, torch.bfloat16, "repeated")
 
 
+@pytest.mark.parametrize("H,G,d,dtype", [(4, 2, 128, torch.bfloat16), (2, 2, 128, torch.bfloat16),
+                                         (4, 4, 64, torch.float32)])
+def test_balanced_mode_ragged_and_empty(lib, H, G, d, dtype):
+    """Balanced mode (paged cache, library choice): the workgroups' equal tile
+    shares cut pairs at arbitrary tiles, one long pair spans ~150 workgroups,
+    a three-tile pair spans two, and empty sequences sit first, inside and last."""
+    lengths = torch.tensor([0, 5000, 0, 37, 1, 0], dtype=torch.int32)
+    B, L = len(lengths), 5008
+    say(f"balanced H={H} G={G} d={d} dtype={dtype}")
+    cache = synth.normal((B, G, L, d), 16, 1, 1.0, dtype)
+    q = synth.normal((B, H, d), 16, 2, 1.0, dtype)
+    data, table = _paged(cache, lengths, 16, 6)
+    vc = kb.ValueCache(data.to(DEV), table.to(DEV))
+    ref = K.keyless_decode(to64(q), to64(data), lengths.numpy(), H, G,
+                           block_table=table.numpy(), block_size=16)
+    # The workspace starts as NaN bytes and is reused: nothing may depend on its contents.
+    ws = torch.full((kb.decode_workspace_bytes(vc, B, H),), 0xFF, dtype=torch.uint8, device=DEV)
+    for rep in range(2):
+        out = kb.keyless_decode(q.to(DEV), vc, lengths.to(DEV), workspace=ws)
+        torch.cuda.synchronize()
+        assert_parity(out, ref, dtype, f"balanced call {rep}")
+        assert torch.all(out.cpu()[lengths == 0] == 0)
+
+
 def test_lengths_beyond_capacity_are_clamped(lib):
     B, G, H, L, d = 2, 2, 2, 100, 64
     say("length clamp")
