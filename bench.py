@@ -53,6 +53,11 @@ def parse():
                     help="target length of the CPU oracle sample")
     ap.add_argument("--profile-pass", action="store_true",
                     help="run a 1 GiB copy (counter calibration) and a few steps, print nothing else")
+    ap.add_argument("--reduce-counters", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
+                    help="reduce two rocprofv3 --pmc runs of --profile-pass (FETCH_SIZE, then "
+                         "WRITE_SIZE) to the traffic summary JSON, printed to stdout")
+    ap.add_argument("--summarize-trace", metavar="TRACE_DIR",
+                    help="print a markdown summary of a rocprofv3 --kernel-trace run of this script")
     return ap.parse_args()
 
 
@@ -70,9 +75,25 @@ def timed_steps(step, steps, warmup, torch):
     return t0.elapsed_time(t1) / steps
 
 
+def batch_avg_ms(launch, n, torch):
+    """Average time per launch of n back-to-back launches on the current stream,
+    between two HIP events recorded on that stream."""
+    launch(0)
+    torch.cuda.synchronize()
+    a = torch.cuda.Event(enable_timing=True)
+    b = torch.cuda.Event(enable_timing=True)
+    a.record()
+    for i in range(n):
+        launch(i)
+    b.record()
+    torch.cuda.synchronize()
+    return a.elapsed_time(b) / n
+
+
 def kernel_avg_ms(step, steps, torch, kb):
     """Average duration of the decode split kernel alone, from HIP events that the
-    library records around it on the launch stream."""
+    library records around each launch on the launch stream (used when a call
+    runs more than one kernel)."""
     evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
            for _ in range(steps)]
     for a, b in evs:  # create the underlying events
@@ -128,8 +149,83 @@ def traffic_from_profile(per_launch_rows):
     return prof.get("traffic_bytes_per_launch")
 
 
+CALIB_BYTES = 1 << 30         # fp32 elements read, and written, by the calibration kernel
+DECODE_KERNEL = "decode_partial_kernel"
+DECODE_GRID = 8 * 32 * 256   # work-items of the split kernel on the decode_bf16 workload
+
+
+def _csv_rows(root, suffix):
+    import csv
+    import glob
+    rows = []
+    for f in sorted(glob.glob(os.path.join(root, "**", "*" + suffix), recursive=True)):
+        with open(f, newline="") as fh:
+            rows.extend(csv.DictReader(fh))
+    if not rows:
+        raise SystemExit(f"no *{suffix} under {root}")
+    return rows
+
+
+def _grid(row):
+    return int(row.get("Grid_Size", 0) or 0) or (
+        int(row.get("Grid_Size_X", 1)) * int(row.get("Grid_Size_Y", 1)) *
+        int(row.get("Grid_Size_Z", 1)))
+
+
+def reduce_counters(fetch_dir, write_dir):
+    """Per-launch HBM traffic of the decode split kernel from FETCH_SIZE and
+    WRITE_SIZE (KiB per dispatch), each scaled by what the same counter reads for
+    an elementwise kernel (neg) that reads and writes CALIB_BYTES."""
+    out = {"source_hash": source_hash(DECODE_SOURCES), "kernel": DECODE_KERNEL,
+           "decode_grid_workitems": DECODE_GRID, "calibration_bytes": CALIB_BYTES}
+    for counter, root in (("FETCH_SIZE", fetch_dir), ("WRITE_SIZE", write_dir)):
+        rows = [r for r in _csv_rows(root, "counter_collection.csv")
+                if r.get("Counter_Name") == counter]
+        dec = [float(r["Counter_Value"]) for r in rows
+               if DECODE_KERNEL in r["Kernel_Name"] and _grid(r) == DECODE_GRID]
+        cal = [float(r["Counter_Value"]) for r in rows if "neg" in r["Kernel_Name"]]
+        if not dec or not cal:
+            raise SystemExit(f"{counter}: decode dispatches {len(dec)}, calibration {len(cal)}")
+        factor = max(cal) * 1024 / CALIB_BYTES
+        key = counter.lower()
+        out[f"{key}_kib_per_launch"] = round(sum(dec) / len(dec), 1)
+        out[f"{key}_calibration_kib"] = round(max(cal), 1)
+        out[f"{key}_factor"] = round(factor, 4)
+        out[f"{key}_bytes_per_launch"] = round(sum(dec) / len(dec) * 1024 / factor)
+        out[f"{key}_dispatches"] = len(dec)
+    out["traffic_bytes_per_launch"] = out["fetch_size_bytes_per_launch"] + \
+        out["write_size_bytes_per_launch"]
+    print(json.dumps(out, indent=1))
+
+
+def summarize_trace(trace_dir):
+    """Markdown table of kernel durations from a rocprofv3 --kernel-trace run:
+    per kernel name and grid, launches and average / min / max microseconds."""
+    rows = _csv_rows(trace_dir, "kernel_trace.csv")
+    groups = {}
+    for r in rows:
+        name = r["Kernel_Name"]
+        if "kl::" not in name:  # this library's kernels only (not the input generation)
+            continue
+        short = name.replace("void ", "").replace("(anonymous namespace)::", "")
+        short = short[:short.rfind("(")] if "(" in short else short
+        dur = (int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3
+        groups.setdefault((short, _grid(r)), []).append(dur)
+    print("| kernel | grid (work-items) | launches | avg us | min us | max us |")
+    print("|---|---|---|---|---|---|")
+    for (name, grid), d in sorted(groups.items(), key=lambda kv: -sum(kv[1])):
+        print(f"| `{name}` | {grid} | {len(d)} | {sum(d) / len(d):.2f} | {min(d):.2f} | "
+              f"{max(d):.2f} |")
+
+
 def main():
     args = parse()
+    if args.reduce_counters:
+        reduce_counters(*args.reduce_counters)
+        return
+    if args.summarize_trace:
+        summarize_trace(args.summarize_trace)
+        return
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only (got --gpus {args.gpus}); "
               "multi-GPU runs are not part of this build", file=sys.stderr)
@@ -143,9 +239,9 @@ def main():
     torch.cuda.set_device(dev)
 
     if args.profile_pass:
-        src = torch.empty(1 << 30, dtype=torch.uint8, device=dev)
+        src = torch.zeros(CALIB_BYTES // 4, dtype=torch.float32, device=dev)
         dst = torch.empty_like(src)
-        dst.copy_(src)
+        torch.neg(src, out=dst)
         torch.cuda.synchronize()
         del src, dst
 
@@ -170,7 +266,17 @@ def main():
         return
 
     ms = timed_steps(step, args.steps, args.warmup, torch)
-    k_ms = kernel_avg_ms(step, args.steps, torch, kb)
+
+    def decode_only(i):
+        kb.keyless_decode(q, caches[i % len(caches)], lengths, out=out, workspace=ws,
+                          chunk_rows=args.chunk)
+    if ws.numel() == 0:  # one kernel per call (no merge): time the calls back to back
+        k_ms = batch_avg_ms(decode_only, args.steps, torch)
+        k_how = "HIP events around back-to-back decode calls (one kernel each), average"
+    else:
+        k_ms = kernel_avg_ms(step, args.steps, torch, kb)
+        k_how = "HIP events recorded by the library around each split-kernel launch, average"
+    call_ms = batch_avg_ms(decode_only, args.steps, torch)
     cache_bytes = B * H * L * d * 2
     q_bytes = B * H * d * 2
     step_bytes = cache_bytes + 2 * q_bytes + 2 * B * H * d * 2  # + out, + appended rows (r+w)
@@ -194,11 +300,13 @@ def main():
                    "batch": B, "heads": H, "cache_rows": L, "d_head": d,
                    "cache_copies_rotated": len(caches)},
         "step_hbm_gbps": round(step_bytes / (ms * 1e-3) / 1e9, 1),
+        "decode_call": {"ms": round(call_ms, 5), "tokens_per_s": round(B / (call_ms * 1e-3), 1),
+                        "note": "keyless_decode alone (no append), back to back"},
         "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBPS,
                      "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBPS, 4),
                      "traffic": traffic_from_profile(B * H * L),
-                     "kernel": "decode_partial_kernel (split kernel)",
-                     "kernel_avg_us": round(k_ms * 1e3, 2),
+                     "kernel": "decode_partial_kernel<bf16, 128, R=1, contiguous> (one split)",
+                     "kernel_avg_us": round(k_ms * 1e3, 2), "kernel_timing": k_how,
                      "algorithmic_bytes_per_launch": cache_bytes + q_bytes},
     }
     del caches, c

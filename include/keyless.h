@@ -158,21 +158,31 @@ int keyless_prefill_packed(const void* x, const void* packed, int B, int N, int 
  *   ws       at least keyless_decode_workspace_size(...) bytes (may be 0, then
  *            ws may be NULL). Calls that run at the same time must not share it.
  * Each cached value tile is read from HBM once and used both for the scores
- * and for the weighted sum. When the cache length is split, a second kernel
- * merges the splits of each (b, h) in split order, so results are
- * reproducible.
+ * and for the weighted sum. Work split (the built-in choice): a contiguous
+ * cache with at least 256 (b, group) pairs gets one workgroup per pair and no
+ * merge; otherwise a fixed set of 512 workgroups shares the 16-row tiles of
+ * all pairs evenly (a plan kernel prefix-sums the lengths on the device), and
+ * a merge kernel combines the pairs that several workgroups shared, always in
+ * the same order, so results are reproducible for fixed inputs. The workspace
+ * contents need not be initialised and are not preserved.
  */
 int keyless_decode(const void* q_routed, const kl_value_cache* cache, const int32_t* lengths,
                    int B, int H, float scale, void* out, void* ws, size_t ws_bytes, void* stream);
 
-/* As keyless_decode, with the number of cache rows per split fixed by the
- * caller (a multiple of 64; 0 selects the built-in choice). A chunk at least
- * as long as the capacity gives one split and no merge kernel. At most 1024
- * splits per sequence. */
+/* As keyless_decode, with the cache length split into chunks of chunk_rows
+ * rows fixed by the caller (a multiple of 64; 0 selects the built-in choice):
+ * one workgroup per (b, group, chunk), then a merge of the chunks of each
+ * (b, h) in chunk order. A chunk at least as long as the capacity gives one
+ * split and no merge kernel. At most 1024 splits per sequence. */
 int keyless_decode_chunked(const void* q_routed, const kl_value_cache* cache,
                            const int32_t* lengths, int B, int H, float scale, void* out,
                            void* ws, size_t ws_bytes, int chunk_rows, void* stream);
 
+/* Workspace bytes for keyless_decode_chunked / standard_decode_chunked with
+ * these arguments (chunk_rows 0 for keyless_decode / standard_decode): fp32
+ * partial rows (d_head + 2 floats per head and split) plus, in the shared-tile
+ * mode, a plan of B + 3 ints; 0 when no merge is needed. Host-only; depends on
+ * the descriptor's layout and capacity, not on the lengths. */
 size_t keyless_decode_workspace_size(const kl_value_cache* cache, int B, int H, int chunk_rows);
 
 /*
