@@ -36,13 +36,20 @@ typedef __attribute__((address_space(3))) unsigned char lds_u8;
 
 constexpr int BQ = 128;     // query rows per workgroup
 constexpr int BKV = 64;     // value rows per tile
-constexpr int NSTAGE = 3;   // value tiles in flight
+constexpr int NSTAGE = 3;   // value tiles in flight (the tile loop is unrolled by 3)
 constexpr int kThreads = 256;
 
 __device__ __forceinline__ uint32_t pack2(float lo, float hi) {
   typedef __attribute__((__vector_size__(2 * sizeof(__bf16)))) __bf16 b2;
   b2 v = {(__bf16)lo, (__bf16)hi};
   return __builtin_bit_cast(uint32_t, v);
+}
+
+// max(a, b, c) in one instruction; the operands are finite scores or -inf.
+__device__ __forceinline__ float max3(float a, float b, float c) {
+  float r;
+  asm("v_max3_f32 %0, %1, %2, %3" : "=v"(r) : "v"(a), "v"(b), "v"(c));
+  return r;
 }
 
 template <int D>
@@ -78,22 +85,35 @@ __global__ __launch_bounds__(kThreads, 2) void attn_bf16_kernel(AttnParams p) {
   const uint16_t* __restrict__ Q = reinterpret_cast<const uint16_t*>(p.q);
 
   // Routed-query fragments (B operand of S^T): query row q0 + 16 qb + fr,
-  // columns 32 ks + 8 grp .. + 7. Rows past the end are clamped (never stored).
+  // columns 32 ks + 8 grp .. + 7, multiplied by c = scale * log2(e) and rounded
+  // to bf16 once, so the products come out in exponent (log2) units. Rows past
+  // the end are clamped (never stored).
+  const float c = p.scale_log2;
   bf16x8_t qf[2][KS];
 #pragma unroll
   for (int qb = 0; qb < 2; ++qb) {
     const int qq = min(q0 + qb * 16 + fr, p.N - 1);
     const uint16_t* src = Q + ((size_t)b * p.N + qq) * p.q_stride + (size_t)h * D + grp * 8;
 #pragma unroll
-    for (int ks = 0; ks < KS; ++ks)
-      qf[qb][ks] = *reinterpret_cast<const bf16x8_t*>(src + ks * 32);
+    for (int ks = 0; ks < KS; ++ks) {
+      const u32x4 raw = *reinterpret_cast<const u32x4*>(src + ks * 32);
+      u32x4 w;
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+        w[j] = pack2(__uint_as_float(raw[j] << 16) * c, __uint_as_float(raw[j] & 0xFFFF0000u) * c);
+      qf[qb][ks] = __builtin_bit_cast(bf16x8_t, w);
+    }
   }
 
   f32x4_t o[DB][2];
 #pragma unroll
   for (int i = 0; i < DB; ++i) o[i][0] = o[i][1] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-  float m[2] = {-INFINITY, -INFINITY};  // reference exponent (log2 units) per query block
-  float lsum[2] = {0.f, 0.f};  // per-lane partial sums; reduced at the end
+  // Row sums of the weights, from the same MFMA with an all-ones A operand: every
+  // row of the product is the column sum of P^T, i.e. the weight sum per query.
+  f32x4_t osum[2] = {f32x4_t{0.f, 0.f, 0.f, 0.f}, f32x4_t{0.f, 0.f, 0.f, 0.f}};
+  const bf16x8_t ones = __builtin_bit_cast(
+      bf16x8_t, u32x4{0x3F803F80u, 0x3F803F80u, 0x3F803F80u, 0x3F803F80u});
+  float m[2] = {0.f, 0.f};  // reference exponent per query block; set by the first tile
 
   // Tile copies: wave copy c of this wave fills tile rows 4 (c * 4 + wave) ..
   // + 3; lane L lands at row + L / CHUNKS, physical chunk L % CHUNKS. Rows past
@@ -140,26 +160,35 @@ __global__ __launch_bounds__(kThreads, 2) void attn_bf16_kernel(AttnParams p) {
     offT[db] = T::off(grp * 4 + (fr >> 2), col >> 3) + (col & 7) * 2;
   }
 
-  const float c = p.scale_log2;  // scores are kept raw; c folds into the exponent
   const int last_row = p.causal ? min(qt * BQ + BQ, p.N) : p.N;
   const int ntiles = (last_row + BKV - 1) / BKV;
 #pragma unroll
   for (int s = 0; s < NSTAGE - 1; ++s)
     if (s < ntiles) issue(s, s);
 
-  auto process = [&](const int jt, auto stage_tag) {
+  // One value tile. Scores come out of the MFMA already shifted by the
+  // reference: the accumulation starts from -m (in log2 units, as q carries c).
+  // The reference moves lazily, only when a score exceeds it by more than 2^8,
+  // which keeps every weight below 256 and skips the rescale of O on most
+  // tiles; the first tile (row 0 is always unmasked) sets it exactly.
+  auto process = [&](const int jt, auto stage_tag, auto first_tag) {
     constexpr int STAGE = decltype(stage_tag)::value;
+    constexpr bool FIRST = decltype(first_tag)::value;
     // Tile jt has landed once at most the copies of the later issued tile remain.
     if (jt + 1 < ntiles) KL_WAIT_VMCNT(T::COPIES);
     else KL_WAIT_VMCNT(0);
     __syncthreads();
     if (jt + NSTAGE - 1 < ntiles) issue(jt + NSTAGE - 1, (STAGE + NSTAGE - 1) % NSTAGE);
     const int j0 = jt * BKV;
-    // Skip tiles entirely above the diagonal for this wave.
-    if (p.causal && j0 > q0 + 31) return;
+    // Skip tiles entirely above the diagonal for this wave (never the first).
+    if (!FIRST && p.causal && j0 > q0 + 31) return;
     const lds_u8* tile = (const lds_u8*)smem + STAGE * T::BYTES;
 
-    // S^T[kv][q] for kv blocks kb (16 rows) and query blocks qb, raw (unscaled).
+    // S^T[kv][q] - m[q] for kv blocks kb (16 rows) and query blocks qb.
+    f32x4_t init[2];
+#pragma unroll
+    for (int qb = 0; qb < 2; ++qb)
+      init[qb] = FIRST ? f32x4_t{0.f, 0.f, 0.f, 0.f} : f32x4_t{-m[qb], -m[qb], -m[qb], -m[qb]};
     f32x4_t sc[4][2];
 #pragma unroll
     for (int kb = 0; kb < 4; ++kb) {
@@ -167,13 +196,8 @@ __global__ __launch_bounds__(kThreads, 2) void attn_bf16_kernel(AttnParams p) {
       for (int ks = 0; ks < KS; ++ks) {
         const bf16x8_t a = *reinterpret_cast<const __attribute__((address_space(3))) bf16x8_t*>(
             tile + offS[ks] + kb * 16 * T::ROW);
-        if (ks == 0) {
-          sc[kb][0] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, qf[0][0], f32x4_t{0.f, 0.f, 0.f, 0.f}, 0, 0, 0);
-          sc[kb][1] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, qf[1][0], f32x4_t{0.f, 0.f, 0.f, 0.f}, 0, 0, 0);
-        } else {
-          sc[kb][0] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, qf[0][ks], sc[kb][0], 0, 0, 0);
-          sc[kb][1] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, qf[1][ks], sc[kb][1], 0, 0, 0);
-        }
+        sc[kb][0] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, qf[0][ks], ks == 0 ? init[0] : sc[kb][0], 0, 0, 0);
+        sc[kb][1] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, qf[1][ks], ks == 0 ? init[1] : sc[kb][1], 0, 0, 0);
       }
     }
     // Lane holds scores of query q0 + 16 qb + fr against rows j0 + 16 kb + 4 grp + r.
@@ -190,46 +214,44 @@ __global__ __launch_bounds__(kThreads, 2) void attn_bf16_kernel(AttnParams p) {
           }
       }
     }
-    // Online softmax with a lazily moved reference: weights are 2^(c s - m) with
-    // m only raised when a score exceeds it by more than 2^8, which keeps every
-    // weight below 256 and skips the rescale of O on most tiles.
-    float mx[2];
+    float lm[2];  // this lane's maximum per query block (16 scores: 8 three-way maxima)
 #pragma unroll
     for (int qb = 0; qb < 2; ++qb) {
-      float v = -INFINITY;
-#pragma unroll
-      for (int kb = 0; kb < 4; ++kb)
-        v = fmaxf(v, fmaxf(fmaxf(sc[kb][qb][0], sc[kb][qb][1]), fmaxf(sc[kb][qb][2], sc[kb][qb][3])));
-      v = fmaxf(v, __shfl_xor(v, 16));
-      v = fmaxf(v, __shfl_xor(v, 32));
-      mx[qb] = v * c;
+      float v = max3(sc[0][qb][0], sc[0][qb][1], sc[0][qb][2]);
+      v = max3(v, sc[0][qb][3], sc[1][qb][0]);
+      v = max3(v, sc[1][qb][1], sc[1][qb][2]);
+      v = max3(v, sc[1][qb][3], sc[2][qb][0]);
+      v = max3(v, sc[2][qb][1], sc[2][qb][2]);
+      v = max3(v, sc[2][qb][3], sc[3][qb][0]);
+      v = max3(v, sc[3][qb][1], sc[3][qb][2]);
+      lm[qb] = fmaxf(v, sc[3][qb][3]);
     }
-    const bool grow = (mx[0] > m[0] + 8.f) || (mx[1] > m[1] + 8.f);
-    if (__builtin_amdgcn_ballot_w64(grow)) {
+    const bool grow = FIRST || (lm[0] > 8.f) || (lm[1] > 8.f);
+    if (FIRST || __builtin_amdgcn_ballot_w64(grow)) {
 #pragma unroll
       for (int qb = 0; qb < 2; ++qb) {
-        const float mn = (mx[qb] > m[qb] + 8.f) ? mx[qb] : m[qb];
-        const float alpha = (m[qb] == -INFINITY) ? 0.f : fast_exp2(m[qb] - mn);
-        m[qb] = mn;
-        lsum[qb] *= alpha;
+        // Tile maximum of each query over its four lane groups.
+        float t = fmaxf(lm[qb], __shfl_xor(lm[qb], 16));
+        t = fmaxf(t, __shfl_xor(t, 32));
+        const float d = FIRST ? t : (t > 8.f ? t : 0.f);
+        m[qb] += d;
+        if (!FIRST) {
+          const float alpha = fast_exp2(-d);
 #pragma unroll
-        for (int i = 0; i < DB; ++i) o[i][qb] *= alpha;
+          for (int i = 0; i < DB; ++i) o[i][qb] *= alpha;
+          osum[qb] *= alpha;
+        }
+#pragma unroll
+        for (int kb = 0; kb < 4; ++kb) sc[kb][qb] -= d;
       }
     }
     bf16x8_t pf[2][2];
 #pragma unroll
     for (int qb = 0; qb < 2; ++qb) {
-      const float nm = (m[qb] == -INFINITY) ? 0.f : -m[qb];
-      float ps = 0.f;
 #pragma unroll
       for (int kb = 0; kb < 4; ++kb)
 #pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          const float w = fast_exp2(fmaf(sc[kb][qb][r], c, nm));
-          sc[kb][qb][r] = w;
-          ps += w;
-        }
-      lsum[qb] += ps;
+        for (int r = 0; r < 4; ++r) sc[kb][qb][r] = fast_exp2(sc[kb][qb][r]);
       // P^T fragments: k-step ks covers rows 32 ks + {4 grp .. 4 grp + 3, 16 + 4 grp ..}.
 #pragma unroll
       for (int ks = 0; ks < 2; ++ks) {
@@ -257,21 +279,30 @@ __global__ __launch_bounds__(kThreads, 2) void attn_bf16_kernel(AttnParams p) {
         o[db][1] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, pf[1][ks], o[db][1], 0, 0, 0);
       }
     }
+#pragma unroll
+    for (int ks = 0; ks < 2; ++ks) {
+      osum[0] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ones, pf[0][ks], osum[0], 0, 0, 0);
+      osum[1] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ones, pf[1][ks], osum[1], 0, 0, 0);
+    }
   };
 
-  for (int jt = 0; jt < ntiles; jt += NSTAGE) {
-    process(jt, std::integral_constant<int, 0>{});
-    if (jt + 1 < ntiles) process(jt + 1, std::integral_constant<int, 1>{});
-    if (jt + 2 < ntiles) process(jt + 2, std::integral_constant<int, 2>{});
+  using I0 = std::integral_constant<int, 0>;
+  using I1 = std::integral_constant<int, 1>;
+  using I2 = std::integral_constant<int, 2>;
+  process(0, I0{}, std::true_type{});  // tile 0 is never above the diagonal
+  if (1 < ntiles) process(1, I1{}, std::false_type{});
+  if (2 < ntiles) process(2, I2{}, std::false_type{});
+  for (int jt = NSTAGE; jt < ntiles; jt += NSTAGE) {
+    process(jt, I0{}, std::false_type{});
+    if (jt + 1 < ntiles) process(jt + 1, I1{}, std::false_type{});
+    if (jt + 2 < ntiles) process(jt + 2, I2{}, std::false_type{});
   }
 
   // Normalise and store: lane holds O[q][16 db + 4 grp + r] for its query rows.
   uint16_t* __restrict__ O = reinterpret_cast<uint16_t*>(p.out);
 #pragma unroll
   for (int qb = 0; qb < 2; ++qb) {
-    float l = lsum[qb];
-    l += __shfl_xor(l, 16);
-    l += __shfl_xor(l, 32);
+    const float l = osum[qb][0];
     const float inv = l > 0.f ? 1.f / l : 0.f;
     const int q = q0 + qb * 16 + fr;
     if (q < p.N) {
