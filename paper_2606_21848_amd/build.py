@@ -36,13 +36,24 @@ def hipcc() -> str:
     raise RuntimeError("hipcc not found; a ROCm install is required to build libkeyless.so")
 
 
+# Per-source code-generation options. The GEMM's k-step wants all of its LDS
+# fragment reads in flight before the MFMAs (one wait instead of one per
+# fragment pair); LLVM's iterative ILP scheduler produces that schedule. The
+# attention's scores are finite or -inf, never NaN: without NaN semantics its
+# maxima become v_max3_f32 with no canonicalising moves.
+PER_SOURCE = {
+    "gemm_bf16.hip": ["-mllvm", "-amdgpu-sched-strategy=iterative-ilp"],
+    "prefill_attn.hip": ["-fno-honor-nans"],
+}
+
+
 def sources() -> list[str]:
     return sorted(glob.glob(os.path.join(CSRC, "*.hip"))) + [os.path.join(CSRC, "api.cpp")]
 
 
 def _compile(src: str, cc: str, extra: list[str]) -> str:
     obj = os.path.join(BUILD, os.path.basename(src) + ".o")
-    cmd = [cc, *COMMON, *extra, "-c", src, "-o", obj]
+    cmd = [cc, *COMMON, *PER_SOURCE.get(os.path.basename(src), []), *extra, "-c", src, "-o", obj]
     r = subprocess.run(cmd, capture_output=True, text=True)
     if r.returncode != 0:
         raise RuntimeError(f"compile failed: {' '.join(cmd)}\n{r.stdout}\n{r.stderr}")

@@ -47,7 +47,10 @@ __device__ __forceinline__ int swz(int row, int chunk) {
   return row * (BK * 2) + ((chunk ^ ((row >> 1) & 7)) << 4);
 }
 
-__global__ __launch_bounds__(kThreads) void gemm_bf16_kernel(GemmParams2 p) {
+// Two waves per SIMD (the 128 KiB of LDS allow one workgroup per CU): the
+// register budget is 256, enough to hold all fragments of a k-step.
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2)))
+void gemm_bf16_kernel(GemmParams2 p) {
   const int tilesM = (p.M + BM - 1) / BM, tilesN = (p.N + BN - 1) / BN;
   const int ntiles = tilesM * tilesN;
   int wg = blockIdx.x;
@@ -140,6 +143,9 @@ __global__ __launch_bounds__(kThreads) void gemm_bf16_kernel(GemmParams2 p) {
     }
     __syncthreads();
     compute(stageA(cur), stageW(cur));
+    // The next iteration's copies refill this stage: every wave's LDS reads of
+    // it must have returned first (the barrier does not wait for them).
+    asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
     __syncthreads();
   }
 

@@ -45,12 +45,10 @@ __device__ __forceinline__ uint32_t pack2(float lo, float hi) {
   return __builtin_bit_cast(uint32_t, v);
 }
 
-// max(a, b, c) in one instruction; the operands are finite scores or -inf.
-__device__ __forceinline__ float max3(float a, float b, float c) {
-  float r;
-  asm("v_max3_f32 %0, %1, %2, %3" : "=v"(r) : "v"(a), "v"(b), "v"(c));
-  return r;
-}
+// max(a, b, c); written for the compiler (not as inline assembly, which would
+// hide a read of a fresh MFMA result from its hazard checks), which forms
+// v_max3_f32 since this file is built without NaN semantics.
+__device__ __forceinline__ float max3(float a, float b, float c) { return fmaxf(fmaxf(a, b), c); }
 
 template <int D>
 struct Tile {
@@ -177,6 +175,10 @@ __global__ __launch_bounds__(kThreads, 2) void attn_bf16_kernel(AttnParams p) {
     // Tile jt has landed once at most the copies of the later issued tile remain.
     if (jt + 1 < ntiles) KL_WAIT_VMCNT(T::COPIES);
     else KL_WAIT_VMCNT(0);
+    // The copies issued below refill the stage of tile jt - 1: every wave's LDS
+    // reads of it must have returned before the barrier (the barrier itself does
+    // not wait for outstanding LDS reads).
+    asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
     __syncthreads();
     if (jt + NSTAGE - 1 < ntiles) issue(jt + NSTAGE - 1, (STAGE + NSTAGE - 1) % NSTAGE);
     const int j0 = jt * BKV;
