@@ -65,7 +65,7 @@ struct Tile {
 };
 
 template <int D>
-__global__ __launch_bounds__(kThreads, 2) void attn_bf16_kernel(AttnParams p) {
+__global__ __launch_bounds__(kThreads, 3) void attn_bf16_kernel(AttnParams p) {
   using T = Tile<D>;
   constexpr int KS = D / 32;  // MFMA k-steps over d_head for S^T
   constexpr int DB = D / 16;  // 16-wide column blocks of the output
