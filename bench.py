@@ -124,7 +124,7 @@ def cpu_baseline(c, seconds, torch):
     # Time single (b, h) decodes until the budget is spent; scale to tokens/s.
     pairs = [(b, h) for b in range(B) for h in range(H)]
     done, t0 = 0, time.perf_counter()
-    while time.perf_counter() - t0 < seconds and done < 64 * len(pairs):
+    while time.perf_counter() - t0 < seconds:
         b, h = pairs[done % len(pairs)]
         K.keyless_decode(q, V, lengths, H, H, pairs=[(b, h)])
         done += 1
