@@ -2,8 +2,8 @@
 // of Eq. 4): O_h = softmax(tau * Q~_h V_g^T) V_g, where the value tile is both
 // the "key" of the score and the value of the weighted sum.
 //
-// A workgroup (4 waves) owns 128 query rows of one head; each wave owns 32 rows
-// and keeps their routed-query fragments in registers. Value tiles of 64 rows
+// A workgroup (4 waves) owns 4 * 16 * QB query rows of one head; each wave owns
+// 16 * QB rows and keeps their routed-query fragments in registers. Value tiles of 64 rows
 // move from memory straight into LDS (global_load_lds, 16 bytes per lane), one
 // copy per tile, three tiles in flight. With v_mfma_f32_16x16x32_bf16:
 //   S^T = V Q~^T     A operand = value rows (ds_read_b128 of the row-major tile)
@@ -34,7 +34,9 @@ typedef short s16x4 __attribute__((ext_vector_type(4)));
 typedef unsigned int u32x2 __attribute__((ext_vector_type(2)));
 typedef __attribute__((address_space(3))) unsigned char lds_u8;
 
-constexpr int BQ = 128;     // query rows per workgroup
+constexpr int QB = 3;       // 16-row query blocks per wave
+constexpr int WQ = 16 * QB; // query rows per wave
+constexpr int BQ = 4 * WQ;  // query rows per workgroup
 constexpr int BKV = 64;     // value rows per tile
 constexpr int NSTAGE = 3;   // value tiles in flight (the tile loop is unrolled by 3)
 constexpr int kThreads = 256;
@@ -65,7 +67,7 @@ struct Tile {
 };
 
 template <int D>
-__global__ __launch_bounds__(kThreads, 3) void attn_bf16_kernel(AttnParams p) {
+__global__ __launch_bounds__(kThreads, QB == 2 ? 3 : 2) void attn_bf16_kernel(AttnParams p) {
   using T = Tile<D>;
   constexpr int KS = D / 32;  // MFMA k-steps over d_head for S^T
   constexpr int DB = D / 16;  // 16-wide column blocks of the output
@@ -78,7 +80,7 @@ __global__ __launch_bounds__(kThreads, 3) void attn_bf16_kernel(AttnParams p) {
   const int t = threadIdx.x, lane = t & 63;
   const int wave = __builtin_amdgcn_readfirstlane(t >> 6);
   const int fr = lane & 15, grp = lane >> 4;
-  const int q0 = qt * BQ + wave * 32;  // this wave's first query row
+  const int q0 = qt * BQ + wave * WQ;  // this wave's first query row
 
   const uint16_t* __restrict__ Q = reinterpret_cast<const uint16_t*>(p.q);
 
@@ -87,9 +89,9 @@ __global__ __launch_bounds__(kThreads, 3) void attn_bf16_kernel(AttnParams p) {
   // to bf16 once, so the products come out in exponent (log2) units. Rows past
   // the end are clamped (never stored).
   const float c = p.scale_log2;
-  bf16x8_t qf[2][KS];
+  bf16x8_t qf[QB][KS];
 #pragma unroll
-  for (int qb = 0; qb < 2; ++qb) {
+  for (int qb = 0; qb < QB; ++qb) {
     const int qq = min(q0 + qb * 16 + fr, p.N - 1);
     const uint16_t* src = Q + ((size_t)b * p.N + qq) * p.q_stride + (size_t)h * D + grp * 8;
 #pragma unroll
@@ -103,15 +105,21 @@ __global__ __launch_bounds__(kThreads, 3) void attn_bf16_kernel(AttnParams p) {
     }
   }
 
-  f32x4_t o[DB][2];
+  f32x4_t o[DB][QB];
 #pragma unroll
-  for (int i = 0; i < DB; ++i) o[i][0] = o[i][1] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+  for (int i = 0; i < DB; ++i)
+#pragma unroll
+    for (int qb = 0; qb < QB; ++qb) o[i][qb] = f32x4_t{0.f, 0.f, 0.f, 0.f};
   // Row sums of the weights, from the same MFMA with an all-ones A operand: every
   // row of the product is the column sum of P^T, i.e. the weight sum per query.
-  f32x4_t osum[2] = {f32x4_t{0.f, 0.f, 0.f, 0.f}, f32x4_t{0.f, 0.f, 0.f, 0.f}};
+  f32x4_t osum[QB];
+#pragma unroll
+  for (int qb = 0; qb < QB; ++qb) osum[qb] = f32x4_t{0.f, 0.f, 0.f, 0.f};
   const bf16x8_t ones = __builtin_bit_cast(
       bf16x8_t, u32x4{0x3F803F80u, 0x3F803F80u, 0x3F803F80u, 0x3F803F80u});
-  float m[2] = {0.f, 0.f};  // reference exponent per query block; set by the first tile
+  float m[QB];  // reference exponent per query block; set by the first tile
+#pragma unroll
+  for (int qb = 0; qb < QB; ++qb) m[qb] = 0.f;
 
   // Tile copies: wave copy c of this wave fills tile rows 4 (c * 4 + wave) ..
   // + 3; lane L lands at row + L / CHUNKS, physical chunk L % CHUNKS. Rows past
@@ -183,29 +191,30 @@ __global__ __launch_bounds__(kThreads, 3) void attn_bf16_kernel(AttnParams p) {
     if (jt + NSTAGE - 1 < ntiles) issue(jt + NSTAGE - 1, (STAGE + NSTAGE - 1) % NSTAGE);
     const int j0 = jt * BKV;
     // Skip tiles entirely above the diagonal for this wave (never the first).
-    if (!FIRST && p.causal && j0 > q0 + 31) return;
+    if (!FIRST && p.causal && j0 > q0 + WQ - 1) return;
     const lds_u8* tile = (const lds_u8*)smem + STAGE * T::BYTES;
 
     // S^T[kv][q] - m[q] for kv blocks kb (16 rows) and query blocks qb.
-    f32x4_t init[2];
+    f32x4_t init[QB];
 #pragma unroll
-    for (int qb = 0; qb < 2; ++qb)
+    for (int qb = 0; qb < QB; ++qb)
       init[qb] = FIRST ? f32x4_t{0.f, 0.f, 0.f, 0.f} : f32x4_t{-m[qb], -m[qb], -m[qb], -m[qb]};
-    f32x4_t sc[4][2];
+    f32x4_t sc[4][QB];
 #pragma unroll
     for (int kb = 0; kb < 4; ++kb) {
 #pragma unroll
       for (int ks = 0; ks < KS; ++ks) {
         const bf16x8_t a = *reinterpret_cast<const __attribute__((address_space(3))) bf16x8_t*>(
             tile + offS[ks] + kb * 16 * T::ROW);
-        sc[kb][0] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, qf[0][ks], ks == 0 ? init[0] : sc[kb][0], 0, 0, 0);
-        sc[kb][1] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, qf[1][ks], ks == 0 ? init[1] : sc[kb][1], 0, 0, 0);
+#pragma unroll
+        for (int qb = 0; qb < QB; ++qb)
+          sc[kb][qb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, qf[qb][ks], ks == 0 ? init[qb] : sc[kb][qb], 0, 0, 0);
       }
     }
     // Lane holds scores of query q0 + 16 qb + fr against rows j0 + 16 kb + 4 grp + r.
     if ((p.causal && j0 + BKV - 1 > q0) || (j0 + BKV > p.N)) {
 #pragma unroll
-      for (int qb = 0; qb < 2; ++qb) {
+      for (int qb = 0; qb < QB; ++qb) {
         const int q = q0 + qb * 16 + fr;
 #pragma unroll
         for (int kb = 0; kb < 4; ++kb)
@@ -216,9 +225,9 @@ __global__ __launch_bounds__(kThreads, 3) void attn_bf16_kernel(AttnParams p) {
           }
       }
     }
-    float lm[2];  // this lane's maximum per query block (16 scores: 8 three-way maxima)
+    float lm[QB];  // this lane's maximum per query block (16 scores: 8 three-way maxima)
 #pragma unroll
-    for (int qb = 0; qb < 2; ++qb) {
+    for (int qb = 0; qb < QB; ++qb) {
       float v = max3(sc[0][qb][0], sc[0][qb][1], sc[0][qb][2]);
       v = max3(v, sc[0][qb][3], sc[1][qb][0]);
       v = max3(v, sc[1][qb][1], sc[1][qb][2]);
@@ -228,10 +237,12 @@ __global__ __launch_bounds__(kThreads, 3) void attn_bf16_kernel(AttnParams p) {
       v = max3(v, sc[3][qb][1], sc[3][qb][2]);
       lm[qb] = fmaxf(v, sc[3][qb][3]);
     }
-    const bool grow = FIRST || (lm[0] > 8.f) || (lm[1] > 8.f);
+    bool grow = FIRST;
+#pragma unroll
+    for (int qb = 0; qb < QB; ++qb) grow |= lm[qb] > 8.f;
     if (FIRST || __builtin_amdgcn_ballot_w64(grow)) {
 #pragma unroll
-      for (int qb = 0; qb < 2; ++qb) {
+      for (int qb = 0; qb < QB; ++qb) {
         // Tile maximum of each query over its four lane groups.
         float t = fmaxf(lm[qb], __shfl_xor(lm[qb], 16));
         t = fmaxf(t, __shfl_xor(t, 32));
@@ -247,9 +258,9 @@ __global__ __launch_bounds__(kThreads, 3) void attn_bf16_kernel(AttnParams p) {
         for (int kb = 0; kb < 4; ++kb) sc[kb][qb] -= d;
       }
     }
-    bf16x8_t pf[2][2];
+    bf16x8_t pf[QB][2];
 #pragma unroll
-    for (int qb = 0; qb < 2; ++qb) {
+    for (int qb = 0; qb < QB; ++qb) {
 #pragma unroll
       for (int kb = 0; kb < 4; ++kb)
 #pragma unroll
@@ -277,15 +288,16 @@ __global__ __launch_bounds__(kThreads, 3) void attn_bf16_kernel(AttnParams p) {
         const s16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
             (__attribute__((address_space(3))) s16x4*)(src + 16 * T::ROW));
         const bf16x8_t a = __builtin_bit_cast(bf16x8_t, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
-        o[db][0] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, pf[0][ks], o[db][0], 0, 0, 0);
-        o[db][1] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, pf[1][ks], o[db][1], 0, 0, 0);
+#pragma unroll
+        for (int qb = 0; qb < QB; ++qb)
+          o[db][qb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, pf[qb][ks], o[db][qb], 0, 0, 0);
       }
     }
 #pragma unroll
-    for (int ks = 0; ks < 2; ++ks) {
-      osum[0] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ones, pf[0][ks], osum[0], 0, 0, 0);
-      osum[1] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ones, pf[1][ks], osum[1], 0, 0, 0);
-    }
+    for (int ks = 0; ks < 2; ++ks)
+#pragma unroll
+      for (int qb = 0; qb < QB; ++qb)
+        osum[qb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ones, pf[qb][ks], osum[qb], 0, 0, 0);
   };
 
   using I0 = std::integral_constant<int, 0>;
@@ -303,7 +315,7 @@ __global__ __launch_bounds__(kThreads, 3) void attn_bf16_kernel(AttnParams p) {
   // Normalise and store: lane holds O[q][16 db + 4 grp + r] for its query rows.
   uint16_t* __restrict__ O = reinterpret_cast<uint16_t*>(p.out);
 #pragma unroll
-  for (int qb = 0; qb < 2; ++qb) {
+  for (int qb = 0; qb < QB; ++qb) {
     const float l = osum[qb][0];
     const float inv = l > 0.f ? 1.f / l : 0.f;
     const int q = q0 + qb * 16 + fr;
