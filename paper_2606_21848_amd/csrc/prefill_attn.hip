@@ -258,30 +258,32 @@ __global__ __launch_bounds__(kThreads, QB == 2 ? 3 : 2) void attn_bf16_kernel(At
         for (int kb = 0; kb < 4; ++kb) sc[kb][qb] -= d;
       }
     }
+    // Weights and P^T fragments of one 32-row k-step (rows 32 ks + {4 grp ..
+    // 4 grp + 3, 16 + 4 grp ..}), for every query block.
     bf16x8_t pf[QB][2];
+    auto weights = [&](const int ks) {
 #pragma unroll
-    for (int qb = 0; qb < QB; ++qb) {
-#pragma unroll
-      for (int kb = 0; kb < 4; ++kb)
-#pragma unroll
-        for (int r = 0; r < 4; ++r) sc[kb][qb][r] = fast_exp2(sc[kb][qb][r]);
-      // P^T fragments: k-step ks covers rows 32 ks + {4 grp .. 4 grp + 3, 16 + 4 grp ..}.
-#pragma unroll
-      for (int ks = 0; ks < 2; ++ks) {
+      for (int qb = 0; qb < QB; ++qb) {
         u32x4 w;
-        w[0] = pack2(sc[2 * ks][qb][0], sc[2 * ks][qb][1]);
-        w[1] = pack2(sc[2 * ks][qb][2], sc[2 * ks][qb][3]);
-        w[2] = pack2(sc[2 * ks + 1][qb][0], sc[2 * ks + 1][qb][1]);
-        w[3] = pack2(sc[2 * ks + 1][qb][2], sc[2 * ks + 1][qb][3]);
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+          f32x4_t& x = sc[2 * ks + h][qb];
+          x[0] = fast_exp2(x[0]);
+          x[1] = fast_exp2(x[1]);
+          x[2] = fast_exp2(x[2]);
+          x[3] = fast_exp2(x[3]);
+          w[2 * h] = pack2(x[0], x[1]);
+          w[2 * h + 1] = pack2(x[2], x[3]);
+        }
         pf[qb][ks] = __builtin_bit_cast(bf16x8_t, w);
       }
-    }
-    // O^T[d][q] += V^T P^T: the transposed read hands lane fr the 4 rows of
-    // column 16 db + fr (rows 32 ks + 4 grp .., and 16 further for the high half).
+    };
+    // O^T[d][q] += V^T P^T over one k-step: the transposed read hands lane fr
+    // the 4 rows of column 16 db + fr (rows 32 ks + 4 grp .., and 16 further
+    // for the high half); the all-ones operand adds the weight sums.
+    auto pv = [&](const int ks) {
 #pragma unroll
-    for (int db = 0; db < DB; ++db) {
-#pragma unroll
-      for (int ks = 0; ks < 2; ++ks) {
+      for (int db = 0; db < DB; ++db) {
         const lds_u8* src = tile + offT[db] + ks * 32 * T::ROW;
         const s16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
             (__attribute__((address_space(3))) s16x4*)(src));
@@ -292,12 +294,14 @@ __global__ __launch_bounds__(kThreads, QB == 2 ? 3 : 2) void attn_bf16_kernel(At
         for (int qb = 0; qb < QB; ++qb)
           o[db][qb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, pf[qb][ks], o[db][qb], 0, 0, 0);
       }
-    }
-#pragma unroll
-    for (int ks = 0; ks < 2; ++ks)
 #pragma unroll
       for (int qb = 0; qb < QB; ++qb)
         osum[qb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ones, pf[qb][ks], osum[qb], 0, 0, 0);
+    };
+    weights(0);
+    pv(0);
+    weights(1);
+    pv(1);
   };
 
   using I0 = std::integral_constant<int, 0>;
