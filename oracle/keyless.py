@@ -150,6 +150,33 @@ def keyless_prefill_rows(x, Wt_Q, W_V, rows, H: int, G: int, d_head: int,
 # Section 3: value-only cache, append and decode
 # ---------------------------------------------------------------------------
 
+def decode_step_projections(x, W_Q, W_R, W_V, H: int, G: int, d_head: int):
+    """The projections of one decode step (Section 3): for the current token of
+    each sequence, its routed query q~_{n+1} (the q of the decode weights) and
+    its value v_{n+1} (the row appended to the value-only cache).
+
+      q~_h = (x W^Q_h) W^R_h   for every query head h
+      v_g  = x W^V_g           for every value group g
+    If W_R is None, W_Q is taken as the already folded W~^Q.
+
+    x: [B, d]; W_Q: [d, H*d_k]; W_R: [H, d_k, d_k] or None; W_V: [d, G*d_k].
+    Returns (q~ [B, H, d_k], v [B, G, d_k]).
+    """
+    x = _f64(x)
+    W_Q = _f64(W_Q)
+    W_V = _f64(W_V)
+    B = x.shape[0]
+    q = np.zeros((B, H, d_head))
+    v = np.zeros((B, G, d_head))
+    for b in range(B):
+        for h in range(H):
+            qh = x[b] @ W_Q[:, h * d_head:(h + 1) * d_head]
+            q[b, h] = qh if W_R is None else qh @ _f64(W_R)[h]
+        for g in range(G):
+            v[b, g] = x[b] @ W_V[:, g * d_head:(g + 1) * d_head]
+    return q, v
+
+
 def cache_rows(cache, b: int, g: int, n: int, block_table=None, block_size: int = 16):
     """The first n value rows of sequence b, group g, as an [n, d_k] array.
 

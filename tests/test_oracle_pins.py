@@ -52,6 +52,42 @@ def test_closed_form_prefill():
     np.testing.assert_allclose(O2[0, :, 0, :], case["expected_out"], rtol=0, atol=1e-15)
 
 
+def test_closed_form_decode_step_projections():
+    case = json.load(open(os.path.join(GOLD, "closed_form_cases.json")))["decode_step_projections"]
+    q, v = K.decode_step_projections(np.array(case["x"])[None], np.array(case["W_Q"]),
+                                     np.array(case["W_R"]), np.array(case["W_V"]), H=2, G=1, d_head=2)
+    np.testing.assert_array_equal(q[0], case["expected_q"])
+    np.testing.assert_array_equal(v[0], case["expected_v"])
+
+
+def test_decode_step_with_projections_equals_prefill_last_row():
+    """Project the current token, append its value, decode: the causal prefill's
+    row for that token (the Section 3 decode over all n+1 values)."""
+    B, N, d, H, G, dk = 3, 9, 12, 4, 2, 3
+    x = rng.standard_normal((B, N, d))
+    W_Q, W_V = rng.standard_normal((d, H * dk)), rng.standard_normal((d, G * dk))
+    W_R = rng.standard_normal((H, dk, dk)) / 2
+    O, _, V = K.keyless_prefill(x, W_Q, W_R, W_V, H=H, G=G, d_head=dk, causal=True)
+    cache = np.zeros((B, G, N, dk))
+    cache[:, :, :N - 1] = V[:, :N - 1].transpose(0, 2, 1, 3)  # the first n tokens, cached
+    q, v = K.decode_step_projections(x[:, N - 1], W_Q, W_R, W_V, H=H, G=G, d_head=dk)
+    cache = K.value_cache_append(cache, v[:, None], np.full(B, N - 1))
+    out = K.keyless_decode(q, cache, np.full(B, N), H=H, G=G)
+    np.testing.assert_allclose(out, O[:, N - 1], rtol=0, atol=1e-12)
+
+
+def test_decode_step_projections_are_linear_in_x():
+    d, H, G, dk = 8, 2, 1, 4
+    W_Q, W_V = rng.standard_normal((d, H * dk)), rng.standard_normal((d, G * dk))
+    W_R = rng.standard_normal((H, dk, dk))
+    a, b = rng.standard_normal((2, d))
+    qa, va = K.decode_step_projections(a[None], W_Q, W_R, W_V, H, G, dk)
+    qb, vb = K.decode_step_projections(b[None], W_Q, W_R, W_V, H, G, dk)
+    qs, vs = K.decode_step_projections((2 * a - 3 * b)[None], W_Q, W_R, W_V, H, G, dk)
+    np.testing.assert_allclose(qs, 2 * qa - 3 * qb, atol=1e-12)
+    np.testing.assert_allclose(vs, 2 * va - 3 * vb, atol=1e-12)
+
+
 @pytest.mark.parametrize("n", [1, 2, 7, 64])
 def test_weights_are_a_distribution(n):
     V = rng.standard_normal((n, 16))
