@@ -351,6 +351,32 @@ def extra_measurements(torch, kb, configs, dev):
                              "tokens_per_s": round(g["B"] / (ms * 1e-3), 1),
                              "cache_gbps": round(tot / (ms * 1e-3) / 1e9, 1)}
     del g, vc, ws, out
+    # A full decode step with the projections: x -> (q~, v appended) -> decode.
+    st = configs.decode_step_bf16(device=dev)
+    Bs, Hs, Gs, dks = st["B"], st["H"], st["G"], st["d_head"]
+    packed = kb.keyless_pack_weights(st["W_Q"], st["W_R"], st["W_V"], Hs, Gs)  # once
+    vc = kb.ValueCache(st["cache"])
+    q_out = torch.empty((Bs, Hs, dks), dtype=torch.bfloat16, device=dev)
+    out = torch.empty_like(q_out)
+    ws = torch.zeros(max(kb.decode_workspace_bytes(vc, Bs, Hs), 256), dtype=torch.uint8,
+                     device=dev)
+
+    def proj(i):
+        kb.keyless_decode_project(st["x"], packed, Hs, Gs, cache=vc,
+                                  lengths_before=st["lengths_before"], q_routed_out=q_out)
+
+    def full(i):
+        proj(i)
+        kb.keyless_decode(q_out, vc, st["lengths"], out=out, workspace=ws)
+    ms_p = batch_avg_ms(proj, 50, torch)
+    ms_s = timed_steps(full, 50, 5, torch)
+    wbytes = packed.numel() * 2
+    res["decode_step_bf16"] = {
+        "workload": "batch 8, d_model 4096, 32 heads x 128: keyless_decode_project (q~ and v "
+                    "from 64 MiB of packed weights, v appended) + keyless_decode over 4096 rows",
+        "project_ms": round(ms_p, 4), "project_weight_gbps": round(wbytes / (ms_p * 1e-3) / 1e9, 1),
+        "step_ms": round(ms_s, 4), "step_tokens_per_s": round(Bs / (ms_s * 1e-3), 1)}
+    del st, packed, vc, q_out, out, ws
     # Head-to-head: keyless value-only vs standard K+V, same structure.
     hh = configs.head_to_head_bf16(device=dev)
     vcache, kcache = kb.ValueCache(hh["V"]), kb.ValueCache(hh["K"])

@@ -145,6 +145,31 @@ int keyless_prefill_packed(const void* x, const void* packed, int B, int N, int 
                            void* stream);
 
 /*
+ * keyless_decode_project - the projections of one decode step (Section 3: the
+ * current token's routed query q~_{n+1} and its value v_{n+1}, i.e. the
+ * projections of Eq. 2 for one token per sequence), from weights prepared by
+ * keyless_pack_weights:
+ *   q~[b, h] = x[b] W~^Q_h      v[b, g] = x[b] W^V_g
+ *   x              [B, d_model] bf16, the current tokens
+ *   packed         [(H + G) * d_head, d_model] bf16 (keyless_pack_weights)
+ *   q_routed_out   [B, H, d_head] bf16
+ *   v_out          [B, G, d_head] bf16, or NULL
+ *   cache          bf16 value cache with G groups of d_head, or NULL: when given,
+ *                  v[b] is also written at position lengths_before[b] of sequence b
+ *                  (value_cache_append with T = 1, same dropping rules), so the
+ *                  decode that follows (with lengths_before[b] + 1) reads it
+ *   lengths_before [B] int32 on the device; required with a cache
+ * bf16 only; d_model a multiple of 32 and at most 16384; x and packed 16-byte
+ * aligned. fp32 accumulation, one rounding to bf16 (the cached value and v_out are
+ * the same bits). Bound by the weight bytes: each packed row is read once per 16
+ * sequences. Errors: KL_ERR_INVALID_ARG / KL_ERR_UNSUPPORTED before any launch.
+ */
+int keyless_decode_project(const void* x, const void* packed, int B, int d_model, int H, int G,
+                           int d_head, kl_dtype dtype, void* q_routed_out, void* v_out,
+                           const kl_value_cache* cache, const int32_t* lengths_before,
+                           void* stream);
+
+/*
  * keyless_decode - one decode step over a value-only cache (Section 3):
  *   out[b,h] = sum_{i < lengths[b]} alpha_i v_i,
  *   alpha_i = exp(scale <q_routed[b,h], v_i>) / sum_j exp(scale <q_routed[b,h], v_j>)

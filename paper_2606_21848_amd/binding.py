@@ -23,7 +23,7 @@ KL_CONTIGUOUS, KL_PAGED = 0, 1
 EXPORTS = (
     "keyless_fold_routing", "keyless_prefill", "keyless_prefill_workspace_size",
     "keyless_packed_weights_size", "keyless_pack_weights", "keyless_prefill_packed",
-    "keyless_decode", "keyless_decode_chunked", "keyless_decode_workspace_size",
+    "keyless_decode_project", "keyless_decode", "keyless_decode_chunked", "keyless_decode_workspace_size",
     "value_cache_append", "standard_decode", "standard_decode_chunked",
     "keyless_set_kernel_timer", "keyless_last_error", "keyless_version",
 )
@@ -66,6 +66,7 @@ def load(path: str = LIB_PATH):
         "keyless_packed_weights_size": (sz, [i, i, i, i, i]),
         "keyless_pack_weights": (i, [vp, vp, vp, i, i, i, i, i, vp, vp]),
         "keyless_prefill_packed": (i, [vp, vp, i, i, i, i, i, i, i, f, i, vp, vp, vp, vp, sz, vp]),
+        "keyless_decode_project": (i, [vp, vp, i, i, i, i, i, i, vp, vp, cp, vp, vp]),
         "keyless_decode": (i, [vp, cp, vp, i, i, f, vp, vp, sz, vp]),
         "keyless_decode_chunked": (i, [vp, cp, vp, i, i, f, vp, vp, sz, i, vp]),
         "keyless_decode_workspace_size": (sz, [cp, i, i, i]),
@@ -253,6 +254,27 @@ def keyless_pack_weights(W_Q: torch.Tensor, W_R: torch.Tensor | None, W_V: torch
     _check(_lib.keyless_pack_weights(_ptr(W_Q), _ptr(W_R), _ptr(W_V), d_model, H, G, dk, _dt(W_Q),
                                      _ptr(packed), _stream(W_Q)))
     return packed
+
+
+def keyless_decode_project(x: torch.Tensor, packed: torch.Tensor, H: int, G: int,
+                           cache: "ValueCache | None" = None, lengths_before=None,
+                           q_routed_out=None, v_out=None, return_v: bool = False):
+    """Decode-step projections q~ = x W~^Q [B, H, d], v = x W^V [B, G, d] from
+    packed weights; with ``cache`` the values are also appended at lengths_before."""
+    load()
+    B, d_model = x.shape
+    dk = packed.shape[0] // (H + G)
+    if q_routed_out is None:
+        q_routed_out = torch.empty((B, H, dk), dtype=x.dtype, device=x.device)
+    if return_v and v_out is None:
+        v_out = torch.empty((B, G, dk), dtype=x.dtype, device=x.device)
+    _check(_lib.keyless_decode_project(_ptr(x), _ptr(packed), B, d_model, H, G, dk, _dt(x),
+                                       _ptr(q_routed_out), _ptr(v_out),
+                                       None if cache is None else cache.ref, _ptr(lengths_before),
+                                       _stream(x)))
+    if return_v:
+        return q_routed_out, v_out
+    return q_routed_out
 
 
 def keyless_prefill_packed(x: torch.Tensor, packed: torch.Tensor, H: int, G: int,

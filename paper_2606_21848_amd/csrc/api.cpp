@@ -439,6 +439,61 @@ int keyless_prefill_packed(const void* x, const void* packed, int B, int N, int 
                              vv, static_cast<hipStream_t>(stream));
 }
 
+int keyless_decode_project(const void* x, const void* packed, int B, int d_model, int H, int G,
+                           int d_head, kl_dtype dtype, void* q_routed_out, void* v_out,
+                           const kl_value_cache* cache, const int32_t* lengths_before,
+                           void* stream) {
+  const char* who = "keyless_decode_project";
+  if (!x || !packed || !q_routed_out)
+    return fail(KL_ERR_INVALID_ARG, "%s: x, packed and q_routed_out must be non-NULL", who);
+  if (B < 0 || d_model <= 0 || H <= 0 || G <= 0)
+    return fail(KL_ERR_INVALID_ARG, "%s: bad B=%d, d_model=%d, H=%d or G=%d", who, B, d_model, H, G);
+  if (H % G != 0) return fail(KL_ERR_INVALID_ARG, "%s: H=%d is not a multiple of G=%d", who, H, G);
+  if (d_head != 64 && d_head != 128)
+    return fail(KL_ERR_UNSUPPORTED, "%s: d_head %d not supported (64 or 128)", who, d_head);
+  if (dtype != KL_BF16) return fail(KL_ERR_UNSUPPORTED, "%s: packed weights are bf16 only", who);
+  if (!kl::project_supported(d_model))
+    return fail(KL_ERR_UNSUPPORTED, "%s: d_model=%d must be a multiple of 32 and at most 16384",
+                who, d_model);
+  if (!aligned16(x) || !aligned16(packed))
+    return fail(KL_ERR_INVALID_ARG, "%s: x and packed must be 16-byte aligned", who);
+  if (cache) {
+    int st = check_cache(cache, "cache");
+    if (st != KL_OK) return st;
+    if (cache->dtype != KL_BF16 || cache->G != G || cache->d_head != d_head)
+      return fail(KL_ERR_INVALID_ARG, "%s: cache must be bf16 with G=%d groups of d_head=%d", who,
+                  G, d_head);
+    if (!lengths_before)
+      return fail(KL_ERR_INVALID_ARG, "%s: lengths_before is required with a cache", who);
+  }
+  if (B == 0) return KL_OK;
+  kl::ProjectParams p{};
+  p.x = static_cast<const uint16_t*>(x);
+  p.Wp = static_cast<const uint16_t*>(packed);
+  p.q_out = static_cast<uint16_t*>(q_routed_out);
+  p.v_out = static_cast<uint16_t*>(v_out);
+  p.B = B;
+  p.K = d_model;
+  p.N = (H + G) * d_head;
+  p.NQ = H * d_head;
+  p.G = G;
+  p.D = d_head;
+  p.ldx = d_model;
+  p.ldq = (long)H * d_head;
+  p.ldv = (long)G * d_head;
+  if (cache) {
+    p.cache = static_cast<uint16_t*>(cache->data);
+    p.table = cache->layout == KL_PAGED ? cache->block_table : nullptr;
+    p.lengths_before = lengths_before;
+    p.paged = cache->layout == KL_PAGED;
+    p.L_max = cache->L_max;
+    p.block_shift = p.paged ? log2_exact(cache->block_size) : 0;
+    p.num_blocks = cache->num_blocks;
+    p.max_blocks = cache->max_blocks_per_seq;
+  }
+  return hip_status(kl::launch_project(p, static_cast<hipStream_t>(stream)), who);
+}
+
 int keyless_prefill(const void* x, const void* W_Q, const void* W_R, const void* W_V, int B,
                     int N, int d_model, int H, int G, int d_head, int causal, float scale,
                     kl_dtype dtype, void* out, void* q_routed_out, void* v_out, void* ws,

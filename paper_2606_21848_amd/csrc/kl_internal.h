@@ -66,6 +66,26 @@ struct AppendParams {
 
 hipError_t launch_append(const AppendParams& p, hipStream_t stream);
 
+// Decode-step projections against packed weights Wp [N, K] (N = (H + G) D):
+// out[b][n] = sum_k x[b][k] Wp[n][k], columns below NQ = H D to q_out, the rest
+// to v_out and/or appended to the value cache at lengths_before[b]. bf16.
+struct ProjectParams {
+  const uint16_t* x;   // [B, K], row stride ldx
+  const uint16_t* Wp;  // [N, K]
+  uint16_t* q_out;     // [B, NQ], row stride ldq
+  uint16_t* v_out;     // [B, N - NQ], row stride ldv, or nullptr
+  uint16_t* cache;     // value cache data, or nullptr
+  const int32_t* table;
+  const int32_t* lengths_before;
+  int B, K, N, NQ, G, D;
+  long ldx, ldq, ldv;
+  bool paged;
+  int L_max, block_shift, num_blocks, max_blocks;
+};
+
+bool project_supported(int K);
+hipError_t launch_project(const ProjectParams& p, hipStream_t stream);
+
 // C[b] (M x N) = A[b] (M x K) * B[b] (K x N), row-major with leading
 // dimensions, fp32 accumulation; batched by pointer strides. Generic tiled
 // kernel for the small products (routing fold, fp32 prefill projections).

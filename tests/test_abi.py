@@ -116,6 +116,23 @@ def test_append_and_prefill_reject_bad_arguments(lib):
     expect(lib, st, kb.KL_ERR_INVALID_ARG, "non-NULL")
 
 
+def test_decode_project_rejects_bad_arguments(lib):
+    def proj(x=FAKE, packed=FAKE, B=2, d=256, H=4, G=2, dk=128, dt=kb.KL_BF16, q=FAKE, c=None,
+             lb=None):
+        return lib.keyless_decode_project(x, packed, B, d, H, G, dk, dt, q, None,
+                                          None if c is None else ctypes.byref(c), lb, None)
+    expect(lib, proj(q=None), kb.KL_ERR_INVALID_ARG, "non-NULL")
+    expect(lib, proj(H=4, G=3), kb.KL_ERR_INVALID_ARG, "multiple")
+    expect(lib, proj(dk=96), kb.KL_ERR_UNSUPPORTED, "d_head 96")
+    expect(lib, proj(dt=kb.KL_F32), kb.KL_ERR_UNSUPPORTED, "bf16")
+    expect(lib, proj(d=100), kb.KL_ERR_UNSUPPORTED, "multiple of 32")
+    expect(lib, proj(d=32768), kb.KL_ERR_UNSUPPORTED, "16384")
+    expect(lib, proj(x=ctypes.c_void_p(0x100008)), kb.KL_ERR_INVALID_ARG, "aligned")
+    expect(lib, proj(c=cache(G=2)), kb.KL_ERR_INVALID_ARG, "lengths_before")
+    expect(lib, proj(c=cache(G=4), lb=FAKE), kb.KL_ERR_INVALID_ARG, "G=2")
+    assert proj(B=0) == kb.KL_OK
+
+
 def test_zero_batch_is_a_no_op(lib):
     assert decode(lib, cache(), B=0, ws_bytes=0, ws=None) == kb.KL_OK
     assert lib.value_cache_append(ctypes.byref(cache()), FAKE, FAKE, 0, 1, None) == kb.KL_OK

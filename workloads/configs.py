@@ -14,7 +14,8 @@ import torch
 
 from .synth import normal, permutation, uniform_int
 
-NAMES = ("tiny_fp32", "decode_bf16", "prefill_bf16", "paged_gqa_bf16", "head_to_head_bf16")
+NAMES = ("tiny_fp32", "decode_bf16", "prefill_bf16", "paged_gqa_bf16", "head_to_head_bf16",
+         "decode_step_bf16")
 
 # Stream ids (one per drawn tensor).
 S_X, S_WQ, S_WR, S_WV, S_XNEXT, S_V, S_Q, S_K, S_LEN, S_PERM, S_VNEW = range(11)
@@ -115,3 +116,24 @@ def head_to_head_bf16(device="cpu", seed=4, B=32, H=32, L=16384, d_head=128, wit
     q = normal((B, H, d_head), seed, S_Q, 1.0, torch.bfloat16, device)
     lengths = torch.full((B,), L, dtype=torch.int32, device=device)
     return dict(V=V, K=K, q=q, lengths=lengths, B=B, H=H, G=H, L=L, d_head=d_head)
+
+
+def decode_step_bf16(device="cpu", seed=5, B=8, d_model=4096, H=32, G=32, d_head=128, L=4096):
+    """One full decode step of a layer shaped like the prefill workload: the
+    current tokens x [B, d_model] ~ N(0,1), projection weights as in
+    ``prefill_bf16`` (W_Q, W_V ~ N(0, 1/d_model), W_R [H, d_head, d_head]), and a
+    contiguous value cache [B, G, L, d_head] ~ N(0,1) whose first L - 1 rows are
+    cached; the step appends the new value at row L - 1 and decodes over L rows.
+    """
+    std_w = 1.0 / math.sqrt(d_model)
+    f = torch.bfloat16
+    return dict(
+        x=normal((B, d_model), seed, S_X, 1.0, f, device),
+        W_Q=normal((d_model, H * d_head), seed, S_WQ, std_w, f, device),
+        W_R=normal((H, d_head, d_head), seed, S_WR, std_w, f, device),
+        W_V=normal((d_model, G * d_head), seed, S_WV, std_w, f, device),
+        cache=normal((B, G, L, d_head), seed, S_V, 1.0, f, device),
+        lengths_before=torch.full((B,), L - 1, dtype=torch.int32, device=device),
+        lengths=torch.full((B,), L, dtype=torch.int32, device=device),
+        B=B, H=H, G=G, d_head=d_head, L=L, d_model=d_model,
+    )
