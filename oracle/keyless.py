@@ -147,6 +147,51 @@ def keyless_prefill_rows(x, Wt_Q, W_V, rows, H: int, G: int, d_head: int,
 
 
 # ---------------------------------------------------------------------------
+# Section 2.5, Eq. 14: keyless cross-attention
+# ---------------------------------------------------------------------------
+
+def keyless_cross_attention(xa, xb, W_Q, W_R, W_V, H: int, G: int, d_head: int,
+                            scale: float | None = None):
+    """Keyless cross-attention of Eq. 14: the queries come from one sequence, the
+    values (which also do the routing) from another, with no mask.
+
+    For batch b and query head h with group g = h // (H // G):
+      Q~_h = X^(a) W^Q_h W^R_h      [N_a, d_k]
+      V_g  = X^(b) W^V_g            [N_b, d_k]
+      O_h  = softmax(tau * Q~_h V_g^T) V_g
+    If W_R is None, W_Q is taken as the already folded W~^Q.
+
+    xa: [B, N_a, d]; xb: [B, N_b, d]; the weights as in keyless_prefill.
+    Returns (O [B, N_a, H, d_k], Q~ [B, N_a, H, d_k], V [B, N_b, G, d_k]).
+    An empty X^(b) (N_b = 0) gives zero output rows, as an empty cache does.
+    """
+    xa = _f64(xa)
+    xb = _f64(xb)
+    W_Q = _f64(W_Q)
+    W_V = _f64(W_V)
+    B, Na, _ = xa.shape
+    Nb = xb.shape[1]
+    tau = default_scale(d_head) if scale is None else float(scale)
+    rep = H // G
+    O = np.zeros((B, Na, H, d_head))
+    Qr = np.zeros((B, Na, H, d_head))
+    V = np.zeros((B, Nb, G, d_head))
+    for b in range(B):
+        for g in range(G):
+            V[b, :, g, :] = xb[b] @ W_V[:, g * d_head:(g + 1) * d_head]
+        for h in range(H):
+            Q_h = xa[b] @ W_Q[:, h * d_head:(h + 1) * d_head]
+            Qt_h = Q_h if W_R is None else Q_h @ _f64(W_R)[h]
+            Qr[b, :, h, :] = Qt_h
+            if Nb == 0:
+                continue
+            V_g = V[b, :, h // rep, :]
+            S = tau * (Qt_h @ V_g.T)  # [N_a, N_b], every query sees every value
+            O[b, :, h, :] = softmax_rows(S) @ V_g
+    return O, Qr, V
+
+
+# ---------------------------------------------------------------------------
 # Section 3: value-only cache, append and decode
 # ---------------------------------------------------------------------------
 

@@ -34,6 +34,17 @@ MUTATIONS = [
      "q[b, h] = qh if W_R is None else qh @ _f64(W_R)[h].T",
      "routing matrix transposed in the decode-step projection"),
     ("decode_one", "s = tau * (V_rows @ q)", "s = (V_rows @ q)", "decode without the scale"),
+    ("keyless_cross_attention", "Qt_h = Q_h if W_R is None else Q_h @ _f64(W_R)[h]",
+     "Qt_h = Q_h if W_R is None else Q_h @ _f64(W_R)[h].T", "routing matrix transposed in cross-attention"),
+    ("keyless_cross_attention", "V[b, :, g, :] = xb[b] @", "V[b, :, g, :] = xa[b] @",
+     "cross-attention values taken from the query sequence"),
+    ("keyless_cross_attention", "V_g = V[b, :, h // rep, :]", "V_g = V[b, :, h % G, :]",
+     "cross-attention head-to-group map h % G"),
+    ("keyless_cross_attention", "O[b, :, h, :] = softmax_rows(S) @ V_g",
+     "O[b, :, h, :] = softmax_rows(np.where(np.tril(np.ones(S.shape, dtype=bool)), S, -np.inf)) @ V_g",
+     "cross-attention with a causal mask"),
+    ("keyless_cross_attention", "S = tau * (Qt_h @ V_g.T)", "S = (Qt_h @ V_g.T)",
+     "cross-attention without the scale"),
 ]
 
 

@@ -9,6 +9,8 @@ the oracle itself. CPU only.
   torch's scaled_dot_product_attention (float64, CPU) on (Q~, V, V);
 * brute-force scalar loops over Eq. 4 on tiny inputs;
 * decode over a prefix equals the prefill row of the same token;
+* cross-attention (Eq. 14): a hand-derived case, the library call with
+  N_a != N_b, X^(a) = X^(b) gives unmasked self-attention, rows are decodes;
 * paged equals contiguous, block order does not matter, grouped heads equal
   MHA over repeated values;
 * the byte accounting of Section 5.5 and Table 2.
@@ -181,6 +183,76 @@ def test_brute_force_against_library():
     Q = (X @ Wt)[None, :, None, :]
     V = (X @ Wv)[None, :, None, :]
     np.testing.assert_allclose(_sdpa(Q, V, V, True)[0, :, 0, :], ref, rtol=0, atol=1e-12)
+
+
+def test_closed_form_cross_attention():
+    case = json.load(open(os.path.join(GOLD, "closed_form_cases.json")))["cross_three_queries_two_values"]
+    Xa, Xb = np.array(case["Xa"])[None], np.array(case["Xb"])[None]
+    W_R = (_sym(case["W_R_factor"]) * np.array(case["W_R_matrix"]))[None]
+    O, _, _ = K.keyless_cross_attention(Xa, Xb, np.eye(2), W_R, np.eye(2), H=1, G=1, d_head=2)
+    np.testing.assert_allclose(O[0, :, 0, :], case["expected_out"], rtol=0, atol=1e-15)
+
+
+def test_cross_attention_matches_library_sdpa():
+    """Eq. 14 is unmasked attention with queries from X^(a) and keys = values
+    from X^(b); N_a != N_b on both sides of the square."""
+    B, Na, Nb, d, dk = 2, 9, 14, 20, 5
+    for H, G in ((4, 4), (4, 2), (4, 1)):
+        xa, xb = rng.standard_normal((B, Na, d)), rng.standard_normal((B, Nb, d))
+        W_Q = rng.standard_normal((d, H * dk)) / math.sqrt(d)
+        W_R = rng.standard_normal((H, dk, dk)) / math.sqrt(dk)
+        W_V = rng.standard_normal((d, G * dk)) / math.sqrt(d)
+        O, Qr, V = K.keyless_cross_attention(xa, xb, W_Q, W_R, W_V, H=H, G=G, d_head=dk)
+        Qt = np.einsum("bnd,dhk->bnhk", xa, W_Q.reshape(d, H, dk))
+        Qt = np.einsum("bnhk,hkj->bnhj", Qt, W_R)
+        Vg = (xb @ W_V).reshape(B, Nb, G, dk)
+        Vh = np.repeat(Vg, H // G, axis=2)
+        np.testing.assert_allclose(O, _sdpa(Qt, Vh, Vh, False), rtol=0, atol=1e-12)
+        np.testing.assert_allclose(Qr, Qt, rtol=0, atol=1e-12)
+        np.testing.assert_allclose(V, Vg, rtol=0, atol=1e-12)
+        # And the other way round: more queries than values.
+        O2, _, _ = K.keyless_cross_attention(xb, xa, W_Q, W_R, W_V, H=H, G=G, d_head=dk)
+        Qt2 = np.einsum("bnhk,hkj->bnhj", np.einsum("bnd,dhk->bnhk", xb, W_Q.reshape(d, H, dk)), W_R)
+        Vh2 = np.repeat((xa @ W_V).reshape(B, Na, G, dk), H // G, axis=2)
+        np.testing.assert_allclose(O2, _sdpa(Qt2, Vh2, Vh2, False), rtol=0, atol=1e-12)
+
+
+def test_cross_attention_of_a_sequence_with_itself_is_unmasked_self_attention():
+    B, N, d, H, G, dk = 2, 11, 12, 4, 2, 3
+    x = rng.standard_normal((B, N, d))
+    W_Q, W_V = rng.standard_normal((d, H * dk)), rng.standard_normal((d, G * dk))
+    W_R = rng.standard_normal((H, dk, dk)) / 2
+    O, Qr, V = K.keyless_cross_attention(x, x, W_Q, W_R, W_V, H=H, G=G, d_head=dk)
+    O_s, Qr_s, V_s = K.keyless_prefill(x, W_Q, W_R, W_V, H=H, G=G, d_head=dk, causal=False)
+    np.testing.assert_allclose(O, O_s, rtol=0, atol=1e-12)
+    np.testing.assert_allclose(Qr, Qr_s, rtol=0, atol=1e-12)
+    np.testing.assert_allclose(V, V_s, rtol=0, atol=1e-12)
+
+
+def test_cross_attention_rows_are_decodes_over_all_values():
+    """Each query row of Eq. 14 is the value-only decode of that routed query
+    over every value of X^(b), the Section 3 weighted average."""
+    B, Na, Nb, d, H, G, dk = 2, 5, 8, 10, 4, 2, 3
+    xa, xb = rng.standard_normal((B, Na, d)), rng.standard_normal((B, Nb, d))
+    W_Q, W_V = rng.standard_normal((d, H * dk)), rng.standard_normal((d, G * dk))
+    W_R = rng.standard_normal((H, dk, dk)) / 2
+    O, Qr, V = K.keyless_cross_attention(xa, xb, W_Q, W_R, W_V, H=H, G=G, d_head=dk)
+    cache = np.ascontiguousarray(V.transpose(0, 2, 1, 3))  # [B, G, N_b, dk]
+    for i in range(Na):
+        out = K.keyless_decode(Qr[:, i], cache, np.full(B, Nb), H=H, G=G)
+        np.testing.assert_allclose(out, O[:, i], rtol=0, atol=1e-12)
+
+
+def test_cross_attention_one_value_and_no_values():
+    B, Na, d, H, G, dk = 1, 4, 6, 2, 1, 3
+    xa, xb = rng.standard_normal((B, Na, d)), rng.standard_normal((B, 1, d))
+    W_Q, W_V = rng.standard_normal((d, H * dk)), rng.standard_normal((d, G * dk))
+    O, _, V = K.keyless_cross_attention(xa, xb, W_Q, None, W_V, H=H, G=G, d_head=dk)
+    for i in range(Na):
+        for h in range(H):
+            np.testing.assert_allclose(O[0, i, h], V[0, 0, 0], rtol=0, atol=1e-14)
+    O0, _, _ = K.keyless_cross_attention(xa, xb[:, :0], W_Q, None, W_V, H=H, G=G, d_head=dk)
+    assert O0.shape == (B, Na, H, dk) and not O0.any()
 
 
 def test_decode_over_prefix_equals_prefill_row():
