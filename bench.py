@@ -335,6 +335,23 @@ def extra_measurements(torch, kb, configs, dev):
                            "frac_of_bf16_mfma_peak": round(flops / (ms * 1e-3) / 1e12 /
                                                           BF16_MFMA_PEAK_TFLOPS, 4)}
     del p, packed, x, outs
+    # Cross-attention (Eq. 14): 1024 attending tokens against 4096 attended ones.
+    c = configs.cross_bf16(device=dev)
+    B, Na, Nb, dm, H, G, dk = (c[k] for k in ("B", "N_a", "N_b", "d_model", "H", "G", "d_head"))
+    packed = kb.keyless_pack_weights(c["W_Q"], c["W_R"], c["W_V"], H, G)  # once
+    outs = kb.keyless_cross_attention_packed(c["xa"], c["xb"], packed, H, G, return_qv=True)
+
+    def cstep(i):
+        kb.keyless_cross_attention_packed(c["xa"], c["xb"], packed, H, G, out=outs[0],
+                                          q_routed_out=outs[1], v_out=outs[2])
+    ms = timed_steps(cstep, 10, 3, torch)
+    flops = 2 * B * dm * dk * (Na * H + Nb * G) + 4 * B * H * Na * Nb * dk
+    res["cross_bf16"] = {"workload": "batch 4, 1024 attending x 4096 attended tokens, d_model "
+                                     "4096, 32 heads x 128, no mask",
+                         "ms": round(ms, 3), "tflops": round(flops / (ms * 1e-3) / 1e12, 2),
+                         "frac_of_bf16_mfma_peak": round(flops / (ms * 1e-3) / 1e12 /
+                                                        BF16_MFMA_PEAK_TFLOPS, 4)}
+    del c, packed, outs
     # Paged grouped-head decode.
     g = configs.paged_gqa_bf16(device=dev)
     vc = kb.ValueCache(g["data"], g["block_table"])

@@ -145,6 +145,48 @@ int keyless_prefill_packed(const void* x, const void* packed, int B, int N, int 
                            void* stream);
 
 /*
+ * keyless_cross_attention - keyless cross-attention (Section 2.5, Eq. 14): the
+ * queries come from one sequence, the values, which also route, from another:
+ *   out[b, i, h] = softmax_j(scale <q~_i, v_j>) summed against v_j, where
+ *   q~_i = xa[b, i] W~^Q_h (i < N_a) and v_j = xb[b, j] W^V_g (j < N_b),
+ *   g = h / (H / G); every query sees every value (no mask).
+ *   xa      [B, N_a, d_model]   the attending sequence (e.g. the decoder side)
+ *   xb      [B, N_b, d_model]   the attended sequence (e.g. an encoder or
+ *                               another modality); N_a and N_b are independent;
+ *                               NULL is accepted when N_b = 0
+ *   W_Q, W_R, W_V, scale, dtype as for keyless_prefill
+ *   out     [B, N_a, H, d_head]
+ *   q_routed_out  [B, N_a, H, d_head] or NULL
+ *   v_out         [B, N_b, G, d_head] or NULL (the values, cacheable once per xb)
+ *   ws, ws_bytes  workspace of at least keyless_cross_attention_workspace_size(...)
+ * N_b = 0 gives zero output rows (nothing to average). xa == xb with N_a == N_b
+ * is keyless_prefill with causal = 0. Same precision and errors as
+ * keyless_prefill.
+ */
+int keyless_cross_attention(const void* xa, const void* xb, const void* W_Q, const void* W_R,
+                            const void* W_V, int B, int N_a, int N_b, int d_model, int H, int G,
+                            int d_head, float scale, kl_dtype dtype, void* out,
+                            void* q_routed_out, void* v_out, void* ws, size_t ws_bytes,
+                            void* stream);
+
+size_t keyless_cross_attention_workspace_size(int B, int N_a, int N_b, int d_model, int H, int G,
+                                              int d_head, kl_dtype dtype, int has_W_R,
+                                              int has_q_routed_out, int has_v_out);
+
+/*
+ * keyless_cross_attention_packed - keyless_cross_attention with weights prepared
+ * by keyless_pack_weights (bf16 only; d_model a multiple of 64): the routed
+ * queries come from the first H*d_head packed rows applied to xa, the values
+ * from the remaining G*d_head rows applied to xb. The workspace is needed only
+ * for q_routed / v when those outputs are NULL: B*N_a*H*d_head*2 and
+ * B*N_b*G*d_head*2 bytes, each rounded up to 256.
+ */
+int keyless_cross_attention_packed(const void* xa, const void* xb, const void* packed, int B,
+                                   int N_a, int N_b, int d_model, int H, int G, int d_head,
+                                   float scale, kl_dtype dtype, void* out, void* q_routed_out,
+                                   void* v_out, void* ws, size_t ws_bytes, void* stream);
+
+/*
  * keyless_decode_project - the projections of one decode step (Section 3: the
  * current token's routed query q~_{n+1} and its value v_{n+1}, i.e. the
  * projections of Eq. 2 for one token per sequence), from weights prepared by

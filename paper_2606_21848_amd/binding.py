@@ -23,6 +23,8 @@ KL_CONTIGUOUS, KL_PAGED = 0, 1
 EXPORTS = (
     "keyless_fold_routing", "keyless_prefill", "keyless_prefill_workspace_size",
     "keyless_packed_weights_size", "keyless_pack_weights", "keyless_prefill_packed",
+    "keyless_cross_attention", "keyless_cross_attention_workspace_size",
+    "keyless_cross_attention_packed",
     "keyless_decode_project", "keyless_decode", "keyless_decode_chunked", "keyless_decode_workspace_size",
     "value_cache_append", "standard_decode", "standard_decode_chunked",
     "keyless_set_kernel_timer", "keyless_last_error", "keyless_version",
@@ -66,6 +68,11 @@ def load(path: str = LIB_PATH):
         "keyless_packed_weights_size": (sz, [i, i, i, i, i]),
         "keyless_pack_weights": (i, [vp, vp, vp, i, i, i, i, i, vp, vp]),
         "keyless_prefill_packed": (i, [vp, vp, i, i, i, i, i, i, i, f, i, vp, vp, vp, vp, sz, vp]),
+        "keyless_cross_attention": (i, [vp, vp, vp, vp, vp, i, i, i, i, i, i, i, f, i, vp, vp, vp,
+                                        vp, sz, vp]),
+        "keyless_cross_attention_workspace_size": (sz, [i, i, i, i, i, i, i, i, i, i, i]),
+        "keyless_cross_attention_packed": (i, [vp, vp, vp, i, i, i, i, i, i, i, f, i, vp, vp, vp,
+                                               vp, sz, vp]),
         "keyless_decode_project": (i, [vp, vp, i, i, i, i, i, i, vp, vp, cp, vp, vp]),
         "keyless_decode": (i, [vp, cp, vp, i, i, f, vp, vp, sz, vp]),
         "keyless_decode_chunked": (i, [vp, cp, vp, i, i, f, vp, vp, sz, i, vp]),
@@ -302,6 +309,69 @@ def keyless_prefill_packed(x: torch.Tensor, packed: torch.Tensor, H: int, G: int
                                        scale, _dt(x), _ptr(out), _ptr(q_routed_out), _ptr(v_out),
                                        _ptr(workspace), 0 if workspace is None else workspace.numel(),
                                        _stream(x)))
+    if return_qv:
+        return out, q_routed_out, v_out
+    return out
+
+
+def _cross_outputs(xa, xb, H, G, dk, return_qv, out, q_routed_out, v_out):
+    B, Na, Nb = xa.shape[0], xa.shape[1], xb.shape[1]
+    if out is None:
+        out = torch.empty((B, Na, H, dk), dtype=xa.dtype, device=xa.device)
+    if return_qv:
+        if q_routed_out is None:
+            q_routed_out = torch.empty((B, Na, H, dk), dtype=xa.dtype, device=xa.device)
+        if v_out is None:
+            v_out = torch.empty((B, Nb, G, dk), dtype=xa.dtype, device=xa.device)
+    return out, q_routed_out, v_out
+
+
+def keyless_cross_attention(xa: torch.Tensor, xb: torch.Tensor, W_Q: torch.Tensor,
+                            W_R: torch.Tensor | None, W_V: torch.Tensor, H: int, G: int,
+                            scale: float = 0.0, return_qv: bool = False, out=None,
+                            q_routed_out=None, v_out=None, workspace=None):
+    """Keyless cross-attention (queries from xa [B, N_a, d], values from xb
+    [B, N_b, d]); returns out [B, N_a, H, d_k] (and Q~, V if return_qv)."""
+    load()
+    B, Na, d_model = xa.shape
+    Nb = xb.shape[1]
+    dk = W_Q.shape[1] // H
+    out, q_routed_out, v_out = _cross_outputs(xa, xb, H, G, dk, return_qv, out, q_routed_out, v_out)
+    need = int(_lib.keyless_cross_attention_workspace_size(
+        B, Na, Nb, d_model, H, G, dk, _dt(xa), int(W_R is not None), int(q_routed_out is not None),
+        int(v_out is not None)))
+    if workspace is None:
+        workspace = torch.empty(max(need, 256), dtype=torch.uint8, device=xa.device)
+    _check(_lib.keyless_cross_attention(_ptr(xa), _ptr(xb), _ptr(W_Q), _ptr(W_R), _ptr(W_V), B, Na,
+                                        Nb, d_model, H, G, dk, scale, _dt(xa), _ptr(out),
+                                        _ptr(q_routed_out), _ptr(v_out), _ptr(workspace),
+                                        workspace.numel(), _stream(xa)))
+    if return_qv:
+        return out, q_routed_out, v_out
+    return out
+
+
+def keyless_cross_attention_packed(xa: torch.Tensor, xb: torch.Tensor, packed: torch.Tensor,
+                                   H: int, G: int, scale: float = 0.0, return_qv: bool = False,
+                                   out=None, q_routed_out=None, v_out=None, workspace=None):
+    """keyless_cross_attention with weights from keyless_pack_weights."""
+    load()
+    B, Na, d_model = xa.shape
+    Nb = xb.shape[1]
+    dk = packed.shape[0] // (H + G)
+    out, q_routed_out, v_out = _cross_outputs(xa, xb, H, G, dk, return_qv, out, q_routed_out, v_out)
+    need = 0
+    if q_routed_out is None:
+        need += -(-B * Na * H * dk * 2 // 256) * 256
+    if v_out is None:
+        need += -(-B * Nb * G * dk * 2 // 256) * 256
+    if workspace is None and need:
+        workspace = torch.empty(need, dtype=torch.uint8, device=xa.device)
+    _check(_lib.keyless_cross_attention_packed(_ptr(xa), _ptr(xb), _ptr(packed), B, Na, Nb, d_model,
+                                               H, G, dk, scale, _dt(xa), _ptr(out),
+                                               _ptr(q_routed_out), _ptr(v_out), _ptr(workspace),
+                                               0 if workspace is None else workspace.numel(),
+                                               _stream(xa)))
     if return_qv:
         return out, q_routed_out, v_out
     return out

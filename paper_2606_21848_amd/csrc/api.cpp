@@ -4,6 +4,7 @@
 
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
@@ -343,15 +344,22 @@ int keyless_pack_weights(const void* W_Q, const void* W_R, const void* W_V, int 
 size_t keyless_prefill_workspace_size(int B, int N, int d_model, int H, int G, int d_head,
                                       kl_dtype dtype, int has_W_R, int has_q_routed_out,
                                       int has_v_out) {
-  if (B < 0 || N < 0 || d_model <= 0 || H <= 0 || G <= 0 || d_head <= 0) return 0;
+  return keyless_cross_attention_workspace_size(B, N, N, d_model, H, G, d_head, dtype, has_W_R,
+                                                has_q_routed_out, has_v_out);
+}
+
+size_t keyless_cross_attention_workspace_size(int B, int N_a, int N_b, int d_model, int H, int G,
+                                              int d_head, kl_dtype dtype, int has_W_R,
+                                              int has_q_routed_out, int has_v_out) {
+  if (B < 0 || N_a < 0 || N_b < 0 || d_model <= 0 || H <= 0 || G <= 0 || d_head <= 0) return 0;
   const size_t e = elem_bytes(dtype);
   size_t n = 0;
   if (dtype == KL_BF16)
     n += keyless_packed_weights_size(d_model, H, G, d_head, dtype);
   else if (has_W_R)
     n += align256((size_t)d_model * H * d_head * e);
-  if (!has_q_routed_out) n += align256((size_t)B * N * H * d_head * e);
-  if (!has_v_out) n += align256((size_t)B * N * G * d_head * e);
+  if (!has_q_routed_out) n += align256((size_t)B * N_a * H * d_head * e);
+  if (!has_v_out) n += align256((size_t)B * N_b * G * d_head * e);
   return n;
 }
 
@@ -374,10 +382,21 @@ int check_prefill_args(const char* who, const void* x, const void* W, const void
   return KL_OK;
 }
 
-// Attention over the routed queries and values (Eq. 2 with the Eq. 4 score).
+// Cross-attention adds the value sequence: its length in range, and non-NULL
+// unless it is empty.
+int check_cross_args(const char* who, const void* xb, int B, int N_b) {
+  if (!xb && N_b > 0) return fail(KL_ERR_INVALID_ARG, "%s: xb must be non-NULL", who);
+  if (N_b < 0) return fail(KL_ERR_INVALID_ARG, "%s: bad N_b=%d", who, N_b);
+  if ((long)B * N_b > (1L << 30)) return fail(KL_ERR_UNSUPPORTED, "%s: B*N_b too large", who);
+  return KL_OK;
+}
+
+// Attention over the routed queries [B, N, H, d_head] and values [B, Nk, G,
+// d_head] (Eq. 2 with the Eq. 4 score; Eq. 14 when the two come from different
+// sequences).
 int run_attention(const char* who, const void* qr, long q_stride, const void* vv, long v_stride,
-                  void* out, int B, int N, int H, int G, int d_head, int causal, float scale,
-                  kl_dtype dtype, hipStream_t st) {
+                  void* out, int B, int N, int Nk, int H, int G, int d_head, int causal,
+                  float scale, kl_dtype dtype, hipStream_t st) {
   kl::AttnParams a{};
   a.q = qr;
   a.v = vv;
@@ -387,30 +406,150 @@ int run_attention(const char* who, const void* qr, long q_stride, const void* vv
   a.o_stride = (long)H * d_head;
   a.B = B;
   a.N = N;
+  a.Nk = Nk;
   a.H = H;
   a.G = G;
   a.D = d_head;
   a.causal = causal ? 1 : 0;
   a.scale_log2 = scale_or_default(scale, d_head) * kLog2e;
   a.dtype = dtype;
-  if (kl::attn_bf16_supported(a)) return hip_status(kl::launch_prefill_attention(a, st), who);
+  // No value rows (an empty X^(b)): the VALU kernel writes the zero rows.
+  if (Nk > 0 && kl::attn_bf16_supported(a))
+    return hip_status(kl::launch_prefill_attention(a, st), who);
   return hip_status(kl::launch_prefill_attention_simple(a, st), who);
 }
 
-// bf16 prefill against packed weights; qr / vv are where the routed queries and
-// values go (caller outputs or workspace).
-int prefill_packed_core(const char* who, const void* x, const void* packed, int B, int N,
-                        int d_model, int H, int G, int d_head, int causal, float scale, void* out,
-                        void* qr, void* vv, hipStream_t st) {
-  const int M = B * N, NQ = H * d_head, NV = G * d_head;
-  if (!kl::gemm_bf16_supported(M, NQ + NV, d_model, d_model, NQ, NV))
+// Workspace carve-out shared by the entry points: routed queries and values go
+// to the caller's buffers when given, else to the workspace (queries first).
+struct QV {
+  void* qr;
+  void* vv;
+};
+QV carve_qv(char* w, int B, int N_a, int N_b, int H, int G, int d_head, size_t e,
+            void* q_routed_out, void* v_out) {
+  QV r{q_routed_out, v_out};
+  if (!r.qr) {
+    r.qr = w;
+    w += align256((size_t)B * N_a * H * d_head * e);
+  }
+  if (!r.vv) r.vv = w;
+  return r;
+}
+
+// bf16 projections and attention against packed weights, queries from xa
+// [B, N_a, d_model], values from xb [B, N_b, d_model]. Self-attention (xa == xb,
+// N_a == N_b) projects both in one GEMM launch; cross-attention takes two, the
+// value one on the packed rows from H d_head on.
+int attend_packed_core(const char* who, const void* xa, const void* xb, const void* packed, int B,
+                       int N_a, int N_b, int d_model, int H, int G, int d_head, int causal,
+                       float scale, void* out, void* qr, void* vv, hipStream_t st) {
+  const int NQ = H * d_head, NV = G * d_head;
+  const int Ma = B * N_a, Mb = B * N_b;
+  if (!kl::gemm_bf16_supported(std::max(std::max(Ma, Mb), 1), NQ + NV, d_model, d_model, NQ, NV))
     return fail(KL_ERR_UNSUPPORTED, "%s: d_model=%d must be a multiple of 64 for bf16", who,
                 d_model);
-  int s = hip_status(kl::launch_gemm_bf16_packed(x, M, d_model, d_model, packed, NQ + NV, NQ, qr,
+  int s = KL_OK;
+  if (xa == xb && N_a == N_b) {
+    if (Ma > 0)
+      s = hip_status(kl::launch_gemm_bf16_packed(xa, Ma, d_model, d_model, packed, NQ + NV, NQ, qr,
                                                  NQ, vv, NV, st),
                      who);
+  } else {
+    if (Ma > 0)
+      s = hip_status(kl::launch_gemm_bf16_packed(xa, Ma, d_model, d_model, packed, NQ, NQ, qr, NQ,
+                                                 qr, NQ, st),
+                     who);
+    if (s == KL_OK && Mb > 0) {
+      const void* pv = static_cast<const uint16_t*>(packed) + (size_t)NQ * d_model;
+      s = hip_status(kl::launch_gemm_bf16_packed(xb, Mb, d_model, d_model, pv, NV, 0, vv, NV, vv,
+                                                 NV, st),
+                     who);
+    }
+  }
+  if (s != KL_OK || Ma == 0) return s;
+  return run_attention(who, qr, NQ, vv, NV, out, B, N_a, N_b, H, G, d_head, causal, scale, KL_BF16,
+                       st);
+}
+
+int attend_packed_entry(const char* who, const void* xa, const void* xb, const void* packed, int B,
+                        int N_a, int N_b, int d_model, int H, int G, int d_head, int causal,
+                        float scale, kl_dtype dtype, void* out, void* q_routed_out, void* v_out,
+                        void* ws, size_t ws_bytes, hipStream_t st) {
+  if (dtype != KL_BF16) return fail(KL_ERR_UNSUPPORTED, "%s: packed weights are bf16 only", who);
+  const size_t e = 2;
+  const size_t qbytes = q_routed_out ? 0 : align256((size_t)B * N_a * H * d_head * e);
+  const size_t vbytes = v_out ? 0 : align256((size_t)B * N_b * G * d_head * e);
+  if (qbytes + vbytes && (!ws || ws_bytes < qbytes + vbytes))
+    return fail(KL_ERR_WORKSPACE, "%s: workspace of %zu bytes needed, %zu given", who,
+                qbytes + vbytes, ws_bytes);
+  if (B == 0 || (N_a == 0 && N_b == 0)) return KL_OK;
+  const QV qv = carve_qv(static_cast<char*>(ws), B, N_a, N_b, H, G, d_head, e, q_routed_out, v_out);
+  return attend_packed_core(who, xa, xb, packed, B, N_a, N_b, d_model, H, G, d_head, causal, scale,
+                            out, qv.qr, qv.vv, st);
+}
+
+// Projections and attention from the weights as given: bf16 folds and packs them
+// into the workspace and takes the packed path; fp32 runs the VALU kernels.
+int attend_entry(const char* who, const void* xa, const void* xb, const void* W_Q,
+                 const void* W_R, const void* W_V, int B, int N_a, int N_b, int d_model, int H,
+                 int G, int d_head, int causal, float scale, kl_dtype dtype, void* out,
+                 void* q_routed_out, void* v_out, void* ws, size_t ws_bytes, hipStream_t st) {
+  if (!W_V) return fail(KL_ERR_INVALID_ARG, "%s: W_V must be non-NULL", who);
+  const size_t need = keyless_cross_attention_workspace_size(
+      B, N_a, N_b, d_model, H, G, d_head, dtype, W_R != nullptr, q_routed_out != nullptr,
+      v_out != nullptr);
+  if (need && (!ws || ws_bytes < need))
+    return fail(KL_ERR_WORKSPACE, "%s: workspace of %zu bytes needed, %zu given", who, need, ws_bytes);
+  if (B == 0 || (N_a == 0 && N_b == 0)) return KL_OK;
+  const size_t e = elem_bytes(dtype);
+  char* w = static_cast<char*>(ws);
+  int s;
+  if (dtype == KL_BF16) {
+    if (d_model % 64 != 0)
+      return fail(KL_ERR_UNSUPPORTED, "%s: d_model=%d must be a multiple of 64 for bf16", who,
+                  d_model);
+    void* packed = w;
+    w += keyless_packed_weights_size(d_model, H, G, d_head, dtype);
+    s = keyless_pack_weights(W_Q, W_R, W_V, d_model, H, G, d_head, dtype, packed, st);
+    if (s != KL_OK) return s;
+    const QV qv = carve_qv(w, B, N_a, N_b, H, G, d_head, e, q_routed_out, v_out);
+    return attend_packed_core(who, xa, xb, packed, B, N_a, N_b, d_model, H, G, d_head, causal,
+                              scale, out, qv.qr, qv.vv, st);
+  }
+  // fp32: VALU kernels on the weights as given.
+  const void* Wt = W_Q;
+  if (W_R) {
+    void* fold = w;
+    w += align256((size_t)d_model * H * d_head * e);
+    s = keyless_fold_routing(W_Q, W_R, d_model, H, d_head, dtype, fold, st);
+    if (s != KL_OK) return s;
+    Wt = fold;
+  }
+  const QV qv = carve_qv(w, B, N_a, N_b, H, G, d_head, e, q_routed_out, v_out);
+  const int NQ = H * d_head, NV = G * d_head;
+  kl::GemmParams g{};
+  g.K = d_model;
+  g.lda = d_model;
+  g.batch = 1;
+  g.dtype = dtype;
+  g.A = xa;
+  g.M = B * N_a;
+  g.Bm = Wt;
+  g.C = qv.qr;
+  g.N = NQ;
+  g.ldb = g.ldc = NQ;
+  s = hip_status(kl::launch_gemm_simple(g, st), who);
   if (s != KL_OK) return s;
-  return run_attention(who, qr, NQ, vv, NV, out, B, N, H, G, d_head, causal, scale, KL_BF16, st);
+  g.A = xb;
+  g.M = B * N_b;
+  g.Bm = W_V;
+  g.C = qv.vv;
+  g.N = NV;
+  g.ldb = g.ldc = NV;
+  s = hip_status(kl::launch_gemm_simple(g, st), who);
+  if (s != KL_OK || N_a == 0) return s;
+  return run_attention(who, qv.qr, NQ, qv.vv, NV, out, B, N_a, N_b, H, G, d_head, causal, scale,
+                       dtype, st);
 }
 
 }  // namespace
@@ -424,19 +563,22 @@ int keyless_prefill_packed(const void* x, const void* packed, int B, int N, int 
   const char* who = "keyless_prefill_packed";
   int s = check_prefill_args(who, x, packed, out, B, N, d_model, H, G, d_head, dtype, scale);
   if (s != KL_OK) return s;
-  if (dtype != KL_BF16) return fail(KL_ERR_UNSUPPORTED, "%s: packed weights are bf16 only", who);
-  const size_t e = 2;
-  const size_t qbytes = q_routed_out ? 0 : align256((size_t)B * N * H * d_head * e);
-  const size_t vbytes = v_out ? 0 : align256((size_t)B * N * G * d_head * e);
-  if (qbytes + vbytes && (!ws || ws_bytes < qbytes + vbytes))
-    return fail(KL_ERR_WORKSPACE, "%s: workspace of %zu bytes needed, %zu given", who,
-                qbytes + vbytes, ws_bytes);
-  if (B == 0 || N == 0) return KL_OK;
-  char* w = static_cast<char*>(ws);
-  void* qr = q_routed_out ? q_routed_out : w;
-  void* vv = v_out ? v_out : w + qbytes;
-  return prefill_packed_core(who, x, packed, B, N, d_model, H, G, d_head, causal, scale, out, qr,
-                             vv, static_cast<hipStream_t>(stream));
+  return attend_packed_entry(who, x, x, packed, B, N, N, d_model, H, G, d_head, causal, scale,
+                             dtype, out, q_routed_out, v_out, ws, ws_bytes,
+                             static_cast<hipStream_t>(stream));
+}
+
+int keyless_cross_attention_packed(const void* xa, const void* xb, const void* packed, int B,
+                                   int N_a, int N_b, int d_model, int H, int G, int d_head,
+                                   float scale, kl_dtype dtype, void* out, void* q_routed_out,
+                                   void* v_out, void* ws, size_t ws_bytes, void* stream) {
+  const char* who = "keyless_cross_attention_packed";
+  int s = check_prefill_args(who, xa, packed, out, B, N_a, d_model, H, G, d_head, dtype, scale);
+  if (s == KL_OK) s = check_cross_args(who, xb, B, N_b);
+  if (s != KL_OK) return s;
+  return attend_packed_entry(who, xa, xb, packed, B, N_a, N_b, d_model, H, G, d_head, 0, scale,
+                             dtype, out, q_routed_out, v_out, ws, ws_bytes,
+                             static_cast<hipStream_t>(stream));
 }
 
 int keyless_decode_project(const void* x, const void* packed, int B, int d_model, int H, int G,
@@ -501,70 +643,23 @@ int keyless_prefill(const void* x, const void* W_Q, const void* W_R, const void*
   const char* who = "keyless_prefill";
   int s = check_prefill_args(who, x, W_Q, out, B, N, d_model, H, G, d_head, dtype, scale);
   if (s != KL_OK) return s;
-  if (!W_V) return fail(KL_ERR_INVALID_ARG, "%s: W_V must be non-NULL", who);
-  const size_t need = keyless_prefill_workspace_size(B, N, d_model, H, G, d_head, dtype,
-                                                     W_R != nullptr, q_routed_out != nullptr,
-                                                     v_out != nullptr);
-  if (need && (!ws || ws_bytes < need))
-    return fail(KL_ERR_WORKSPACE, "%s: workspace of %zu bytes needed, %zu given", who, need, ws_bytes);
-  if (B == 0 || N == 0) return KL_OK;
-  hipStream_t st = static_cast<hipStream_t>(stream);
-  const size_t e = elem_bytes(dtype);
-  char* w = static_cast<char*>(ws);
-  if (dtype == KL_BF16) {
-    // Fold and pack the weights into the workspace, then the packed path.
-    if (d_model % 64 != 0)
-      return fail(KL_ERR_UNSUPPORTED, "%s: d_model=%d must be a multiple of 64 for bf16", who,
-                  d_model);
-    void* packed = w;
-    w += keyless_packed_weights_size(d_model, H, G, d_head, dtype);
-    s = keyless_pack_weights(W_Q, W_R, W_V, d_model, H, G, d_head, dtype, packed, stream);
-    if (s != KL_OK) return s;
-    void* qr = q_routed_out;
-    if (!qr) {
-      qr = w;
-      w += align256((size_t)B * N * H * d_head * e);
-    }
-    void* vv = v_out ? v_out : w;
-    return prefill_packed_core(who, x, packed, B, N, d_model, H, G, d_head, causal, scale, out,
-                               qr, vv, st);
-  }
-  // fp32: VALU kernels on the weights as given.
-  const void* Wt = W_Q;
-  if (W_R) {
-    void* fold = w;
-    w += align256((size_t)d_model * H * d_head * e);
-    s = keyless_fold_routing(W_Q, W_R, d_model, H, d_head, dtype, fold, stream);
-    if (s != KL_OK) return s;
-    Wt = fold;
-  }
-  void* qr = q_routed_out;
-  if (!qr) {
-    qr = w;
-    w += align256((size_t)B * N * H * d_head * e);
-  }
-  void* vv = v_out ? v_out : w;
-  const int NQ = H * d_head, NV = G * d_head;
-  kl::GemmParams g{};
-  g.A = x;
-  g.M = B * N;
-  g.K = d_model;
-  g.lda = d_model;
-  g.batch = 1;
-  g.dtype = dtype;
-  g.Bm = Wt;
-  g.C = qr;
-  g.N = NQ;
-  g.ldb = g.ldc = NQ;
-  s = hip_status(kl::launch_gemm_simple(g, st), who);
+  return attend_entry(who, x, x, W_Q, W_R, W_V, B, N, N, d_model, H, G, d_head, causal, scale,
+                      dtype, out, q_routed_out, v_out, ws, ws_bytes,
+                      static_cast<hipStream_t>(stream));
+}
+
+int keyless_cross_attention(const void* xa, const void* xb, const void* W_Q, const void* W_R,
+                            const void* W_V, int B, int N_a, int N_b, int d_model, int H, int G,
+                            int d_head, float scale, kl_dtype dtype, void* out,
+                            void* q_routed_out, void* v_out, void* ws, size_t ws_bytes,
+                            void* stream) {
+  const char* who = "keyless_cross_attention";
+  int s = check_prefill_args(who, xa, W_Q, out, B, N_a, d_model, H, G, d_head, dtype, scale);
+  if (s == KL_OK) s = check_cross_args(who, xb, B, N_b);
   if (s != KL_OK) return s;
-  g.Bm = W_V;
-  g.C = vv;
-  g.N = NV;
-  g.ldb = g.ldc = NV;
-  s = hip_status(kl::launch_gemm_simple(g, st), who);
-  if (s != KL_OK) return s;
-  return run_attention(who, qr, NQ, vv, NV, out, B, N, H, G, d_head, causal, scale, dtype, st);
+  return attend_entry(who, xa, xb, W_Q, W_R, W_V, B, N_a, N_b, d_model, H, G, d_head, 0, scale,
+                      dtype, out, q_routed_out, v_out, ws, ws_bytes,
+                      static_cast<hipStream_t>(stream));
 }
 
 }  // extern "C"

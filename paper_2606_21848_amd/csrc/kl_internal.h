@@ -120,11 +120,12 @@ hipError_t launch_pack_weights(const PackParams& p, hipStream_t stream);
 
 struct AttnParams {
   const void* q;   // routed queries, [B, N, H, D] with row stride q_stride (elements per token)
-  const void* v;   // values, [B, N, G, D] with row stride v_stride
+  const void* v;   // values, [B, Nk, G, D] with row stride v_stride
   void* out;       // [B, N, H, D]
   long q_stride, v_stride, o_stride;
   int B, N, H, G, D;
-  int causal;
+  int Nk;          // value rows per sequence: N for self-attention, N_b for cross-attention
+  int causal;      // only with Nk == N
   float scale_log2;
   kl_dtype dtype;
 };

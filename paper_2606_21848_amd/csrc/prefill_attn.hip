@@ -146,9 +146,9 @@ __global__ __launch_bounds__(kThreads, QB == 2 ? 3 : 2) void attn_bf16_kernel(At
 #pragma unroll
     for (int c = 0; c < T::COPIES; ++c) {
       const int r0 = jt * BKV + (c * 4 + wave) * ROWS_PER_COPY;  // uniform
-      const int r0c = min(r0, p.N - 1);
-      const int rl = min(r0 + lane / T::CHUNKS, p.N - 1) - r0c;  // 0 .. ROWS_PER_COPY - 1
-      const unsigned char* base = gV + ((size_t)b * p.N + r0c) * row_bytes;
+      const int r0c = min(r0, p.Nk - 1);
+      const int rl = min(r0 + lane / T::CHUNKS, p.Nk - 1) - r0c;  // 0 .. ROWS_PER_COPY - 1
+      const unsigned char* base = gV + ((size_t)b * p.Nk + r0c) * row_bytes;
       copy_to_lds(base, (uint32_t)(rl * row_bytes) + col_off[c],
                   lds0 + stage * T::BYTES + (c * 4 + wave) * 1024);
     }
@@ -166,7 +166,7 @@ __global__ __launch_bounds__(kThreads, QB == 2 ? 3 : 2) void attn_bf16_kernel(At
     offT[db] = T::off(grp * 4 + (fr >> 2), col >> 3) + (col & 7) * 2;
   }
 
-  const int last_row = p.causal ? min(qt * BQ + BQ, p.N) : p.N;
+  const int last_row = p.causal ? min(qt * BQ + BQ, p.Nk) : p.Nk;
   const int ntiles = (last_row + BKV - 1) / BKV;
 #pragma unroll
   for (int s = 0; s < NSTAGE - 1; ++s)
@@ -212,7 +212,7 @@ __global__ __launch_bounds__(kThreads, QB == 2 ? 3 : 2) void attn_bf16_kernel(At
       }
     }
     // Lane holds scores of query q0 + 16 qb + fr against rows j0 + 16 kb + 4 grp + r.
-    if ((p.causal && j0 + BKV - 1 > q0) || (j0 + BKV > p.N)) {
+    if ((p.causal && j0 + BKV - 1 > q0) || (j0 + BKV > p.Nk)) {
 #pragma unroll
       for (int qb = 0; qb < QB; ++qb) {
         const int q = q0 + qb * 16 + fr;
@@ -221,7 +221,7 @@ __global__ __launch_bounds__(kThreads, QB == 2 ? 3 : 2) void attn_bf16_kernel(At
 #pragma unroll
           for (int r = 0; r < 4; ++r) {
             const int kv = j0 + kb * 16 + grp * 4 + r;
-            if (kv >= p.N || (p.causal && kv > q)) sc[kb][qb][r] = -INFINITY;
+            if (kv >= p.Nk || (p.causal && kv > q)) sc[kb][qb][r] = -INFINITY;
           }
       }
     }
@@ -353,6 +353,7 @@ bool attn_bf16_supported(const AttnParams& p) {
 
 hipError_t launch_prefill_attention(const AttnParams& p, hipStream_t st) {
   if (p.N == 0 || p.B == 0) return hipSuccess;
+  if (p.Nk <= 0 || (p.causal && p.Nk != p.N)) return hipErrorInvalidValue;
   if (p.D == 128) return launch_attn<128>(p, st);
   if (p.D == 64) return launch_attn<64>(p, st);
   return hipErrorInvalidValue;

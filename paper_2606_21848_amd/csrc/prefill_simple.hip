@@ -91,16 +91,16 @@ __global__ __launch_bounds__(64) void attn_simple_kernel(AttnParams p) {
     acc[c] = 0.f;
   }
   float m = -INFINITY, l = 0.f;
-  const int jend = p.causal ? min(p.N, i0 + 64) : p.N;
+  const int jend = p.causal ? min(p.Nk, i0 + 64) : p.Nk;
   for (int j0 = 0; j0 < jend; j0 += 64) {
     __syncthreads();
     for (int e = threadIdx.x; e < 64 * D; e += 64) {
       const int jj = e / D, c = e % D;
       const int j = j0 + jj;
-      sV[jj][c] = (j < p.N) ? ld(V, ((size_t)b * p.N + j) * p.v_stride + (size_t)g * D + c) : 0.f;
+      sV[jj][c] = (j < p.Nk) ? ld(V, ((size_t)b * p.Nk + j) * p.v_stride + (size_t)g * D + c) : 0.f;
     }
     __syncthreads();
-    const int jmax = min(64, (p.causal ? min(i + 1, p.N) : p.N) - j0);
+    const int jmax = min(64, (p.causal ? min(i + 1, p.Nk) : p.Nk) - j0);
     for (int jj = 0; jj < jmax; ++jj) {
       float s = 0.f;
 #pragma unroll
@@ -116,7 +116,7 @@ __global__ __launch_bounds__(64) void attn_simple_kernel(AttnParams p) {
   }
   if (live) {
     T* O = reinterpret_cast<T*>(p.out);
-    const float inv = 1.f / l;
+    const float inv = l > 0.f ? 1.f / l : 0.f;  // no value rows: a zero row
 #pragma unroll
     for (int c = 0; c < D; ++c) st(O, ((size_t)b * p.N + i) * p.o_stride + (size_t)h * D + c, acc[c] * inv);
   }
@@ -136,6 +136,7 @@ hipError_t launch_gemm_simple(const GemmParams& p, hipStream_t st) {
 
 hipError_t launch_prefill_attention_simple(const AttnParams& p, hipStream_t st) {
   if (p.N == 0 || p.B == 0) return hipSuccess;
+  if (p.Nk < 0 || (p.causal && p.Nk != p.N)) return hipErrorInvalidValue;
   dim3 grid((p.N + 63) / 64, p.H, p.B);
   if (p.dtype == KL_BF16) {
     if (p.D == 64) hipLaunchKernelGGL((attn_simple_kernel<uint16_t, 64>), grid, dim3(64), 0, st, p);

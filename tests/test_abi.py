@@ -136,3 +136,41 @@ def test_decode_project_rejects_bad_arguments(lib):
 def test_zero_batch_is_a_no_op(lib):
     assert decode(lib, cache(), B=0, ws_bytes=0, ws=None) == kb.KL_OK
     assert lib.value_cache_append(ctypes.byref(cache()), FAKE, FAKE, 0, 1, None) == kb.KL_OK
+
+
+def test_cross_attention_workspace_and_rejects(lib):
+    # fp32 with W_R: folded weights, then Q~ over N_a rows and V over N_b rows.
+    n = lib.keyless_cross_attention_workspace_size(2, 3, 100, 256, 4, 2, 64, kb.KL_F32, 1, 0, 0)
+    r256 = lambda b: -(-b // 256) * 256
+    assert n == r256(256 * 256 * 4) + r256(2 * 3 * 256 * 4) + r256(2 * 100 * 128 * 4)
+    # bf16: packed weights, then 384 and 640 bytes, each rounded up to 512 and 768.
+    n = lib.keyless_cross_attention_workspace_size(1, 3, 5, 128, 1, 1, 64, kb.KL_BF16, 0, 0, 0)
+    assert n == 2 * 64 * 128 * 2 + 512 + 768
+    assert lib.keyless_cross_attention_workspace_size(2, 5, 7, 256, 4, 2, 64, kb.KL_F32, 0, 1, 1) == 0
+    assert lib.keyless_prefill_workspace_size(1, 9, 256, 4, 2, 64, kb.KL_BF16, 1, 0, 0) == \
+        lib.keyless_cross_attention_workspace_size(1, 9, 9, 256, 4, 2, 64, kb.KL_BF16, 1, 0, 0)
+
+    def cross(xa=FAKE, xb=FAKE, B=1, Na=16, Nb=40, d=64, H=4, G=2, dk=64, dt=kb.KL_BF16,
+              ws_bytes=1 << 30, scale=0.0):
+        return lib.keyless_cross_attention(xa, xb, FAKE, None, FAKE, B, Na, Nb, d, H, G, dk, scale,
+                                           dt, FAKE, None, None, FAKE, ws_bytes, None)
+
+    def cross_packed(xb=FAKE, B=1, Na=16, Nb=40, dt=kb.KL_BF16, ws_bytes=1 << 30):
+        return lib.keyless_cross_attention_packed(FAKE, xb, FAKE, B, Na, Nb, 64, 4, 2, 64, 0.0, dt,
+                                                  FAKE, None, None, FAKE, ws_bytes, None)
+    expect(lib, cross(xb=None), kb.KL_ERR_INVALID_ARG, "xb")
+    expect(lib, cross(xa=None), kb.KL_ERR_INVALID_ARG, "non-NULL")
+    expect(lib, cross(Nb=-1), kb.KL_ERR_INVALID_ARG, "N_b")
+    expect(lib, cross(Na=-1), kb.KL_ERR_INVALID_ARG, "bad sizes")
+    expect(lib, cross(G=3), kb.KL_ERR_INVALID_ARG, "multiple")
+    expect(lib, cross(dk=32), kb.KL_ERR_UNSUPPORTED, "d_head 32")
+    expect(lib, cross(scale=-1.0), kb.KL_ERR_INVALID_ARG, "scale")
+    expect(lib, cross(ws_bytes=10), kb.KL_ERR_WORKSPACE, "workspace")
+    expect(lib, cross(B=1 << 16, Nb=1 << 15), kb.KL_ERR_UNSUPPORTED, "B*N_b")
+    expect(lib, cross_packed(xb=None), kb.KL_ERR_INVALID_ARG, "xb")
+    expect(lib, cross_packed(dt=kb.KL_F32), kb.KL_ERR_UNSUPPORTED, "bf16")
+    expect(lib, cross_packed(ws_bytes=10), kb.KL_ERR_WORKSPACE, "workspace")
+    # Nothing to do: no launch, no error.
+    assert cross(B=0) == kb.KL_OK
+    assert cross(Na=0, Nb=0) == kb.KL_OK
+    assert cross_packed(B=0) == kb.KL_OK

@@ -1,4 +1,4 @@
-"""The five synthetic workloads, by name, with their sizes and draw recipes.
+"""The synthetic workloads, by name, with their sizes and draw recipes.
 
 Each builder returns a dict of tensors on ``device``. Streams (the second key
 of every draw) are fixed per tensor so that one tensor's draw never depends
@@ -15,10 +15,10 @@ import torch
 from .synth import normal, permutation, uniform_int
 
 NAMES = ("tiny_fp32", "decode_bf16", "prefill_bf16", "paged_gqa_bf16", "head_to_head_bf16",
-         "decode_step_bf16")
+         "decode_step_bf16", "cross_bf16")
 
 # Stream ids (one per drawn tensor).
-S_X, S_WQ, S_WR, S_WV, S_XNEXT, S_V, S_Q, S_K, S_LEN, S_PERM, S_VNEW = range(11)
+S_X, S_WQ, S_WR, S_WV, S_XNEXT, S_V, S_Q, S_K, S_LEN, S_PERM, S_VNEW, S_XB = range(12)
 
 
 def tiny_fp32(device="cpu", seed=0, N=128, d_model=256, H=4, d_head=64):
@@ -136,4 +136,22 @@ def decode_step_bf16(device="cpu", seed=5, B=8, d_model=4096, H=32, G=32, d_head
         lengths_before=torch.full((B,), L - 1, dtype=torch.int32, device=device),
         lengths=torch.full((B,), L, dtype=torch.int32, device=device),
         B=B, H=H, G=G, d_head=d_head, L=L, d_model=d_model,
+    )
+
+
+def cross_bf16(device="cpu", seed=6, B=4, N_a=1024, N_b=4096, d_model=4096, H=32, G=32,
+               d_head=128):
+    """Keyless cross-attention (Eq. 14) in a layer shaped like the prefill
+    workload: B pairs of a 1024-token attending sequence xa and a 4096-token
+    attended sequence xb (an encoder output or another modality), both ~ N(0,1);
+    projection weights as in ``prefill_bf16``."""
+    std_w = 1.0 / math.sqrt(d_model)
+    b = torch.bfloat16
+    return dict(
+        xa=normal((B, N_a, d_model), seed, S_X, 1.0, b, device),
+        xb=normal((B, N_b, d_model), seed, S_XB, 1.0, b, device),
+        W_Q=normal((d_model, H * d_head), seed, S_WQ, std_w, b, device),
+        W_R=normal((H, d_head, d_head), seed, S_WR, std_w, b, device),
+        W_V=normal((d_model, G * d_head), seed, S_WV, std_w, b, device),
+        B=B, N_a=N_a, N_b=N_b, d_model=d_model, H=H, G=G, d_head=d_head,
     )
