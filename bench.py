@@ -216,6 +216,28 @@ def summarize_trace(trace_dir):
     for (name, grid), d in sorted(groups.items(), key=lambda kv: -sum(kv[1])):
         print(f"| `{name}` | {grid} | {len(d)} | {sum(d) / len(d):.2f} | {min(d):.2f} | "
               f"{max(d):.2f} |")
+    # Prefill-shaped calls: the projection GEMMs launched since the previous
+    # attention launch, grouped by the attention grid (kernels of one grid can
+    # serve two workloads, e.g. two GEMMs with the same tile count).
+    seq = sorted((r for r in rows if "kl::" in r["Kernel_Name"]),
+                 key=lambda r: int(r["Start_Timestamp"]))
+    calls, pending = {}, []
+    for r in seq:
+        dur = (int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3
+        if "gemm_bf16_kernel" in r["Kernel_Name"]:
+            pending.append((_grid(r), dur))
+        elif "attn_bf16_kernel" in r["Kernel_Name"]:
+            key = (_grid(r), tuple(g for g, _ in pending))
+            calls.setdefault(key, []).append([d for _, d in pending] + [dur])
+            pending = []
+    if calls:
+        print()
+        print("| attention grid | GEMM grids before it | calls | avg us per launch (GEMMs, attention) |")
+        print("|---|---|---|---|")
+        for (grid, gemms), lists in sorted(calls.items()):
+            avg = [sum(x[i] for x in lists) / len(lists) for i in range(len(lists[0]))]
+            print(f"| {grid} | {', '.join(map(str, gemms))} | {len(lists)} | "
+                  f"{', '.join(f'{a:.2f}' for a in avg)} |")
 
 
 def main():
