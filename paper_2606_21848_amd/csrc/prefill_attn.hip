@@ -1,6 +1,8 @@
 // Causal (or full) keyless attention for the bf16 prefill (Eq. 2 with the score
 // of Eq. 4): O_h = softmax(tau * Q~_h V_g^T) V_g, where the value tile is both
-// the "key" of the score and the value of the weighted sum.
+// the "key" of the score and the value of the weighted sum. Unmasked, with the
+// values taken from another sequence of Nk rows, it is the cross-attention of
+// Eq. 14.
 //
 // A workgroup (4 waves) owns 4 * 16 * QB query rows of one head; each wave owns
 // 16 * QB rows and keeps their routed-query fragments in registers. Value tiles of 64 rows
