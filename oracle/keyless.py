@@ -26,6 +26,12 @@ notes):
   GQA paragraph, leaves the assignment open; contiguous grouping is used).
 * No bias, no positional rotation and no output projection: Eq. 2 has none.
 * A cache of length 0 gives a zero output row (no value to average).
+* Latent cache (Eq. 15): the scale is 1/sqrt(r) as printed; the compression
+  W_pre is given per latent group (G = 1 shares it over all heads, G = H makes
+  it per head) and the expansion W_post per query head; query head h reads
+  latent group h // (H // G), as for grouped values.
+* Cross-attention (Eq. 14) takes the multi-head and grouped forms of Section 3
+  unchanged, with no mask; an empty X^(b) gives zero rows.
 """
 
 from __future__ import annotations
@@ -323,6 +329,80 @@ def value_cache_append(cache, values, lengths_before, block_table=None, block_si
                 else:
                     blk = int(block_table[b][p // block_size])
                     out[blk, g, p % block_size, :] = values[b, t, g, :]
+    return out
+
+
+# ---------------------------------------------------------------------------
+# Section 3, Eq. 15: multi-head attention over a latent value-only cache
+# ---------------------------------------------------------------------------
+
+def latent_prefill(x, W_Q, W_R, W_pre, W_post, H: int, G: int, d_head: int, r: int,
+                   causal: bool = True, scale: float | None = None):
+    """Keyless attention whose values are factored through a rank-r latent
+    (Eq. 15). For batch b, query head h and latent group g = h // (H // G):
+      Q_h   = X W^Q_h W^R_h             [N, d_k]  (routed query)
+      V*_g  = X W^V_{g,pre}             [N, r]    (the only cached rows)
+      Q*_h  = Q_h (W^V_{h,post})^T      [N, r]    (absorbed query)
+      O_h   = softmax(Q*_h V*_g^T / sqrt(r)) V*_g W^V_{h,post}
+    with the causal mask j <= i when ``causal``. The compression W_pre may be
+    shared (G = 1), per group or per head (G = H); the expansion W_post is given
+    per query head (a shared one is the same matrix repeated).
+
+    x: [B, N, d]; W_Q: [d, H*d_k]; W_R: [H, d_k, d_k] or None; W_pre: [d, G*r];
+    W_post: [H, r, d_k]. Returns (O [B, N, H, d_k], Q* [B, N, H, r],
+    V* [B, N, G, r]).
+    """
+    x = _f64(x)
+    W_Q = _f64(W_Q)
+    W_pre = _f64(W_pre)
+    W_post = _f64(W_post)
+    B, N, _ = x.shape
+    tau = default_scale(r) if scale is None else float(scale)
+    rep = H // G
+    O = np.zeros((B, N, H, d_head))
+    Qs = np.zeros((B, N, H, r))
+    Vs = np.zeros((B, N, G, r))
+    for b in range(B):
+        X = x[b]
+        for g in range(G):
+            Vs[b, :, g, :] = X @ W_pre[:, g * r:(g + 1) * r]
+        for h in range(H):
+            Q_h = X @ W_Q[:, h * d_head:(h + 1) * d_head]
+            if W_R is not None:
+                Q_h = Q_h @ _f64(W_R)[h]
+            Qstar = Q_h @ W_post[h].T
+            Qs[b, :, h, :] = Qstar
+            V_g = Vs[b, :, h // rep, :]
+            S = tau * (Qstar @ V_g.T)
+            if causal:
+                S = np.where(np.tril(np.ones((N, N), dtype=bool)), S, -np.inf)
+            O[b, :, h, :] = (softmax_rows(S) @ V_g) @ W_post[h]
+    return O, Qs, Vs
+
+
+def latent_decode(q_routed, W_post, latent_cache, lengths, H: int, G: int, block_table=None,
+                  block_size: int = 16, scale: float | None = None):
+    """One decode step over a latent value-only cache (Eq. 15 for the newest
+    token): for each (b, h) with g = h // (H // G), the absorbed query
+    q* = q~ (W^V_{h,post})^T, the Section 3 decode of q* over the first
+    lengths[b] latent rows of group g (scale 1/sqrt(r) unless given), and the
+    expansion of that weighted average by W^V_{h,post}.
+
+    q_routed: [B, H, d_k]; W_post: [H, r, d_k]; latent_cache laid out like a
+    value cache with r-wide rows. Returns [B, H, d_k]; an empty cache gives zeros.
+    """
+    q_routed = _f64(q_routed)
+    W_post = _f64(W_post)
+    B = q_routed.shape[0]
+    r = W_post.shape[1]
+    tau = default_scale(r) if scale is None else float(scale)
+    rep = H // G
+    out = np.zeros(q_routed.shape)
+    for b in range(B):
+        for h in range(H):
+            rows = cache_rows(latent_cache, b, h // rep, int(lengths[b]), block_table, block_size)
+            qstar = W_post[h] @ q_routed[b, h]  # = q~ W_post^T as a column
+            out[b, h] = decode_one(qstar, rows, tau) @ W_post[h]
     return out
 
 

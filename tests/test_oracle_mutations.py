@@ -34,6 +34,19 @@ MUTATIONS = [
      "q[b, h] = qh if W_R is None else qh @ _f64(W_R)[h].T",
      "routing matrix transposed in the decode-step projection"),
     ("decode_one", "s = tau * (V_rows @ q)", "s = (V_rows @ q)", "decode without the scale"),
+    ("latent_prefill", "Qstar = Q_h @ W_post[h].T", "Qstar = Q_h @ W_post[h]",
+     "latent: expansion matrix not transposed in the absorbed query"),
+    ("latent_prefill", "tau = default_scale(r)", "tau = default_scale(d_head)",
+     "latent prefill at 1/sqrt(d_k) instead of 1/sqrt(r)"),
+    ("latent_prefill", "O[b, :, h, :] = (softmax_rows(S) @ V_g) @ W_post[h]",
+     "O[b, :, h, :] = (softmax_rows(S) @ V_g) @ W_post[h // rep]",
+     "latent output expanded with the group's matrix instead of the head's"),
+    ("latent_decode", "qstar = W_post[h] @ q_routed[b, h]", "qstar = W_post[h].T @ q_routed[b, h]",
+     "latent decode: absorbed query with W_post instead of its transpose"),
+    ("latent_decode", "tau = default_scale(r)", "tau = default_scale(q_routed.shape[-1])",
+     "latent decode at 1/sqrt(d_k)"),
+    ("latent_decode", "rows = cache_rows(latent_cache, b, h // rep,",
+     "rows = cache_rows(latent_cache, b, h % G,", "latent decode head-to-group map h % G"),
     ("keyless_cross_attention", "Qt_h = Q_h if W_R is None else Q_h @ _f64(W_R)[h]",
      "Qt_h = Q_h if W_R is None else Q_h @ _f64(W_R)[h].T", "routing matrix transposed in cross-attention"),
     ("keyless_cross_attention", "V[b, :, g, :] = xb[b] @", "V[b, :, g, :] = xa[b] @",

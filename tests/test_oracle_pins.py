@@ -9,6 +9,9 @@ the oracle itself. CPU only.
   torch's scaled_dot_product_attention (float64, CPU) on (Q~, V, V);
 * brute-force scalar loops over Eq. 4 on tiny inputs;
 * decode over a prefix equals the prefill row of the same token;
+* the latent cache (Eq. 15): a hand-derived rank-one decode, torch's attention
+  over the expanded per-head values at scale 1/sqrt(r), W_post = I reduces to
+  Eq. 2, decode over a prefix (contiguous and paged) equals the prefill row;
 * cross-attention (Eq. 14): a hand-derived case, the library call with
   N_a != N_b, X^(a) = X^(b) gives unmasked self-attention, rows are decodes;
 * paged equals contiguous, block order does not matter, grouped heads equal
@@ -253,6 +256,77 @@ def test_cross_attention_one_value_and_no_values():
             np.testing.assert_allclose(O[0, i, h], V[0, 0, 0], rtol=0, atol=1e-14)
     O0, _, _ = K.keyless_cross_attention(xa, xb[:, :0], W_Q, None, W_V, H=H, G=G, d_head=dk)
     assert O0.shape == (B, Na, H, dk) and not O0.any()
+
+
+def test_closed_form_latent_decode():
+    case = json.load(open(os.path.join(GOLD, "closed_form_cases.json")))["latent_decode_rank_one"]
+    q = np.array([math.log(3) if v == "ln3" else v for v in case["q_routed"]])[None, None]
+    cache = np.array(case["latent_cache"])[None, None]  # [B=1, G=1, L=2, r=1]
+    out = K.latent_decode(q, np.array(case["W_post"])[None], cache, [2], H=1, G=1)
+    np.testing.assert_allclose(out[0, 0], case["expected_out"], rtol=0, atol=1e-15)
+
+
+@pytest.mark.parametrize("causal", [True, False])
+def test_latent_matches_library_sdpa_with_expanded_values(causal):
+    """Eq. 15 is keyless attention whose per-head values are V*_g W_post_h, at
+    the scale 1/sqrt(r): torch's attention on (Q~, V_h, V_h) with that scale."""
+    B, N, d, dk = 2, 11, 20, 6
+    for H, G, r in ((4, 4, 3), (4, 2, 6), (4, 1, 5), (2, 1, 6)):
+        x = rng.standard_normal((B, N, d))
+        W_Q = rng.standard_normal((d, H * dk)) / math.sqrt(d)
+        W_R = rng.standard_normal((H, dk, dk)) / math.sqrt(dk)
+        W_pre = rng.standard_normal((d, G * r)) / math.sqrt(d)
+        W_post = rng.standard_normal((H, r, dk)) / math.sqrt(r)
+        O, Qs, Vs = K.latent_prefill(x, W_Q, W_R, W_pre, W_post, H, G, dk, r, causal=causal)
+        Qt = np.einsum("bnhk,hkj->bnhj", np.einsum("bnd,dhk->bnhk", x, W_Q.reshape(d, H, dk)), W_R)
+        Vstar = (x @ W_pre).reshape(B, N, G, r)
+        Vh = np.einsum("bnhr,hrk->bnhk", np.repeat(Vstar, H // G, axis=2), W_post)
+        t = lambda a: torch.from_numpy(np.ascontiguousarray(a.transpose(0, 2, 1, 3)))
+        ref = torch.nn.functional.scaled_dot_product_attention(
+            t(Qt), t(Vh), t(Vh), is_causal=causal, scale=1 / math.sqrt(r)).numpy().transpose(0, 2, 1, 3)
+        np.testing.assert_allclose(O, ref, rtol=0, atol=1e-12)
+        np.testing.assert_allclose(Vs, Vstar, rtol=0, atol=1e-12)
+        np.testing.assert_allclose(Qs, np.einsum("bnhk,hrk->bnhr", Qt, W_post), rtol=0, atol=1e-12)
+
+
+def test_latent_with_identity_expansion_is_keyless_attention():
+    """r = d_k and W_post = I: the latent cache is the value cache of Eq. 2."""
+    B, N, d, H, G, dk = 2, 9, 12, 4, 2, 3
+    x = rng.standard_normal((B, N, d))
+    W_Q, W_V = rng.standard_normal((d, H * dk)), rng.standard_normal((d, G * dk))
+    W_R = rng.standard_normal((H, dk, dk)) / 2
+    eye = np.broadcast_to(np.eye(dk), (H, dk, dk))
+    O, _, Vs = K.latent_prefill(x, W_Q, W_R, W_V, eye, H, G, dk, dk)
+    O_k, _, V_k = K.keyless_prefill(x, W_Q, W_R, W_V, H, G, dk)
+    np.testing.assert_allclose(O, O_k, rtol=0, atol=1e-12)
+    np.testing.assert_allclose(Vs, V_k, rtol=0, atol=1e-12)
+
+
+def test_latent_decode_over_prefix_equals_latent_prefill_row():
+    B, N, d, H, G, dk, r = 2, 17, 10, 4, 2, 4, 4  # r = d_k, so orientation slips do not fail by shape
+    x = rng.standard_normal((B, N, d))
+    W_Q = rng.standard_normal((d, H * dk))
+    W_R = rng.standard_normal((H, dk, dk)) / 2
+    W_pre = rng.standard_normal((d, G * r))
+    W_post = rng.standard_normal((H, r, dk)) / 2
+    O, _, Vs = K.latent_prefill(x, W_Q, W_R, W_pre, W_post, H, G, dk, r)
+    Qr = np.einsum("bnhk,hkj->bnhj", np.einsum("bnd,dhk->bnhk", x, W_Q.reshape(d, H, dk)), W_R)
+    cache = np.ascontiguousarray(Vs.transpose(0, 2, 1, 3))  # [B, G, N, r]
+    for i in (0, 6, N - 1):
+        out = K.latent_decode(Qr[:, i], W_post, cache, np.full(B, i + 1), H, G)
+        np.testing.assert_allclose(out, O[:, i], rtol=0, atol=1e-12)
+    # Paged: 4-row blocks in a shuffled order hold the same rows.
+    bs, nblk = 4, (N + 3) // 4
+    perm = rng.permutation(B * nblk)
+    paged = np.full((B * nblk, G, bs, r), np.nan)
+    for b in range(B):
+        for i in range(N):
+            paged[perm[b * nblk + i // bs], :, i % bs] = cache[b, :, i]
+    table = perm.reshape(B, nblk)
+    out = K.latent_decode(Qr[:, N - 1], W_post, paged, np.full(B, N), H, G, table, bs)
+    np.testing.assert_allclose(out, O[:, N - 1], rtol=0, atol=1e-12)
+    empty = K.latent_decode(Qr[:, 0], W_post, cache, np.zeros(B, dtype=int), H, G)
+    assert not empty.any()
 
 
 def test_decode_over_prefix_equals_prefill_row():
