@@ -78,6 +78,37 @@ typedef struct {
 } kl_value_cache;
 
 /*
+ * keyless_latent_decode - one decode step over a latent value-only cache
+ * (Section 3, Eq. 15). The cache holds V* = X W^V_pre (rank r rows) instead of
+ * the values; each query head h expands them with its own W^V_{h,post}:
+ *   q*[b,h]  = q_routed[b,h] W_post[h]^T                 (absorbed query, r wide)
+ *   o*[b,h]  = sum_{i < lengths[b]} alpha_i V*_i,  alpha = softmax_i(scale <q*, V*_i>)
+ *   out[b,h] = o*[b,h] W_post[h]
+ * over latent group g = h / (H / G) of the cache.
+ *   q_routed      [B, H, d_head], the routed queries q~ (cache dtype)
+ *   W_post        [H, r, d_head]: W^V_{h,post} per query head (a shared or per-group
+ *                 expansion is passed repeated), cache dtype
+ *   latent_cache  descriptor as for keyless_decode with d_head = r (64 or 128) and
+ *                 G latent groups (G = 1: one latent shared by all heads)
+ *   lengths       [B] int32 on the device, clamped to [0, capacity]
+ *   d_head        64 or 128
+ *   scale         >= 0; 0 selects 1/sqrt(r) as in Eq. 15
+ *   out           [B, H, d_head]
+ *   ws, ws_bytes  keyless_latent_decode_workspace_size(...) bytes, 16-byte aligned:
+ *                 q* and o* (B*H*r elements each, rounded up to 256 bytes) and the
+ *                 decode's own workspace
+ * H/G as for keyless_decode (16 or 32 only for bf16 with r = 128). q* and o* are
+ * rounded to the cache dtype; fp32 accumulation throughout. An empty cache gives
+ * a zero row. Errors: KL_ERR_* before any launch.
+ */
+int keyless_latent_decode(const void* q_routed, const void* W_post,
+                          const kl_value_cache* latent_cache, const int32_t* lengths, int B, int H,
+                          int d_head, float scale, void* out, void* ws, size_t ws_bytes,
+                          void* stream);
+size_t keyless_latent_decode_workspace_size(const kl_value_cache* latent_cache, int B, int H,
+                                            int d_head);
+
+/*
  * keyless_fold_routing - folded query weight W~^Q_h = W^Q_h W^R_h for every
  * head h (Section 2.1: the two query matrices are composed once before
  * inference; Section 5.5 uses the fused matrix for decoding).
@@ -215,7 +246,8 @@ int keyless_decode_project(const void* x, const void* packed, int B, int d_model
  * keyless_decode - one decode step over a value-only cache (Section 3):
  *   out[b,h] = sum_{i < lengths[b]} alpha_i v_i,
  *   alpha_i = exp(scale <q_routed[b,h], v_i>) / sum_j exp(scale <q_routed[b,h], v_j>)
- * with v_i the rows of group h / (H / G) of sequence b.
+ * with v_i the rows of group h / (H / G) of sequence b. H / G is 1, 2, 4 or 8,
+ * and also 16 or 32 for a bf16 cache with d_head 128 (KL_ERR_UNSUPPORTED otherwise).
  *   q_routed [B, H, d_head]  routed queries x W~^Q of the current tokens (cache dtype)
  *   cache    value-only cache descriptor (host pointer)
  *   lengths  [B] int32, device: rows per sequence, the current token's value

@@ -25,6 +25,7 @@ EXPORTS = (
     "keyless_packed_weights_size", "keyless_pack_weights", "keyless_prefill_packed",
     "keyless_cross_attention", "keyless_cross_attention_workspace_size",
     "keyless_cross_attention_packed",
+    "keyless_latent_decode", "keyless_latent_decode_workspace_size",
     "keyless_decode_project", "keyless_decode", "keyless_decode_chunked", "keyless_decode_workspace_size",
     "value_cache_append", "standard_decode", "standard_decode_chunked",
     "keyless_set_kernel_timer", "keyless_last_error", "keyless_version",
@@ -77,6 +78,8 @@ def load(path: str = LIB_PATH):
         "keyless_decode": (i, [vp, cp, vp, i, i, f, vp, vp, sz, vp]),
         "keyless_decode_chunked": (i, [vp, cp, vp, i, i, f, vp, vp, sz, i, vp]),
         "keyless_decode_workspace_size": (sz, [cp, i, i, i]),
+        "keyless_latent_decode": (i, [vp, vp, cp, vp, i, i, i, f, vp, vp, sz, vp]),
+        "keyless_latent_decode_workspace_size": (sz, [cp, i, i, i]),
         "value_cache_append": (i, [cp, vp, vp, i, i, vp]),
         "standard_decode": (i, [vp, cp, cp, vp, i, i, f, vp, vp, sz, vp]),
         "standard_decode_chunked": (i, [vp, cp, cp, vp, i, i, f, vp, vp, sz, i, vp]),
@@ -374,4 +377,27 @@ def keyless_cross_attention_packed(xa: torch.Tensor, xb: torch.Tensor, packed: t
                                                _stream(xa)))
     if return_qv:
         return out, q_routed_out, v_out
+    return out
+
+
+def latent_decode_workspace_bytes(cache: "ValueCache", B: int, H: int, d_head: int) -> int:
+    load()
+    return int(_lib.keyless_latent_decode_workspace_size(cache.ref, B, H, d_head))
+
+
+def keyless_latent_decode(q_routed: torch.Tensor, W_post: torch.Tensor, cache: "ValueCache",
+                          lengths: torch.Tensor, scale: float = 0.0, out=None, workspace=None):
+    """Decode over a latent value-only cache (r-wide rows): q* = q~ W_post^T,
+    decode of q* at scale 1/sqrt(r), out = o* W_post. q_routed [B, H, d_k],
+    W_post [H, r, d_k]; returns [B, H, d_k]."""
+    load()
+    B, H, dk = q_routed.shape
+    if out is None:
+        out = torch.empty_like(q_routed)
+    if workspace is None:
+        n = latent_decode_workspace_bytes(cache, B, H, dk)
+        workspace = torch.empty(max(n, 256), dtype=torch.uint8, device=q_routed.device)
+    _check(_lib.keyless_latent_decode(_ptr(q_routed), _ptr(W_post), cache.ref, _ptr(lengths), B, H,
+                                      dk, scale, _ptr(out), _ptr(workspace), workspace.numel(),
+                                      _stream(q_routed)))
     return out

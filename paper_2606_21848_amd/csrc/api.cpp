@@ -139,6 +139,16 @@ size_t partials_bytes(const DecodePlan& pl, int B, int H, int G, int d_head) {
   return pl.S > 1 ? align256((size_t)B * H * pl.S * (d_head + 2) * sizeof(float)) : 0;
 }
 
+// Query heads per cached group the decode kernels handle.
+int check_group_ratio(const char* who, const kl_value_cache* c, int R) {
+  const bool wide_groups = c->dtype == KL_BF16 && c->d_head == 128;
+  if (R != 1 && R != 2 && R != 4 && R != 8 && !((R == 16 || R == 32) && wide_groups))
+    return fail(KL_ERR_UNSUPPORTED,
+                "%s: H/G=%d not supported (1, 2, 4 or 8; also 16 or 32 for bf16 with d_head 128)",
+                who, R);
+  return KL_OK;
+}
+
 int decode_common(const void* q, const kl_value_cache* k_cache, const kl_value_cache* v_cache,
                   const int32_t* lengths, int B, int H, float scale, void* out, void* ws,
                   size_t ws_bytes, int chunk_rows, void* stream, const char* who) {
@@ -161,8 +171,8 @@ int decode_common(const void* q, const kl_value_cache* k_cache, const kl_value_c
   const int G = v_cache->G;
   if (H % G != 0) return fail(KL_ERR_INVALID_ARG, "%s: H=%d is not a multiple of G=%d", who, H, G);
   const int R = H / G;
-  if (R != 1 && R != 2 && R != 4 && R != 8)
-    return fail(KL_ERR_UNSUPPORTED, "%s: H/G=%d not supported (1, 2, 4 or 8)", who, R);
+  st = check_group_ratio(who, v_cache, R);
+  if (st != KL_OK) return st;
   if (chunk_rows < 0 || chunk_rows % 64 != 0)
     return fail(KL_ERR_INVALID_ARG, "%s: chunk_rows=%d must be a multiple of 64", who, chunk_rows);
   if (B == 0) return KL_OK;
@@ -242,6 +252,50 @@ int keyless_decode_chunked(const void* q_routed, const kl_value_cache* cache,
                            size_t ws_bytes, int chunk_rows, void* stream) {
   return decode_common(q_routed, nullptr, cache, lengths, B, H, scale, out, ws, ws_bytes,
                        chunk_rows, stream, "keyless_decode_chunked");
+}
+
+size_t keyless_latent_decode_workspace_size(const kl_value_cache* latent_cache, int B, int H,
+                                            int d_head) {
+  if (!latent_cache || B <= 0 || H <= 0 || latent_cache->G <= 0 || d_head <= 0) return 0;
+  const size_t v = align256((size_t)B * H * latent_cache->d_head * elem_bytes(latent_cache->dtype));
+  return 2 * v + keyless_decode_workspace_size(latent_cache, B, H, 0);
+}
+
+int keyless_latent_decode(const void* q_routed, const void* W_post,
+                          const kl_value_cache* latent_cache, const int32_t* lengths, int B, int H,
+                          int d_head, float scale, void* out, void* ws, size_t ws_bytes,
+                          void* stream) {
+  const char* who = "keyless_latent_decode";
+  if (!q_routed || !W_post || !out || !lengths)
+    return fail(KL_ERR_INVALID_ARG, "%s: q_routed, W_post, lengths and out must be non-NULL", who);
+  int s = check_cache(latent_cache, who);
+  if (s != KL_OK) return s;
+  if (d_head != 64 && d_head != 128)
+    return fail(KL_ERR_UNSUPPORTED, "%s: d_head %d not supported (64 or 128)", who, d_head);
+  if (B < 0 || H <= 0) return fail(KL_ERR_INVALID_ARG, "%s: bad B=%d or H=%d", who, B, H);
+  const int G = latent_cache->G;
+  if (H % G != 0) return fail(KL_ERR_INVALID_ARG, "%s: H=%d is not a multiple of G=%d", who, H, G);
+  s = check_group_ratio(who, latent_cache, H / G);
+  if (s != KL_OK) return s;
+  if (!(scale >= 0.f)) return fail(KL_ERR_INVALID_ARG, "%s: scale must be >= 0 (0 = 1/sqrt(r))", who);
+  if (B == 0) return KL_OK;
+  const size_t need = keyless_latent_decode_workspace_size(latent_cache, B, H, d_head);
+  if (!ws || ws_bytes < need)
+    return fail(KL_ERR_WORKSPACE, "%s: workspace of %zu bytes needed, %zu given", who, need, ws_bytes);
+  if (!aligned16(ws)) return fail(KL_ERR_INVALID_ARG, "%s: workspace must be 16-byte aligned", who);
+  const int r = latent_cache->d_head;
+  const size_t v = align256((size_t)B * H * r * elem_bytes(latent_cache->dtype));
+  char* w = static_cast<char*>(ws);
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  // q* = q~ W_post^T, the decode of q* over the latent rows (o*), out = o* W_post.
+  kl::LatentParams lp{q_routed, W_post, w, B, H, r, d_head, 1, latent_cache->dtype};
+  s = hip_status(kl::launch_latent_product(lp, st), who);
+  if (s != KL_OK) return s;
+  s = decode_common(w, nullptr, latent_cache, lengths, B, H, scale, w + v, w + 2 * v,
+                    ws_bytes - 2 * v, 0, stream, who);
+  if (s != KL_OK) return s;
+  lp = kl::LatentParams{w + v, W_post, out, B, H, r, d_head, 0, latent_cache->dtype};
+  return hip_status(kl::launch_latent_product(lp, st), who);
 }
 
 int standard_decode(const void* q, const kl_value_cache* k_cache, const kl_value_cache* v_cache,

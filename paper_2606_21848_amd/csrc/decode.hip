@@ -506,8 +506,9 @@ __global__ __launch_bounds__(NW * 64) void decode_partial_kernel(DecodeParams p)
 }
 
 // Matrix-core consumer for grouped heads over a 128-wide bf16 cache (R >= 2).
-// Per 16-row tile, with the R heads of the group as the N = 16 columns (the
-// rest zero):
+// Per 16-row tile, with the R heads of the group as the N = 16 columns of
+// ceil(R / 16) column blocks (unused columns zero; every block reuses the same
+// LDS operand reads):
 //   scores   S[row][h]  = sum_d V[row][d] q~[h][d]       4 x MFMA 16x16x32,
 //   weights  P[row][h]  = 2^(S - m_h)  (lazy reference m_h, as above),
 //   output   O^T[d][h] += sum_row V^T[d][row] P[row][h]  8 x MFMA 16x16x16.
@@ -524,7 +525,8 @@ __global__ __launch_bounds__(NW * 64) void decode_mfma_kernel(DecodeParams p) {
   using RS = Ring<T, D, KEYS, NW>;
   constexpr int TB = RS::TB, NBUF = RS::NBUF, SB = RS::SB;
   constexpr float kLazy = 8.f;
-  static_assert(R >= 2 && R <= 16, "heads per group");
+  static_assert(R >= 2 && R <= 32, "heads per group");
+  constexpr int NB = (R + 15) / 16;  // 16-head column blocks
 
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
@@ -553,70 +555,91 @@ __global__ __launch_bounds__(NW * 64) void decode_mfma_kernel(DecodeParams p) {
   auto segment = [&](int b, int g, int start, int end, SegOut so) {
   const size_t bh0 = (size_t)b * p.H + g * R;
 
-  // Score B operand: q~[h][32 kk + 8 grp .. +7] for h = hl < R, zero otherwise.
-  bf16x8_t qf[4];
+  // Score B operand of block nb: q~[h][32 kk + 8 grp .. +7] for h = 16 nb + hl
+  // when h < R, zero otherwise.
+  bf16x8_t qf[NB][4];
   const T* __restrict__ qp = reinterpret_cast<const T*>(p.q);
 #pragma unroll
-  for (int kk = 0; kk < 4; ++kk) {
-    u32x4 x = u32x4{0u, 0u, 0u, 0u};
-    if (hl < R) x = *reinterpret_cast<const u32x4*>(qp + ((bh0 + hl) * D + 32 * kk + 8 * grp));
-    qf[kk] = __builtin_bit_cast(bf16x8_t, x);
-  }
-  float m = -INFINITY, lsum = 0.f;
-  f32x4_t acc[8];
+  for (int nb = 0; nb < NB; ++nb)
 #pragma unroll
-  for (int dd = 0; dd < 8; ++dd) acc[dd] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+    for (int kk = 0; kk < 4; ++kk) {
+      u32x4 x = u32x4{0u, 0u, 0u, 0u};
+      if (16 * nb + hl < R)
+        x = *reinterpret_cast<const u32x4*>(qp + ((bh0 + 16 * nb + hl) * D + 32 * kk + 8 * grp));
+      qf[nb][kk] = __builtin_bit_cast(bf16x8_t, x);
+    }
+  float m[NB], lsum[NB];
+  f32x4_t acc[NB][8];
+#pragma unroll
+  for (int nb = 0; nb < NB; ++nb) {
+    m[nb] = -INFINITY;
+    lsum[nb] = 0.f;
+#pragma unroll
+    for (int dd = 0; dd < 8; ++dd) acc[nb][dd] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+  }
 
   auto ready = [&]() {
 #pragma unroll
-    for (int kk = 0; kk < 4; ++kk) asm volatile("" ::"v"(qf[kk]));
+    for (int nb = 0; nb < NB; ++nb)
+#pragma unroll
+      for (int kk = 0; kk < 4; ++kk) asm volatile("" ::"v"(qf[nb][kk]));
   };
 
   auto consume = [&](const lds_u8* stage, int t0, bool blk_ok) {
     if (!blk_ok) return;  // uniform: a block outside the cache contributes nothing
     const lds_u8* ks = KEYS ? stage + TB : stage;
-    f32x4_t sc = f32x4_t{0.f, 0.f, 0.f, 0.f};
+    f32x4_t sc[NB];
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb) sc[nb] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int kk = 0; kk < 4; ++kk) {
       const bf16x8_t a =
           *reinterpret_cast<const __attribute__((address_space(3))) bf16x8_t*>(ks + offS[kk]);
-      sc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, qf[kk], sc, 0, 0, 0);
-    }
-    float s4[4];
-    float tmax = -INFINITY;
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      float x = sc[i] * p.scale_log2;
-      if (t0 + 4 * grp + i >= end) x = -INFINITY;
-      s4[i] = x;
-      tmax = fmaxf(tmax, x);
+      for (int nb = 0; nb < NB; ++nb)
+        sc[nb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, qf[nb][kk], sc[nb], 0, 0, 0);
     }
-    if (__builtin_amdgcn_ballot_w64(tmax > m + kLazy)) {
-      // New reference for each head: the tile maximum over its four lane
-      // groups, so the reference stays identical across them.
-      float tm = fmaxf(tmax, __shfl_xor(tmax, 16));
-      tm = fmaxf(tm, __shfl_xor(tm, 32));
-      const float mn = (tm > m + kLazy) ? tm : m;
-      const float alpha = (m == -INFINITY) ? 0.f : fast_exp2(m - mn);
-      lsum *= alpha;
+    s16x4 pf[NB];
 #pragma unroll
-      for (int dd = 0; dd < 8; ++dd) acc[dd] *= alpha;
-      m = mn;
-    }
-    const float nm = (m == -INFINITY) ? 0.f : -m;
-    float w[4];
+    for (int nb = 0; nb < NB; ++nb) {
+      float s4[4];
+      float tmax = -INFINITY;
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      w[i] = fast_exp2(s4[i] + nm);
-      lsum += w[i];
+      for (int i = 0; i < 4; ++i) {
+        float x = sc[nb][i] * p.scale_log2;
+        if (t0 + 4 * grp + i >= end) x = -INFINITY;
+        s4[i] = x;
+        tmax = fmaxf(tmax, x);
+      }
+      if (__builtin_amdgcn_ballot_w64(tmax > m[nb] + kLazy)) {
+        // New reference for each head: the tile maximum over its four lane
+        // groups, so the reference stays identical across them.
+        float tm = fmaxf(tmax, __shfl_xor(tmax, 16));
+        tm = fmaxf(tm, __shfl_xor(tm, 32));
+        const float mn = (tm > m[nb] + kLazy) ? tm : m[nb];
+        const float alpha = (m[nb] == -INFINITY) ? 0.f : fast_exp2(m[nb] - mn);
+        lsum[nb] *= alpha;
+#pragma unroll
+        for (int dd = 0; dd < 8; ++dd) acc[nb][dd] *= alpha;
+        m[nb] = mn;
+      }
+      const float nm = (m[nb] == -INFINITY) ? 0.f : -m[nb];
+      float w[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        w[i] = fast_exp2(s4[i] + nm);
+        lsum[nb] += w[i];
+      }
+      pf[nb] = __builtin_bit_cast(
+          s16x4, u32x2{pack_bf16_rne(w[0], w[1]), pack_bf16_rne(w[2], w[3])});
     }
-    const s16x4 pf = __builtin_bit_cast(
-        s16x4, u32x2{pack_bf16_rne(w[0], w[1]), pack_bf16_rne(w[2], w[3])});
 #pragma unroll
     for (int dd = 0; dd < 8; ++dd) {
       const s16x4 a = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
           (__attribute__((address_space(3))) s16x4*)(stage + offT[dd]));
-      acc[dd] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(a, pf, acc[dd], 0, 0, 0);
+#pragma unroll
+      for (int nb = 0; nb < NB; ++nb)
+        acc[nb][dd] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(a, pf[nb], acc[nb][dd], 0, 0, 0);
     }
   };
 
@@ -624,16 +647,21 @@ __global__ __launch_bounds__(NW * 64) void decode_mfma_kernel(DecodeParams p) {
                                       consume);
 
   // Row sums of each head over the four lane groups (the reference is shared).
-  lsum += __shfl_xor(lsum, 16);
-  lsum += __shfl_xor(lsum, 32);
-  if (hl < R) {
 #pragma unroll
-    for (int dd = 0; dd < 8; ++dd)
+  for (int nb = 0; nb < NB; ++nb) {
+    float ls = lsum[nb];
+    ls += __shfl_xor(ls, 16);
+    ls += __shfl_xor(ls, 32);
+    const int h = 16 * nb + hl;
+    if (h < R) {
 #pragma unroll
-      for (int i = 0; i < 4; ++i) s_acc[wave][hl][16 * dd + 4 * grp + i] = acc[dd][i];
-    if (grp == 0) {
-      s_ml[wave][hl][0] = m;
-      s_ml[wave][hl][1] = lsum;
+      for (int dd = 0; dd < 8; ++dd)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) s_acc[wave][h][16 * dd + 4 * grp + i] = acc[nb][dd][i];
+      if (grp == 0) {
+        s_ml[wave][h][0] = m[nb];
+        s_ml[wave][h][1] = ls;
+      }
     }
   }
   merge_waves<T, D, R, NW>(p, s_acc, s_ml, bh0, so);
@@ -797,8 +825,10 @@ hipError_t pick_waves(const DecodeParams& p, hipStream_t st) {
   switch (p.waves) {
     case 4: return launch_t<T, D, R, PAGED, KEYS, 4>(p, st);
     case 8:
-      // Fall back to 4 waves where an 8-wave ring would not fit in LDS.
-      if constexpr (Ring<T, D, KEYS, 8>::BYTES > 98304) return launch_t<T, D, R, PAGED, KEYS, 4>(p, st);
+      // Fall back to 4 waves where an 8-wave ring, or the merge rows of 16 or
+      // more heads per group, would not fit in LDS.
+      if constexpr (Ring<T, D, KEYS, 8>::BYTES > 98304 || R >= 16)
+        return launch_t<T, D, R, PAGED, KEYS, 4>(p, st);
       else return launch_t<T, D, R, PAGED, KEYS, 8>(p, st);
     default: return hipErrorInvalidValue;
   }
@@ -819,6 +849,12 @@ hipError_t pick_r(const DecodeParams& p, hipStream_t st) {
     case 2: return pick_layout<T, D, 2>(p, st);
     case 4: return pick_layout<T, D, 4>(p, st);
     case 8: return pick_layout<T, D, 8>(p, st);
+    case 16:
+    case 32:
+      // 16 or 32 heads per group: bf16, 128-wide rows only (the matrix-core consumer).
+      if constexpr (sizeof(T) == 2 && D == 128)
+        return p.R == 16 ? pick_layout<T, D, 16>(p, st) : pick_layout<T, D, 32>(p, st);
+      else return hipErrorInvalidValue;
     default: return hipErrorInvalidValue;
   }
 }

@@ -130,6 +130,18 @@ struct AttnParams {
   kl_dtype dtype;
 };
 
+// Latent cache products (Eq. 15): absorb y = x W_post_h^T (d_k -> r) or expand
+// y = x W_post_h (r -> d_k) for every (sequence, head); r and d_k are 64 or 128.
+struct LatentParams {
+  const void* x;   // [B, H, n_in]
+  const void* W;   // [H, r, d_k]
+  void* y;         // [B, H, n_out]
+  int B, H, r, dk;
+  int absorb;
+  kl_dtype dtype;
+};
+hipError_t launch_latent_product(const LatentParams& p, hipStream_t stream);
+
 // bf16 MFMA flash-style keyless attention (d_head 64 or 128).
 bool attn_bf16_supported(const AttnParams& p);
 hipError_t launch_prefill_attention(const AttnParams& p, hipStream_t stream);

@@ -71,7 +71,9 @@ def test_decode_rejects_bad_arguments(lib):
     expect(lib, decode(lib, cache(), q=None), kb.KL_ERR_INVALID_ARG, "non-NULL")
     expect(lib, decode(lib, cache(d=96)), kb.KL_ERR_UNSUPPORTED, "d_head 96")
     expect(lib, decode(lib, cache(G=3), H=8), kb.KL_ERR_INVALID_ARG, "multiple")
-    expect(lib, decode(lib, cache(G=1), H=16), kb.KL_ERR_UNSUPPORTED, "H/G=16")
+    expect(lib, decode(lib, cache(G=1), H=64), kb.KL_ERR_UNSUPPORTED, "H/G=64")
+    expect(lib, decode(lib, cache(G=1, dtype=kb.KL_F32), H=16), kb.KL_ERR_UNSUPPORTED, "H/G=16")
+    expect(lib, decode(lib, cache(G=1, d=64), H=32), kb.KL_ERR_UNSUPPORTED, "H/G=32")
     expect(lib, decode(lib, cache(), ws_bytes=1000), kb.KL_ERR_WORKSPACE, "workspace")
     expect(lib, decode(lib, cache(), chunk=100), kb.KL_ERR_INVALID_ARG, "multiple of 64")
     expect(lib, decode(lib, cache(L_max=1 << 20), chunk=64), kb.KL_ERR_UNSUPPORTED, "splits")
@@ -174,3 +176,24 @@ def test_cross_attention_workspace_and_rejects(lib):
     assert cross(B=0) == kb.KL_OK
     assert cross(Na=0, Nb=0) == kb.KL_OK
     assert cross_packed(B=0) == kb.KL_OK
+
+
+def test_latent_decode_workspace_and_rejects(lib):
+    c = cache(G=1, d=128, L_max=4096)
+    # q* and o* (B*H*r bf16 each) ahead of the decode's own workspace.
+    dec = lib.keyless_decode_workspace_size(ctypes.byref(c), 4, 32, 0)
+    assert lib.keyless_latent_decode_workspace_size(ctypes.byref(c), 4, 32, 128) == \
+        2 * 4 * 32 * 128 * 2 + dec
+
+    def lat(c=c, B=4, H=32, dk=128, q=FAKE, w=FAKE, ws_bytes=1 << 30, scale=0.0):
+        return lib.keyless_latent_decode(q, w, ctypes.byref(c), FAKE, B, H, dk, scale, FAKE, FAKE,
+                                         ws_bytes, None)
+    expect(lib, lat(w=None), kb.KL_ERR_INVALID_ARG, "non-NULL")
+    expect(lib, lat(dk=96), kb.KL_ERR_UNSUPPORTED, "d_head 96")
+    expect(lib, lat(c=cache(G=1, d=96)), kb.KL_ERR_UNSUPPORTED, "d_head 96")
+    expect(lib, lat(H=64), kb.KL_ERR_UNSUPPORTED, "H/G=64")
+    expect(lib, lat(c=cache(G=3)), kb.KL_ERR_INVALID_ARG, "multiple")
+    expect(lib, lat(c=cache(G=1, dtype=kb.KL_F32)), kb.KL_ERR_UNSUPPORTED, "H/G=32")
+    expect(lib, lat(scale=-2.0), kb.KL_ERR_INVALID_ARG, "scale")
+    expect(lib, lat(ws_bytes=100), kb.KL_ERR_WORKSPACE, "workspace")
+    assert lat(B=0, ws_bytes=0) == kb.KL_OK

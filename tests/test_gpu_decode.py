@@ -52,6 +52,9 @@ CASES = [
     (torch.bfloat16, 128, 8, 2),
     (torch.bfloat16, 128, 8, 1),
     (torch.bfloat16, 128, 16, 2),
+    (torch.bfloat16, 128, 16, 1),   # 16 heads per group: one full MFMA column block
+    (torch.bfloat16, 128, 32, 1),   # 32 heads per group: two column blocks
+    (torch.bfloat16, 128, 32, 2),
     (torch.bfloat16, 64, 4, 4),
     (torch.bfloat16, 64, 8, 2),
     (torch.float32, 64, 4, 4),
@@ -119,7 +122,7 @@ def test_grouped_equals_mha_over_repeated_values(lib):
 
 
 @pytest.mark.parametrize("H,G,d,dtype", [(4, 2, 128, torch.bfloat16), (2, 2, 128, torch.bfloat16),
-                                         (4, 4, 64, torch.float32)])
+                                         (4, 4, 64, torch.float32), (32, 1, 128, torch.bfloat16)])
 def test_balanced_mode_ragged_and_empty(lib, H, G, d, dtype):
     """Balanced mode (paged cache, library choice): the workgroups' equal tile
     shares cut pairs at arbitrary tiles, one long pair spans ~150 workgroups,

@@ -15,10 +15,10 @@ import torch
 from .synth import normal, permutation, uniform_int
 
 NAMES = ("tiny_fp32", "decode_bf16", "prefill_bf16", "paged_gqa_bf16", "head_to_head_bf16",
-         "decode_step_bf16", "cross_bf16")
+         "decode_step_bf16", "cross_bf16", "latent_bf16")
 
 # Stream ids (one per drawn tensor).
-S_X, S_WQ, S_WR, S_WV, S_XNEXT, S_V, S_Q, S_K, S_LEN, S_PERM, S_VNEW, S_XB = range(12)
+S_X, S_WQ, S_WR, S_WV, S_XNEXT, S_V, S_Q, S_K, S_LEN, S_PERM, S_VNEW, S_XB, S_WPOST = range(13)
 
 
 def tiny_fp32(device="cpu", seed=0, N=128, d_model=256, H=4, d_head=64):
@@ -154,4 +154,20 @@ def cross_bf16(device="cpu", seed=6, B=4, N_a=1024, N_b=4096, d_model=4096, H=32
         W_R=normal((H, d_head, d_head), seed, S_WR, std_w, b, device),
         W_V=normal((d_model, G * d_head), seed, S_WV, std_w, b, device),
         B=B, N_a=N_a, N_b=N_b, d_model=d_model, H=H, G=G, d_head=d_head,
+    )
+
+
+def latent_bf16(device="cpu", seed=7, B=32, H=32, G=1, r=128, d_head=128, L=16384):
+    """Decode over a latent value-only cache (Eq. 15) at the head-to-head shape:
+    one r = 128 latent shared by all 32 heads (G = 1), 16384 cached rows per
+    sequence, so the cache is 1/32 of the value-only cache of that shape.
+    Latent rows and routed queries ~ N(0,1); expansion matrices W_post
+    [H, r, d_head] ~ N(0, 1/d_head), which keeps the absorbed query ~ N(0,1)."""
+    f = torch.bfloat16
+    return dict(
+        cache=normal((B, G, L, r), seed, S_V, 1.0, f, device),
+        q=normal((B, H, d_head), seed, S_Q, 1.0, f, device),
+        W_post=normal((H, r, d_head), seed, S_WPOST, 1.0 / math.sqrt(d_head), f, device),
+        lengths=torch.full((B,), L, dtype=torch.int32, device=device),
+        B=B, H=H, G=G, r=r, d_head=d_head, L=L,
     )
