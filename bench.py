@@ -75,6 +75,35 @@ def timed_steps(step, steps, warmup, torch):
     return t0.elapsed_time(t1) / steps
 
 
+def graph_step_ms(step, steps, torch):
+    """Average time of one step replayed from a HIP graph: the step's launches
+    are captured once (after an eager warm-up on the capture stream) and the
+    graph is replayed `steps` times between two events, which removes the
+    host's per-launch cost from launch-bound steps."""
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        for i in range(3):
+            step(i)
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        step(0)
+    for _ in range(3):
+        g.replay()
+    torch.cuda.synchronize()
+    a = torch.cuda.Event(enable_timing=True)
+    b = torch.cuda.Event(enable_timing=True)
+    a.record()
+    for _ in range(steps):
+        g.replay()
+    b.record()
+    torch.cuda.synchronize()
+    del g
+    return a.elapsed_time(b) / steps
+
+
 def batch_avg_ms(launch, n, torch):
     """Average time per launch of n back-to-back launches on the current stream,
     between two HIP events recorded on that stream."""
@@ -416,6 +445,30 @@ def extra_measurements(torch, kb, configs, dev):
         "project_ms": round(ms_p, 4), "project_weight_gbps": round(wbytes / (ms_p * 1e-3) / 1e9, 1),
         "step_ms": round(ms_s, 4), "step_tokens_per_s": round(Bs / (ms_s * 1e-3), 1)}
     del st, packed, vc, q_out, out, ws
+    # Latent value-only cache (Eq. 15): one r = 128 latent shared by 32 heads.
+    la = configs.latent_bf16(device=dev)
+    lvc = kb.ValueCache(la["cache"])
+    lws = torch.zeros(kb.latent_decode_workspace_bytes(lvc, la["B"], la["H"], la["d_head"]),
+                      dtype=torch.uint8, device=dev)
+    lout = torch.empty_like(la["q"])
+
+    def lstep(i):
+        kb.keyless_latent_decode(la["q"], la["W_post"], lvc, la["lengths"], out=lout,
+                                 workspace=lws)
+    ms = timed_steps(lstep, 20, 3, torch)
+    ms_g = graph_step_ms(lstep, 50, torch)
+    lbytes = la["B"] * la["G"] * la["L"] * la["r"] * 2
+    res["latent_bf16"] = {"workload": "batch 32, 32 heads x 128 on one shared r = 128 latent "
+                                      "(Eq. 15), 16384 cached rows: absorb + decode + expand",
+                          "cache_bytes": lbytes, "ms": round(ms, 4),
+                          "tokens_per_s": round(la["B"] / (ms * 1e-3), 1),
+                          "graph_ms": round(ms_g, 4),
+                          "graph_tokens_per_s": round(la["B"] / (ms_g * 1e-3), 1),
+                          "graph_cache_gbps": round(lbytes / (ms_g * 1e-3) / 1e9, 1),
+                          "note": "ms: eager calls back to back (host-launch bound: five "
+                                  "kernels per call); graph_ms: the call replayed from a "
+                                  "captured HIP graph"}
+    del la, lvc, lws, lout
     # Head-to-head: keyless value-only vs standard K+V, same structure.
     hh = configs.head_to_head_bf16(device=dev)
     vcache, kcache = kb.ValueCache(hh["V"]), kb.ValueCache(hh["K"])

@@ -97,7 +97,8 @@ typedef struct {
  *   ws, ws_bytes  keyless_latent_decode_workspace_size(...) bytes, 16-byte aligned:
  *                 q* and o* (B*H*r elements each, rounded up to 256 bytes) and the
  *                 decode's own workspace
- * H/G as for keyless_decode (16 or 32 only for bf16 with r = 128). q* and o* are
+ * q_routed and W_post 16-byte aligned. H/G as for keyless_decode (16 or 32 only
+ * for bf16 with r = 128). q* and o* are
  * rounded to the cache dtype; fp32 accumulation throughout. An empty cache gives
  * a zero row. Errors: KL_ERR_* before any launch.
  */

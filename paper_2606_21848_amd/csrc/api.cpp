@@ -268,6 +268,8 @@ int keyless_latent_decode(const void* q_routed, const void* W_post,
   const char* who = "keyless_latent_decode";
   if (!q_routed || !W_post || !out || !lengths)
     return fail(KL_ERR_INVALID_ARG, "%s: q_routed, W_post, lengths and out must be non-NULL", who);
+  if (!aligned16(q_routed) || !aligned16(W_post))
+    return fail(KL_ERR_INVALID_ARG, "%s: q_routed and W_post must be 16-byte aligned", who);
   int s = check_cache(latent_cache, who);
   if (s != KL_OK) return s;
   if (d_head != 64 && d_head != 128)

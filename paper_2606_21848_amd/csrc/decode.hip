@@ -201,29 +201,44 @@ struct SegOut {
   int stride;
 };
 
-// Merge the per-wave states (acc[R][D], m, l in LDS) of the workgroup and
-// store them to `o`. Ends with a barrier, so the LDS can be refilled.
-template <typename T, int D, int R, int NW>
-__device__ __forceinline__ void merge_waves(const DecodeParams& p, const float (*s_acc)[R][D],
+// Merge the per-wave states (acc[R][D] of wave w at s_acc + w WS, m and l in
+// s_ml) of the workgroup and store them to `o`. Ends with a barrier, so the LDS
+// can be refilled.
+template <typename T, int D, int R, int NW, int WS = R * D>
+__device__ __forceinline__ void merge_waves(const DecodeParams& p, const float* s_acc,
                                             const float (*s_ml)[R][2], size_t bh0, SegOut o) {
+  // Per head, once: the common reference (the largest wave maximum), each
+  // wave's factor 2^(m_w - reference) and the merged weight sum.
+  __shared__ float s_f[NW][R];
+  __shared__ float s_h[R][2];
   __syncthreads();
-  for (int i = threadIdx.x; i < R * (D + 2); i += NW * 64) {
-    const int r = i / (D + 2);
-    const int c = i % (D + 2);
+  for (int r = threadIdx.x; r < R; r += NW * 64) {
     float mm = -INFINITY;
 #pragma unroll
     for (int w = 0; w < NW; ++w) mm = fmaxf(mm, s_ml[w][r][0]);
     const float ms = (mm == -INFINITY) ? 0.f : mm;
     float lsum = 0.f;
 #pragma unroll
-    for (int w = 0; w < NW; ++w) lsum += s_ml[w][r][1] * fast_exp2(s_ml[w][r][0] - ms);
+    for (int w = 0; w < NW; ++w) {
+      const float f = fast_exp2(s_ml[w][r][0] - ms);  // 0 for a wave that saw no row
+      s_f[w][r] = f;
+      lsum += s_ml[w][r][1] * f;
+    }
+    s_h[r][0] = mm;
+    s_h[r][1] = lsum;
+  }
+  __syncthreads();
+  for (int i = threadIdx.x; i < R * (D + 2); i += NW * 64) {
+    const int r = i / (D + 2);
+    const int c = i % (D + 2);
+    const float lsum = s_h[r][1];
     float val;
     if (c < D) {
       val = 0.f;
 #pragma unroll
-      for (int w = 0; w < NW; ++w) val += s_acc[w][r][c] * fast_exp2(s_ml[w][r][0] - ms);
+      for (int w = 0; w < NW; ++w) val += s_acc[w * WS + r * D + c] * s_f[w][r];
     } else {
-      val = (c == D) ? mm : lsum;
+      val = (c == D) ? s_h[r][0] : lsum;
     }
     if (o.part == nullptr) {
       if (c < D) store_out<T>(p.out, (bh0 + r) * D + c, lsum > 0.f ? val / lsum : 0.f);
@@ -500,7 +515,7 @@ __global__ __launch_bounds__(NW * 64) void decode_partial_kernel(DecodeParams p)
       }
     }
   }
-  merge_waves<T, D, R, NW>(p, s_acc, s_ml, bh0, so);
+  merge_waves<T, D, R, NW>(p, &s_acc[0][0][0], s_ml, bh0, so);
   };
   for_each_segment<T, D, R, PAGED, NW>(p, segment);
 }
@@ -535,7 +550,14 @@ __global__ __launch_bounds__(NW * 64) void decode_mfma_kernel(DecodeParams p) {
   auto fsw = [](int r) { return ((r & 7) << 1) | ((r >> 3) & 1); };
   extern __shared__ __attribute__((aligned(1024))) unsigned char dyn_lds[];
   lds_u8* const ring = (lds_u8*)dyn_lds + wave * (NBUF * SB);
-  __shared__ float s_acc[NW][R][D];
+  // A wave's merge rows (acc[R][D]) go into its own ring once its stream has
+  // ended (its copies have all landed and been read), when they fit there; the
+  // ring is refilled only after the merge's closing barrier. This keeps the
+  // LDS of 16 or 32 heads per group at the ring's size.
+  constexpr bool kAlias = R * D * 4 <= NBUF * SB;
+  constexpr int WS = kAlias ? NBUF * SB / 4 : R * D;  // floats between waves' rows
+  __shared__ float s_acc_own[kAlias ? 1 : NW * R * D];
+  float* const s_acc = kAlias ? (float*)dyn_lds : s_acc_own;
   __shared__ float s_ml[NW][R][2];
 
   // LDS byte offsets within a stage. Score A operand: row hl, chunk 4 kk + grp.
@@ -657,14 +679,14 @@ __global__ __launch_bounds__(NW * 64) void decode_mfma_kernel(DecodeParams p) {
 #pragma unroll
       for (int dd = 0; dd < 8; ++dd)
 #pragma unroll
-        for (int i = 0; i < 4; ++i) s_acc[wave][h][16 * dd + 4 * grp + i] = acc[nb][dd][i];
+        for (int i = 0; i < 4; ++i) s_acc[wave * WS + h * D + 16 * dd + 4 * grp + i] = acc[nb][dd][i];
       if (grp == 0) {
         s_ml[wave][h][0] = m[nb];
         s_ml[wave][h][1] = ls;
       }
     }
   }
-  merge_waves<T, D, R, NW>(p, s_acc, s_ml, bh0, so);
+  merge_waves<T, D, R, NW, WS>(p, s_acc, s_ml, bh0, so);
   };
   for_each_segment<T, D, R, PAGED, NW>(p, segment);
 }

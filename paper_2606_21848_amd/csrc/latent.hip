@@ -3,12 +3,16 @@
 // matrix W_post_h [r, d_k]:
 //   absorb:  q*[b, h] = q~[b, h] W_post_h^T     (d_k -> r, before the decode)
 //   expand:  out[b, h] = o*[b, h] W_post_h      (r -> d_k, after the decode)
-// Both are y = x M with M = W_post_h^T or W_post_h. A workgroup takes one head
-// and up to 32 sequences: it stages M in LDS as fp32 laid out [contraction]
-// [output] (row pitch n_out + 1, so the transposing stores of the absorb hit
-// distinct banks), stages the 32 input vectors, and each thread accumulates one
-// output column for 8 or 16 sequences in fp32. The matrices are read once per
-// 32 sequences; both products are tiny next to the cache stream they bracket.
+// Both are y = x M with M = W_post_h^T or W_post_h, tiny next to the cache
+// stream they bracket, so they are built for latency: bf16 runs one wave per
+// (head, 16 sequences, 64 output columns) on v_mfma_f32_16x16x32_bf16 with
+// both operands loaded straight into registers (the absorb's weight fragments
+// are 16-byte row pieces of W_post_h; the expand's are 8 column elements,
+// loaded 2 bytes at a time, 16 lanes covering 32 contiguous bytes). fp32 runs
+// a VALU kernel: a workgroup takes one head and up to 32 sequences, stages M
+// in LDS as [contraction][output] (row pitch n_out + 1, so the transposing
+// stores of the absorb hit distinct banks) and each thread accumulates one
+// output column for 8 or 16 sequences.
 
 #include "kl_device.h"
 #include "kl_internal.h"
@@ -76,6 +80,71 @@ __global__ __launch_bounds__(kThreads) void latent_product_kernel(LatentParams p
   }
 }
 
+typedef __attribute__((__vector_size__(8 * sizeof(__bf16)))) __bf16 bf16x8_t;
+typedef __attribute__((__vector_size__(4 * sizeof(float)))) float f32x4_t;
+
+// bf16: y[b, h, n] for b in [16 by, +16), n in [64 bz, +64); NIN, NOUT in {64, 128}.
+template <int NIN, int NOUT, bool ABSORB>
+__global__ __launch_bounds__(64) void latent_mfma_kernel(LatentParams p) {
+  const int h = blockIdx.x, b0 = blockIdx.y * 16, n0 = blockIdx.z * 64;
+  const int lane = threadIdx.x, fr = lane & 15, grp = lane >> 4;
+  const uint16_t* __restrict__ X = reinterpret_cast<const uint16_t*>(p.x);
+  const uint16_t* __restrict__ W = reinterpret_cast<const uint16_t*>(p.W) + (size_t)h * p.r * p.dk;
+  // A operand: x row b0 + fr (clamped; rows past B are never stored), k = 32 ks + 8 grp .. + 7.
+  const uint16_t* xrow = X + ((size_t)min(b0 + fr, p.B - 1) * p.H + h) * NIN + 8 * grp;
+  f32x4_t acc[4];
+#pragma unroll
+  for (int nb = 0; nb < 4; ++nb) acc[nb] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int ks = 0; ks < NIN / 32; ++ks) {
+    const bf16x8_t a = __builtin_bit_cast(bf16x8_t, *reinterpret_cast<const u32x4*>(xrow + 32 * ks));
+#pragma unroll
+    for (int nb = 0; nb < 4; ++nb) {
+      const int n = n0 + 16 * nb + fr;  // output column of this lane
+      const int k0 = 32 * ks + 8 * grp;
+      u32x4 w;
+      if constexpr (ABSORB) {
+        // M[k][n] = W_post_h[n][k]: eight consecutive k of row n.
+        w = *reinterpret_cast<const u32x4*>(W + (size_t)n * NIN + k0);
+      } else {
+        // M[k][n] = W_post_h[k][n]: column n, rows k0 .. k0 + 7.
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+          w[i] = (uint32_t)W[(size_t)(k0 + 2 * i) * NOUT + n] |
+                 ((uint32_t)W[(size_t)(k0 + 2 * i + 1) * NOUT + n] << 16);
+      }
+      acc[nb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, __builtin_bit_cast(bf16x8_t, w),
+                                                        acc[nb], 0, 0, 0);
+    }
+  }
+  // Lane holds y[b0 + 4 grp + i][n0 + 16 nb + fr].
+  uint16_t* __restrict__ Y = reinterpret_cast<uint16_t*>(p.y);
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int b = b0 + 4 * grp + i;
+    if (b >= p.B) continue;
+#pragma unroll
+    for (int nb = 0; nb < 4; ++nb)
+      Y[((size_t)b * p.H + h) * NOUT + n0 + 16 * nb + fr] =
+          __builtin_bit_cast(uint16_t, (__bf16)acc[nb][i]);
+  }
+}
+
+template <bool ABSORB>
+hipError_t launch_mfma(const LatentParams& p, hipStream_t st) {
+  const int nin = ABSORB ? p.dk : p.r, nout = ABSORB ? p.r : p.dk;
+  const dim3 grid(p.H, (p.B + 15) / 16, nout / 64);
+  if (nin == 128 && nout == 128)
+    hipLaunchKernelGGL((latent_mfma_kernel<128, 128, ABSORB>), grid, dim3(64), 0, st, p);
+  else if (nin == 128 && nout == 64)
+    hipLaunchKernelGGL((latent_mfma_kernel<128, 64, ABSORB>), grid, dim3(64), 0, st, p);
+  else if (nin == 64 && nout == 128)
+    hipLaunchKernelGGL((latent_mfma_kernel<64, 128, ABSORB>), grid, dim3(64), 0, st, p);
+  else
+    hipLaunchKernelGGL((latent_mfma_kernel<64, 64, ABSORB>), grid, dim3(64), 0, st, p);
+  return hipGetLastError();
+}
+
 template <typename T, bool ABSORB>
 hipError_t launch_dims(const LatentParams& p, hipStream_t st) {
   const dim3 grid(p.H, (p.B + kSeq - 1) / kSeq);
@@ -98,8 +167,7 @@ hipError_t launch_dims(const LatentParams& p, hipStream_t st) {
 hipError_t launch_latent_product(const LatentParams& p, hipStream_t st) {
   if (p.B <= 0 || p.H <= 0) return hipSuccess;
   if ((p.r != 64 && p.r != 128) || (p.dk != 64 && p.dk != 128)) return hipErrorInvalidValue;
-  if (p.dtype == KL_BF16)
-    return p.absorb ? launch_dims<uint16_t, true>(p, st) : launch_dims<uint16_t, false>(p, st);
+  if (p.dtype == KL_BF16) return p.absorb ? launch_mfma<true>(p, st) : launch_mfma<false>(p, st);
   return p.absorb ? launch_dims<float, true>(p, st) : launch_dims<float, false>(p, st);
 }
 

@@ -196,4 +196,5 @@ def test_latent_decode_workspace_and_rejects(lib):
     expect(lib, lat(c=cache(G=1, dtype=kb.KL_F32)), kb.KL_ERR_UNSUPPORTED, "H/G=32")
     expect(lib, lat(scale=-2.0), kb.KL_ERR_INVALID_ARG, "scale")
     expect(lib, lat(ws_bytes=100), kb.KL_ERR_WORKSPACE, "workspace")
+    expect(lib, lat(w=ctypes.c_void_p(0x100008)), kb.KL_ERR_INVALID_ARG, "aligned")
     assert lat(B=0, ws_bytes=0) == kb.KL_OK
