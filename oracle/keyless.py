@@ -32,6 +32,9 @@ notes):
   latent group h // (H // G), as for grouped values.
 * Cross-attention (Eq. 14) takes the multi-head and grouped forms of Section 3
   unchanged, with no mask; an empty X^(b) gives zero rows.
+* Backward (Section 2.3): Eqs. 5 and 6 are written for one head; per head the
+  routing gradient contracts that head's un-routed query X W^Q_h with dQ~_h, and
+  a value group's gradient sums the retrieval and score terms of all its heads.
 """
 
 from __future__ import annotations
@@ -477,6 +480,86 @@ def brute_force_keyless(X, Wt_Q, W_V, causal: bool = True, scale: float | None =
         z = sum(e.values())
         out.append([sum(e[j] / z * v[j][c] for j in js) for c in range(dk)])
     return np.array(out)
+
+
+# ---------------------------------------------------------------------------
+# Section 2.3, Eqs. 5 and 6: the backward pass
+# ---------------------------------------------------------------------------
+
+def keyless_attention_backward(Qr, V, dO, H: int, G: int, d_head: int, causal: bool = True,
+                               scale: float | None = None):
+    """Gradients of the keyless attention O_h = softmax(tau Q~_h V_g^T) V_g with
+    respect to the routed queries and the values, given dL/dO. Per batch b and
+    head h (group g = h // (H // G)), with P the masked softmax:
+      dP    = dO_h V_g^T
+      dS    = P * (dP - rowsum(P * dP))        (softmax backward; dL/dS of Section 2.3)
+      dQ~_h = tau dS V_g
+      dV_g += P^T dO_h                         (retrieval: V as the averaged values)
+            + tau dS^T Q~_h                    (routing: V inside the scores)
+    The last two are the two terms of Eq. 6 before the product with X^T; a group's
+    value gradient sums them over its heads.
+
+    Qr: [B, N, H, d_k]; V: [B, N, G, d_k]; dO: [B, N, H, d_k].
+    Returns (dQ~ [B, N, H, d_k], dV [B, N, G, d_k]).
+    """
+    Qr = _f64(Qr)
+    V = _f64(V)
+    dO = _f64(dO)
+    B, N = Qr.shape[0], Qr.shape[1]
+    tau = default_scale(d_head) if scale is None else float(scale)
+    rep = H // G
+    dQr = np.zeros(Qr.shape)
+    dV = np.zeros(V.shape)
+    for b in range(B):
+        for h in range(H):
+            g = h // rep
+            Q_h, V_g, dO_h = Qr[b, :, h, :], V[b, :, g, :], dO[b, :, h, :]
+            S = tau * (Q_h @ V_g.T)
+            if causal:
+                S = np.where(np.tril(np.ones((N, N), dtype=bool)), S, -np.inf)
+            P = softmax_rows(S)
+            dP = dO_h @ V_g.T
+            dS = P * (dP - np.sum(P * dP, axis=1, keepdims=True))
+            dQr[b, :, h, :] = tau * (dS @ V_g)
+            dV[b, :, g, :] += P.T @ dO_h + tau * (dS.T @ Q_h)
+    return dQr, dV
+
+
+def keyless_backward(x, W_Q, W_R, W_V, dO, H: int, G: int, d_head: int, causal: bool = True,
+                     scale: float | None = None):
+    """The backward pass of the layer of Eq. 2 through its projections
+    (Section 2.3). With Q_h = X W^Q_h, Q~_h = Q_h W^R_h, V_g = X W^V_g and the
+    attention gradients dQ~, dV of keyless_attention_backward:
+      dW^R_h = Q_h^T dQ~_h                      (Eq. 5)
+      dQ_h   = dQ~_h (W^R_h)^T
+      dW^Q   = X^T dQ                           (heads side by side)
+      dW^V   = X^T dV                           (Eq. 6, both terms inside dV)
+      dX     = dQ (W^Q)^T + dV (W^V)^T
+    summed over the batch. x: [B, N, d]; weights as in keyless_prefill; dO
+    [B, N, H, d_k]. Returns a dict with dX [B, N, d], dW_Q [d, H d_k],
+    dW_R [H, d_k, d_k], dW_V [d, G d_k], dQr, dV.
+    """
+    x = _f64(x)
+    W_Q = _f64(W_Q)
+    W_R = _f64(W_R)
+    W_V = _f64(W_V)
+    B, N, d = x.shape
+    _, Qr, V = keyless_prefill(x, W_Q, W_R, W_V, H, G, d_head, causal=causal, scale=scale)
+    dQr, dV = keyless_attention_backward(Qr, V, dO, H, G, d_head, causal=causal, scale=scale)
+    dW_R = np.zeros((H, d_head, d_head))
+    dQ = np.zeros((B, N, H, d_head))
+    for h in range(H):
+        cols = slice(h * d_head, (h + 1) * d_head)
+        for b in range(B):
+            Q_h = x[b] @ W_Q[:, cols]
+            dW_R[h] += Q_h.T @ dQr[b, :, h, :]
+            dQ[b, :, h, :] = dQr[b, :, h, :] @ W_R[h].T
+    dQf = dQ.reshape(B, N, H * d_head)
+    dVf = dV.reshape(B, N, G * d_head)
+    dW_Q = sum(x[b].T @ dQf[b] for b in range(B))
+    dW_V = sum(x[b].T @ dVf[b] for b in range(B))
+    dX = np.stack([dQf[b] @ W_Q.T + dVf[b] @ W_V.T for b in range(B)])
+    return dict(dX=dX, dW_Q=dW_Q, dW_R=dW_R, dW_V=dW_V, dQr=dQr, dV=dV)
 
 
 # ---------------------------------------------------------------------------

@@ -9,6 +9,7 @@ import textwrap
 import pytest
 
 from oracle import keyless as K
+from tests import test_oracle_backward as BW
 from tests import test_oracle_pins as P
 from tests import test_oracle_theorems as T
 
@@ -47,6 +48,18 @@ MUTATIONS = [
      "latent decode at 1/sqrt(d_k)"),
     ("latent_decode", "rows = cache_rows(latent_cache, b, h // rep,",
      "rows = cache_rows(latent_cache, b, h % G,", "latent decode head-to-group map h % G"),
+    ("keyless_attention_backward", "dV[b, :, g, :] += P.T @ dO_h + tau * (dS.T @ Q_h)",
+     "dV[b, :, g, :] += tau * (dS.T @ Q_h)", "value gradient without the retrieval term"),
+    ("keyless_attention_backward", "dV[b, :, g, :] += P.T @ dO_h + tau * (dS.T @ Q_h)",
+     "dV[b, :, g, :] += P.T @ dO_h", "value gradient without the score term"),
+    ("keyless_attention_backward", "dS = P * (dP - np.sum(P * dP, axis=1, keepdims=True))",
+     "dS = P * (dP + np.sum(P * dP, axis=1, keepdims=True))", "softmax backward sign"),
+    ("keyless_attention_backward", "dQr[b, :, h, :] = tau * (dS @ V_g)",
+     "dQr[b, :, h, :] = dS @ V_g", "routed-query gradient without the scale"),
+    ("keyless_backward", "dW_R[h] += Q_h.T @ dQr[b, :, h, :]",
+     "dW_R[h] += dQr[b, :, h, :].T @ Q_h", "routing gradient transposed (Eq. 5)"),
+    ("keyless_backward", "dQ[b, :, h, :] = dQr[b, :, h, :] @ W_R[h].T",
+     "dQ[b, :, h, :] = dQr[b, :, h, :] @ W_R[h]", "query gradient through W^R untransposed"),
     ("keyless_cross_attention", "Qt_h = Q_h if W_R is None else Q_h @ _f64(W_R)[h]",
      "Qt_h = Q_h if W_R is None else Q_h @ _f64(W_R)[h].T", "routing matrix transposed in cross-attention"),
     ("keyless_cross_attention", "V[b, :, g, :] = xb[b] @", "V[b, :, g, :] = xa[b] @",
@@ -64,7 +77,7 @@ MUTATIONS = [
 def _pins():
     """Every pin function with a representative argument set."""
     pins = []
-    for mod in (P, T):
+    for mod in (P, T, BW):
         for name, fn in sorted(vars(mod).items()):
             if not name.startswith("test_") or not callable(fn):
                 continue
