@@ -219,6 +219,63 @@ int keyless_cross_attention_packed(const void* xa, const void* xb, const void* p
                                    void* v_out, void* ws, size_t ws_bytes, void* stream);
 
 /*
+ * keyless_attention_forward - the attention of Eq. 2 (score Eq. 4) on routed
+ * queries and values already projected, also writing each row's log-sum-exp for
+ * the backward pass:
+ *   q_routed [B, N, H, d_head], v [B, N, G, d_head], out [B, N, H, d_head], all
+ *   contiguous and 16-byte aligned, in `dtype`
+ *   lse      [B, H, N] fp32, or NULL: ln sum_j exp(scale <q~_i, v_j>) over the
+ *            rows j that row i sees
+ * causal, scale, precision and errors as for keyless_prefill.
+ */
+int keyless_attention_forward(const void* q_routed, const void* v, int B, int N, int H, int G,
+                              int d_head, int causal, float scale, kl_dtype dtype, void* out,
+                              float* lse, void* stream);
+
+/*
+ * keyless_attention_backward - gradients of the keyless attention (Section 2.3)
+ * with respect to the routed queries and the values, given dL/dO:
+ *   dS  = P * (dO V^T - rowsum(dO * O)),  P the forward's weights (from lse)
+ *   dq_routed = scale dS V
+ *   dv        = P^T dO + scale dS^T Q~   (the retrieval and routing terms of
+ *               Eq. 6; a value group sums them over its H/G heads)
+ *   q_routed, v, out (the forward's output), dout [B, N, H, d_head] and lse as
+ *   written by keyless_attention_forward with the same causal and scale;
+ *   dq_routed [B, N, H, d_head], dv [B, N, G, d_head]; all 16-byte aligned.
+ *   ws, ws_bytes  keyless_attention_backward_workspace_size(B, N, H) bytes (the
+ *                 per-row rowsum(dO * O), B*H*N floats)
+ * Self-attention only (the value rows are the query rows). bf16 with d_head 64
+ * or 128 runs on MFMA (P and dS rounded to bf16 for the products, fp32
+ * accumulation); fp32 on the vector ALU. Every output element is written once
+ * (no atomics): results are deterministic.
+ */
+int keyless_attention_backward(const void* q_routed, const void* v, const void* out,
+                               const void* dout, const float* lse, int B, int N, int H, int G,
+                               int d_head, int causal, float scale, kl_dtype dtype, void* dq_routed,
+                               void* dv, void* ws, size_t ws_bytes, void* stream);
+size_t keyless_attention_backward_workspace_size(int B, int N, int H);
+
+/*
+ * keyless_weight_gradients - the rest of the backward pass through the
+ * projections Q_h = X W^Q_h, Q~_h = Q_h W^R_h, V = X W^V (Section 2.3):
+ *   dW_R[h] = (X W^Q_h)^T dq_routed_h           (Eq. 5)
+ *   dQ_h    = dq_routed_h W_R[h]^T
+ *   dW_Q    = X^T dQ,   dW_V = X^T dv           (Eq. 6; dv holds both terms)
+ *   dx      = dQ W_Q^T + dv W_V^T
+ * summed over the batch. x [B, N, d_model]; W_Q [d_model, H*d_head], W_R [H,
+ * d_head, d_head], W_V [d_model, G*d_head]; dq_routed, dv as written by
+ * keyless_attention_backward. Outputs dW_Q, dW_R, dW_V (the weights' shapes) and
+ * dx [B, N, d_model]; any of them may be NULL to skip it. ws, ws_bytes:
+ * keyless_weight_gradients_workspace_size(...) bytes (X W^Q and dQ). These are
+ * plain contractions on the generic fp32-arithmetic kernel (not tuned).
+ */
+int keyless_weight_gradients(const void* x, const void* W_Q, const void* W_R, const void* W_V,
+                             const void* dq_routed, const void* dv, int B, int N, int d_model,
+                             int H, int G, int d_head, kl_dtype dtype, void* dW_Q, void* dW_R,
+                             void* dW_V, void* dx, void* ws, size_t ws_bytes, void* stream);
+size_t keyless_weight_gradients_workspace_size(int B, int N, int H, int d_head, kl_dtype dtype);
+
+/*
  * keyless_decode_project - the projections of one decode step (Section 3: the
  * current token's routed query q~_{n+1} and its value v_{n+1}, i.e. the
  * projections of Eq. 2 for one token per sequence), from weights prepared by

@@ -525,6 +525,67 @@ def keyless_attention_backward(Qr, V, dO, H: int, G: int, d_head: int, causal: b
     return dQr, dV
 
 
+def attention_logsumexp(Qr, V, H: int, G: int, d_head: int, causal: bool = True,
+                        scale: float | None = None):
+    """ln sum_j exp(tau <q~_i, v_j>) over the rows j that row i sees, per batch,
+    head and row: the normaliser of the Eq. 2 softmax. Returns [B, H, N]."""
+    Qr = _f64(Qr)
+    V = _f64(V)
+    B, N = Qr.shape[0], Qr.shape[1]
+    tau = default_scale(d_head) if scale is None else float(scale)
+    rep = H // G
+    out = np.zeros((B, H, N))
+    for b in range(B):
+        for h in range(H):
+            S = tau * (Qr[b, :, h, :] @ V[b, :, h // rep, :].T)
+            if causal:
+                S = np.where(np.tril(np.ones((N, N), dtype=bool)), S, -np.inf)
+            m = np.max(S, axis=1, keepdims=True)
+            out[b, h] = (m + np.log(np.sum(np.exp(S - m), axis=1, keepdims=True)))[:, 0]
+    return out
+
+
+def keyless_attention_backward_rows(Qr, V, dO, H: int, G: int, d_head: int, dq_rows, dv_rows,
+                                    causal: bool = True, scale: float | None = None):
+    """Rows of keyless_attention_backward for batch 0, for sizes where the whole
+    N x N problem is too large: dQ~ of the query rows ``dq_rows`` and dV of the
+    value rows ``dv_rows``. Every query row that can see a requested value row
+    is evaluated in full (its softmax and rowsum(P * dP)).
+    Returns (dQ~ [len(dq_rows), H, d_k], dV [len(dv_rows), G, d_k])."""
+    Qr = _f64(Qr)[0]
+    V = _f64(V)[0]
+    dO = _f64(dO)[0]
+    N = Qr.shape[0]
+    tau = default_scale(d_head) if scale is None else float(scale)
+    rep = H // G
+    dq_rows = [int(i) for i in dq_rows]
+    dv_rows = [int(j) for j in dv_rows]
+
+    def row(i, h):  # P, dS of query row i (head h) over the rows it sees
+        g = h // rep
+        seen = i + 1 if causal else N
+        s = tau * (V[:seen, g, :] @ Qr[i, h])
+        P = softmax_rows(s[None, :])[0]
+        dP = V[:seen, g, :] @ dO[i, h]
+        return P, P * (dP - np.sum(P * dP))
+
+    dQ = np.zeros((len(dq_rows), H, d_head))
+    for k, i in enumerate(dq_rows):
+        for h in range(H):
+            _, dS = row(i, h)
+            dQ[k, h] = tau * (dS @ V[:len(dS), h // rep, :])
+    dV = np.zeros((len(dv_rows), G, d_head))
+    if dv_rows:
+        first = min(dv_rows) if causal else 0
+        for i in range(first, N):
+            for h in range(H):
+                P, dS = row(i, h)
+                for k, j in enumerate(dv_rows):
+                    if j < len(P):
+                        dV[k, h // rep] += P[j] * dO[i, h] + tau * dS[j] * Qr[i, h]
+    return dQ, dV
+
+
 def keyless_backward(x, W_Q, W_R, W_V, dO, H: int, G: int, d_head: int, causal: bool = True,
                      scale: float | None = None):
     """The backward pass of the layer of Eq. 2 through its projections

@@ -26,6 +26,9 @@ EXPORTS = (
     "keyless_cross_attention", "keyless_cross_attention_workspace_size",
     "keyless_cross_attention_packed",
     "keyless_latent_decode", "keyless_latent_decode_workspace_size",
+    "keyless_attention_forward", "keyless_attention_backward",
+    "keyless_attention_backward_workspace_size", "keyless_weight_gradients",
+    "keyless_weight_gradients_workspace_size",
     "keyless_decode_project", "keyless_decode", "keyless_decode_chunked", "keyless_decode_workspace_size",
     "value_cache_append", "standard_decode", "standard_decode_chunked",
     "keyless_set_kernel_timer", "keyless_last_error", "keyless_version",
@@ -80,6 +83,13 @@ def load(path: str = LIB_PATH):
         "keyless_decode_workspace_size": (sz, [cp, i, i, i]),
         "keyless_latent_decode": (i, [vp, vp, cp, vp, i, i, i, f, vp, vp, sz, vp]),
         "keyless_latent_decode_workspace_size": (sz, [cp, i, i, i]),
+        "keyless_attention_forward": (i, [vp, vp, i, i, i, i, i, i, f, i, vp, vp, vp]),
+        "keyless_attention_backward": (i, [vp, vp, vp, vp, vp, i, i, i, i, i, i, f, i, vp, vp,
+                                           vp, sz, vp]),
+        "keyless_attention_backward_workspace_size": (sz, [i, i, i]),
+        "keyless_weight_gradients": (i, [vp, vp, vp, vp, vp, vp, i, i, i, i, i, i, i, vp, vp, vp,
+                                         vp, vp, sz, vp]),
+        "keyless_weight_gradients_workspace_size": (sz, [i, i, i, i, i]),
         "value_cache_append": (i, [cp, vp, vp, i, i, vp]),
         "standard_decode": (i, [vp, cp, cp, vp, i, i, f, vp, vp, sz, vp]),
         "standard_decode_chunked": (i, [vp, cp, cp, vp, i, i, f, vp, vp, sz, i, vp]),
@@ -401,3 +411,60 @@ def keyless_latent_decode(q_routed: torch.Tensor, W_post: torch.Tensor, cache: "
                                       dk, scale, _ptr(out), _ptr(workspace), workspace.numel(),
                                       _stream(q_routed)))
     return out
+
+
+def keyless_attention_forward(q_routed: torch.Tensor, v: torch.Tensor, causal: bool = True,
+                              scale: float = 0.0, out=None, lse=None):
+    """Attention over projected routed queries [B, N, H, d] and values [B, N, G, d];
+    returns (out, lse [B, H, N] fp32, the natural-log log-sum-exp per row)."""
+    load()
+    B, N, H, dk = q_routed.shape
+    G = v.shape[2]
+    if out is None:
+        out = torch.empty_like(q_routed)
+    if lse is None:
+        lse = torch.empty((B, H, N), dtype=torch.float32, device=q_routed.device)
+    _check(_lib.keyless_attention_forward(_ptr(q_routed), _ptr(v), B, N, H, G, dk, int(causal),
+                                          scale, _dt(q_routed), _ptr(out), _ptr(lse),
+                                          _stream(q_routed)))
+    return out, lse
+
+
+def keyless_attention_backward(q_routed: torch.Tensor, v: torch.Tensor, out: torch.Tensor,
+                               dout: torch.Tensor, lse: torch.Tensor, causal: bool = True,
+                               scale: float = 0.0, dq=None, dv=None, workspace=None):
+    """(dq_routed, dv) of the keyless attention from dout and the forward's out, lse."""
+    load()
+    B, N, H, dk = q_routed.shape
+    G = v.shape[2]
+    if dq is None:
+        dq = torch.empty_like(q_routed)
+    if dv is None:
+        dv = torch.empty_like(v)
+    if workspace is None:
+        n = int(_lib.keyless_attention_backward_workspace_size(B, N, H))
+        workspace = torch.empty(max(n, 256), dtype=torch.uint8, device=q_routed.device)
+    _check(_lib.keyless_attention_backward(_ptr(q_routed), _ptr(v), _ptr(out), _ptr(dout), _ptr(lse),
+                                           B, N, H, G, dk, int(causal), scale, _dt(q_routed),
+                                           _ptr(dq), _ptr(dv), _ptr(workspace), workspace.numel(),
+                                           _stream(q_routed)))
+    return dq, dv
+
+
+def keyless_weight_gradients(x: torch.Tensor, W_Q: torch.Tensor, W_R: torch.Tensor,
+                             W_V: torch.Tensor, dq_routed: torch.Tensor, dv: torch.Tensor,
+                             H: int, G: int, workspace=None):
+    """dict(dW_Q, dW_R, dW_V, dX) from the attention gradients (Eqs. 5 and 6)."""
+    load()
+    B, N, d_model = x.shape
+    dk = W_Q.shape[1] // H
+    res = dict(dW_Q=torch.empty_like(W_Q), dW_R=torch.empty_like(W_R), dW_V=torch.empty_like(W_V),
+               dX=torch.empty_like(x))
+    if workspace is None:
+        n = int(_lib.keyless_weight_gradients_workspace_size(B, N, H, dk, _dt(x)))
+        workspace = torch.empty(max(n, 256), dtype=torch.uint8, device=x.device)
+    _check(_lib.keyless_weight_gradients(_ptr(x), _ptr(W_Q), _ptr(W_R), _ptr(W_V), _ptr(dq_routed),
+                                         _ptr(dv), B, N, d_model, H, G, dk, _dt(x), _ptr(res["dW_Q"]),
+                                         _ptr(res["dW_R"]), _ptr(res["dW_V"]), _ptr(res["dX"]),
+                                         _ptr(workspace), workspace.numel(), _stream(x)))
+    return res

@@ -452,7 +452,7 @@ int check_cross_args(const char* who, const void* xb, int B, int N_b) {
 // sequences).
 int run_attention(const char* who, const void* qr, long q_stride, const void* vv, long v_stride,
                   void* out, int B, int N, int Nk, int H, int G, int d_head, int causal,
-                  float scale, kl_dtype dtype, hipStream_t st) {
+                  float scale, kl_dtype dtype, hipStream_t st, float* lse = nullptr) {
   kl::AttnParams a{};
   a.q = qr;
   a.v = vv;
@@ -469,6 +469,7 @@ int run_attention(const char* who, const void* qr, long q_stride, const void* vv
   a.causal = causal ? 1 : 0;
   a.scale_log2 = scale_or_default(scale, d_head) * kLog2e;
   a.dtype = dtype;
+  a.lse = lse;
   // No value rows (an empty X^(b)): the VALU kernel writes the zero rows.
   if (Nk > 0 && kl::attn_bf16_supported(a))
     return hip_status(kl::launch_prefill_attention(a, st), who);
@@ -716,6 +717,133 @@ int keyless_cross_attention(const void* xa, const void* xb, const void* W_Q, con
   return attend_entry(who, xa, xb, W_Q, W_R, W_V, B, N_a, N_b, d_model, H, G, d_head, 0, scale,
                       dtype, out, q_routed_out, v_out, ws, ws_bytes,
                       static_cast<hipStream_t>(stream));
+}
+
+int keyless_attention_forward(const void* q_routed, const void* v, int B, int N, int H, int G,
+                              int d_head, int causal, float scale, kl_dtype dtype, void* out,
+                              float* lse, void* stream) {
+  const char* who = "keyless_attention_forward";
+  int s = check_prefill_args(who, q_routed, v, out, B, N, 64, H, G, d_head, dtype, scale);
+  if (s != KL_OK) return s;
+  if (!aligned16(q_routed) || !aligned16(v) || !aligned16(out))
+    return fail(KL_ERR_INVALID_ARG, "%s: q_routed, v and out must be 16-byte aligned", who);
+  if (B == 0 || N == 0) return KL_OK;
+  return run_attention(who, q_routed, (long)H * d_head, v, (long)G * d_head, out, B, N, N, H, G,
+                       d_head, causal, scale, dtype, static_cast<hipStream_t>(stream), lse);
+}
+
+size_t keyless_attention_backward_workspace_size(int B, int N, int H) {
+  if (B < 0 || N < 0 || H <= 0) return 0;
+  return align256((size_t)B * H * N * sizeof(float));
+}
+
+int keyless_attention_backward(const void* q_routed, const void* v, const void* out,
+                               const void* dout, const float* lse, int B, int N, int H, int G,
+                               int d_head, int causal, float scale, kl_dtype dtype, void* dq_routed,
+                               void* dv, void* ws, size_t ws_bytes, void* stream) {
+  const char* who = "keyless_attention_backward";
+  int s = check_prefill_args(who, q_routed, v, out, B, N, 64, H, G, d_head, dtype, scale);
+  if (s != KL_OK) return s;
+  if (!dout || !lse || !dq_routed || !dv)
+    return fail(KL_ERR_INVALID_ARG, "%s: dout, lse, dq_routed and dv must be non-NULL", who);
+  if (!aligned16(q_routed) || !aligned16(v) || !aligned16(out) || !aligned16(dout) ||
+      !aligned16(dq_routed) || !aligned16(dv))
+    return fail(KL_ERR_INVALID_ARG, "%s: tensors must be 16-byte aligned", who);
+  const size_t need = keyless_attention_backward_workspace_size(B, N, H);
+  if (need && (!ws || ws_bytes < need))
+    return fail(KL_ERR_WORKSPACE, "%s: workspace of %zu bytes needed, %zu given", who, need, ws_bytes);
+  if (B == 0 || N == 0) return KL_OK;
+  kl::BwdParams p{};
+  p.q = q_routed;
+  p.v = v;
+  p.out = out;
+  p.dout = dout;
+  p.lse = lse;
+  p.Dd = static_cast<float*>(ws);
+  p.dq = dq_routed;
+  p.dv = dv;
+  p.q_stride = p.o_stride = p.dq_stride = (long)H * d_head;
+  p.v_stride = p.dv_stride = (long)G * d_head;
+  p.B = B;
+  p.N = N;
+  p.H = H;
+  p.G = G;
+  p.D = d_head;
+  p.causal = causal ? 1 : 0;
+  p.scale = scale_or_default(scale, d_head);
+  p.scale_log2 = p.scale * kLog2e;
+  p.dtype = dtype;
+  return hip_status(kl::launch_attention_backward(p, static_cast<hipStream_t>(stream)), who);
+}
+
+size_t keyless_weight_gradients_workspace_size(int B, int N, int H, int d_head, kl_dtype dtype) {
+  if (B < 0 || N < 0 || H <= 0 || d_head <= 0) return 0;
+  return 2 * align256((size_t)B * N * H * d_head * elem_bytes(dtype));
+}
+
+int keyless_weight_gradients(const void* x, const void* W_Q, const void* W_R, const void* W_V,
+                             const void* dq_routed, const void* dv, int B, int N, int d_model,
+                             int H, int G, int d_head, kl_dtype dtype, void* dW_Q, void* dW_R,
+                             void* dW_V, void* dx, void* ws, size_t ws_bytes, void* stream) {
+  const char* who = "keyless_weight_gradients";
+  if (!x || !W_Q || !W_R || !W_V || !dq_routed || !dv)
+    return fail(KL_ERR_INVALID_ARG, "%s: x, the weights, dq_routed and dv must be non-NULL", who);
+  if (!dtype_ok(dtype)) return fail(KL_ERR_UNSUPPORTED, "%s: unknown dtype", who);
+  if (B < 0 || N < 0 || d_model <= 0 || H <= 0 || G <= 0 || d_head <= 0)
+    return fail(KL_ERR_INVALID_ARG, "%s: bad sizes", who);
+  if (H % G != 0) return fail(KL_ERR_INVALID_ARG, "%s: H=%d is not a multiple of G=%d", who, H, G);
+  if ((long)B * N > (1L << 30)) return fail(KL_ERR_UNSUPPORTED, "%s: B*N too large", who);
+  const size_t need = keyless_weight_gradients_workspace_size(B, N, H, d_head, dtype);
+  if (!ws || ws_bytes < need)
+    return fail(KL_ERR_WORKSPACE, "%s: workspace of %zu bytes needed, %zu given", who, need, ws_bytes);
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  const long M = (long)B * N, NQ = (long)H * d_head, NV = (long)G * d_head;
+  char* w = static_cast<char*>(ws);
+  void* Q = w;                                                   // X W^Q       [M, NQ]
+  void* dQ = w + align256((size_t)M * NQ * elem_bytes(dtype));    // dQ~ W^R^T   [M, NQ]
+  auto gemm = [&](const void* A, long lda, long a_cs, const void* Bm, long ldb, long b_cs, void* C,
+                  long ldc, long Mm, long Nn, long Kk, int batch, long sA, long sB, long sC,
+                  int accumulate) {
+    kl::GemmParams g{};
+    g.A = A;
+    g.Bm = Bm;
+    g.C = C;
+    g.M = (int)Mm;
+    g.N = (int)Nn;
+    g.K = (int)Kk;
+    g.lda = lda;
+    g.a_cs = a_cs;
+    g.ldb = ldb;
+    g.b_cs = b_cs;
+    g.ldc = ldc;
+    g.batch = batch;
+    g.strideA = sA;
+    g.strideB = sB;
+    g.strideC = sC;
+    g.dtype = dtype;
+    g.accumulate = accumulate;
+    return hip_status(kl::launch_gemm_simple(g, st), who);
+  };
+  const long dk = d_head;
+  // With no tokens (M = 0) the contractions over tokens have K = 0 and write
+  // zero weight gradients; the token-shaped outputs are empty.
+  int s = KL_OK;
+  // dQ_h = dQ~_h (W^R_h)^T: B(k, n) = W^R_h[n][k].
+  if (dW_Q || dx) s = gemm(dq_routed, NQ, 1, W_R, 1, dk, dQ, NQ, M, dk, dk, H, dk, dk * dk, dk, 0);
+  // Eq. 5: dW^R_h = (X W^Q_h)^T dQ~_h, a contraction over the tokens.
+  if (s == KL_OK && dW_R) {
+    s = gemm(x, d_model, 1, W_Q, NQ, 1, Q, NQ, M, NQ, d_model, 1, 0, 0, 0, 0);
+    if (s == KL_OK) s = gemm(Q, 1, NQ, dq_routed, NQ, 1, dW_R, dk, dk, dk, M, H, dk, dk, dk * dk, 0);
+  }
+  // dW^Q = X^T dQ, and Eq. 6: dW^V = X^T dV (both of its terms are inside dV).
+  if (s == KL_OK && dW_Q) s = gemm(x, 1, d_model, dQ, NQ, 1, dW_Q, NQ, d_model, NQ, M, 1, 0, 0, 0, 0);
+  if (s == KL_OK && dW_V) s = gemm(x, 1, d_model, dv, NV, 1, dW_V, NV, d_model, NV, M, 1, 0, 0, 0, 0);
+  // dX = dQ (W^Q)^T + dV (W^V)^T.
+  if (s == KL_OK && dx) {
+    s = gemm(dQ, NQ, 1, W_Q, 1, NQ, dx, d_model, M, d_model, NQ, 1, 0, 0, 0, 0);
+    if (s == KL_OK) s = gemm(dv, NV, 1, W_V, 1, NV, dx, d_model, M, d_model, NV, 1, 0, 0, 0, 1);
+  }
+  return s;
 }
 
 }  // extern "C"

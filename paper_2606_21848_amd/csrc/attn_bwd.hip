@@ -1,0 +1,624 @@
+// Backward pass of keyless attention (Section 2.3): given dL/dO, the gradients
+// of the routed queries and of the values. Per batch b and head h (group g):
+//   P   = exp(tau Q~ V^T - lse)        (the forward's weights, from its log-sum-exp)
+//   dP  = dO V^T
+//   dS  = P * (dP - Dd),  Dd = rowsum(dO * O)   (softmax backward)
+//   dQ~ = tau dS V
+//   dV  = P^T dO + tau dS^T Q~        (retrieval and routing terms of Eq. 6)
+// The value tile is read once per product it enters, exactly as in the
+// forward: as the score operand and as the retrieved values (dQ~ kernel), and
+// the value gradient collects both of its roles in the same accumulators.
+//
+// Three kernels: bwd_prep_kernel (Dd), bwd_dq_kernel (one workgroup per
+// 128-row query tile and head; value tiles stream through LDS as in the
+// forward, queries and dO stay in registers) and bwd_dv_kernel (one workgroup
+// per 128-row value tile and value group; query and dO tiles of every head of
+// the group stream through LDS, the values stay in registers). No atomics:
+// every output element is written once, by one lane.
+//
+// bf16 runs on v_mfma_f32_16x16x32_bf16 with the forward's operand layouts:
+// scores come out with one query per lane (S^T = V Q~^T) in the dQ~ kernel and
+// one value row per lane (S = Q~ V^T) in the dV kernel, and in both the weights
+// feed the next product as its B operand without a transpose; the transposed
+// A operands come from ds_read_b64_tr_b16 on the row-major tiles. fp32 runs
+// VALU kernels of the same structure.
+
+#include <type_traits>
+
+#include "attn_tile.h"
+#include "kl_device.h"
+#include "kl_internal.h"
+
+namespace kl {
+namespace {
+
+typedef __attribute__((__vector_size__(8 * sizeof(__bf16)))) __bf16 bf16x8_t;
+typedef __attribute__((__vector_size__(4 * sizeof(float)))) float f32x4_t;
+typedef short s16x4 __attribute__((ext_vector_type(4)));
+typedef unsigned int u32x2 __attribute__((ext_vector_type(2)));
+typedef __attribute__((address_space(3))) unsigned char lds_u8;
+
+constexpr int kThreads = 256;
+constexpr int kTileRows = 64;   // rows per staged tile
+constexpr float kLog2e = 1.4426950408889634f;
+
+template <typename T>
+__device__ __forceinline__ float ldx(const T* p, size_t i) {
+  if constexpr (sizeof(T) == 2) return __uint_as_float((uint32_t)p[i] << 16);
+  else return p[i];
+}
+template <typename T>
+__device__ __forceinline__ void stx(T* p, size_t i, float v) {
+  if constexpr (sizeof(T) == 2) p[i] = __builtin_bit_cast(uint16_t, (__bf16)v);
+  else p[i] = v;
+}
+
+// Dd[b, h, q] = sum_d dO[b, q, h, d] O[b, q, h, d]; 16 lanes per row.
+template <typename T, int D>
+__global__ __launch_bounds__(256) void bwd_prep_kernel(BwdParams p) {
+  const long rows = (long)p.B * p.N * p.H;
+  const long row = (long)blockIdx.x * 16 + threadIdx.x / 16;
+  const int j = threadIdx.x % 16;
+  float s = 0.f;
+  int b = 0, q = 0, h = 0;
+  if (row < rows) {
+    h = (int)(row % p.H);
+    const long bq = row / p.H;
+    b = (int)(bq / p.N);
+    q = (int)(bq % p.N);
+    const T* o = reinterpret_cast<const T*>(p.out) + (size_t)bq * p.o_stride + (size_t)h * D;
+    const T* g = reinterpret_cast<const T*>(p.dout) + (size_t)bq * p.o_stride + (size_t)h * D;
+#pragma unroll
+    for (int c = j; c < D; c += 16) s = fmaf(ldx(o, c), ldx(g, c), s);
+  }
+  s += __shfl_xor(s, 8);
+  s += __shfl_xor(s, 4);
+  s += __shfl_xor(s, 2);
+  s += __shfl_xor(s, 1);
+  if (row < rows && j == 0) p.Dd[((size_t)b * p.H + h) * p.N + q] = s;
+}
+
+// ---------------------------------------------------------------------------
+// bf16, matrix cores
+// ---------------------------------------------------------------------------
+
+constexpr int QBD = 2;                 // 16-row query blocks per wave (dQ~ kernel)
+constexpr int BQD = 4 * 16 * QBD;      // query rows per workgroup
+constexpr int NSTAGE = 3;              // value tiles in flight (dQ~ kernel)
+constexpr int KVB = 2;                 // 16-row value blocks per wave (dV kernel)
+constexpr int BKVD = 4 * 16 * KVB;     // value rows per workgroup
+
+// Direct-to-LDS copy of rows [row0, row0 + 64) (clamped to n_rows - 1) of a
+// row-major bf16 matrix, columns [col, col + D), into an AttnTile<D, 64>. Wave
+// copy c fills tile rows 4 (c * 4 + wave) .. + 3 (D = 128) or 8 (..) .. + 7
+// (D = 64); lane L lands at physical chunk L % CHUNKS of its row and fetches
+// the logical chunk that the swizzle puts there.
+template <int D>
+struct TileCopier {
+  using TL = AttnTile<D, kTileRows>;
+  static constexpr int ROWS_PER_COPY = 1024 / TL::ROW;
+  uint32_t chunk_off[TL::COPIES];  // bytes of the fetched logical chunk
+  __device__ __forceinline__ explicit TileCopier(int wave, int lane) {
+#pragma unroll
+    for (int c = 0; c < TL::COPIES; ++c) {
+      const int r = (c * 4 + wave) * ROWS_PER_COPY + lane / TL::CHUNKS;
+      const int pc = lane % TL::CHUNKS;
+      int lc = pc;
+#pragma unroll
+      for (int x = 0; x < TL::CHUNKS; ++x)
+        if (TL::swz(r, x) == pc) lc = x;
+      chunk_off[c] = (uint32_t)(lc * 16);
+    }
+  }
+  __device__ __forceinline__ void issue(const unsigned char* g, size_t row_bytes, uint32_t col_bytes,
+                                        int row0, int n_rows, int wave, int lane,
+                                        uint32_t lds) const {
+#pragma unroll
+    for (int c = 0; c < TL::COPIES; ++c) {
+      const int r0 = row0 + (c * 4 + wave) * ROWS_PER_COPY;  // uniform
+      const int r0c = min(r0, n_rows - 1);
+      const int rl = min(r0 + lane / TL::CHUNKS, n_rows - 1) - r0c;
+      copy_to_lds(g + (size_t)r0c * row_bytes, (uint32_t)(rl * row_bytes) + col_bytes + chunk_off[c],
+                  lds + (c * 4 + wave) * 1024);
+    }
+  }
+};
+
+// dQ~ for 128 query rows of one head. Mirrors the forward kernel: S^T = V Q~^T
+// and dP^T = V dO^T share each value-row fragment read; dS^T feeds
+// dQ~^T += V^T dS^T as the B operand.
+template <int D>
+__global__ __launch_bounds__(kThreads, 2) void bwd_dq_kernel(BwdParams p) {
+  using TL = AttnTile<D, kTileRows>;
+  constexpr int KS = D / 32, DB = D / 16;
+  extern __shared__ __attribute__((aligned(1024))) unsigned char smem[];
+  const int ntq = (p.N + BQD - 1) / BQD;
+  const int qt = p.causal ? (ntq - 1 - (int)blockIdx.x) : (int)blockIdx.x;
+  const int h = blockIdx.y, b = blockIdx.z;
+  const int g = h / (p.H / p.G);
+  const int t = threadIdx.x, lane = t & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(t >> 6);
+  const int fr = lane & 15, grp = lane >> 4;
+  const int q0 = qt * BQD + wave * 16 * QBD;
+  const uint16_t* __restrict__ Q = reinterpret_cast<const uint16_t*>(p.q);
+  const uint16_t* __restrict__ dO = reinterpret_cast<const uint16_t*>(p.dout);
+  const float c = p.scale_log2;
+
+  // B operands: query row q0 + 16 qb + fr, columns 32 ks + 8 grp .. + 7; the
+  // routed query multiplied by c and rounded to bf16 as in the forward.
+  bf16x8_t qf[QBD][KS], df[QBD][KS];
+  float lse2[QBD], dd[QBD];
+#pragma unroll
+  for (int qb = 0; qb < QBD; ++qb) {
+    const int qq = min(q0 + qb * 16 + fr, p.N - 1);
+    const uint16_t* sq = Q + ((size_t)b * p.N + qq) * p.q_stride + (size_t)h * D + grp * 8;
+    const uint16_t* sd = dO + ((size_t)b * p.N + qq) * p.o_stride + (size_t)h * D + grp * 8;
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) {
+      const u32x4 raw = *reinterpret_cast<const u32x4*>(sq + ks * 32);
+      u32x4 w;
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+        w[j] = pack2(__uint_as_float(raw[j] << 16) * c, __uint_as_float(raw[j] & 0xFFFF0000u) * c);
+      qf[qb][ks] = __builtin_bit_cast(bf16x8_t, w);
+      df[qb][ks] = __builtin_bit_cast(bf16x8_t, *reinterpret_cast<const u32x4*>(sd + ks * 32));
+    }
+    const size_t li = ((size_t)b * p.H + h) * p.N + qq;
+    lse2[qb] = p.lse[li] * kLog2e;
+    dd[qb] = p.Dd[li];
+  }
+  f32x4_t acc[DB][QBD];
+#pragma unroll
+  for (int i = 0; i < DB; ++i)
+#pragma unroll
+    for (int qb = 0; qb < QBD; ++qb) acc[i][qb] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+
+  const TileCopier<D> cp(wave, lane);
+  const unsigned char* gV = reinterpret_cast<const unsigned char*>(p.v);
+  const size_t vrow = (size_t)p.v_stride * 2;
+  const uint32_t lds0 = (uint32_t)(uintptr_t)(lds_u8*)smem;
+  auto issue = [&](int jt, int stage) {
+    cp.issue(gV + (size_t)b * p.N * vrow, vrow, (uint32_t)(g * D * 2), jt * kTileRows, p.N, wave,
+             lane, lds0 + stage * TL::BYTES);
+  };
+  int offS[KS];
+#pragma unroll
+  for (int ks = 0; ks < KS; ++ks) offS[ks] = TL::off(fr, ks * 4 + grp);
+  int offT[DB];
+#pragma unroll
+  for (int db = 0; db < DB; ++db) {
+    const int col = db * 16 + (fr & 3) * 4;
+    offT[db] = TL::off(grp * 4 + (fr >> 2), col >> 3) + (col & 7) * 2;
+  }
+  const int last_row = p.causal ? min(qt * BQD + BQD, p.N) : p.N;
+  const int ntiles = (last_row + kTileRows - 1) / kTileRows;
+#pragma unroll
+  for (int s = 0; s < NSTAGE - 1; ++s)
+    if (s < ntiles) issue(s, s);
+
+  for (int jt = 0; jt < ntiles; ++jt) {
+    const int stage = jt % NSTAGE;
+    if (jt + 1 < ntiles) KL_WAIT_VMCNT(TL::COPIES);
+    else KL_WAIT_VMCNT(0);
+    asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+    __syncthreads();
+    if (jt + NSTAGE - 1 < ntiles) issue(jt + NSTAGE - 1, (jt + NSTAGE - 1) % NSTAGE);
+    const int j0 = jt * kTileRows;
+    if (p.causal && j0 > q0 + 16 * QBD - 1) continue;  // above this wave's diagonal
+    const lds_u8* tile = (const lds_u8*)smem + stage * TL::BYTES;
+
+    f32x4_t sc[4][QBD], dp[4][QBD];
+#pragma unroll
+    for (int kb = 0; kb < 4; ++kb)
+#pragma unroll
+      for (int qb = 0; qb < QBD; ++qb) {
+        sc[kb][qb] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+        dp[kb][qb] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+      }
+#pragma unroll
+    for (int kb = 0; kb < 4; ++kb)
+#pragma unroll
+      for (int ks = 0; ks < KS; ++ks) {
+        const bf16x8_t a = *reinterpret_cast<const __attribute__((address_space(3))) bf16x8_t*>(
+            tile + offS[ks] + kb * 16 * TL::ROW);
+#pragma unroll
+        for (int qb = 0; qb < QBD; ++qb) {
+          sc[kb][qb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, qf[qb][ks], sc[kb][qb], 0, 0, 0);
+          dp[kb][qb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, df[qb][ks], dp[kb][qb], 0, 0, 0);
+        }
+      }
+    // Lane: rows j0 + 16 kb + 4 grp + r of query q0 + 16 qb + fr.
+    const bool edge = (p.causal && j0 + kTileRows - 1 > q0) || (j0 + kTileRows > p.N);
+    // dS^T fragments of one 32-row k-step (rows 32 ks + {4 grp .., 16 + 4 grp ..}).
+#pragma unroll
+    for (int ks = 0; ks < 2; ++ks) {
+      bf16x8_t pf[QBD];
+#pragma unroll
+      for (int qb = 0; qb < QBD; ++qb) {
+        const int q = q0 + qb * 16 + fr;
+        u32x4 w;
+#pragma unroll
+        for (int hh = 0; hh < 2; ++hh) {
+          const int kb = 2 * ks + hh;
+          float ds[4];
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            float pr = fast_exp2(sc[kb][qb][r] - lse2[qb]);
+            if (edge) {
+              const int kv = j0 + kb * 16 + grp * 4 + r;
+              if (kv >= p.N || (p.causal && kv > q)) pr = 0.f;
+            }
+            ds[r] = pr * (dp[kb][qb][r] - dd[qb]);
+          }
+          w[2 * hh] = pack2(ds[0], ds[1]);
+          w[2 * hh + 1] = pack2(ds[2], ds[3]);
+        }
+        pf[qb] = __builtin_bit_cast(bf16x8_t, w);
+      }
+#pragma unroll
+      for (int db = 0; db < DB; ++db) {
+        const lds_u8* src = tile + offT[db] + ks * 32 * TL::ROW;
+        const s16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+            (__attribute__((address_space(3))) s16x4*)(src));
+        const s16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+            (__attribute__((address_space(3))) s16x4*)(src + 16 * TL::ROW));
+        const bf16x8_t a = __builtin_bit_cast(bf16x8_t, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
+#pragma unroll
+        for (int qb = 0; qb < QBD; ++qb)
+          acc[db][qb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, pf[qb], acc[db][qb], 0, 0, 0);
+      }
+    }
+  }
+
+  // Lane holds dQ~^T[16 db + 4 grp + r][q]; dQ~ = tau dS V.
+  uint16_t* __restrict__ out = reinterpret_cast<uint16_t*>(p.dq);
+#pragma unroll
+  for (int qb = 0; qb < QBD; ++qb) {
+    const int q = q0 + qb * 16 + fr;
+    if (q >= p.N) continue;
+    uint16_t* dst = out + ((size_t)b * p.N + q) * p.dq_stride + (size_t)h * D + grp * 4;
+#pragma unroll
+    for (int db = 0; db < DB; ++db) {
+      const u32x2 w{pack2(acc[db][qb][0] * p.scale, acc[db][qb][1] * p.scale),
+                    pack2(acc[db][qb][2] * p.scale, acc[db][qb][3] * p.scale)};
+      *reinterpret_cast<u32x2*>(dst + db * 16) = w;
+    }
+  }
+}
+
+// dV for 128 value rows of one group: every head of the group and every query
+// tile that can see these rows stream through LDS (routed queries and dO, two
+// stages); the wave's 32 value rows stay in registers as the B operand of
+// S = Q~ V^T and dP = dO V^T, whose results (one value row per lane) are the B
+// operands of dV^T += dO^T P + tau Q~^T dS.
+template <int D>
+__global__ __launch_bounds__(kThreads, 2) void bwd_dv_kernel(BwdParams p) {
+  using TL = AttnTile<D, kTileRows>;
+  constexpr int KS = D / 32, DB = D / 16;
+  extern __shared__ __attribute__((aligned(1024))) unsigned char smem[];
+  const int kvt = blockIdx.x, g = blockIdx.y, b = blockIdx.z;
+  const int R = p.H / p.G;
+  const int t = threadIdx.x, lane = t & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(t >> 6);
+  const int fr = lane & 15, grp = lane >> 4;
+  const int kv0 = kvt * BKVD + wave * 16 * KVB;  // this wave's first value row
+  const float c = p.scale_log2;
+
+  // B operands: value row kv0 + 16 kb + fr, columns 32 ks + 8 grp .. + 7.
+  bf16x8_t vf[KVB][KS];
+  const uint16_t* __restrict__ V = reinterpret_cast<const uint16_t*>(p.v);
+#pragma unroll
+  for (int kb = 0; kb < KVB; ++kb) {
+    const int kv = min(kv0 + kb * 16 + fr, p.N - 1);
+    const uint16_t* sv = V + ((size_t)b * p.N + kv) * p.v_stride + (size_t)g * D + grp * 8;
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks)
+      vf[kb][ks] = __builtin_bit_cast(bf16x8_t, *reinterpret_cast<const u32x4*>(sv + ks * 32));
+  }
+  f32x4_t acc[DB][KVB];
+#pragma unroll
+  for (int i = 0; i < DB; ++i)
+#pragma unroll
+    for (int kb = 0; kb < KVB; ++kb) acc[i][kb] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+
+  // Work items: (head of the group, query tile) pairs, query tiles from the
+  // first one that can see row kvt * 128.
+  const int ntq = (p.N + kTileRows - 1) / kTileRows;
+  const int qt0 = p.causal ? (kvt * BKVD) / kTileRows : 0;
+  const int per_head = ntq - qt0;
+  const int items = R * per_head;
+  const TileCopier<D> cp(wave, lane);
+  const unsigned char* gQ = reinterpret_cast<const unsigned char*>(p.q);
+  const unsigned char* gD = reinterpret_cast<const unsigned char*>(p.dout);
+  const size_t qrow = (size_t)p.q_stride * 2, drow = (size_t)p.o_stride * 2;
+  const uint32_t lds0 = (uint32_t)(uintptr_t)(lds_u8*)smem;
+  auto issue = [&](int it) {
+    const int h = g * R + it / per_head, qt = qt0 + it % per_head;
+    const uint32_t st = lds0 + (it & 1) * 2 * TL::BYTES;
+    cp.issue(gQ + (size_t)b * p.N * qrow, qrow, (uint32_t)(h * D * 2), qt * kTileRows, p.N, wave,
+             lane, st);
+    cp.issue(gD + (size_t)b * p.N * drow, drow, (uint32_t)(h * D * 2), qt * kTileRows, p.N, wave,
+             lane, st + TL::BYTES);
+  };
+  int offS[KS];
+#pragma unroll
+  for (int ks = 0; ks < KS; ++ks) offS[ks] = TL::off(fr, ks * 4 + grp);
+  int offT[DB];
+#pragma unroll
+  for (int db = 0; db < DB; ++db) {
+    const int col = db * 16 + (fr & 3) * 4;
+    offT[db] = TL::off(grp * 4 + (fr >> 2), col >> 3) + (col & 7) * 2;
+  }
+
+  if (items > 0) issue(0);
+  for (int it = 0; it < items; ++it) {
+    KL_WAIT_VMCNT(0);
+    asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+    __syncthreads();
+    if (it + 1 < items) issue(it + 1);
+    const int h = g * R + it / per_head, qt = qt0 + it % per_head;
+    const int q0 = qt * kTileRows;
+    if (p.causal && q0 + kTileRows - 1 < kv0) continue;  // every row of the tile is before ours
+    const lds_u8* tq = (const lds_u8*)smem + (it & 1) * 2 * TL::BYTES;
+    const lds_u8* td = tq + TL::BYTES;
+    const float* lse = p.lse + ((size_t)b * p.H + h) * p.N;
+    const float* ddv = p.Dd + ((size_t)b * p.H + h) * p.N;
+    const bool edge = (p.causal && q0 < kv0 + 16 * KVB - 1) || (q0 + kTileRows > p.N);
+    // Two 32-row query steps; each is one K = 32 step of the dV products.
+#pragma unroll
+    for (int qs = 0; qs < 2; ++qs) {
+      bf16x8_t pp[KVB], ps[KVB];
+      u32x4 wp[KVB], wsv[KVB];
+#pragma unroll
+      for (int hh = 0; hh < 2; ++hh) {
+        const int qb = 2 * qs + hh;  // 16-row query block of the tile
+        f32x4_t sc[KVB], dp[KVB];
+#pragma unroll
+        for (int kb = 0; kb < KVB; ++kb) {
+          sc[kb] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+          dp[kb] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+        }
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks) {
+          const bf16x8_t aq = *reinterpret_cast<const __attribute__((address_space(3))) bf16x8_t*>(
+              tq + offS[ks] + qb * 16 * TL::ROW);
+          const bf16x8_t ad = *reinterpret_cast<const __attribute__((address_space(3))) bf16x8_t*>(
+              td + offS[ks] + qb * 16 * TL::ROW);
+#pragma unroll
+          for (int kb = 0; kb < KVB; ++kb) {
+            sc[kb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(aq, vf[kb][ks], sc[kb], 0, 0, 0);
+            dp[kb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ad, vf[kb][ks], dp[kb], 0, 0, 0);
+          }
+        }
+        // Lane: query rows q0 + 16 qb + 4 grp + r against value row kv0 + 16 kb + fr.
+        float l2[4], dq[4];
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int q = min(q0 + qb * 16 + grp * 4 + r, p.N - 1);
+          l2[r] = lse[q] * kLog2e;
+          dq[r] = ddv[q];
+        }
+#pragma unroll
+        for (int kb = 0; kb < KVB; ++kb) {
+          const int kv = kv0 + kb * 16 + fr;
+          float pr[4], ds[4];
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            pr[r] = fast_exp2(sc[kb][r] * c - l2[r]);
+            if (edge) {
+              const int q = q0 + qb * 16 + grp * 4 + r;
+              if (q >= p.N || (p.causal && kv > q)) pr[r] = 0.f;
+            }
+            ds[r] = pr[r] * (dp[kb][r] - dq[r]) * p.scale;
+          }
+          wp[kb][2 * hh] = pack2(pr[0], pr[1]);
+          wp[kb][2 * hh + 1] = pack2(pr[2], pr[3]);
+          wsv[kb][2 * hh] = pack2(ds[0], ds[1]);
+          wsv[kb][2 * hh + 1] = pack2(ds[2], ds[3]);
+        }
+      }
+#pragma unroll
+      for (int kb = 0; kb < KVB; ++kb) {
+        pp[kb] = __builtin_bit_cast(bf16x8_t, wp[kb]);
+        ps[kb] = __builtin_bit_cast(bf16x8_t, wsv[kb]);
+      }
+      // dV^T[d][kv] += dO^T P + Q~^T (tau dS) over query rows 32 qs + {4 grp .., 16 + 4 grp ..}.
+#pragma unroll
+      for (int db = 0; db < DB; ++db) {
+        const int o = offT[db] + qs * 32 * TL::ROW;
+        const s16x4 dlo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) s16x4*)(td + o));
+        const s16x4 dhi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) s16x4*)(td + o + 16 * TL::ROW));
+        const s16x4 qlo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) s16x4*)(tq + o));
+        const s16x4 qhi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) s16x4*)(tq + o + 16 * TL::ROW));
+        const bf16x8_t ad = __builtin_bit_cast(bf16x8_t, __builtin_shufflevector(dlo, dhi, 0, 1, 2, 3, 4, 5, 6, 7));
+        const bf16x8_t aq = __builtin_bit_cast(bf16x8_t, __builtin_shufflevector(qlo, qhi, 0, 1, 2, 3, 4, 5, 6, 7));
+#pragma unroll
+        for (int kb = 0; kb < KVB; ++kb) {
+          acc[db][kb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ad, pp[kb], acc[db][kb], 0, 0, 0);
+          acc[db][kb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(aq, ps[kb], acc[db][kb], 0, 0, 0);
+        }
+      }
+    }
+  }
+
+  // Lane holds dV^T[16 db + 4 grp + r][kv0 + 16 kb + fr].
+  uint16_t* __restrict__ out = reinterpret_cast<uint16_t*>(p.dv);
+#pragma unroll
+  for (int kb = 0; kb < KVB; ++kb) {
+    const int kv = kv0 + kb * 16 + fr;
+    if (kv >= p.N) continue;
+    uint16_t* dst = out + ((size_t)b * p.N + kv) * p.dv_stride + (size_t)g * D + grp * 4;
+#pragma unroll
+    for (int db = 0; db < DB; ++db) {
+      const u32x2 w{pack2(acc[db][kb][0], acc[db][kb][1]), pack2(acc[db][kb][2], acc[db][kb][3])};
+      *reinterpret_cast<u32x2*>(dst + db * 16) = w;
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
+// fp32 (and any dtype): VALU, one thread per query row (dQ~) or value row (dV)
+// ---------------------------------------------------------------------------
+
+template <typename T, int D>
+__global__ __launch_bounds__(64) void bwd_dq_simple_kernel(BwdParams p) {
+  const int i0 = blockIdx.x * 64;
+  const int h = blockIdx.y, b = blockIdx.z;
+  const int g = h / (p.H / p.G);
+  const int i = i0 + threadIdx.x;
+  const bool live = i < p.N;
+  const T* Q = reinterpret_cast<const T*>(p.q);
+  const T* V = reinterpret_cast<const T*>(p.v);
+  const T* G = reinterpret_cast<const T*>(p.dout);
+  __shared__ float sV[64][D];
+  float q[D], go[D], acc[D];
+  float l2 = 0.f, dd = 0.f;
+  if (live) {
+    l2 = p.lse[((size_t)b * p.H + h) * p.N + i] * kLog2e;
+    dd = p.Dd[((size_t)b * p.H + h) * p.N + i];
+  }
+#pragma unroll
+  for (int c = 0; c < D; ++c) {
+    q[c] = live ? ldx(Q, ((size_t)b * p.N + i) * p.q_stride + (size_t)h * D + c) * p.scale_log2 : 0.f;
+    go[c] = live ? ldx(G, ((size_t)b * p.N + i) * p.o_stride + (size_t)h * D + c) : 0.f;
+    acc[c] = 0.f;
+  }
+  const int jend = p.causal ? min(p.N, i0 + 64) : p.N;
+  for (int j0 = 0; j0 < jend; j0 += 64) {
+    __syncthreads();
+    for (int e = threadIdx.x; e < 64 * D; e += 64) {
+      const int jj = e / D, c = e % D, j = j0 + jj;
+      sV[jj][c] = j < p.N ? ldx(V, ((size_t)b * p.N + j) * p.v_stride + (size_t)g * D + c) : 0.f;
+    }
+    __syncthreads();
+    const int jmax = min(64, (p.causal ? min(i + 1, p.N) : p.N) - j0);
+    for (int jj = 0; jj < jmax; ++jj) {
+      float s = 0.f, dp = 0.f;
+#pragma unroll
+      for (int c = 0; c < D; ++c) {
+        s = fmaf(q[c], sV[jj][c], s);
+        dp = fmaf(go[c], sV[jj][c], dp);
+      }
+      const float ds = fast_exp2(s - l2) * (dp - dd);
+#pragma unroll
+      for (int c = 0; c < D; ++c) acc[c] = fmaf(ds, sV[jj][c], acc[c]);
+    }
+  }
+  if (live) {
+    T* out = reinterpret_cast<T*>(p.dq);
+#pragma unroll
+    for (int c = 0; c < D; ++c)
+      stx(out, ((size_t)b * p.N + i) * p.dq_stride + (size_t)h * D + c, acc[c] * p.scale);
+  }
+}
+
+template <typename T, int D>
+__global__ __launch_bounds__(64) void bwd_dv_simple_kernel(BwdParams p) {
+  const int j0 = blockIdx.x * 64;
+  const int g = blockIdx.y, b = blockIdx.z;
+  const int R = p.H / p.G;
+  const int j = j0 + threadIdx.x;
+  const bool live = j < p.N;
+  const T* Q = reinterpret_cast<const T*>(p.q);
+  const T* V = reinterpret_cast<const T*>(p.v);
+  const T* G = reinterpret_cast<const T*>(p.dout);
+  __shared__ float sQ[32][D];
+  __shared__ float sG[32][D];
+  __shared__ float sL[32], sD[32];
+  float v[D], acc[D];
+#pragma unroll
+  for (int c = 0; c < D; ++c) {
+    v[c] = live ? ldx(V, ((size_t)b * p.N + j) * p.v_stride + (size_t)g * D + c) : 0.f;
+    acc[c] = 0.f;
+  }
+  const int ibeg = p.causal ? j0 : 0;
+  for (int h = g * R; h < g * R + R; ++h) {
+    for (int i0 = ibeg; i0 < p.N; i0 += 32) {
+      __syncthreads();
+      for (int e = threadIdx.x; e < 32 * D; e += 64) {
+        const int ii = e / D, c = e % D, i = i0 + ii;
+        const bool ok = i < p.N;
+        sQ[ii][c] = ok ? ldx(Q, ((size_t)b * p.N + i) * p.q_stride + (size_t)h * D + c) : 0.f;
+        sG[ii][c] = ok ? ldx(G, ((size_t)b * p.N + i) * p.o_stride + (size_t)h * D + c) : 0.f;
+      }
+      if (threadIdx.x < 32) {
+        const int i = i0 + threadIdx.x;
+        const bool ok = i < p.N;
+        sL[threadIdx.x] = ok ? p.lse[((size_t)b * p.H + h) * p.N + i] * kLog2e : 0.f;
+        sD[threadIdx.x] = ok ? p.Dd[((size_t)b * p.H + h) * p.N + i] : 0.f;
+      }
+      __syncthreads();
+      const int imax = min(32, p.N - i0);
+      for (int ii = 0; ii < imax; ++ii) {
+        if (p.causal && i0 + ii < j) continue;
+        float s = 0.f, dp = 0.f;
+#pragma unroll
+        for (int c = 0; c < D; ++c) {
+          s = fmaf(sQ[ii][c], v[c], s);
+          dp = fmaf(sG[ii][c], v[c], dp);
+        }
+        const float pr = fast_exp2(s * p.scale_log2 - sL[ii]);
+        const float ds = pr * (dp - sD[ii]) * p.scale;
+#pragma unroll
+        for (int c = 0; c < D; ++c) acc[c] = fmaf(pr, sG[ii][c], fmaf(ds, sQ[ii][c], acc[c]));
+      }
+    }
+  }
+  if (live) {
+    T* out = reinterpret_cast<T*>(p.dv);
+#pragma unroll
+    for (int c = 0; c < D; ++c) stx(out, ((size_t)b * p.N + j) * p.dv_stride + (size_t)g * D + c, acc[c]);
+  }
+}
+
+template <typename T, int D>
+hipError_t launch_simple(const BwdParams& p, hipStream_t st) {
+  hipLaunchKernelGGL((bwd_dq_simple_kernel<T, D>), dim3((p.N + 63) / 64, p.H, p.B), dim3(64), 0, st, p);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL((bwd_dv_simple_kernel<T, D>), dim3((p.N + 63) / 64, p.G, p.B), dim3(64), 0, st, p);
+  return hipGetLastError();
+}
+
+template <int D>
+hipError_t launch_mfma(const BwdParams& p, hipStream_t st) {
+  using TL = AttnTile<D, kTileRows>;
+  hipLaunchKernelGGL(bwd_dq_kernel<D>, dim3((p.N + BQD - 1) / BQD, p.H, p.B), dim3(kThreads),
+                     NSTAGE * TL::BYTES, st, p);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(bwd_dv_kernel<D>, dim3((p.N + BKVD - 1) / BKVD, p.G, p.B), dim3(kThreads),
+                     4 * TL::BYTES, st, p);
+  return hipGetLastError();
+}
+
+template <typename T>
+hipError_t launch_prep(const BwdParams& p, hipStream_t st) {
+  const long rows = (long)p.B * p.N * p.H;
+  const dim3 grid((unsigned)((rows + 15) / 16));
+  if (p.D == 128) hipLaunchKernelGGL((bwd_prep_kernel<T, 128>), grid, dim3(256), 0, st, p);
+  else hipLaunchKernelGGL((bwd_prep_kernel<T, 64>), grid, dim3(256), 0, st, p);
+  return hipGetLastError();
+}
+
+}  // namespace
+
+bool attn_bwd_mfma_supported(const BwdParams& p) {
+  return p.dtype == KL_BF16 && (p.D == 64 || p.D == 128) && p.q_stride % 8 == 0 &&
+         p.v_stride % 8 == 0 && p.o_stride % 8 == 0 && p.dq_stride % 4 == 0 &&
+         p.dv_stride % 4 == 0 && (size_t)p.v_stride * 2 * 8 < (1u << 31) &&
+         (size_t)p.q_stride * 2 * 8 < (1u << 31) && (size_t)p.o_stride * 2 * 8 < (1u << 31);
+}
+
+hipError_t launch_attention_backward(const BwdParams& p, hipStream_t st) {
+  if (p.B == 0 || p.N == 0) return hipSuccess;
+  if (p.D != 64 && p.D != 128) return hipErrorInvalidValue;
+  hipError_t e = p.dtype == KL_BF16 ? launch_prep<uint16_t>(p, st) : launch_prep<float>(p, st);
+  if (e != hipSuccess) return e;
+  if (attn_bwd_mfma_supported(p)) return p.D == 128 ? launch_mfma<128>(p, st) : launch_mfma<64>(p, st);
+  if (p.dtype == KL_BF16)
+    return p.D == 128 ? launch_simple<uint16_t, 128>(p, st) : launch_simple<uint16_t, 64>(p, st);
+  return p.D == 128 ? launch_simple<float, 128>(p, st) : launch_simple<float, 64>(p, st);
+}
+
+}  // namespace kl

@@ -89,6 +89,9 @@ hipError_t launch_project(const ProjectParams& p, hipStream_t stream);
 // C[b] (M x N) = A[b] (M x K) * B[b] (K x N), row-major with leading
 // dimensions, fp32 accumulation; batched by pointer strides. Generic tiled
 // kernel for the small products (routing fold, fp32 prefill projections).
+// C (M x N) = A (M x K) B (K x N) [+ C], fp32 arithmetic. Element (m, k) of A
+// is at m lda + k a_cs, element (k, n) of B at k ldb + n b_cs (a_cs, b_cs of 0
+// mean 1), so transposed operands are a choice of strides.
 struct GemmParams {
   const void* A; const void* Bm; void* C;
   int M, N, K;
@@ -96,6 +99,8 @@ struct GemmParams {
   long strideA, strideB, strideC;  // elements between batch items
   int batch;
   kl_dtype dtype;
+  long a_cs, b_cs;
+  int accumulate;                  // nonzero: C += A B
 };
 
 hipError_t launch_gemm_simple(const GemmParams& p, hipStream_t stream);
@@ -126,6 +131,7 @@ struct AttnParams {
   int B, N, H, G, D;
   int Nk;          // value rows per sequence: N for self-attention, N_b for cross-attention
   int causal;      // only with Nk == N
+  float* lse;      // [B, H, N] natural-log log-sum-exp of each row's scaled scores, or null
   float scale_log2;
   kl_dtype dtype;
 };
@@ -141,6 +147,30 @@ struct LatentParams {
   kl_dtype dtype;
 };
 hipError_t launch_latent_product(const LatentParams& p, hipStream_t stream);
+
+// Backward of the keyless self-attention (Section 2.3): dQ~ and dV from dO,
+// the forward's output and log-sum-exp. q [B, N, H, D] (q_stride), v [B, N, G,
+// D] (v_stride), out and dout [B, N, H, D] (o_stride), lse and Dd [B, H, N]
+// fp32 (Dd is scratch: rowsum(dout * out)), dq [B, N, H, D] (dq_stride),
+// dv [B, N, G, D] (dv_stride).
+struct BwdParams {
+  const void* q;
+  const void* v;
+  const void* out;
+  const void* dout;
+  const float* lse;
+  float* Dd;
+  void* dq;
+  void* dv;
+  long q_stride, v_stride, o_stride, dq_stride, dv_stride;
+  int B, N, H, G, D;
+  int causal;
+  float scale;       // tau
+  float scale_log2;  // tau * log2(e)
+  kl_dtype dtype;
+};
+bool attn_bwd_mfma_supported(const BwdParams& p);
+hipError_t launch_attention_backward(const BwdParams& p, hipStream_t stream);
 
 // bf16 MFMA flash-style keyless attention (d_head 64 or 128).
 bool attn_bf16_supported(const AttnParams& p);

@@ -24,6 +24,7 @@
 
 #include <type_traits>
 
+#include "attn_tile.h"
 #include "kl_device.h"
 #include "kl_internal.h"
 
@@ -43,30 +44,13 @@ constexpr int BKV = 64;     // value rows per tile
 constexpr int NSTAGE = 3;   // value tiles in flight (the tile loop is unrolled by 3)
 constexpr int kThreads = 256;
 
-__device__ __forceinline__ uint32_t pack2(float lo, float hi) {
-  typedef __attribute__((__vector_size__(2 * sizeof(__bf16)))) __bf16 b2;
-  b2 v = {(__bf16)lo, (__bf16)hi};
-  return __builtin_bit_cast(uint32_t, v);
-}
-
 // max(a, b, c); written for the compiler (not as inline assembly, which would
 // hide a read of a fresh MFMA result from its hazard checks), which forms
 // v_max3_f32 since this file is built without NaN semantics.
 __device__ __forceinline__ float max3(float a, float b, float c) { return fmaxf(fmaxf(a, b), c); }
 
 template <int D>
-struct Tile {
-  static constexpr int ROW = D * 2;              // bytes per value row
-  static constexpr int CHUNKS = D / 8;           // 16-byte chunks per row
-  static constexpr int BYTES = BKV * ROW;        // one tile
-  static constexpr int COPIES = BYTES / 1024 / 4;  // wave copies per wave per tile
-  // Physical chunk of logical chunk c in row r.
-  static __device__ __forceinline__ int swz(int r, int c) {
-    if constexpr (D == 128) return c ^ (((r & 7) << 1) | ((r >> 3) & 1));
-    else return c ^ ((r >> 1) & 7);
-  }
-  static __device__ __forceinline__ int off(int r, int c) { return r * ROW + (swz(r, c) << 4); }
-};
+using Tile = AttnTile<D, BKV>;
 
 template <int D>
 __global__ __launch_bounds__(kThreads, QB == 2 ? 3 : 2) void attn_bf16_kernel(AttnParams p) {
@@ -325,6 +309,8 @@ __global__ __launch_bounds__(kThreads, QB == 2 ? 3 : 2) void attn_bf16_kernel(At
     const float l = osum[qb][0];
     const float inv = l > 0.f ? 1.f / l : 0.f;
     const int q = q0 + qb * 16 + fr;
+    if (p.lse && q < p.N && grp == 0)  // scores are in log2 units relative to m
+      p.lse[((size_t)b * p.H + h) * p.N + q] = (m[qb] + __log2f(l)) * 0.69314718055994531f;
     if (q < p.N) {
       uint16_t* dst = O + ((size_t)b * p.N + q) * p.o_stride + (size_t)h * D + grp * 4;
 #pragma unroll

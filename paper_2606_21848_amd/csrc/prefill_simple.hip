@@ -39,14 +39,15 @@ __global__ __launch_bounds__(256) void gemm_simple_kernel(GemmParams p) {
   const int tx = threadIdx.x % 16, ty = threadIdx.x / 16;
   const int m0 = blockIdx.y * GT, n0 = blockIdx.x * GT;
   float c[4][4] = {};
+  const size_t acs = p.a_cs ? p.a_cs : 1, bcs = p.b_cs ? p.b_cs : 1;
   for (int k0 = 0; k0 < p.K; k0 += GK) {
     for (int i = threadIdx.x; i < GK * GT; i += 256) {
       const int kk = i % GK, mm = i / GK;  // A tile: GT rows x GK cols
       const int gm = m0 + mm, gk = k0 + kk;
-      sA[kk][mm] = (gm < p.M && gk < p.K) ? ld(A, (size_t)gm * p.lda + gk) : 0.f;
+      sA[kk][mm] = (gm < p.M && gk < p.K) ? ld(A, (size_t)gm * p.lda + gk * acs) : 0.f;
       const int nn = i % GT, kb = i / GT;  // B tile: GK rows x GT cols
       const int gn = n0 + nn, gkb = k0 + kb;
-      sB[kb][nn] = (gn < p.N && gkb < p.K) ? ld(Bm, (size_t)gkb * p.ldb + gn) : 0.f;
+      sB[kb][nn] = (gn < p.N && gkb < p.K) ? ld(Bm, (size_t)gkb * p.ldb + gn * bcs) : 0.f;
     }
     __syncthreads();
 #pragma unroll
@@ -68,7 +69,10 @@ __global__ __launch_bounds__(256) void gemm_simple_kernel(GemmParams p) {
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
       const int gm = m0 + ty + 16 * i, gn = n0 + tx + 16 * j;
-      if (gm < p.M && gn < p.N) st(C, (size_t)gm * p.ldc + gn, c[i][j]);
+      if (gm < p.M && gn < p.N) {
+        const size_t at = (size_t)gm * p.ldc + gn;
+        st(C, at, p.accumulate ? ld(reinterpret_cast<const T*>(C), at) + c[i][j] : c[i][j]);
+      }
     }
 }
 
@@ -117,6 +121,9 @@ __global__ __launch_bounds__(64) void attn_simple_kernel(AttnParams p) {
   if (live) {
     T* O = reinterpret_cast<T*>(p.out);
     const float inv = l > 0.f ? 1.f / l : 0.f;  // no value rows: a zero row
+    if (p.lse)  // m and the scores are in log2 units
+      p.lse[((size_t)b * p.H + h) * p.N + i] =
+          l > 0.f ? (m + __log2f(l)) * 0.69314718055994531f : -INFINITY;
 #pragma unroll
     for (int c = 0; c < D; ++c) st(O, ((size_t)b * p.N + i) * p.o_stride + (size_t)h * D + c, acc[c] * inv);
   }

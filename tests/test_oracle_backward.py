@@ -82,3 +82,33 @@ def test_zero_routing_leaves_only_the_retrieval_term(causal):
             for j in seen:
                 expect[b, j, 0] += dO[b, i].sum(axis=0) / len(seen)  # both heads share group 0
     np.testing.assert_allclose(dV, expect, rtol=0, atol=1e-13)
+
+
+def test_logsumexp_closed_form_and_softmax_normaliser():
+    """The 3-token causal case of the closed-form fixtures (tau <q_i, v_j> = ln 2
+    <x_i, x_j>): row sums e = [2], [1, 2], [2, 2, 4], so lse = ln 2, ln 3, ln 8;
+    and exp(S - lse) sums to 1 on every row of a random problem."""
+    X = np.array([[1.0, 0.0], [0.0, 1.0], [1.0, 1.0]])[None]
+    c = math.sqrt(2) * math.log(2)
+    _, Qr, V = K.keyless_prefill(X, c * np.eye(2), None, np.eye(2), H=1, G=1, d_head=2)
+    lse = K.attention_logsumexp(Qr, V, 1, 1, 2)
+    np.testing.assert_allclose(lse[0, 0], [math.log(2), math.log(3), math.log(8)], rtol=0, atol=1e-14)
+    x, W_Q, W_R, W_V, _ = _problem(2, 8, 6, 4, 2, 3)
+    _, Qr, V = K.keyless_prefill(x, W_Q, W_R, W_V, 4, 2, 3)
+    lse = K.attention_logsumexp(Qr, V, 4, 2, 3, causal=False)
+    for b in range(2):
+        for h in range(4):
+            S = (Qr[b, :, h] @ V[b, :, h // 2].T) / math.sqrt(3)
+            np.testing.assert_allclose(np.exp(S - lse[b, h][:, None]).sum(axis=1), 1.0, rtol=0, atol=1e-13)
+
+
+@pytest.mark.parametrize("causal", [True, False])
+def test_backward_rows_helper_matches_full(causal):
+    B, N, d, H, G, dk = 1, 12, 8, 4, 2, 3
+    x, W_Q, W_R, W_V, dO = _problem(B, N, d, H, G, dk)
+    _, Qr, V = K.keyless_prefill(x, W_Q, W_R, W_V, H, G, dk, causal=causal)
+    dQ, dV = K.keyless_attention_backward(Qr, V, dO, H, G, dk, causal=causal)
+    rq, rv = [0, 5, 11], [0, 7, 11]
+    dQr, dVr = K.keyless_attention_backward_rows(Qr, V, dO, H, G, dk, rq, rv, causal=causal)
+    np.testing.assert_allclose(dQr, dQ[0, rq], rtol=0, atol=1e-12)
+    np.testing.assert_allclose(dVr, dV[0, rv], rtol=0, atol=1e-12)

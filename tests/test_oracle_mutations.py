@@ -60,6 +60,10 @@ MUTATIONS = [
      "dW_R[h] += dQr[b, :, h, :].T @ Q_h", "routing gradient transposed (Eq. 5)"),
     ("keyless_backward", "dQ[b, :, h, :] = dQr[b, :, h, :] @ W_R[h].T",
      "dQ[b, :, h, :] = dQr[b, :, h, :] @ W_R[h]", "query gradient through W^R untransposed"),
+    ("attention_logsumexp", "out[b, h] = (m + np.log(", "out[b, h] = (np.log(",
+     "log-sum-exp without its shift"),
+    ("keyless_attention_backward_rows", "+= P[j] * dO[i, h] + tau * dS[j] * Qr[i, h]",
+     "+= P[j] * dO[i, h] + dS[j] * Qr[i, h]", "sampled value gradient without the scale"),
     ("keyless_cross_attention", "Qt_h = Q_h if W_R is None else Q_h @ _f64(W_R)[h]",
      "Qt_h = Q_h if W_R is None else Q_h @ _f64(W_R)[h].T", "routing matrix transposed in cross-attention"),
     ("keyless_cross_attention", "V[b, :, g, :] = xb[b] @", "V[b, :, g, :] = xa[b] @",
