@@ -2,19 +2,22 @@
 // of the routed queries and of the values. Per batch b and head h (group g):
 //   P   = exp(tau Q~ V^T - lse)        (the forward's weights, from its log-sum-exp)
 //   dP  = dO V^T
-//   dS  = P * (dP - Dd),  Dd = rowsum(dO * O)   (softmax backward)
+//   dS  = P * (dP - Dd),  Dd = rowsum(P * dP) = rowsum(dO * O)   (softmax backward)
 //   dQ~ = tau dS V
 //   dV  = P^T dO + tau dS^T Q~        (retrieval and routing terms of Eq. 6)
 // The value tile is read once per product it enters, exactly as in the
 // forward: as the score operand and as the retrieved values (dQ~ kernel), and
 // the value gradient collects both of its roles in the same accumulators.
 //
-// Three kernels: bwd_prep_kernel (Dd), bwd_dq_kernel (one workgroup per
-// 128-row query tile and head; value tiles stream through LDS as in the
-// forward, queries and dO stay in registers) and bwd_dv_kernel (one workgroup
-// per 128-row value tile and value group; query and dO tiles of every head of
-// the group stream through LDS, the values stay in registers). No atomics:
-// every output element is written once, by one lane.
+// bf16: bwd_dq_kernel (one workgroup per 128-row query tile and head; value
+// tiles stream through LDS as in the forward, queries and dO stay in
+// registers; a first sweep forms Dd as rowsum(P * dP) in fp32, since
+// rowsum(dO * O) over the bf16-rounded output would put that rounding into
+// every dP - Dd) and then bwd_dv_kernel (one workgroup per 128-row value tile
+// and value group; query and dO tiles of every head of the group stream
+// through LDS, the values stay in registers). fp32: bwd_prep_kernel (Dd from
+// the fp32 output) and two vector-ALU kernels. No atomics: every output
+// element is written once, by one lane.
 //
 // bf16 runs on v_mfma_f32_16x16x32_bf16 with the forward's operand layouts:
 // scores come out with one query per lane (S^T = V Q~^T) in the dQ~ kernel and
@@ -163,9 +166,8 @@ __global__ __launch_bounds__(kThreads, 2) void bwd_dq_kernel(BwdParams p) {
       qf[qb][ks] = __builtin_bit_cast(bf16x8_t, w);
       df[qb][ks] = __builtin_bit_cast(bf16x8_t, *reinterpret_cast<const u32x4*>(sd + ks * 32));
     }
-    const size_t li = ((size_t)b * p.H + h) * p.N + qq;
-    lse2[qb] = p.lse[li] * kLog2e;
-    dd[qb] = p.Dd[li];
+    lse2[qb] = p.lse[((size_t)b * p.H + h) * p.N + qq] * kLog2e;
+    dd[qb] = 0.f;  // formed by the first sweep
   }
   f32x4_t acc[DB][QBD];
 #pragma unroll
@@ -192,80 +194,116 @@ __global__ __launch_bounds__(kThreads, 2) void bwd_dq_kernel(BwdParams p) {
   }
   const int last_row = p.causal ? min(qt * BQD + BQD, p.N) : p.N;
   const int ntiles = (last_row + kTileRows - 1) / kTileRows;
-#pragma unroll
-  for (int s = 0; s < NSTAGE - 1; ++s)
-    if (s < ntiles) issue(s, s);
 
-  for (int jt = 0; jt < ntiles; ++jt) {
-    const int stage = jt % NSTAGE;
-    if (jt + 1 < ntiles) KL_WAIT_VMCNT(TL::COPIES);
-    else KL_WAIT_VMCNT(0);
-    asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
-    __syncthreads();
-    if (jt + NSTAGE - 1 < ntiles) issue(jt + NSTAGE - 1, (jt + NSTAGE - 1) % NSTAGE);
-    const int j0 = jt * kTileRows;
-    if (p.causal && j0 > q0 + 16 * QBD - 1) continue;  // above this wave's diagonal
-    const lds_u8* tile = (const lds_u8*)smem + stage * TL::BYTES;
+  // Two sweeps over the value tiles. The first forms Dd = sum_j P_ij dP_ij in
+  // fp32 (the definition, rather than rowsum(dO * O) from the rounded output,
+  // whose rounding the subtraction dP - Dd would amplify) and writes it for the
+  // dV kernel; the second forms dS and accumulates dQ~.
+#pragma unroll 1
+  for (int sweep = 0; sweep < 2; ++sweep) {
+    if (sweep == 1) {
+      // Every wave's reads of the first sweep's last stages have returned.
+      asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+      __syncthreads();
+    }
+#pragma unroll
+    for (int s = 0; s < NSTAGE - 1; ++s)
+      if (s < ntiles) issue(s, s);
+    float dsum[QBD];
+#pragma unroll
+    for (int qb = 0; qb < QBD; ++qb) dsum[qb] = 0.f;
 
-    f32x4_t sc[4][QBD], dp[4][QBD];
+    for (int jt = 0; jt < ntiles; ++jt) {
+      const int stage = jt % NSTAGE;
+      if (jt + 1 < ntiles) KL_WAIT_VMCNT(TL::COPIES);
+      else KL_WAIT_VMCNT(0);
+      asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+      __syncthreads();
+      if (jt + NSTAGE - 1 < ntiles) issue(jt + NSTAGE - 1, (jt + NSTAGE - 1) % NSTAGE);
+      const int j0 = jt * kTileRows;
+      if (p.causal && j0 > q0 + 16 * QBD - 1) continue;  // above this wave's diagonal
+      const lds_u8* tile = (const lds_u8*)smem + stage * TL::BYTES;
+
+      f32x4_t sc[4][QBD], dp[4][QBD];
 #pragma unroll
-    for (int kb = 0; kb < 4; ++kb)
-#pragma unroll
-      for (int qb = 0; qb < QBD; ++qb) {
-        sc[kb][qb] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-        dp[kb][qb] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-      }
-#pragma unroll
-    for (int kb = 0; kb < 4; ++kb)
-#pragma unroll
-      for (int ks = 0; ks < KS; ++ks) {
-        const bf16x8_t a = *reinterpret_cast<const __attribute__((address_space(3))) bf16x8_t*>(
-            tile + offS[ks] + kb * 16 * TL::ROW);
+      for (int kb = 0; kb < 4; ++kb)
 #pragma unroll
         for (int qb = 0; qb < QBD; ++qb) {
-          sc[kb][qb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, qf[qb][ks], sc[kb][qb], 0, 0, 0);
-          dp[kb][qb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, df[qb][ks], dp[kb][qb], 0, 0, 0);
+          sc[kb][qb] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+          dp[kb][qb] = f32x4_t{0.f, 0.f, 0.f, 0.f};
         }
-      }
-    // Lane: rows j0 + 16 kb + 4 grp + r of query q0 + 16 qb + fr.
-    const bool edge = (p.causal && j0 + kTileRows - 1 > q0) || (j0 + kTileRows > p.N);
-    // dS^T fragments of one 32-row k-step (rows 32 ks + {4 grp .., 16 + 4 grp ..}).
 #pragma unroll
-    for (int ks = 0; ks < 2; ++ks) {
-      bf16x8_t pf[QBD];
+      for (int kb = 0; kb < 4; ++kb)
 #pragma unroll
-      for (int qb = 0; qb < QBD; ++qb) {
-        const int q = q0 + qb * 16 + fr;
-        u32x4 w;
+        for (int ks = 0; ks < KS; ++ks) {
+          const bf16x8_t a = *reinterpret_cast<const __attribute__((address_space(3))) bf16x8_t*>(
+              tile + offS[ks] + kb * 16 * TL::ROW);
 #pragma unroll
-        for (int hh = 0; hh < 2; ++hh) {
-          const int kb = 2 * ks + hh;
-          float ds[4];
-#pragma unroll
-          for (int r = 0; r < 4; ++r) {
-            float pr = fast_exp2(sc[kb][qb][r] - lse2[qb]);
-            if (edge) {
-              const int kv = j0 + kb * 16 + grp * 4 + r;
-              if (kv >= p.N || (p.causal && kv > q)) pr = 0.f;
-            }
-            ds[r] = pr * (dp[kb][qb][r] - dd[qb]);
+          for (int qb = 0; qb < QBD; ++qb) {
+            sc[kb][qb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, qf[qb][ks], sc[kb][qb], 0, 0, 0);
+            dp[kb][qb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, df[qb][ks], dp[kb][qb], 0, 0, 0);
           }
-          w[2 * hh] = pack2(ds[0], ds[1]);
-          w[2 * hh + 1] = pack2(ds[2], ds[3]);
         }
-        pf[qb] = __builtin_bit_cast(bf16x8_t, w);
-      }
-#pragma unroll
-      for (int db = 0; db < DB; ++db) {
-        const lds_u8* src = tile + offT[db] + ks * 32 * TL::ROW;
-        const s16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-            (__attribute__((address_space(3))) s16x4*)(src));
-        const s16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-            (__attribute__((address_space(3))) s16x4*)(src + 16 * TL::ROW));
-        const bf16x8_t a = __builtin_bit_cast(bf16x8_t, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
+      // Lane: rows j0 + 16 kb + 4 grp + r of query q0 + 16 qb + fr.
+      const bool edge = (p.causal && j0 + kTileRows - 1 > q0) || (j0 + kTileRows > p.N);
+      auto weight = [&](int kb, int qb, int r) {
+        float pr = fast_exp2(sc[kb][qb][r] - lse2[qb]);
+        if (edge) {
+          const int kv = j0 + kb * 16 + grp * 4 + r;
+          if (kv >= p.N || (p.causal && kv > q0 + qb * 16 + fr)) pr = 0.f;
+        }
+        return pr;
+      };
+      if (sweep == 0) {
 #pragma unroll
         for (int qb = 0; qb < QBD; ++qb)
-          acc[db][qb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, pf[qb], acc[db][qb], 0, 0, 0);
+#pragma unroll
+          for (int kb = 0; kb < 4; ++kb)
+#pragma unroll
+            for (int r = 0; r < 4; ++r) dsum[qb] = fmaf(weight(kb, qb, r), dp[kb][qb][r], dsum[qb]);
+        continue;
+      }
+      // dS^T fragments of one 32-row k-step (rows 32 ks + {4 grp .., 16 + 4 grp ..}).
+#pragma unroll
+      for (int ks = 0; ks < 2; ++ks) {
+        bf16x8_t pf[QBD];
+#pragma unroll
+        for (int qb = 0; qb < QBD; ++qb) {
+          u32x4 w;
+#pragma unroll
+          for (int hh = 0; hh < 2; ++hh) {
+            const int kb = 2 * ks + hh;
+            float ds[4];
+#pragma unroll
+            for (int r = 0; r < 4; ++r) ds[r] = weight(kb, qb, r) * (dp[kb][qb][r] - dd[qb]);
+            w[2 * hh] = pack2(ds[0], ds[1]);
+            w[2 * hh + 1] = pack2(ds[2], ds[3]);
+          }
+          pf[qb] = __builtin_bit_cast(bf16x8_t, w);
+        }
+#pragma unroll
+        for (int db = 0; db < DB; ++db) {
+          const lds_u8* src = tile + offT[db] + ks * 32 * TL::ROW;
+          const s16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+              (__attribute__((address_space(3))) s16x4*)(src));
+          const s16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+              (__attribute__((address_space(3))) s16x4*)(src + 16 * TL::ROW));
+          const bf16x8_t a = __builtin_bit_cast(bf16x8_t, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
+#pragma unroll
+          for (int qb = 0; qb < QBD; ++qb)
+            acc[db][qb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, pf[qb], acc[db][qb], 0, 0, 0);
+        }
+      }
+    }
+    if (sweep == 0) {
+      // Sum each query's rows over the four lane groups; publish Dd.
+#pragma unroll
+      for (int qb = 0; qb < QBD; ++qb) {
+        float t = dsum[qb] + __shfl_xor(dsum[qb], 16);
+        t += __shfl_xor(t, 32);
+        dd[qb] = t;
+        const int q = q0 + qb * 16 + fr;
+        if (grp == 0 && q < p.N) p.Dd[((size_t)b * p.H + h) * p.N + q] = t;
       }
     }
   }
@@ -613,9 +651,11 @@ bool attn_bwd_mfma_supported(const BwdParams& p) {
 hipError_t launch_attention_backward(const BwdParams& p, hipStream_t st) {
   if (p.B == 0 || p.N == 0) return hipSuccess;
   if (p.D != 64 && p.D != 128) return hipErrorInvalidValue;
+  // The matrix-core dQ~ kernel forms Dd itself (exactly, from P and dP); the
+  // vector-ALU path takes it from the fp32 output.
+  if (attn_bwd_mfma_supported(p)) return p.D == 128 ? launch_mfma<128>(p, st) : launch_mfma<64>(p, st);
   hipError_t e = p.dtype == KL_BF16 ? launch_prep<uint16_t>(p, st) : launch_prep<float>(p, st);
   if (e != hipSuccess) return e;
-  if (attn_bwd_mfma_supported(p)) return p.D == 128 ? launch_mfma<128>(p, st) : launch_mfma<64>(p, st);
   if (p.dtype == KL_BF16)
     return p.D == 128 ? launch_simple<uint16_t, 128>(p, st) : launch_simple<uint16_t, 64>(p, st);
   return p.D == 128 ? launch_simple<float, 128>(p, st) : launch_simple<float, 64>(p, st);

@@ -1,0 +1,140 @@
+"""GPU parity of the backward pass (Section 2.3, Eqs. 5 and 6) against the CPU
+oracle: the attention forward's log-sum-exp, the attention gradients dQ~ and dV
+(both of its terms), and the weight and input gradients."""
+
+import numpy as np
+import pytest
+import torch
+
+from oracle import keyless as K
+from paper_2606_21848_amd import binding as kb
+from tests.parity import assert_parity, say, to64
+from workloads import configs, synth
+
+pytestmark = pytest.mark.gpu
+DEV = "cuda"
+
+# N spans one query tile, ragged tails of the 64-row staged tiles and of the
+# 128-row work tiles, and a single row.
+# Gradient rows can cancel to zero (dQ~ of the first causal row is exactly 0):
+# such rows are compared against 1% of the tensor's largest row.
+FLOOR = 1e-2
+
+SHAPES = [(2, 200, 4, 2, 128), (1, 77, 2, 2, 64), (2, 1, 4, 1, 128), (1, 300, 8, 2, 64),
+          (1, 385, 4, 4, 128)]
+
+
+def _qvd(B, N, H, G, dk, seed, dtype):
+    Qr = synth.normal((B, N, H, dk), seed, 1, 1.0, dtype)
+    V = synth.normal((B, N, G, dk), seed, 2, 1.0, dtype)
+    dO = synth.normal((B, N, H, dk), seed, 3, 1.0, dtype)
+    return Qr, V, dO
+
+
+@pytest.mark.parametrize("dtype", [torch.float32, torch.bfloat16])
+@pytest.mark.parametrize("causal", [True, False])
+@pytest.mark.parametrize("B,N,H,G,dk", SHAPES[:3])
+def test_attention_forward_lse(lib, dtype, causal, B, N, H, G, dk):
+    say(f"attention forward + lse dtype={dtype} causal={causal} B={B} N={N} H={H} G={G} dk={dk}")
+    Qr, V, _ = _qvd(B, N, H, G, dk, 71, dtype)
+    out, lse = kb.keyless_attention_forward(Qr.to(DEV), V.to(DEV), causal=causal)
+    torch.cuda.synchronize()
+    ref_lse = K.attention_logsumexp(to64(Qr), to64(V), H, G, dk, causal=causal)
+    # out against the oracle's attention of the same routed queries and values
+    ref_out = np.zeros((B, N, H, dk))
+    q64, v64 = to64(Qr), to64(V)
+    for b in range(B):
+        for i in range(N):
+            seen = i + 1 if causal else N
+            for h in range(H):
+                ref_out[b, i, h] = K.decode_one(q64[b, i, h], v64[b, :seen, h // (H // G)])
+    assert_parity(out, ref_out, dtype, "output")
+    # lse is a per-row scalar: compare with an absolute bar scaled like the rows.
+    err = np.max(np.abs(lse.cpu().numpy() - ref_lse))
+    assert err <= (1e-4 if dtype == torch.float32 else 2e-2), f"lse error {err:.3e}"
+
+
+@pytest.mark.parametrize("dtype", [torch.float32, torch.bfloat16])
+@pytest.mark.parametrize("causal", [True, False])
+@pytest.mark.parametrize("B,N,H,G,dk", SHAPES)
+def test_attention_backward_matches_oracle(lib, dtype, causal, B, N, H, G, dk):
+    say(f"attention backward dtype={dtype} causal={causal} B={B} N={N} H={H} G={G} dk={dk}")
+    Qr, V, dO = _qvd(B, N, H, G, dk, 72, dtype)
+    q, v, g = Qr.to(DEV), V.to(DEV), dO.to(DEV)
+    out, lse = kb.keyless_attention_forward(q, v, causal=causal)
+    dq, dv = kb.keyless_attention_backward(q, v, out, g, lse, causal=causal)
+    torch.cuda.synchronize()
+    ref_dq, ref_dv = K.keyless_attention_backward(to64(Qr), to64(V), to64(dO), H, G, dk,
+                                                  causal=causal)
+    # Where every dQ~ row cancels (a single causal row), the scale of dV stands in.
+    scale = FLOOR * max(np.abs(ref_dq).max(), np.abs(ref_dv).max())
+    assert_parity(dq, ref_dq, dtype, "dQ~", FLOOR, scale)
+    assert_parity(dv, ref_dv, dtype, "dV", FLOOR, scale)
+
+
+def test_attention_backward_is_deterministic(lib):
+    B, N, H, G, dk = 1, 700, 8, 2, 128
+    say("attention backward determinism")
+    Qr, V, dO = (t.to(DEV) for t in _qvd(B, N, H, G, dk, 73, torch.bfloat16))
+    out, lse = kb.keyless_attention_forward(Qr, V)
+    first = kb.keyless_attention_backward(Qr, V, out, dO, lse)
+    for _ in range(2):
+        again = kb.keyless_attention_backward(Qr, V, out, dO, lse)
+        torch.cuda.synchronize()
+        assert torch.equal(first[0], again[0]) and torch.equal(first[1], again[1])
+
+
+@pytest.mark.parametrize("dtype", [torch.float32, torch.bfloat16])
+@pytest.mark.parametrize("B,N,d,H,G,dk", [(2, 130, 256, 4, 2, 64), (1, 64, 128, 2, 1, 128)])
+def test_layer_backward_matches_oracle(lib, dtype, B, N, d, H, G, dk):
+    """x -> routed queries and values -> attention -> dO: every gradient of the
+    layer (dX, dW^Q, dW^R of Eq. 5, dW^V of Eq. 6) against the oracle."""
+    say(f"layer backward dtype={dtype} B={B} N={N} d={d} H={H} G={G} dk={dk}")
+    x = synth.normal((B, N, d), 74, 1, 1.0, dtype)
+    W_Q = synth.normal((d, H * dk), 74, 2, d ** -0.5, dtype)
+    W_R = synth.normal((H, dk, dk), 74, 3, dk ** -0.5, dtype)
+    W_V = synth.normal((d, G * dk), 74, 4, d ** -0.5, dtype)
+    dO = synth.normal((B, N, H, dk), 74, 5, 1.0, dtype)
+    xs, wq, wr, wv, g = (t.to(DEV) for t in (x, W_Q, W_R, W_V, dO))
+    _, qr, v = kb.keyless_prefill(xs, wq, wr, wv, H, G, return_qv=True)
+    out, lse = kb.keyless_attention_forward(qr, v)
+    dq, dv = kb.keyless_attention_backward(qr, v, out, g, lse)
+    grads = kb.keyless_weight_gradients(xs, wq, wr, wv, dq, dv, H, G)
+    torch.cuda.synchronize()
+    ref = K.keyless_backward(to64(x), to64(W_Q), to64(W_R), to64(W_V), to64(dO), H, G, dk)
+    if dtype == torch.float32:
+        ref_dq, ref_dv = ref["dQr"], ref["dV"]
+    else:
+        # The bf16 path stores the folded weights, the routed queries and the
+        # values in bf16 (one rounding each); that rounding alone moves dQ~ by
+        # about the bar, so dQ~ and dV are checked against the oracle's attention
+        # backward on the oracle's projections rounded the same way.
+        bf = lambda a: to64(torch.from_numpy(a).to(torch.bfloat16))
+        Wt = bf(K.fold_routing(to64(W_Q), to64(W_R), H, dk))
+        _, Qr, Vp = K.keyless_prefill(to64(x), Wt, None, to64(W_V), H, G, dk)
+        ref_dq, ref_dv = K.keyless_attention_backward(bf(Qr), bf(Vp), to64(dO), H, G, dk)
+    assert_parity(dq, ref_dq, dtype, "dQ~", FLOOR)
+    assert_parity(dv, ref_dv, dtype, "dV", FLOOR)
+    assert_parity(grads["dW_R"], ref["dW_R"], dtype, "dW^R (Eq. 5)", FLOOR)
+    assert_parity(grads["dW_V"].T, ref["dW_V"].T, dtype, "dW^V (Eq. 6)", FLOOR)
+    assert_parity(grads["dW_Q"].T, ref["dW_Q"].T, dtype, "dW^Q", FLOOR)
+    assert_parity(grads["dX"], ref["dX"], dtype, "dX", FLOOR)
+
+
+def test_backward_full_size_sampled(lib):
+    """The measured backward workload (8192 tokens, 32 heads x 128, causal, the
+    routed queries and values of the prefill workload's layer): 24 sampled dQ~
+    rows anywhere and the dV rows of the last 48 positions against the oracle."""
+    say("backward full size")
+    c = configs.backward_bf16(device=DEV)
+    out, lse = kb.keyless_attention_forward(c["q"], c["v"])
+    dq, dv = kb.keyless_attention_backward(c["q"], c["v"], out, c["dout"], lse)
+    torch.cuda.synchronize()
+    assert torch.isfinite(dq.float()).all() and torch.isfinite(dv.float()).all()
+    N = c["N"]
+    rq = sorted(set([0, N - 1] + synth.uniform_int(22, 1, N - 2, 8, 50).tolist()))
+    rv = list(range(N - 48, N))
+    ref_dq, ref_dv = K.keyless_attention_backward_rows(to64(c["q"]), to64(c["v"]), to64(c["dout"]),
+                                                      c["H"], c["G"], c["d_head"], rq, rv)
+    assert_parity(dq[0, rq], ref_dq, torch.bfloat16, "sampled dQ~ rows", FLOOR)
+    assert_parity(dv[0, rv], ref_dv, torch.bfloat16, "last dV rows", FLOOR)

@@ -15,10 +15,10 @@ import torch
 from .synth import normal, permutation, uniform_int
 
 NAMES = ("tiny_fp32", "decode_bf16", "prefill_bf16", "paged_gqa_bf16", "head_to_head_bf16",
-         "decode_step_bf16", "cross_bf16", "latent_bf16")
+         "decode_step_bf16", "cross_bf16", "latent_bf16", "backward_bf16")
 
 # Stream ids (one per drawn tensor).
-S_X, S_WQ, S_WR, S_WV, S_XNEXT, S_V, S_Q, S_K, S_LEN, S_PERM, S_VNEW, S_XB, S_WPOST = range(13)
+S_X, S_WQ, S_WR, S_WV, S_XNEXT, S_V, S_Q, S_K, S_LEN, S_PERM, S_VNEW, S_XB, S_WPOST, S_DO = range(14)
 
 
 def tiny_fp32(device="cpu", seed=0, N=128, d_model=256, H=4, d_head=64):
@@ -170,4 +170,17 @@ def latent_bf16(device="cpu", seed=7, B=32, H=32, G=1, r=128, d_head=128, L=1638
         W_post=normal((H, r, d_head), seed, S_WPOST, 1.0 / math.sqrt(d_head), f, device),
         lengths=torch.full((B,), L, dtype=torch.int32, device=device),
         B=B, H=H, G=G, r=r, d_head=d_head, L=L,
+    )
+
+
+def backward_bf16(device="cpu", seed=8, B=1, N=8192, H=32, G=32, d_head=128):
+    """The attention backward at the prefill workload's shape (8192 tokens, 32
+    heads x 128, causal): routed queries, values and the incoming gradient dL/dO
+    ~ N(0,1) in bf16 (scores tau <q~, v> then have unit spread)."""
+    f = torch.bfloat16
+    return dict(
+        q=normal((B, N, H, d_head), seed, S_Q, 1.0, f, device),
+        v=normal((B, N, G, d_head), seed, S_V, 1.0, f, device),
+        dout=normal((B, N, H, d_head), seed, S_DO, 1.0, f, device),
+        B=B, N=N, H=H, G=G, d_head=d_head,
     )
