@@ -430,6 +430,11 @@ def keyless_attention_forward(q_routed: torch.Tensor, v: torch.Tensor, causal: b
     return out, lse
 
 
+def attention_backward_workspace_bytes(B: int, N: int, H: int) -> int:
+    load()
+    return int(_lib.keyless_attention_backward_workspace_size(B, N, H))
+
+
 def keyless_attention_backward(q_routed: torch.Tensor, v: torch.Tensor, out: torch.Tensor,
                                dout: torch.Tensor, lse: torch.Tensor, causal: bool = True,
                                scale: float = 0.0, dq=None, dv=None, workspace=None):

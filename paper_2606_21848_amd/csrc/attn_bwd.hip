@@ -224,58 +224,59 @@ __global__ __launch_bounds__(kThreads, 2) void bwd_dq_kernel(BwdParams p) {
       if (p.causal && j0 > q0 + 16 * QBD - 1) continue;  // above this wave's diagonal
       const lds_u8* tile = (const lds_u8*)smem + stage * TL::BYTES;
 
-      f32x4_t sc[4][QBD], dp[4][QBD];
-#pragma unroll
-      for (int kb = 0; kb < 4; ++kb)
-#pragma unroll
-        for (int qb = 0; qb < QBD; ++qb) {
-          sc[kb][qb] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-          dp[kb][qb] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-        }
-#pragma unroll
-      for (int kb = 0; kb < 4; ++kb)
-#pragma unroll
-        for (int ks = 0; ks < KS; ++ks) {
-          const bf16x8_t a = *reinterpret_cast<const __attribute__((address_space(3))) bf16x8_t*>(
-              tile + offS[ks] + kb * 16 * TL::ROW);
-#pragma unroll
-          for (int qb = 0; qb < QBD; ++qb) {
-            sc[kb][qb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, qf[qb][ks], sc[kb][qb], 0, 0, 0);
-            dp[kb][qb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, df[qb][ks], dp[kb][qb], 0, 0, 0);
-          }
-        }
-      // Lane: rows j0 + 16 kb + 4 grp + r of query q0 + 16 qb + fr.
       const bool edge = (p.causal && j0 + kTileRows - 1 > q0) || (j0 + kTileRows > p.N);
-      auto weight = [&](int kb, int qb, int r) {
-        float pr = fast_exp2(sc[kb][qb][r] - lse2[qb]);
-        if (edge) {
-          const int kv = j0 + kb * 16 + grp * 4 + r;
-          if (kv >= p.N || (p.causal && kv > q0 + qb * 16 + fr)) pr = 0.f;
-        }
-        return pr;
-      };
-      if (sweep == 0) {
-#pragma unroll
-        for (int qb = 0; qb < QBD; ++qb)
-#pragma unroll
-          for (int kb = 0; kb < 4; ++kb)
-#pragma unroll
-            for (int r = 0; r < 4; ++r) dsum[qb] = fmaf(weight(kb, qb, r), dp[kb][qb][r], dsum[qb]);
-        continue;
-      }
-      // dS^T fragments of one 32-row k-step (rows 32 ks + {4 grp .., 16 + 4 grp ..}).
+      // One 32-row k-step at a time (value blocks kb = 2 ks, 2 ks + 1), which
+      // keeps half of the tile's scores live.
 #pragma unroll
       for (int ks = 0; ks < 2; ++ks) {
+        f32x4_t sc[2][QBD], dp[2][QBD];
+#pragma unroll
+        for (int hh = 0; hh < 2; ++hh)
+#pragma unroll
+          for (int qb = 0; qb < QBD; ++qb) {
+            sc[hh][qb] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+            dp[hh][qb] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+          }
+#pragma unroll
+        for (int hh = 0; hh < 2; ++hh)
+#pragma unroll
+          for (int kd = 0; kd < KS; ++kd) {
+            const bf16x8_t a = *reinterpret_cast<const __attribute__((address_space(3))) bf16x8_t*>(
+                tile + offS[kd] + (2 * ks + hh) * 16 * TL::ROW);
+#pragma unroll
+            for (int qb = 0; qb < QBD; ++qb) {
+              sc[hh][qb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, qf[qb][kd], sc[hh][qb], 0, 0, 0);
+              dp[hh][qb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, df[qb][kd], dp[hh][qb], 0, 0, 0);
+            }
+          }
+        // Lane: rows j0 + 16 (2 ks + hh) + 4 grp + r of query q0 + 16 qb + fr.
+        auto weight = [&](int hh, int qb, int r) {
+          float pr = fast_exp2(sc[hh][qb][r] - lse2[qb]);
+          if (edge) {
+            const int kv = j0 + (2 * ks + hh) * 16 + grp * 4 + r;
+            if (kv >= p.N || (p.causal && kv > q0 + qb * 16 + fr)) pr = 0.f;
+          }
+          return pr;
+        };
+        if (sweep == 0) {
+#pragma unroll
+          for (int qb = 0; qb < QBD; ++qb)
+#pragma unroll
+            for (int hh = 0; hh < 2; ++hh)
+#pragma unroll
+              for (int r = 0; r < 4; ++r) dsum[qb] = fmaf(weight(hh, qb, r), dp[hh][qb][r], dsum[qb]);
+          continue;
+        }
+        // dS^T fragments of the k-step (rows 32 ks + {4 grp .., 16 + 4 grp ..}).
         bf16x8_t pf[QBD];
 #pragma unroll
         for (int qb = 0; qb < QBD; ++qb) {
           u32x4 w;
 #pragma unroll
           for (int hh = 0; hh < 2; ++hh) {
-            const int kb = 2 * ks + hh;
             float ds[4];
 #pragma unroll
-            for (int r = 0; r < 4; ++r) ds[r] = weight(kb, qb, r) * (dp[kb][qb][r] - dd[qb]);
+            for (int r = 0; r < 4; ++r) ds[r] = weight(hh, qb, r) * (dp[hh][qb][r] - dd[qb]);
             w[2 * hh] = pack2(ds[0], ds[1]);
             w[2 * hh + 1] = pack2(ds[2], ds[3]);
           }
