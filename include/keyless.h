@@ -326,6 +326,24 @@ int keyless_decode_project(const void* x, const void* packed, int B, int d_model
 int keyless_decode(const void* q_routed, const kl_value_cache* cache, const int32_t* lengths,
                    int B, int H, float scale, void* out, void* ws, size_t ws_bytes, void* stream);
 
+/*
+ * keyless_decode_append - one whole decode step over the value-only cache
+ * (Section 3: the step's value v_{n+1} joins the cache and the step's query
+ * attends over all n+1 values) in one launch: the same result as
+ * value_cache_append(cache, v_new, lengths_before) followed by keyless_decode
+ * over lengths_before[b] + 1 rows, with the new row taken from v_new rather
+ * than read back from the cache.
+ *   v_new           [B, G, d_head], cache dtype, 16-byte aligned
+ *   lengths_before  [B] int32 on the device: rows already cached; the new row goes
+ *                   to position lengths_before[b] (dropped past the capacity or a
+ *                   block outside the cache, as value_cache_append drops it)
+ * Other arguments, workspace and errors as for keyless_decode (which uses the
+ * same work split for lengths_before + 1 rows).
+ */
+int keyless_decode_append(const void* q_routed, const void* v_new, const kl_value_cache* cache,
+                          const int32_t* lengths_before, int B, int H, float scale, void* out,
+                          void* ws, size_t ws_bytes, void* stream);
+
 /* As keyless_decode, with the cache length split into chunks of chunk_rows
  * rows fixed by the caller (a multiple of 64; 0 selects the built-in choice):
  * one workgroup per (b, group, chunk), then a merge of the chunks of each

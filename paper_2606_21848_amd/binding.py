@@ -30,6 +30,7 @@ EXPORTS = (
     "keyless_attention_backward_workspace_size", "keyless_weight_gradients",
     "keyless_weight_gradients_workspace_size",
     "keyless_decode_project", "keyless_decode", "keyless_decode_chunked", "keyless_decode_workspace_size",
+    "keyless_decode_append",
     "value_cache_append", "standard_decode", "standard_decode_chunked",
     "keyless_set_kernel_timer", "keyless_last_error", "keyless_version",
 )
@@ -80,6 +81,7 @@ def load(path: str = LIB_PATH):
         "keyless_decode_project": (i, [vp, vp, i, i, i, i, i, i, vp, vp, cp, vp, vp]),
         "keyless_decode": (i, [vp, cp, vp, i, i, f, vp, vp, sz, vp]),
         "keyless_decode_chunked": (i, [vp, cp, vp, i, i, f, vp, vp, sz, i, vp]),
+        "keyless_decode_append": (i, [vp, vp, cp, vp, i, i, f, vp, vp, sz, vp]),
         "keyless_decode_workspace_size": (sz, [cp, i, i, i]),
         "keyless_latent_decode": (i, [vp, vp, cp, vp, i, i, i, f, vp, vp, sz, vp]),
         "keyless_latent_decode_workspace_size": (sz, [cp, i, i, i]),
@@ -473,3 +475,21 @@ def keyless_weight_gradients(x: torch.Tensor, W_Q: torch.Tensor, W_R: torch.Tens
                                          _ptr(res["dW_R"]), _ptr(res["dW_V"]), _ptr(res["dX"]),
                                          _ptr(workspace), workspace.numel(), _stream(x)))
     return res
+
+
+def keyless_decode_append(q_routed: torch.Tensor, v_new: torch.Tensor, cache: ValueCache,
+                          lengths_before: torch.Tensor, scale: float = 0.0, out=None,
+                          workspace=None) -> torch.Tensor:
+    """One decode step in one launch: v_new [B, G, d] joins the cache at
+    lengths_before[b], and q~ [B, H, d] attends over lengths_before[b] + 1 rows."""
+    load()
+    B, H, _ = q_routed.shape
+    if out is None:
+        out = torch.empty_like(q_routed)
+    if workspace is None:
+        n = decode_workspace_bytes(cache, B, H)
+        workspace = torch.empty(max(n, 256), dtype=torch.uint8, device=q_routed.device)
+    _check(_lib.keyless_decode_append(_ptr(q_routed), _ptr(v_new), cache.ref, _ptr(lengths_before), B,
+                                      H, scale, _ptr(out), _ptr(workspace), workspace.numel(),
+                                      _stream(q_routed)))
+    return out

@@ -151,7 +151,8 @@ int check_group_ratio(const char* who, const kl_value_cache* c, int R) {
 
 int decode_common(const void* q, const kl_value_cache* k_cache, const kl_value_cache* v_cache,
                   const int32_t* lengths, int B, int H, float scale, void* out, void* ws,
-                  size_t ws_bytes, int chunk_rows, void* stream, const char* who) {
+                  size_t ws_bytes, int chunk_rows, void* stream, const char* who,
+                  const void* vnew = nullptr) {
   int st = check_cache(v_cache, who);
   if (st != KL_OK) return st;
   if (k_cache) {
@@ -192,6 +193,7 @@ int decode_common(const void* q, const kl_value_cache* k_cache, const kl_value_c
   p.kdata = k_cache ? k_cache->data : nullptr;
   p.table = v_cache->layout == KL_PAGED ? v_cache->block_table : nullptr;
   p.lengths = lengths;
+  p.vnew = vnew;
   p.out = out;
   p.balanced = pl.balanced;
   p.nwg = kBalancedWorkgroups;
@@ -245,6 +247,16 @@ int keyless_decode(const void* q_routed, const kl_value_cache* cache, const int3
                    int B, int H, float scale, void* out, void* ws, size_t ws_bytes, void* stream) {
   return decode_common(q_routed, nullptr, cache, lengths, B, H, scale, out, ws, ws_bytes, 0,
                        stream, "keyless_decode");
+}
+
+int keyless_decode_append(const void* q_routed, const void* v_new, const kl_value_cache* cache,
+                          const int32_t* lengths_before, int B, int H, float scale, void* out,
+                          void* ws, size_t ws_bytes, void* stream) {
+  const char* who = "keyless_decode_append";
+  if (!v_new) return fail(KL_ERR_INVALID_ARG, "%s: v_new must be non-NULL", who);
+  if (!aligned16(v_new)) return fail(KL_ERR_INVALID_ARG, "%s: v_new must be 16-byte aligned", who);
+  return decode_common(q_routed, nullptr, cache, lengths_before, B, H, scale, out, ws, ws_bytes, 0,
+                       stream, who, v_new);
 }
 
 int keyless_decode_chunked(const void* q_routed, const kl_value_cache* cache,

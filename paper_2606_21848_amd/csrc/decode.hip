@@ -249,11 +249,64 @@ __device__ __forceinline__ void merge_waves(const DecodeParams& p, const float* 
   __syncthreads();
 }
 
-// Cached rows of sequence b, clamped to the cache capacity.
+// Rows decoded for sequence b (the new row included when the step appends),
+// clamped to the cache capacity.
+// The lengths (and the plan) are read through the constant address space:
+// nothing in the kernel writes them, and the uniform reads then stay scalar
+// loads even where the kernel stores to other global memory (the appended row).
+__device__ __forceinline__ int length_of(const DecodeParams& p, int b) {
+  return ((const __attribute__((address_space(4))) int*)p.lengths)[b];
+}
+__device__ __forceinline__ int decode_rows(const DecodeParams& p, int b, int cap) {
+  return min(max(length_of(p, b) + (p.vnew ? 1 : 0), 0), cap);
+}
 template <bool PAGED>
 __device__ __forceinline__ int seq_len(const DecodeParams& p, int b) {
+  return decode_rows(p, b, PAGED ? (p.max_blocks << p.block_shift) : p.L_max);
+}
+
+// The step's new row of pair (b, g), when this segment [start, end) holds it:
+// its position, else -1. The new row is the last decoded row of the sequence;
+// past the capacity it is dropped (and not decoded), as an append drops it.
+template <bool PAGED>
+__device__ __forceinline__ int new_row_in(const DecodeParams& p, int b, int start, int end) {
+  if (!p.vnew) return -1;
   const int cap = PAGED ? (p.max_blocks << p.block_shift) : p.L_max;
-  return min(max(p.lengths[b], 0), cap);
+  const int pos = length_of(p, b);
+  return (pos >= 0 && pos < cap && pos >= start && pos < end) ? pos : -1;
+}
+
+// The step's new value row of pair (b, g): lane i < ROWB / 16 holds its 16-byte
+// chunk i. Loaded before the cached rows stream, so its latency is hidden.
+template <typename T, int D>
+__device__ __forceinline__ u32x4 load_new_row(const DecodeParams& p, int b, int g, int lane) {
+  constexpr int CH = D * (int)sizeof(T) / 16;
+  const u32x4* src = reinterpret_cast<const u32x4*>(
+      reinterpret_cast<const unsigned char*>(p.vnew) + ((size_t)b * p.G + g) * CH * 16);
+  return lane < CH ? src[lane] : u32x4{0u, 0u, 0u, 0u};
+}
+
+// Appends the new row (held as by load_new_row) to the cache at row pos, and
+// stages it as row 0 of a tile in LDS with the other rows zero, so that masked
+// rows contribute exact zeros to any product. One wave; the stage must be idle.
+template <typename T, int D, bool PAGED>
+__device__ __forceinline__ void append_and_stage(const DecodeParams& p, int b, int g, int pos,
+                                                 u32x4 chunk, lds_u8* stage, int lane) {
+  constexpr int CH = D * (int)sizeof(T) / 16;  // 16-byte chunks per row
+  for (int i = lane; i < kTile * CH; i += 64)
+    *reinterpret_cast<__attribute__((address_space(3))) u32x4*>(stage + i * 16) =
+        i < CH ? chunk : u32x4{0u, 0u, 0u, 0u};
+  size_t row;
+  bool ok = true;
+  if constexpr (PAGED) {
+    const int blk = p.table[(size_t)b * p.max_blocks + (pos >> p.block_shift)];
+    ok = blk >= 0 && blk < p.num_blocks;
+    row = ((((size_t)(ok ? blk : 0)) * p.G + g) << p.block_shift) + (pos & ((1 << p.block_shift) - 1));
+  } else {
+    row = ((size_t)b * p.G + g) * p.L_max + pos;
+  }
+  if (ok && lane < CH)
+    reinterpret_cast<u32x4*>(const_cast<void*>(p.vdata))[row * CH + lane] = chunk;
 }
 
 // Runs seg(b, g, row_begin, row_end, out) for every segment this workgroup owns.
@@ -287,9 +340,9 @@ __device__ __forceinline__ void for_each_segment(const DecodeParams& p, Seg seg)
     seg(b, g, start, min(start + p.chunk, len), o);
     return;
   }
-  const int* __restrict__ plan = p.plan;
+  const __attribute__((address_space(4))) int* plan = (const __attribute__((address_space(4))) int*)p.plan;
   const int total = plan[0], per = plan[1];
-  const int* __restrict__ pre = plan + 2;  // exclusive prefix sums of tiles per sequence, [B + 1]
+  const __attribute__((address_space(4))) int* pre = plan + 2;  // exclusive prefix sums of tiles, [B + 1]
   const int w = blockIdx.x;
   int t = w * per;
   const int t_end = min(total, t + per);
@@ -373,14 +426,17 @@ __global__ __launch_bounds__(NW * 64) void decode_partial_kernel(DecodeParams p)
     for (int r = 0; r < R; ++r) asm volatile("" ::"v"(qv[r]));
   };
 
+  // Rows at or past vend are masked: the segment's end, or the new row's
+  // position while the cached rows stream when the step appends.
+  int vend = end;
   auto consume = [&](const lds_u8* stage, int t0, bool blk_ok) {
-    const bool full = blk_ok && (t0 + kTile <= end);
+    const bool full = blk_ok && (t0 + kTile <= vend);
     u32x4 v[U], k[U];
     bool valid[U];
 #pragma unroll
     for (int u = 0; u < U; ++u) {
       const int rr = u * RPL + rslot;
-      valid[u] = blk_ok && (t0 + rr < end);
+      valid[u] = blk_ok && (t0 + rr < vend);
       const int off = rr * ROWB + lc * 16;
       v[u] = *reinterpret_cast<const __attribute__((address_space(3))) u32x4*>(stage + off);
       if constexpr (KEYS)
@@ -483,8 +539,16 @@ __global__ __launch_bounds__(NW * 64) void decode_partial_kernel(DecodeParams p)
     }
   };
 
-  stream_tiles<T, D, PAGED, KEYS, NW>(p, b, g, lane, ring, start + wave * kTile, end, swz, ready,
+  const int pnew = KEYS ? -1 : new_row_in<PAGED>(p, b, start, end);
+  if (pnew >= 0) vend = pnew;
+  const u32x4 nrow = (pnew >= 0) ? load_new_row<T, D>(p, b, g, lane) : u32x4{0u, 0u, 0u, 0u};
+  stream_tiles<T, D, PAGED, KEYS, NW>(p, b, g, lane, ring, start + wave * kTile, vend, swz, ready,
                                       consume);
+  if (pnew >= 0 && wave == 0) {  // the step's new row: from registers, not from the cache
+    append_and_stage<T, D, PAGED>(p, b, g, pnew, nrow, ring, lane);
+    vend = pnew + 1;
+    consume(ring, pnew, true);
+  }
 
   // Merge the RPL row slots of the wave (lanes LPR apart), then the waves.
 #pragma unroll
@@ -607,6 +671,9 @@ __global__ __launch_bounds__(NW * 64) void decode_mfma_kernel(DecodeParams p) {
       for (int kk = 0; kk < 4; ++kk) asm volatile("" ::"v"(qf[nb][kk]));
   };
 
+  // Rows at or past vend are masked: the segment's end, or the new row's
+  // position while the cached rows stream when the step appends.
+  int vend = end;
   auto consume = [&](const lds_u8* stage, int t0, bool blk_ok) {
     if (!blk_ok) return;  // uniform: a block outside the cache contributes nothing
     const lds_u8* ks = KEYS ? stage + TB : stage;
@@ -629,7 +696,7 @@ __global__ __launch_bounds__(NW * 64) void decode_mfma_kernel(DecodeParams p) {
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
         float x = sc[nb][i] * p.scale_log2;
-        if (t0 + 4 * grp + i >= end) x = -INFINITY;
+        if (t0 + 4 * grp + i >= vend) x = -INFINITY;
         s4[i] = x;
         tmax = fmaxf(tmax, x);
       }
@@ -665,8 +732,16 @@ __global__ __launch_bounds__(NW * 64) void decode_mfma_kernel(DecodeParams p) {
     }
   };
 
-  stream_tiles<T, D, PAGED, KEYS, NW>(p, b, g, lane, ring, start + wave * kTile, end, fsw, ready,
+  const int pnew = KEYS ? -1 : new_row_in<PAGED>(p, b, start, end);
+  if (pnew >= 0) vend = pnew;
+  const u32x4 nrow = (pnew >= 0) ? load_new_row<T, D>(p, b, g, lane) : u32x4{0u, 0u, 0u, 0u};
+  stream_tiles<T, D, PAGED, KEYS, NW>(p, b, g, lane, ring, start + wave * kTile, vend, fsw, ready,
                                       consume);
+  if (pnew >= 0 && wave == 0) {  // the step's new row: from registers, not from the cache
+    append_and_stage<T, D, PAGED>(p, b, g, pnew, nrow, ring, lane);
+    vend = pnew + 1;
+    consume(ring, pnew, true);
+  }
 
   // Row sums of each head over the four lane groups (the reference is shared).
 #pragma unroll
@@ -705,7 +780,7 @@ __global__ __launch_bounds__(1024) void decode_plan_kernel(DecodeParams p) {
   __syncthreads();
   for (int b0 = 0; b0 < p.B; b0 += 1024) {
     const int b = b0 + t;
-    const int n = b < p.B ? (min(max(p.lengths[b], 0), cap) + kTile - 1) / kTile : 0;
+    const int n = b < p.B ? (decode_rows(p, b, cap) + kTile - 1) / kTile : 0;
     s_scan[t] = n;
     __syncthreads();
     for (int off = 1; off < 1024; off <<= 1) {
@@ -740,7 +815,7 @@ __global__ __launch_bounds__(256) void decode_combine_kernel(DecodeParams p) {
   const int b = bh / p.H;
   const int t = threadIdx.x;
   const int cap = p.paged ? (p.max_blocks << p.block_shift) : p.L_max;
-  const int len = min(max(p.lengths[b], 0), cap);
+  const int len = decode_rows(p, b, cap);
   int ns;                      // partials of this head
   const float* part;           // its first partial row
   size_t stride = D + 2;       // floats between consecutive partial rows

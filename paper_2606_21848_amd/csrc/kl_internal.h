@@ -30,7 +30,11 @@ struct DecodeParams {
   const void* vdata;      // value cache data
   const void* kdata;      // key cache data (standard decode) or nullptr
   const int32_t* table;   // paged block table or nullptr
-  const int32_t* lengths; // [B]
+  const int32_t* lengths; // [B]: rows to decode, or rows before the step when vnew is set
+  const void* vnew;       // [B, G, D] the step's new value rows, or nullptr. When set, row
+                          // lengths[b] of each sequence is the new row: it is appended to the
+                          // cache (dropped past the capacity) and the decode covers
+                          // lengths[b] + 1 rows, taking the new row from vnew
   void* out;              // [B, H, D]
   float* part;            // split partials: [B * H, S, D + 2] (split mode, S > 1) or
                           // [B * G + nwg, R, D + 2] (balanced mode)

@@ -279,3 +279,70 @@ def test_head_to_head_full_size_sampled(lib):
         g_s.append(std[b, h])
     assert_parity(torch.stack(g_k), np.stack(r_k), torch.bfloat16, "keyless sampled")
     assert_parity(torch.stack(g_s), np.stack(r_s), torch.bfloat16, "standard sampled")
+
+
+APPEND_CASES = [(torch.bfloat16, 128, 8, 8), (torch.bfloat16, 128, 8, 2), (torch.bfloat16, 128, 32, 1),
+                (torch.bfloat16, 64, 4, 4), (torch.float32, 64, 4, 4), (torch.float32, 128, 4, 2)]
+
+
+@pytest.mark.parametrize("dtype,d,H,G", APPEND_CASES)
+@pytest.mark.parametrize("paged", [False, True])
+def test_decode_append_matches_oracle(lib, dtype, d, H, G, paged):
+    """The fused step (append v_new at lengths_before, decode over one more row)
+    equals the oracle's append then decode; the cache afterwards holds the same
+    bits as after value_cache_append. A new row at the capacity is dropped and
+    the decode covers the cached rows."""
+    B, L = 9, 304  # a whole number of 16-row blocks: no unwritten padding inside the capacity
+    say(f"decode_append dtype={dtype} d={d} H={H} G={G} paged={paged}")
+    cache = synth.normal((B, G, L, d), 18, 1, 1.0, dtype)
+    vnew = synth.normal((B, G, d), 18, 2, 1.0, dtype)
+    q = synth.normal((B, H, d), 18, 3, 1.0, dtype)
+    if paged:
+        data, table = _paged(cache, torch.full((B,), L, dtype=torch.int32), 16, 7)
+        tab = table.numpy()
+        cap = table.shape[1] * 16
+    else:
+        data, table, tab = cache, None, None
+        cap = L
+    # Position cap is past the capacity: that new row is dropped.
+    before = torch.tensor([0, 1, 15, 16, 17, 150, cap - 1, cap, 63], dtype=torch.int32)
+    fits = before < cap
+    # The oracle's append, sequence by sequence (the dropped one skipped).
+    ref_data = to64(data)
+    for b in range(B):
+        if not fits[b]:
+            continue
+        if paged:
+            ref_data = K.value_cache_append(ref_data, to64(vnew[b:b + 1, None]), [int(before[b])],
+                                            tab[b:b + 1], 16)
+        else:
+            one = ref_data[b:b + 1]
+            ref_data[b:b + 1] = K.value_cache_append(one, to64(vnew[b:b + 1, None]), [int(before[b])])
+    lengths = torch.minimum(before + 1, torch.tensor(cap, dtype=torch.int32))
+    ref = K.keyless_decode(to64(q), ref_data, lengths.numpy(), H, G, block_table=tab, block_size=16)
+    dev_data = data.to(DEV)
+    vc = kb.ValueCache(dev_data, None if table is None else table.to(DEV))
+    out = kb.keyless_decode_append(q.to(DEV), vnew.to(DEV), vc, before.to(DEV))
+    # The unfused library path on a copy of the same cache.
+    other = data.to(DEV)
+    vc2 = kb.ValueCache(other, None if table is None else table.to(DEV))
+    kb.value_cache_append(vc2, vnew[:, None].contiguous().to(DEV), before.to(DEV))
+    torch.cuda.synchronize()
+    assert_parity(out, ref, dtype, "fused step")
+    assert torch.equal(torch.nan_to_num(dev_data), torch.nan_to_num(other)), "cache after the step"
+
+
+def test_decode_append_full_size(lib):
+    """The decode_bf16 workload as one fused step per sequence: equal to the
+    unfused append + decode within the bar, the cache bit-equal afterwards."""
+    say("decode_append full size")
+    c = configs.decode_bf16(device=DEV)
+    base = c["V"].clone()
+    before = c["lengths_before"]
+    vnew = c["v_new"][:, 0].contiguous()  # [B, G, d]
+    a = kb.keyless_decode_append(c["q"], vnew, kb.ValueCache(c["V"]), before)
+    kb.value_cache_append(kb.ValueCache(base), c["v_new"], before)
+    b = kb.keyless_decode(c["q"], kb.ValueCache(base), before + 1)
+    torch.cuda.synchronize()
+    assert torch.equal(c["V"], base)
+    assert_parity(a, to64(b), torch.bfloat16, "fused vs unfused")
