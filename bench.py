@@ -422,24 +422,25 @@ def extra_measurements(torch, kb, configs, dev):
     del c, packed, outs
     # Attention backward (Section 2.3) at the prefill shape: dQ~ and dV from dO.
     bw = configs.backward_bf16(device=dev)
-    bout, blse = kb.keyless_attention_forward(bw["q"], bw["v"])
+    bo32 = torch.empty(bw["q"].shape, dtype=torch.float32, device=dev)
+    bout, blse = kb.keyless_attention_forward(bw["q"], bw["v"], out_f32=bo32)
     bdq, bdv = torch.empty_like(bw["q"]), torch.empty_like(bw["v"])
     bws = torch.empty(max(kb.attention_backward_workspace_bytes(bw["B"], bw["N"], bw["H"]), 256),
                       dtype=torch.uint8, device=dev)
 
     def bstep(i):
         kb.keyless_attention_backward(bw["q"], bw["v"], bout, bw["dout"], blse, dq=bdq, dv=bdv,
-                                      workspace=bws)
+                                      workspace=bws, out_f32=bo32)
     ms = timed_steps(bstep, 10, 3, torch)
     Nb, Hb, dkb = bw["N"], bw["H"], bw["d_head"]
     flops = 5 * Hb * dkb * Nb * (Nb + 1)  # five causal products: S, dP, dQ~, P^T dO, dS^T Q~
     res["backward_bf16"] = {"workload": "attention backward, batch 1, 8192 tokens, 32 heads x 128, "
-                                        "causal (dQ~ and dV from dO, the forward's output and "
-                                        "log-sum-exp)",
+                                        "causal (dQ~ and dV from dO, the forward's output, its "
+                                        "fp32 copy and log-sum-exp)",
                             "ms": round(ms, 3), "tflops": round(flops / (ms * 1e-3) / 1e12, 2),
                             "frac_of_bf16_mfma_peak": round(flops / (ms * 1e-3) / 1e12 /
                                                            BF16_MFMA_PEAK_TFLOPS, 4)}
-    del bw, bout, blse, bdq, bdv, bws
+    del bw, bout, blse, bdq, bdv, bws, bo32
     # Paged grouped-head decode.
     g = configs.paged_gqa_bf16(device=dev)
     vc = kb.ValueCache(g["data"], g["block_table"])

@@ -226,11 +226,13 @@ int keyless_cross_attention_packed(const void* xa, const void* xb, const void* p
  *   contiguous and 16-byte aligned, in `dtype`
  *   lse      [B, H, N] fp32, or NULL: ln sum_j exp(scale <q~_i, v_j>) over the
  *            rows j that row i sees
+ *   out_f32  [B, N, H, d_head] fp32, or NULL: the output before its rounding to
+ *            `dtype` (for keyless_attention_backward), 16-byte aligned
  * causal, scale, precision and errors as for keyless_prefill.
  */
 int keyless_attention_forward(const void* q_routed, const void* v, int B, int N, int H, int G,
                               int d_head, int causal, float scale, kl_dtype dtype, void* out,
-                              float* lse, void* stream);
+                              float* lse, float* out_f32, void* stream);
 
 /*
  * keyless_attention_backward - gradients of the keyless attention (Section 2.3)
@@ -241,6 +243,10 @@ int keyless_attention_forward(const void* q_routed, const void* v, int B, int N,
  *               Eq. 6; a value group sums them over its H/G heads)
  *   q_routed, v, out (the forward's output), dout [B, N, H, d_head] and lse as
  *   written by keyless_attention_forward with the same causal and scale;
+ *   out_f32 the forward's fp32 output, or NULL. The row sums rowsum(P * dP) =
+ *   rowsum(dO * O) are taken from out_f32 when given; otherwise, for bf16, from P
+ *   and dP in an extra sweep over the values (rowsum(dO * O) over the bf16
+ *   output would carry its rounding into every dP - rowsum);
  *   dq_routed [B, N, H, d_head], dv [B, N, G, d_head]; all 16-byte aligned.
  *   ws, ws_bytes  keyless_attention_backward_workspace_size(B, N, H) bytes (the
  *                 per-row rowsum(dO * O), B*H*N floats)
@@ -250,7 +256,8 @@ int keyless_attention_forward(const void* q_routed, const void* v, int B, int N,
  * (no atomics): results are deterministic.
  */
 int keyless_attention_backward(const void* q_routed, const void* v, const void* out,
-                               const void* dout, const float* lse, int B, int N, int H, int G,
+                               const float* out_f32, const void* dout, const float* lse, int B,
+                               int N, int H, int G,
                                int d_head, int causal, float scale, kl_dtype dtype, void* dq_routed,
                                void* dv, void* ws, size_t ws_bytes, void* stream);
 size_t keyless_attention_backward_workspace_size(int B, int N, int H);

@@ -85,9 +85,9 @@ def load(path: str = LIB_PATH):
         "keyless_decode_workspace_size": (sz, [cp, i, i, i]),
         "keyless_latent_decode": (i, [vp, vp, cp, vp, i, i, i, f, vp, vp, sz, vp]),
         "keyless_latent_decode_workspace_size": (sz, [cp, i, i, i]),
-        "keyless_attention_forward": (i, [vp, vp, i, i, i, i, i, i, f, i, vp, vp, vp]),
-        "keyless_attention_backward": (i, [vp, vp, vp, vp, vp, i, i, i, i, i, i, f, i, vp, vp,
-                                           vp, sz, vp]),
+        "keyless_attention_forward": (i, [vp, vp, i, i, i, i, i, i, f, i, vp, vp, vp, vp]),
+        "keyless_attention_backward": (i, [vp, vp, vp, vp, vp, vp, i, i, i, i, i, i, f, i, vp,
+                                           vp, vp, sz, vp]),
         "keyless_attention_backward_workspace_size": (sz, [i, i, i]),
         "keyless_weight_gradients": (i, [vp, vp, vp, vp, vp, vp, i, i, i, i, i, i, i, vp, vp, vp,
                                          vp, vp, sz, vp]),
@@ -416,9 +416,10 @@ def keyless_latent_decode(q_routed: torch.Tensor, W_post: torch.Tensor, cache: "
 
 
 def keyless_attention_forward(q_routed: torch.Tensor, v: torch.Tensor, causal: bool = True,
-                              scale: float = 0.0, out=None, lse=None):
+                              scale: float = 0.0, out=None, lse=None, out_f32=None):
     """Attention over projected routed queries [B, N, H, d] and values [B, N, G, d];
-    returns (out, lse [B, H, N] fp32, the natural-log log-sum-exp per row)."""
+    returns (out, lse [B, H, N] fp32, the natural-log log-sum-exp per row). With
+    out_f32 (a [B, N, H, d] fp32 tensor) the unrounded output is written too."""
     load()
     B, N, H, dk = q_routed.shape
     G = v.shape[2]
@@ -427,7 +428,7 @@ def keyless_attention_forward(q_routed: torch.Tensor, v: torch.Tensor, causal: b
     if lse is None:
         lse = torch.empty((B, H, N), dtype=torch.float32, device=q_routed.device)
     _check(_lib.keyless_attention_forward(_ptr(q_routed), _ptr(v), B, N, H, G, dk, int(causal),
-                                          scale, _dt(q_routed), _ptr(out), _ptr(lse),
+                                          scale, _dt(q_routed), _ptr(out), _ptr(lse), _ptr(out_f32),
                                           _stream(q_routed)))
     return out, lse
 
@@ -439,8 +440,9 @@ def attention_backward_workspace_bytes(B: int, N: int, H: int) -> int:
 
 def keyless_attention_backward(q_routed: torch.Tensor, v: torch.Tensor, out: torch.Tensor,
                                dout: torch.Tensor, lse: torch.Tensor, causal: bool = True,
-                               scale: float = 0.0, dq=None, dv=None, workspace=None):
-    """(dq_routed, dv) of the keyless attention from dout and the forward's out, lse."""
+                               scale: float = 0.0, dq=None, dv=None, workspace=None, out_f32=None):
+    """(dq_routed, dv) of the keyless attention from dout and the forward's out, lse
+    (and its fp32 output, when kept)."""
     load()
     B, N, H, dk = q_routed.shape
     G = v.shape[2]
@@ -451,7 +453,8 @@ def keyless_attention_backward(q_routed: torch.Tensor, v: torch.Tensor, out: tor
     if workspace is None:
         n = int(_lib.keyless_attention_backward_workspace_size(B, N, H))
         workspace = torch.empty(max(n, 256), dtype=torch.uint8, device=q_routed.device)
-    _check(_lib.keyless_attention_backward(_ptr(q_routed), _ptr(v), _ptr(out), _ptr(dout), _ptr(lse),
+    _check(_lib.keyless_attention_backward(_ptr(q_routed), _ptr(v), _ptr(out), _ptr(out_f32),
+                                           _ptr(dout), _ptr(lse),
                                            B, N, H, G, dk, int(causal), scale, _dt(q_routed),
                                            _ptr(dq), _ptr(dv), _ptr(workspace), workspace.numel(),
                                            _stream(q_routed)))

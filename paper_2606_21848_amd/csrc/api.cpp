@@ -464,7 +464,8 @@ int check_cross_args(const char* who, const void* xb, int B, int N_b) {
 // sequences).
 int run_attention(const char* who, const void* qr, long q_stride, const void* vv, long v_stride,
                   void* out, int B, int N, int Nk, int H, int G, int d_head, int causal,
-                  float scale, kl_dtype dtype, hipStream_t st, float* lse = nullptr) {
+                  float scale, kl_dtype dtype, hipStream_t st, float* lse = nullptr,
+                  float* out_f32 = nullptr) {
   kl::AttnParams a{};
   a.q = qr;
   a.v = vv;
@@ -482,6 +483,7 @@ int run_attention(const char* who, const void* qr, long q_stride, const void* vv
   a.scale_log2 = scale_or_default(scale, d_head) * kLog2e;
   a.dtype = dtype;
   a.lse = lse;
+  a.out_f32 = out_f32;
   // No value rows (an empty X^(b)): the VALU kernel writes the zero rows.
   if (Nk > 0 && kl::attn_bf16_supported(a))
     return hip_status(kl::launch_prefill_attention(a, st), who);
@@ -733,15 +735,15 @@ int keyless_cross_attention(const void* xa, const void* xb, const void* W_Q, con
 
 int keyless_attention_forward(const void* q_routed, const void* v, int B, int N, int H, int G,
                               int d_head, int causal, float scale, kl_dtype dtype, void* out,
-                              float* lse, void* stream) {
+                              float* lse, float* out_f32, void* stream) {
   const char* who = "keyless_attention_forward";
   int s = check_prefill_args(who, q_routed, v, out, B, N, 64, H, G, d_head, dtype, scale);
   if (s != KL_OK) return s;
-  if (!aligned16(q_routed) || !aligned16(v) || !aligned16(out))
-    return fail(KL_ERR_INVALID_ARG, "%s: q_routed, v and out must be 16-byte aligned", who);
+  if (!aligned16(q_routed) || !aligned16(v) || !aligned16(out) || !aligned16(out_f32))
+    return fail(KL_ERR_INVALID_ARG, "%s: q_routed, v, out and out_f32 must be 16-byte aligned", who);
   if (B == 0 || N == 0) return KL_OK;
   return run_attention(who, q_routed, (long)H * d_head, v, (long)G * d_head, out, B, N, N, H, G,
-                       d_head, causal, scale, dtype, static_cast<hipStream_t>(stream), lse);
+                       d_head, causal, scale, dtype, static_cast<hipStream_t>(stream), lse, out_f32);
 }
 
 size_t keyless_attention_backward_workspace_size(int B, int N, int H) {
@@ -750,7 +752,8 @@ size_t keyless_attention_backward_workspace_size(int B, int N, int H) {
 }
 
 int keyless_attention_backward(const void* q_routed, const void* v, const void* out,
-                               const void* dout, const float* lse, int B, int N, int H, int G,
+                               const float* out_f32, const void* dout, const float* lse, int B,
+                               int N, int H, int G,
                                int d_head, int causal, float scale, kl_dtype dtype, void* dq_routed,
                                void* dv, void* ws, size_t ws_bytes, void* stream) {
   const char* who = "keyless_attention_backward";
@@ -769,6 +772,7 @@ int keyless_attention_backward(const void* q_routed, const void* v, const void* 
   p.q = q_routed;
   p.v = v;
   p.out = out;
+  p.out_f32 = out_f32;
   p.dout = dout;
   p.lse = lse;
   p.Dd = static_cast<float*>(ws);

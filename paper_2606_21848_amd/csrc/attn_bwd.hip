@@ -56,8 +56,9 @@ __device__ __forceinline__ void stx(T* p, size_t i, float v) {
   else p[i] = v;
 }
 
-// Dd[b, h, q] = sum_d dO[b, q, h, d] O[b, q, h, d]; 16 lanes per row.
-template <typename T, int D>
+// Dd[b, h, q] = sum_d dO[b, q, h, d] O[b, q, h, d]; 16 lanes per row. O is the
+// forward's fp32 output when given (TO = float, row stride H D), else `out`.
+template <typename TO, typename T, int D>
 __global__ __launch_bounds__(256) void bwd_prep_kernel(BwdParams p) {
   const long rows = (long)p.B * p.N * p.H;
   const long row = (long)blockIdx.x * 16 + threadIdx.x / 16;
@@ -69,7 +70,8 @@ __global__ __launch_bounds__(256) void bwd_prep_kernel(BwdParams p) {
     const long bq = row / p.H;
     b = (int)(bq / p.N);
     q = (int)(bq % p.N);
-    const T* o = reinterpret_cast<const T*>(p.out) + (size_t)bq * p.o_stride + (size_t)h * D;
+    const TO* o = p.out_f32 ? reinterpret_cast<const TO*>(p.out_f32) + ((size_t)bq * p.H + h) * D
+                            : reinterpret_cast<const TO*>(p.out) + (size_t)bq * p.o_stride + (size_t)h * D;
     const T* g = reinterpret_cast<const T*>(p.dout) + (size_t)bq * p.o_stride + (size_t)h * D;
 #pragma unroll
     for (int c = j; c < D; c += 16) s = fmaf(ldx(o, c), ldx(g, c), s);
@@ -167,7 +169,7 @@ __global__ __launch_bounds__(kThreads, 2) void bwd_dq_kernel(BwdParams p) {
       df[qb][ks] = __builtin_bit_cast(bf16x8_t, *reinterpret_cast<const u32x4*>(sd + ks * 32));
     }
     lse2[qb] = p.lse[((size_t)b * p.H + h) * p.N + qq] * kLog2e;
-    dd[qb] = 0.f;  // formed by the first sweep
+    dd[qb] = p.out_f32 ? p.Dd[((size_t)b * p.H + h) * p.N + qq] : 0.f;  // else the first sweep
   }
   f32x4_t acc[DB][QBD];
 #pragma unroll
@@ -199,8 +201,9 @@ __global__ __launch_bounds__(kThreads, 2) void bwd_dq_kernel(BwdParams p) {
   // fp32 (the definition, rather than rowsum(dO * O) from the rounded output,
   // whose rounding the subtraction dP - Dd would amplify) and writes it for the
   // dV kernel; the second forms dS and accumulates dQ~.
+  // With the forward's fp32 output, Dd comes from bwd_prep_kernel and one sweep does.
 #pragma unroll 1
-  for (int sweep = 0; sweep < 2; ++sweep) {
+  for (int sweep = p.out_f32 ? 1 : 0; sweep < 2; ++sweep) {
     if (sweep == 1) {
       // Every wave's reads of the first sweep's last stages have returned.
       asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
@@ -631,13 +634,17 @@ hipError_t launch_mfma(const BwdParams& p, hipStream_t st) {
   return hipGetLastError();
 }
 
-template <typename T>
-hipError_t launch_prep(const BwdParams& p, hipStream_t st) {
+template <typename TO, typename T>
+hipError_t launch_prep_t(const BwdParams& p, hipStream_t st) {
   const long rows = (long)p.B * p.N * p.H;
   const dim3 grid((unsigned)((rows + 15) / 16));
-  if (p.D == 128) hipLaunchKernelGGL((bwd_prep_kernel<T, 128>), grid, dim3(256), 0, st, p);
-  else hipLaunchKernelGGL((bwd_prep_kernel<T, 64>), grid, dim3(256), 0, st, p);
+  if (p.D == 128) hipLaunchKernelGGL((bwd_prep_kernel<TO, T, 128>), grid, dim3(256), 0, st, p);
+  else hipLaunchKernelGGL((bwd_prep_kernel<TO, T, 64>), grid, dim3(256), 0, st, p);
   return hipGetLastError();
+}
+template <typename T>
+hipError_t launch_prep(const BwdParams& p, hipStream_t st) {
+  return p.out_f32 ? launch_prep_t<float, T>(p, st) : launch_prep_t<T, T>(p, st);
 }
 
 }  // namespace
@@ -652,11 +659,14 @@ bool attn_bwd_mfma_supported(const BwdParams& p) {
 hipError_t launch_attention_backward(const BwdParams& p, hipStream_t st) {
   if (p.B == 0 || p.N == 0) return hipSuccess;
   if (p.D != 64 && p.D != 128) return hipErrorInvalidValue;
-  // The matrix-core dQ~ kernel forms Dd itself (exactly, from P and dP); the
-  // vector-ALU path takes it from the fp32 output.
-  if (attn_bwd_mfma_supported(p)) return p.D == 128 ? launch_mfma<128>(p, st) : launch_mfma<64>(p, st);
-  hipError_t e = p.dtype == KL_BF16 ? launch_prep<uint16_t>(p, st) : launch_prep<float>(p, st);
-  if (e != hipSuccess) return e;
+  // Dd: from the fp32 output when there is one (the prep kernel), else, on the
+  // matrix cores, from P and dP in the dQ~ kernel's first sweep.
+  const bool mfma = attn_bwd_mfma_supported(p);
+  if (!mfma || p.out_f32) {
+    hipError_t e = p.dtype == KL_BF16 ? launch_prep<uint16_t>(p, st) : launch_prep<float>(p, st);
+    if (e != hipSuccess) return e;
+  }
+  if (mfma) return p.D == 128 ? launch_mfma<128>(p, st) : launch_mfma<64>(p, st);
   if (p.dtype == KL_BF16)
     return p.D == 128 ? launch_simple<uint16_t, 128>(p, st) : launch_simple<uint16_t, 64>(p, st);
   return p.D == 128 ? launch_simple<float, 128>(p, st) : launch_simple<float, 64>(p, st);

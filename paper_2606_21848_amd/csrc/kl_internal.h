@@ -136,6 +136,7 @@ struct AttnParams {
   int Nk;          // value rows per sequence: N for self-attention, N_b for cross-attention
   int causal;      // only with Nk == N
   float* lse;      // [B, H, N] natural-log log-sum-exp of each row's scaled scores, or null
+  float* out_f32;  // [B, N, H, D] the output before rounding to the dtype, or null
   float scale_log2;
   kl_dtype dtype;
 };
@@ -163,6 +164,8 @@ struct BwdParams {
   const void* out;
   const void* dout;
   const float* lse;
+  const float* out_f32;  // [B, N, H, D] the forward's fp32 output, or null (then Dd is formed
+                         // from P and dP in a first sweep of the dQ~ kernel)
   float* Dd;
   void* dq;
   void* dv;

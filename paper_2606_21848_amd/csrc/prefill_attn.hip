@@ -311,6 +311,13 @@ __global__ __launch_bounds__(kThreads, QB == 2 ? 3 : 2) void attn_bf16_kernel(At
     const int q = q0 + qb * 16 + fr;
     if (p.lse && q < p.N && grp == 0)  // scores are in log2 units relative to m
       p.lse[((size_t)b * p.H + h) * p.N + q] = (m[qb] + __log2f(l)) * 0.69314718055994531f;
+    if (p.out_f32 && q < p.N) {
+      float* dst = p.out_f32 + (((size_t)b * p.N + q) * p.H + h) * D + grp * 4;
+#pragma unroll
+      for (int db = 0; db < DB; ++db)
+        *reinterpret_cast<f32x4_t*>(dst + db * 16) =
+            f32x4_t{o[db][qb][0] * inv, o[db][qb][1] * inv, o[db][qb][2] * inv, o[db][qb][3] * inv};
+    }
     if (q < p.N) {
       uint16_t* dst = O + ((size_t)b * p.N + q) * p.o_stride + (size_t)h * D + grp * 4;
 #pragma unroll

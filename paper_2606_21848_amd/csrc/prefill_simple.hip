@@ -126,6 +126,10 @@ __global__ __launch_bounds__(64) void attn_simple_kernel(AttnParams p) {
           l > 0.f ? (m + __log2f(l)) * 0.69314718055994531f : -INFINITY;
 #pragma unroll
     for (int c = 0; c < D; ++c) st(O, ((size_t)b * p.N + i) * p.o_stride + (size_t)h * D + c, acc[c] * inv);
+    if (p.out_f32) {
+#pragma unroll
+      for (int c = 0; c < D; ++c) p.out_f32[(((size_t)b * p.N + i) * p.H + h) * D + c] = acc[c] * inv;
+    }
   }
 }
 

@@ -54,15 +54,20 @@ def test_attention_forward_lse(lib, dtype, causal, B, N, H, G, dk):
     assert err <= (1e-4 if dtype == torch.float32 else 2e-2), f"lse error {err:.3e}"
 
 
+@pytest.mark.parametrize("keep_f32", [False, True])
 @pytest.mark.parametrize("dtype", [torch.float32, torch.bfloat16])
 @pytest.mark.parametrize("causal", [True, False])
 @pytest.mark.parametrize("B,N,H,G,dk", SHAPES)
-def test_attention_backward_matches_oracle(lib, dtype, causal, B, N, H, G, dk):
-    say(f"attention backward dtype={dtype} causal={causal} B={B} N={N} H={H} G={G} dk={dk}")
+def test_attention_backward_matches_oracle(lib, dtype, causal, B, N, H, G, dk, keep_f32):
+    """Both ways of forming rowsum(P * dP): from the forward's fp32 output
+    (keep_f32) and, without it, from P and dP in the dQ~ kernel."""
+    say(f"attention backward dtype={dtype} causal={causal} B={B} N={N} H={H} G={G} dk={dk} "
+        f"keep_f32={keep_f32}")
     Qr, V, dO = _qvd(B, N, H, G, dk, 72, dtype)
     q, v, g = Qr.to(DEV), V.to(DEV), dO.to(DEV)
-    out, lse = kb.keyless_attention_forward(q, v, causal=causal)
-    dq, dv = kb.keyless_attention_backward(q, v, out, g, lse, causal=causal)
+    o32 = torch.empty((B, N, H, dk), dtype=torch.float32, device=DEV) if keep_f32 else None
+    out, lse = kb.keyless_attention_forward(q, v, causal=causal, out_f32=o32)
+    dq, dv = kb.keyless_attention_backward(q, v, out, g, lse, causal=causal, out_f32=o32)
     torch.cuda.synchronize()
     ref_dq, ref_dv = K.keyless_attention_backward(to64(Qr), to64(V), to64(dO), H, G, dk,
                                                   causal=causal)
@@ -127,8 +132,9 @@ def test_backward_full_size_sampled(lib):
     rows anywhere and the dV rows of the last 48 positions against the oracle."""
     say("backward full size")
     c = configs.backward_bf16(device=DEV)
-    out, lse = kb.keyless_attention_forward(c["q"], c["v"])
-    dq, dv = kb.keyless_attention_backward(c["q"], c["v"], out, c["dout"], lse)
+    o32 = torch.empty(c["q"].shape, dtype=torch.float32, device=DEV)
+    out, lse = kb.keyless_attention_forward(c["q"], c["v"], out_f32=o32)
+    dq, dv = kb.keyless_attention_backward(c["q"], c["v"], out, c["dout"], lse, out_f32=o32)
     torch.cuda.synchronize()
     assert torch.isfinite(dq.float()).all() and torch.isfinite(dv.float()).all()
     N = c["N"]
