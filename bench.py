@@ -503,9 +503,8 @@ def extra_measurements(torch, kb, configs, dev):
                           "graph_ms": round(ms_g, 4),
                           "graph_tokens_per_s": round(la["B"] / (ms_g * 1e-3), 1),
                           "graph_cache_gbps": round(lbytes / (ms_g * 1e-3) / 1e9, 1),
-                          "note": "ms: eager calls back to back (host-launch bound: five "
-                                  "kernels per call); graph_ms: the call replayed from a "
-                                  "captured HIP graph"}
+                          "note": "ms: eager calls back to back (five kernels per call); "
+                                  "graph_ms: the same call replayed from a captured HIP graph"}
     del la, lvc, lws, lout
     # Head-to-head: keyless value-only vs standard K+V, same structure.
     hh = configs.head_to_head_bf16(device=dev)
