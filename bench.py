@@ -506,6 +506,22 @@ def extra_measurements(torch, kb, configs, dev):
                           "note": "ms: eager calls back to back (five kernels per call); "
                                   "graph_ms: the same call replayed from a captured HIP graph"}
     del la, lvc, lws, lout
+    # Batch-1 decode steps at the paper's context lengths (latency-bound).
+    b1 = {}
+    for L in (512, 2048, 8192):
+        c1 = configs.decode_b1_bf16(device=dev, L=L)
+        vc1 = kb.ValueCache(c1["V"])
+        ws1 = torch.empty(max(kb.decode_workspace_bytes(vc1, 1, c1["H"]), 256), dtype=torch.uint8,
+                          device=dev)
+        o1 = torch.empty_like(c1["q"])
+        us = batch_avg_ms(lambda i: kb.keyless_decode_append(c1["q"], c1["v_new"], vc1,
+                                                             c1["lengths_before"], out=o1,
+                                                             workspace=ws1), 200, torch) * 1e3
+        b1[str(L)] = {"step_us": round(us, 2), "tokens_per_s": round(1e6 / us, 1)}
+        del c1, vc1, ws1, o1
+    res["decode_b1_bf16"] = {"workload": "batch 1, 32 heads x 128, contiguous cache of 512 / 2048 "
+                                         "/ 8192 rows: one fused decode step (the attention part of "
+                                         "a layer's step)", "by_context": b1}
     # Head-to-head: keyless value-only vs standard K+V, same structure.
     hh = configs.head_to_head_bf16(device=dev)
     vcache, kcache = kb.ValueCache(hh["V"]), kb.ValueCache(hh["K"])

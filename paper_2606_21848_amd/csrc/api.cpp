@@ -90,6 +90,8 @@ int cache_capacity(const kl_value_cache* c) {
 //  - chunk_rows > 0: split mode with that many rows per split (grid S x G x B).
 //  - A contiguous cache with at least one (b, g) pair per compute unit: one
 //    workgroup per pair streams its whole cache and writes the output directly.
+//  - At most kSmallBatch sequences: split mode with splits sized from the
+//    capacity (see below).
 //  - Otherwise balanced mode: kBalancedWorkgroups workgroups (two per compute
 //    unit) take equal shares of the 16-row tiles of all pairs, whatever the
 //    spread of lengths, and a merge kernel combines pairs that were shared.
@@ -102,6 +104,8 @@ struct DecodePlan {
 
 constexpr int kComputeUnits = 256;
 constexpr int kBalancedWorkgroups = 2 * kComputeUnits;
+constexpr int kSmallBatch = 4;                        // sequences decoded with fixed splits
+constexpr long kSplitWorkgroups = 2 * kComputeUnits;  // their target split count
 
 DecodePlan plan_decode(const kl_value_cache* c, int B, int chunk_rows) {
   const int cap = cache_capacity(c);
@@ -112,6 +116,15 @@ DecodePlan plan_decode(const kl_value_cache* c, int B, int chunk_rows) {
     pl.chunk = chunk_rows;
   } else if (c->layout == KL_CONTIGUOUS && pairs >= kComputeUnits) {
     pl.chunk = ((cap > 0 ? cap : 1) + 63) / 64 * 64;
+  } else if (B <= kSmallBatch && cap > 0) {
+    // A few sequences (batch-1 serving): fixed splits, about kSplitWorkgroups
+    // of them over the whole capacity and at least 256 rows each; a cache of at
+    // most 1024 rows is one split (no merge). Splits past a sequence's length
+    // exit at once, so raggedness among so few sequences costs little, and no
+    // plan kernel runs.
+    const long per = (cap * pairs + kSplitWorkgroups - 1) / kSplitWorkgroups;
+    const long chunk = cap <= 1024 ? cap : std::max(256L, per);
+    pl.chunk = (int)((chunk + 63) / 64 * 64);
   } else if (pairs * ((long)cap + 15) / 16 < (1L << 30)) {
     pl.balanced = true;
     pl.chunk = 0;

@@ -346,3 +346,31 @@ def test_decode_append_full_size(lib):
     torch.cuda.synchronize()
     assert torch.equal(c["V"], base)
     assert_parity(a, to64(b), torch.bfloat16, "fused vs unfused")
+
+
+@pytest.mark.parametrize("H,G,d,dtype", [(8, 8, 128, torch.bfloat16), (32, 1, 128, torch.bfloat16),
+                                         (4, 2, 64, torch.float32)])
+@pytest.mark.parametrize("paged", [False, True])
+def test_small_batch_split_ragged(lib, H, G, d, dtype, paged):
+    """At most four sequences take fixed splits sized from the capacity (the
+    library's choice): a long sequence spans many splits, a short one leaves
+    most of its splits empty, an empty one gives zero rows."""
+    lengths = torch.tensor([5000, 37, 0, 1], dtype=torch.int32)
+    B, L = len(lengths), 5008
+    say(f"small-batch split H={H} G={G} d={d} dtype={dtype} paged={paged}")
+    cache = synth.normal((B, G, L, d), 19, 1, 1.0, dtype)
+    q = synth.normal((B, H, d), 19, 2, 1.0, dtype)
+    if paged:
+        data, table = _paged(cache, lengths, 16, 8)
+        vc = kb.ValueCache(data.to(DEV), table.to(DEV))
+        ref = K.keyless_decode(to64(q), to64(data), lengths.numpy(), H, G,
+                               block_table=table.numpy(), block_size=16)
+    else:
+        vc = kb.ValueCache(cache.to(DEV))
+        ref = K.keyless_decode(to64(q), to64(cache), lengths.numpy(), H, G)
+    ws = torch.full((max(kb.decode_workspace_bytes(vc, B, H), 256),), 0xFF, dtype=torch.uint8,
+                    device=DEV)
+    out = kb.keyless_decode(q.to(DEV), vc, lengths.to(DEV), workspace=ws)
+    torch.cuda.synchronize()
+    assert_parity(out, ref, dtype, "small-batch split")
+    assert torch.all(out.cpu()[2] == 0)

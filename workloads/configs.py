@@ -15,7 +15,7 @@ import torch
 from .synth import normal, permutation, uniform_int
 
 NAMES = ("tiny_fp32", "decode_bf16", "prefill_bf16", "paged_gqa_bf16", "head_to_head_bf16",
-         "decode_step_bf16", "cross_bf16", "latent_bf16", "backward_bf16")
+         "decode_step_bf16", "cross_bf16", "latent_bf16", "backward_bf16", "decode_b1_bf16")
 
 # Stream ids (one per drawn tensor).
 S_X, S_WQ, S_WR, S_WV, S_XNEXT, S_V, S_Q, S_K, S_LEN, S_PERM, S_VNEW, S_XB, S_WPOST, S_DO = range(14)
@@ -184,3 +184,16 @@ def backward_bf16(device="cpu", seed=8, B=1, N=8192, H=32, G=32, d_head=128):
         dout=normal((B, N, H, d_head), seed, S_DO, 1.0, f, device),
         B=B, N=N, H=H, G=G, d_head=d_head,
     )
+
+
+def decode_b1_bf16(device="cpu", seed=9, L=2048, H=32, d_head=128):
+    """Batch-1 decode at one context length (the setting of the paper's decode
+    throughput measurement: batch 1, contexts 512, 2048 and 8192): a contiguous
+    value-only cache [1, H, L, d_head] and routed queries [1, H, d_head] ~ N(0,1),
+    bf16; the step's new row is the cache's last row."""
+    f = torch.bfloat16
+    V = normal((1, H, L, d_head), seed, S_V, 1.0, f, device)
+    return dict(V=V, q=normal((1, H, d_head), seed, S_Q, 1.0, f, device),
+                v_new=V[:, :, L - 1].contiguous(),
+                lengths_before=torch.full((1,), L - 1, dtype=torch.int32, device=device),
+                H=H, L=L, d_head=d_head)
