@@ -56,6 +56,12 @@ def parse():
     ap.add_argument("--reduce-counters", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
                     help="reduce two rocprofv3 --pmc runs of --profile-pass (FETCH_SIZE, then "
                          "WRITE_SIZE) to the traffic summary JSON, printed to stdout")
+    ap.add_argument("--profile-prefill", action="store_true",
+                    help="run the prefill workload (weights packed once, then 3 calls) and "
+                         "print nothing else: the program for the prefill counter passes")
+    ap.add_argument("--reduce-mfma", nargs="+", metavar="PMC_DIR",
+                    help="summarise rocprofv3 --pmc runs of --profile-prefill (MfmaUtil, "
+                         "MfmaFlopsBF16, ...) per prefill kernel as markdown")
     ap.add_argument("--summarize-trace", metavar="TRACE_DIR",
                     help="print a markdown summary of a rocprofv3 --kernel-trace run of this script")
     return ap.parse_args()
@@ -227,6 +233,36 @@ def reduce_counters(fetch_dir, write_dir):
     print(json.dumps(out, indent=1))
 
 
+PREFILL_KERNELS = ("gemm_bf16_kernel", "attn_bf16_kernel")
+# Algorithmic FLOP per launch on the prefill workload (8192 tokens, d_model
+# 4096, 32 + 32 heads x 128): the projection 2 N d (H + G) d_k, the causal
+# attention 2 H d_k N (N + 1) (masked work not counted).
+PREFILL_FLOP = {"gemm_bf16_kernel": 2 * 8192 * 4096 * 64 * 128,
+                "attn_bf16_kernel": 2 * 32 * 128 * 8192 * 8193}
+
+
+def reduce_mfma(dirs):
+    """Per prefill kernel: the average of each counter over its dispatches, and
+    the executed MFMA FLOP against the algorithmic FLOP."""
+    vals = {}
+    for d in dirs:
+        for r in _csv_rows(d, "counter_collection.csv"):
+            k = next((n for n in PREFILL_KERNELS if n in r["Kernel_Name"]), None)
+            if k:
+                vals.setdefault((k, r["Counter_Name"]), []).append(float(r["Counter_Value"]))
+    print("| kernel | counter | average per dispatch | dispatches |")
+    print("|---|---|---|---|")
+    for (k, c), v in sorted(vals.items()):
+        print(f"| `{k}` | {c} | {sum(v) / len(v):.6g} | {len(v)} |")
+    print()
+    for k in PREFILL_KERNELS:
+        fl = vals.get((k, "MfmaFlopsBF16"))
+        if fl:
+            ex = sum(fl) / len(fl)
+            print(f"- `{k}`: executed MFMA FLOP per launch {ex:.4g}, algorithmic {PREFILL_FLOP[k]:.4g} "
+                  f"(ratio {ex / PREFILL_FLOP[k]:.3f})")
+
+
 def summarize_trace(trace_dir):
     """Markdown table of kernel durations from a rocprofv3 --kernel-trace run:
     per kernel name and grid, launches and average / min / max microseconds."""
@@ -274,6 +310,9 @@ def main():
     if args.reduce_counters:
         reduce_counters(*args.reduce_counters)
         return
+    if args.reduce_mfma:
+        reduce_mfma(args.reduce_mfma)
+        return
     if args.summarize_trace:
         summarize_trace(args.summarize_trace)
         return
@@ -288,6 +327,17 @@ def main():
     kb.load()
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
+
+    if args.profile_prefill:
+        p = configs.prefill_bf16(device=dev)
+        packed = kb.keyless_pack_weights(p["W_Q"], p["W_R"], p["W_V"], p["H"], p["G"])
+        outs = kb.keyless_prefill_packed(p["x"], packed, p["H"], p["G"], return_qv=True)
+        for _ in range(3):
+            kb.keyless_prefill_packed(p["x"], packed, p["H"], p["G"], out=outs[0],
+                                      q_routed_out=outs[1], v_out=outs[2])
+        torch.cuda.synchronize()
+        print("profile prefill done", flush=True)
+        return
 
     if args.profile_pass:
         src = torch.zeros(CALIB_BYTES // 4, dtype=torch.float32, device=dev)
