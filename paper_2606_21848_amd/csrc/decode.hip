@@ -306,7 +306,7 @@ __device__ __forceinline__ void append_and_stage(const DecodeParams& p, int b, i
     row = ((size_t)b * p.G + g) * p.L_max + pos;
   }
   if (ok && lane < CH)
-    reinterpret_cast<u32x4*>(const_cast<void*>(p.vdata))[row * CH + lane] = chunk;
+    reinterpret_cast<u32x4*>(p.vdata)[row * CH + lane] = chunk;
 }
 
 // Runs seg(b, g, row_begin, row_end, out) for every segment this workgroup owns.

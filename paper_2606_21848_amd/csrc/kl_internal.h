@@ -27,7 +27,7 @@ inline hipError_t set_max_lds(const void* fn, int bytes, std::atomic<uint32_t>& 
 
 struct DecodeParams {
   const void* q;          // [B, H, D]
-  const void* vdata;      // value cache data
+  void* vdata;            // value cache data (written only by a fused append)
   const void* kdata;      // key cache data (standard decode) or nullptr
   const int32_t* table;   // paged block table or nullptr
   const int32_t* lengths; // [B]: rows to decode, or rows before the step when vnew is set
