@@ -263,9 +263,12 @@ def reduce_mfma(dirs):
                   f"(ratio {ex / PREFILL_FLOP[k]:.3f})")
 
 
-def summarize_trace(trace_dir):
+def summarize_trace(trace_dir, steps, warmup):
     """Markdown table of kernel durations from a rocprofv3 --kernel-trace run:
-    per kernel name and grid, launches and average / min / max microseconds."""
+    per kernel name and grid, launches and average / min / max microseconds.
+    `steps` and `warmup` are those of the traced bench run: the decode step's
+    timed launches are the split kernel's launches warmup+1 .. warmup+steps at
+    the decode grid (other workloads can launch it at the same grid later)."""
     rows = _csv_rows(trace_dir, "kernel_trace.csv")
     groups = {}
     for r in rows:
@@ -281,6 +284,15 @@ def summarize_trace(trace_dir):
     for (name, grid), d in sorted(groups.items(), key=lambda kv: -sum(kv[1])):
         print(f"| `{name}` | {grid} | {len(d)} | {sum(d) / len(d):.2f} | {min(d):.2f} | "
               f"{max(d):.2f} |")
+    dec = sorted((r for r in rows if DECODE_KERNEL in r["Kernel_Name"] and
+                  _grid(r) == DECODE_GRID), key=lambda r: int(r["Start_Timestamp"]))
+    timed = [(int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3
+             for r in dec[warmup:warmup + steps]]
+    if timed:
+        print()
+        print(f"decode_bf16 step kernel, the {len(timed)} timed launches (the fused append and "
+              f"decode): avg {sum(timed) / len(timed):.2f} us, min {min(timed):.2f}, "
+              f"max {max(timed):.2f}")
     # Prefill-shaped calls: the projection GEMMs launched since the previous
     # attention launch, grouped by the attention grid (kernels of one grid can
     # serve two workloads, e.g. two GEMMs with the same tile count).
@@ -314,7 +326,7 @@ def main():
         reduce_mfma(args.reduce_mfma)
         return
     if args.summarize_trace:
-        summarize_trace(args.summarize_trace)
+        summarize_trace(args.summarize_trace, args.steps, args.warmup)
         return
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only (got --gpus {args.gpus}); "
