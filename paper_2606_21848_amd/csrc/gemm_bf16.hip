@@ -31,6 +31,10 @@ typedef __attribute__((address_space(3))) unsigned char lds_u8;
 constexpr int BM = 256, BN = 256, BK = 64;
 constexpr int kThreads = 512;
 constexpr int TILE_BYTES = 256 * BK * 2;  // one operand tile, 32 KiB
+static_assert(BK == 64, "the fragment schedule assumes two 32-wide k-steps per tile");
+// Instruction classes of __builtin_amdgcn_sched_group_barrier.
+constexpr int kSchedMfma = 0x008;
+constexpr int kSchedDsRead = 0x100;
 
 struct GemmParams2 {
   const uint16_t* A;   // [M, K]
@@ -105,25 +109,42 @@ void gemm_bf16_kernel(GemmParams2 p) {
     for (int j = 0; j < 4; ++j) acc[i][j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 
   const int fr = lane & 15, grp = lane >> 4;
+  // Both k-steps of a tile: every fragment read is issued up front (in order of
+  // first use), and the schedule pins the second k-step's reads between the
+  // first k-step's products, so no product waits on a read issued just before
+  // it (the compiler otherwise interleaves them one by one).
   auto compute = [&](const lds_u8* a, const lds_u8* w) {
+    bf16x8_t af[2][8], bf[2][4];
 #pragma unroll
     for (int ks = 0; ks < BK / 32; ++ks) {
       const int chunk = ks * 4 + grp;
-      bf16x8_t af[8], bf[4];
-#pragma unroll
-      for (int i = 0; i < 8; ++i)
-        af[i] = *reinterpret_cast<const __attribute__((address_space(3))) bf16x8_t*>(
-            a + swz(wm * 128 + i * 16 + fr, chunk));
+      af[ks][0] = *reinterpret_cast<const __attribute__((address_space(3))) bf16x8_t*>(
+          a + swz(wm * 128 + fr, chunk));
 #pragma unroll
       for (int j = 0; j < 4; ++j)
-        bf[j] = *reinterpret_cast<const __attribute__((address_space(3))) bf16x8_t*>(
+        bf[ks][j] = *reinterpret_cast<const __attribute__((address_space(3))) bf16x8_t*>(
             w + swz(wn * 64 + j * 16 + fr, chunk));
+#pragma unroll
+      for (int i = 1; i < 8; ++i)
+        af[ks][i] = *reinterpret_cast<const __attribute__((address_space(3))) bf16x8_t*>(
+            a + swz(wm * 128 + i * 16 + fr, chunk));
+    }
+#pragma unroll
+    for (int ks = 0; ks < BK / 32; ++ks)
 #pragma unroll
       for (int i = 0; i < 8; ++i)
 #pragma unroll
         for (int j = 0; j < 4; ++j)
-          acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[i], bf[j], acc[i][j], 0, 0, 0);
+          acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[ks][i], bf[ks][j], acc[i][j], 0, 0, 0);
+    // Groups in order: 12 reads (k-step 0), then 4 x (8 products of k-step 0,
+    // 3 reads of k-step 1), then the 32 products of k-step 1.
+    __builtin_amdgcn_sched_group_barrier(kSchedDsRead, 12, 0);
+#pragma unroll
+    for (int c = 0; c < 4; ++c) {
+      __builtin_amdgcn_sched_group_barrier(kSchedMfma, 8, 0);
+      __builtin_amdgcn_sched_group_barrier(kSchedDsRead, 3, 0);
     }
+    __builtin_amdgcn_sched_group_barrier(kSchedMfma, 32, 0);
   };
 
   lds_u8* const base = (lds_u8*)smem;

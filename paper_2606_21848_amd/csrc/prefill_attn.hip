@@ -43,6 +43,9 @@ constexpr int BQ = 4 * WQ;  // query rows per workgroup
 constexpr int BKV = 64;     // value rows per tile
 constexpr int NSTAGE = 3;   // value tiles in flight (the tile loop is unrolled by 3)
 constexpr int kThreads = 256;
+// Instruction classes of __builtin_amdgcn_sched_group_barrier.
+constexpr int kSchedMfma = 0x008;
+constexpr int kSchedDsRead = 0x100;
 
 // max(a, b, c); written for the compiler (not as inline assembly, which would
 // hide a read of a fresh MFMA result from its hazard checks), which forms
@@ -185,17 +188,39 @@ __global__ __launch_bounds__(kThreads, QB == 2 ? 3 : 2) void attn_bf16_kernel(At
 #pragma unroll
     for (int qb = 0; qb < QB; ++qb)
       init[qb] = FIRST ? f32x4_t{0.f, 0.f, 0.f, 0.f} : f32x4_t{-m[qb], -m[qb], -m[qb], -m[qb]};
+    // The fragments of block kb + 1 are read while the products of block kb
+    // run (two register sets); the schedule below pins that order, since the
+    // compiler otherwise issues each read just before its use and waits for it.
     f32x4_t sc[4][QB];
+    {
+      bf16x8_t sa[2][KS];
 #pragma unroll
-    for (int kb = 0; kb < 4; ++kb) {
+      for (int ks = 0; ks < KS; ++ks)
+        sa[0][ks] = *reinterpret_cast<const __attribute__((address_space(3))) bf16x8_t*>(tile + offS[ks]);
 #pragma unroll
-      for (int ks = 0; ks < KS; ++ks) {
-        const bf16x8_t a = *reinterpret_cast<const __attribute__((address_space(3))) bf16x8_t*>(
-            tile + offS[ks] + kb * 16 * T::ROW);
+      for (int kb = 0; kb < 4; ++kb) {
+        if (kb + 1 < 4) {
 #pragma unroll
-        for (int qb = 0; qb < QB; ++qb)
-          sc[kb][qb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, qf[qb][ks], ks == 0 ? init[qb] : sc[kb][qb], 0, 0, 0);
+          for (int ks = 0; ks < KS; ++ks)
+            sa[(kb + 1) & 1][ks] = *reinterpret_cast<const __attribute__((address_space(3))) bf16x8_t*>(
+                tile + offS[ks] + (kb + 1) * 16 * T::ROW);
+        }
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks)
+#pragma unroll
+          for (int qb = 0; qb < QB; ++qb)
+            sc[kb][qb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(sa[kb & 1][ks], qf[qb][ks],
+                                                                 ks == 0 ? init[qb] : sc[kb][qb], 0, 0, 0);
       }
+      // Groups in order: the reads of block 0, then (reads of block kb + 1,
+      // products of block kb) for kb < 3, then the products of block 3.
+      __builtin_amdgcn_sched_group_barrier(kSchedDsRead, KS, 0);
+#pragma unroll
+      for (int kb = 0; kb < 3; ++kb) {
+        __builtin_amdgcn_sched_group_barrier(kSchedDsRead, KS, 0);
+        __builtin_amdgcn_sched_group_barrier(kSchedMfma, KS * QB, 0);
+      }
+      __builtin_amdgcn_sched_group_barrier(kSchedMfma, KS * QB, 0);
     }
     // Lane holds scores of query q0 + 16 qb + fr against rows j0 + 16 kb + 4 grp + r.
     if ((p.causal && j0 + BKV - 1 > q0) || (j0 + BKV > p.Nk)) {
@@ -266,8 +291,10 @@ __global__ __launch_bounds__(kThreads, QB == 2 ? 3 : 2) void attn_bf16_kernel(At
     };
     // O^T[d][q] += V^T P^T over one k-step: the transposed read hands lane fr
     // the 4 rows of column 16 db + fr (rows 32 ks + 4 grp .., and 16 further
-    // for the high half); the all-ones operand adds the weight sums.
+    // for the high half); the all-ones operand adds the weight sums. All reads
+    // of the k-step are issued ahead of its products.
     auto pv = [&](const int ks) {
+      bf16x8_t av[DB];
 #pragma unroll
       for (int db = 0; db < DB; ++db) {
         const lds_u8* src = tile + offT[db] + ks * 32 * T::ROW;
@@ -275,18 +302,20 @@ __global__ __launch_bounds__(kThreads, QB == 2 ? 3 : 2) void attn_bf16_kernel(At
             (__attribute__((address_space(3))) s16x4*)(src));
         const s16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
             (__attribute__((address_space(3))) s16x4*)(src + 16 * T::ROW));
-        const bf16x8_t a = __builtin_bit_cast(bf16x8_t, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
+        av[db] = __builtin_bit_cast(bf16x8_t, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
+      }
+#pragma unroll
+      for (int db = 0; db < DB; ++db)
 #pragma unroll
         for (int qb = 0; qb < QB; ++qb)
-          o[db][qb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, pf[qb][ks], o[db][qb], 0, 0, 0);
-      }
+          o[db][qb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av[db], pf[qb][ks], o[db][qb], 0, 0, 0);
 #pragma unroll
       for (int qb = 0; qb < QB; ++qb)
         osum[qb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ones, pf[qb][ks], osum[qb], 0, 0, 0);
     };
     weights(0);
-    pv(0);
     weights(1);
+    pv(0);
     pv(1);
   };
 
