@@ -138,8 +138,10 @@ __global__ __launch_bounds__(kThreads, 2) void bwd_dq_kernel(BwdParams p) {
   constexpr int KS = D / 32, DB = D / 16;
   extern __shared__ __attribute__((aligned(1024))) unsigned char smem[];
   const int ntq = (p.N + BQD - 1) / BQD;
-  const int qt = p.causal ? (ntq - 1 - (int)blockIdx.x) : (int)blockIdx.x;
-  const int h = blockIdx.y, b = blockIdx.z;
+  // Heads fastest in the grid (heaviest causal tiles of every head first; each
+  // XCD, which runs workgroups i with i % 8 fixed, keeps whole heads).
+  const int qt = p.causal ? (ntq - 1 - (int)blockIdx.y) : (int)blockIdx.y;
+  const int h = blockIdx.x, b = blockIdx.z;
   const int g = h / (p.H / p.G);
   const int t = threadIdx.x, lane = t & 63;
   const int wave = __builtin_amdgcn_readfirstlane(t >> 6);
@@ -338,7 +340,9 @@ __global__ __launch_bounds__(kThreads, 2) void bwd_dv_kernel(BwdParams p) {
   using TL = AttnTile<D, kTileRows>;
   constexpr int KS = D / 32, DB = D / 16;
   extern __shared__ __attribute__((aligned(1024))) unsigned char smem[];
-  const int kvt = blockIdx.x, g = blockIdx.y, b = blockIdx.z;
+  // Groups fastest in the grid, as in the dQ~ kernel (value tile 0 is the
+  // heaviest under the causal mask).
+  const int kvt = blockIdx.y, g = blockIdx.x, b = blockIdx.z;
   const int R = p.H / p.G;
   const int t = threadIdx.x, lane = t & 63;
   const int wave = __builtin_amdgcn_readfirstlane(t >> 6);
@@ -625,11 +629,11 @@ hipError_t launch_simple(const BwdParams& p, hipStream_t st) {
 template <int D>
 hipError_t launch_mfma(const BwdParams& p, hipStream_t st) {
   using TL = AttnTile<D, kTileRows>;
-  hipLaunchKernelGGL(bwd_dq_kernel<D>, dim3((p.N + BQD - 1) / BQD, p.H, p.B), dim3(kThreads),
+  hipLaunchKernelGGL(bwd_dq_kernel<D>, dim3(p.H, (p.N + BQD - 1) / BQD, p.B), dim3(kThreads),
                      NSTAGE * TL::BYTES, st, p);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(bwd_dv_kernel<D>, dim3((p.N + BKVD - 1) / BKVD, p.G, p.B), dim3(kThreads),
+  hipLaunchKernelGGL(bwd_dv_kernel<D>, dim3(p.G, (p.N + BKVD - 1) / BKVD, p.B), dim3(kThreads),
                      4 * TL::BYTES, st, p);
   return hipGetLastError();
 }

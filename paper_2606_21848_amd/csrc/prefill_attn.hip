@@ -20,7 +20,7 @@
 // The tile's 16-byte chunks are XOR-swizzled per row so that both the score
 // reads (16 rows, one chunk) and the transposed reads (8 rows, two chunks per
 // pass) hit distinct LDS banks. Causal work grows with the query tile, so the
-// last tiles are scheduled first.
+// last tiles are scheduled first, for all heads before any lighter tile.
 
 #include <type_traits>
 
@@ -63,8 +63,12 @@ __global__ __launch_bounds__(kThreads, QB == 2 ? 3 : 2) void attn_bf16_kernel(At
   extern __shared__ __attribute__((aligned(1024))) unsigned char smem[];  // NSTAGE tiles
 
   const int ntq = (p.N + BQ - 1) / BQ;
-  const int qt = p.causal ? (ntq - 1 - (int)blockIdx.x) : (int)blockIdx.x;
-  const int h = blockIdx.y, b = blockIdx.z;
+  // Heads vary fastest in the grid: workgroups are dispatched in linear-id
+  // order, so every head's heaviest (causal) query tile starts first, and
+  // workgroup i runs on XCD i % 8, so each XCD keeps whole heads' values in
+  // its own L2.
+  const int qt = p.causal ? (ntq - 1 - (int)blockIdx.y) : (int)blockIdx.y;
+  const int h = blockIdx.x, b = blockIdx.z;
   const int g = h / (p.H / p.G);
   const int t = threadIdx.x, lane = t & 63;
   const int wave = __builtin_amdgcn_readfirstlane(t >> 6);
@@ -361,7 +365,7 @@ __global__ __launch_bounds__(kThreads, QB == 2 ? 3 : 2) void attn_bf16_kernel(At
 
 template <int D>
 hipError_t launch_attn(const AttnParams& p, hipStream_t st) {
-  dim3 grid((p.N + BQ - 1) / BQ, p.H, p.B);
+  dim3 grid(p.H, (p.N + BQ - 1) / BQ, p.B);
   hipLaunchKernelGGL(attn_bf16_kernel<D>, grid, dim3(kThreads), NSTAGE * Tile<D>::BYTES, st, p);
   return hipGetLastError();
 }
