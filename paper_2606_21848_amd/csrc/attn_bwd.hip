@@ -43,6 +43,9 @@ typedef __attribute__((address_space(3))) unsigned char lds_u8;
 
 constexpr int kThreads = 256;
 constexpr int kTileRows = 64;   // rows per staged tile
+// Instruction classes of __builtin_amdgcn_sched_group_barrier.
+constexpr int kSchedMfma = 0x008;
+constexpr int kSchedDsRead = 0x100;
 constexpr float kLog2e = 1.4426950408889634f;
 
 template <typename T>
@@ -187,15 +190,7 @@ __global__ __launch_bounds__(kThreads, 2) void bwd_dq_kernel(BwdParams p) {
     cp.issue(gV + (size_t)b * p.N * vrow, vrow, (uint32_t)(g * D * 2), jt * kTileRows, p.N, wave,
              lane, lds0 + stage * TL::BYTES);
   };
-  int offS[KS];
-#pragma unroll
-  for (int ks = 0; ks < KS; ++ks) offS[ks] = TL::off(fr, ks * 4 + grp);
-  int offT[DB];
-#pragma unroll
-  for (int db = 0; db < DB; ++db) {
-    const int col = db * 16 + (fr & 3) * 4;
-    offT[db] = TL::off(grp * 4 + (fr >> 2), col >> 3) + (col & 7) * 2;
-  }
+  const FragOffsets<D> fo(fr, grp);
   const int last_row = p.causal ? min(qt * BQD + BQD, p.N) : p.N;
   const int ntiles = (last_row + kTileRows - 1) / kTileRows;
 
@@ -242,18 +237,31 @@ __global__ __launch_bounds__(kThreads, 2) void bwd_dq_kernel(BwdParams p) {
             sc[hh][qb] = f32x4_t{0.f, 0.f, 0.f, 0.f};
             dp[hh][qb] = f32x4_t{0.f, 0.f, 0.f, 0.f};
           }
+        // Both blocks' value fragments are read up front; the schedule puts the
+        // second block's reads between the first block's products.
+        bf16x8_t va[2][KS];
 #pragma unroll
         for (int hh = 0; hh < 2; ++hh)
 #pragma unroll
-          for (int kd = 0; kd < KS; ++kd) {
-            const bf16x8_t a = *reinterpret_cast<const __attribute__((address_space(3))) bf16x8_t*>(
-                tile + offS[kd] + (2 * ks + hh) * 16 * TL::ROW);
+          for (int kd = 0; kd < KS; ++kd)
+            va[hh][kd] = *reinterpret_cast<const __attribute__((address_space(3))) bf16x8_t*>(
+                tile + fo.s(kd) + (2 * ks + hh) * 16 * TL::ROW);
+#pragma unroll
+        for (int hh = 0; hh < 2; ++hh)
+#pragma unroll
+          for (int kd = 0; kd < KS; ++kd)
 #pragma unroll
             for (int qb = 0; qb < QBD; ++qb) {
-              sc[hh][qb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, qf[qb][kd], sc[hh][qb], 0, 0, 0);
-              dp[hh][qb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, df[qb][kd], dp[hh][qb], 0, 0, 0);
+              sc[hh][qb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(va[hh][kd], qf[qb][kd], sc[hh][qb], 0, 0, 0);
+              dp[hh][qb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(va[hh][kd], df[qb][kd], dp[hh][qb], 0, 0, 0);
             }
-          }
+        __builtin_amdgcn_sched_group_barrier(kSchedDsRead, KS, 0);
+#pragma unroll
+        for (int kd = 0; kd < KS; ++kd) {
+          __builtin_amdgcn_sched_group_barrier(kSchedMfma, 2 * QBD, 0);
+          __builtin_amdgcn_sched_group_barrier(kSchedDsRead, 1, 0);
+        }
+        __builtin_amdgcn_sched_group_barrier(kSchedMfma, 2 * QBD * KS, 0);
         // Lane: rows j0 + 16 (2 ks + hh) + 4 grp + r of query q0 + 16 qb + fr.
         auto weight = [&](int hh, int qb, int r) {
           float pr = fast_exp2(sc[hh][qb][r] - lse2[qb]);
@@ -289,7 +297,7 @@ __global__ __launch_bounds__(kThreads, 2) void bwd_dq_kernel(BwdParams p) {
         }
 #pragma unroll
         for (int db = 0; db < DB; ++db) {
-          const lds_u8* src = tile + offT[db] + ks * 32 * TL::ROW;
+          const lds_u8* src = tile + fo.t(db) + ks * 32 * TL::ROW;
           const s16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
               (__attribute__((address_space(3))) s16x4*)(src));
           const s16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
@@ -386,29 +394,53 @@ __global__ __launch_bounds__(kThreads, 2) void bwd_dv_kernel(BwdParams p) {
     cp.issue(gD + (size_t)b * p.N * drow, drow, (uint32_t)(h * D * 2), qt * kTileRows, p.N, wave,
              lane, st + TL::BYTES);
   };
-  int offS[KS];
-#pragma unroll
-  for (int ks = 0; ks < KS; ++ks) offS[ks] = TL::off(fr, ks * 4 + grp);
-  int offT[DB];
-#pragma unroll
-  for (int db = 0; db < DB; ++db) {
-    const int col = db * 16 + (fr & 3) * 4;
-    offT[db] = TL::off(grp * 4 + (fr >> 2), col >> 3) + (col & 7) * 2;
-  }
+  const FragOffsets<D> fo(fr, grp);
 
-  if (items > 0) issue(0);
+  // The log-sum-exp and Dd of an item's query rows (lane: rows 16 qb + 4 grp + r
+  // of the tile) are loaded one item ahead, after that item's tile copies, and
+  // moved into working registers at the top of the item, right after the wait
+  // that covers both. Loaded where they are used, they would make the compiler
+  // wait for every load in flight, which includes the next item's tile copies
+  // (issued as inline assembly, which it does not count).
+  float lsen[4][4], ddn[4][4];
+  auto prefetch = [&](int it) {
+    const int h = g * R + it / per_head, qt = qt0 + it % per_head;
+    const float* lse = p.lse + ((size_t)b * p.H + h) * p.N;
+    const float* ddv = p.Dd + ((size_t)b * p.H + h) * p.N;
+#pragma unroll
+    for (int qb = 0; qb < 4; ++qb)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int q = min(qt * kTileRows + qb * 16 + grp * 4 + r, p.N - 1);
+        lsen[qb][r] = lse[q];
+        ddn[qb][r] = ddv[q];
+      }
+  };
+  if (items > 0) {
+    issue(0);
+    prefetch(0);
+  }
   for (int it = 0; it < items; ++it) {
     KL_WAIT_VMCNT(0);
     asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
     __syncthreads();
-    if (it + 1 < items) issue(it + 1);
-    const int h = g * R + it / per_head, qt = qt0 + it % per_head;
+    float l2c[4][4], ddc[4][4];
+#pragma unroll
+    for (int qb = 0; qb < 4; ++qb)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        asm volatile("v_mul_f32 %0, %1, %2" : "=v"(l2c[qb][r]) : "v"(kLog2e), "v"(lsen[qb][r]));
+        asm volatile("v_mov_b32 %0, %1" : "=v"(ddc[qb][r]) : "v"(ddn[qb][r]));
+      }
+    if (it + 1 < items) {
+      issue(it + 1);
+      prefetch(it + 1);
+    }
+    const int qt = qt0 + it % per_head;
     const int q0 = qt * kTileRows;
     if (p.causal && q0 + kTileRows - 1 < kv0) continue;  // every row of the tile is before ours
     const lds_u8* tq = (const lds_u8*)smem + (it & 1) * 2 * TL::BYTES;
     const lds_u8* td = tq + TL::BYTES;
-    const float* lse = p.lse + ((size_t)b * p.H + h) * p.N;
-    const float* ddv = p.Dd + ((size_t)b * p.H + h) * p.N;
     const bool edge = (p.causal && q0 < kv0 + 16 * KVB - 1) || (q0 + kTileRows > p.N);
     // Two 32-row query steps; each is one K = 32 step of the dV products.
 #pragma unroll
@@ -424,26 +456,34 @@ __global__ __launch_bounds__(kThreads, 2) void bwd_dv_kernel(BwdParams p) {
           sc[kb] = f32x4_t{0.f, 0.f, 0.f, 0.f};
           dp[kb] = f32x4_t{0.f, 0.f, 0.f, 0.f};
         }
+        // Reads run two k-steps ahead of the products (fenced, order pinned).
+        __builtin_amdgcn_sched_barrier(0);
+        bf16x8_t aq[KS], ad[KS];
 #pragma unroll
         for (int ks = 0; ks < KS; ++ks) {
-          const bf16x8_t aq = *reinterpret_cast<const __attribute__((address_space(3))) bf16x8_t*>(
-              tq + offS[ks] + qb * 16 * TL::ROW);
-          const bf16x8_t ad = *reinterpret_cast<const __attribute__((address_space(3))) bf16x8_t*>(
-              td + offS[ks] + qb * 16 * TL::ROW);
+          aq[ks] = *reinterpret_cast<const __attribute__((address_space(3))) bf16x8_t*>(
+              tq + fo.s(ks) + qb * 16 * TL::ROW);
+          ad[ks] = *reinterpret_cast<const __attribute__((address_space(3))) bf16x8_t*>(
+              td + fo.s(ks) + qb * 16 * TL::ROW);
+        }
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks)
 #pragma unroll
           for (int kb = 0; kb < KVB; ++kb) {
-            sc[kb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(aq, vf[kb][ks], sc[kb], 0, 0, 0);
-            dp[kb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ad, vf[kb][ks], dp[kb], 0, 0, 0);
+            sc[kb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(aq[ks], vf[kb][ks], sc[kb], 0, 0, 0);
+            dp[kb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ad[ks], vf[kb][ks], dp[kb], 0, 0, 0);
           }
-        }
-        // Lane: query rows q0 + 16 qb + 4 grp + r against value row kv0 + 16 kb + fr.
-        float l2[4], dq[4];
+        __builtin_amdgcn_sched_group_barrier(kSchedDsRead, 4, 0);
 #pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          const int q = min(q0 + qb * 16 + grp * 4 + r, p.N - 1);
-          l2[r] = lse[q] * kLog2e;
-          dq[r] = ddv[q];
+        for (int ks = 0; ks + 2 < KS; ++ks) {
+          __builtin_amdgcn_sched_group_barrier(kSchedMfma, 2 * KVB, 0);
+          __builtin_amdgcn_sched_group_barrier(kSchedDsRead, 2, 0);
         }
+        __builtin_amdgcn_sched_group_barrier(kSchedMfma, 4 * KVB, 0);
+        __builtin_amdgcn_sched_barrier(0);
+        // Lane: query rows q0 + 16 qb + 4 grp + r against value row kv0 + 16 kb + fr.
+        const float* l2 = l2c[qb];
+        const float* dq = ddc[qb];
 #pragma unroll
         for (int kb = 0; kb < KVB; ++kb) {
           const int kv = kv0 + kb * 16 + fr;
@@ -469,21 +509,39 @@ __global__ __launch_bounds__(kThreads, 2) void bwd_dv_kernel(BwdParams p) {
         ps[kb] = __builtin_bit_cast(bf16x8_t, wsv[kb]);
       }
       // dV^T[d][kv] += dO^T P + Q~^T (tau dS) over query rows 32 qs + {4 grp .., 16 + 4 grp ..}.
-#pragma unroll
-      for (int db = 0; db < DB; ++db) {
-        const int o = offT[db] + qs * 32 * TL::ROW;
+      // Transposed reads run two column blocks ahead of the products.
+      auto rd = [&](const int db, bf16x8_t& ad, bf16x8_t& aq) {
+        const int o = fo.t(db) + qs * 32 * TL::ROW;
         const s16x4 dlo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) s16x4*)(td + o));
         const s16x4 dhi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) s16x4*)(td + o + 16 * TL::ROW));
         const s16x4 qlo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) s16x4*)(tq + o));
         const s16x4 qhi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) s16x4*)(tq + o + 16 * TL::ROW));
-        const bf16x8_t ad = __builtin_bit_cast(bf16x8_t, __builtin_shufflevector(dlo, dhi, 0, 1, 2, 3, 4, 5, 6, 7));
-        const bf16x8_t aq = __builtin_bit_cast(bf16x8_t, __builtin_shufflevector(qlo, qhi, 0, 1, 2, 3, 4, 5, 6, 7));
+        ad = __builtin_bit_cast(bf16x8_t, __builtin_shufflevector(dlo, dhi, 0, 1, 2, 3, 4, 5, 6, 7));
+        aq = __builtin_bit_cast(bf16x8_t, __builtin_shufflevector(qlo, qhi, 0, 1, 2, 3, 4, 5, 6, 7));
+      };
+      // The block is fenced (nothing moves across the fences) and its order
+      // pinned: reads of blocks 0 and 1, then (products of db, reads of db + 2).
+      __builtin_amdgcn_sched_barrier(0);
+      bf16x8_t ad[DB], aq[DB];
+      rd(0, ad[0], aq[0]);
+      rd(1, ad[1], aq[1]);
+#pragma unroll
+      for (int db = 0; db < DB; ++db) {
+        if (db + 2 < DB) rd(db + 2, ad[db + 2], aq[db + 2]);
 #pragma unroll
         for (int kb = 0; kb < KVB; ++kb) {
-          acc[db][kb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ad, pp[kb], acc[db][kb], 0, 0, 0);
-          acc[db][kb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(aq, ps[kb], acc[db][kb], 0, 0, 0);
+          acc[db][kb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ad[db], pp[kb], acc[db][kb], 0, 0, 0);
+          acc[db][kb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(aq[db], ps[kb], acc[db][kb], 0, 0, 0);
         }
       }
+      __builtin_amdgcn_sched_group_barrier(kSchedDsRead, 8, 0);
+#pragma unroll
+      for (int db = 0; db + 2 < DB; ++db) {
+        __builtin_amdgcn_sched_group_barrier(kSchedMfma, 2 * KVB, 0);
+        __builtin_amdgcn_sched_group_barrier(kSchedDsRead, 4, 0);
+      }
+      __builtin_amdgcn_sched_group_barrier(kSchedMfma, 4 * KVB, 0);
+      __builtin_amdgcn_sched_barrier(0);
     }
   }
 
