@@ -221,7 +221,8 @@ __global__ __launch_bounds__(kThreads, 2) void bwd_dq_kernel(BwdParams p) {
       __syncthreads();
       if (jt + NSTAGE - 1 < ntiles) issue(jt + NSTAGE - 1, (jt + NSTAGE - 1) % NSTAGE);
       const int j0 = jt * kTileRows;
-      if (p.causal && j0 > q0 + 16 * QBD - 1) continue;  // above this wave's diagonal
+      // Above this wave's diagonal, or rows all past the end (a ragged last tile).
+      if (q0 >= p.N || (p.causal && j0 > q0 + 16 * QBD - 1)) continue;
       const lds_u8* tile = (const lds_u8*)smem + stage * TL::BYTES;
 
       const bool edge = (p.causal && j0 + kTileRows - 1 > q0) || (j0 + kTileRows > p.N);

@@ -183,8 +183,10 @@ __global__ __launch_bounds__(kThreads, QB == 2 ? 3 : 2) void attn_bf16_kernel(At
     __syncthreads();
     if (jt + NSTAGE - 1 < ntiles) issue(jt + NSTAGE - 1, (STAGE + NSTAGE - 1) % NSTAGE);
     const int j0 = jt * BKV;
-    // Skip tiles entirely above the diagonal for this wave (never the first).
-    if (!FIRST && p.causal && j0 > q0 + WQ - 1) return;
+    // Skip tiles entirely above the diagonal for this wave (never the first),
+    // and every tile for a wave whose rows all lie past the end (a ragged last
+    // query tile): such a wave still copies and meets the barriers.
+    if (q0 >= p.N || (!FIRST && p.causal && j0 > q0 + WQ - 1)) return;
     const lds_u8* tile = (const lds_u8*)smem + STAGE * T::BYTES;
 
     // S^T[kv][q] - m[q] for kv blocks kb (16 rows) and query blocks qb.
