@@ -374,3 +374,22 @@ def test_small_batch_split_ragged(lib, H, G, d, dtype, paged):
     torch.cuda.synchronize()
     assert_parity(out, ref, dtype, "small-batch split")
     assert torch.all(out.cpu()[2] == 0)
+
+
+@pytest.mark.parametrize("H,G", [(1, 1), (8, 1)])
+def test_long_context_most_splits(lib, H, G):
+    """One sequence of 524,251 rows in a 524,288-row cache: the fixed split takes
+    its largest count (512 splits of 1024 rows, the last one ragged), which the
+    merge then combines; one value group, alone or shared by eight heads."""
+    L, n = 524288, 524288 - 37
+    say(f"long context L={L} n={n} H={H} G={G}")
+    cache = synth.normal((1, G, L, 128), 23, 1)
+    q = synth.normal((1, H, 128), 23, 2)
+    lengths = torch.tensor([n], dtype=torch.int32)
+    vc = kb.ValueCache(cache.to(DEV))
+    ws = torch.full((max(kb.decode_workspace_bytes(vc, 1, H), 256),), 0xFF, dtype=torch.uint8,
+                    device=DEV)
+    out = kb.keyless_decode(q.to(DEV), vc, lengths.to(DEV), workspace=ws)
+    torch.cuda.synchronize()
+    ref = K.keyless_decode(to64(q), to64(cache), lengths.numpy(), H, G)
+    assert_parity(out, ref, torch.bfloat16, "long context")

@@ -22,9 +22,10 @@ def _weights(d, H, G, dk, seed):
 
 
 # B past 16 takes a second row of workgroups; d = 160 leaves most waves without
-# a k-step; d = 8192 gives every wave two chunks of k-steps.
+# a k-step; d = 8192 gives every wave two chunks of k-steps; d = 16384 is the
+# largest d_model the kernel takes (four chunks per wave).
 CASES = [(1, 256, 4, 4, 128), (3, 512, 8, 2, 64), (8, 4096, 4, 4, 128), (16, 1024, 4, 1, 128),
-         (20, 2048, 8, 2, 128), (5, 160, 2, 2, 64), (2, 8192, 2, 1, 128)]
+         (20, 2048, 8, 2, 128), (5, 160, 2, 2, 64), (2, 8192, 2, 1, 128), (3, 16384, 2, 1, 128)]
 
 
 @pytest.mark.parametrize("B,d,H,G,dk", CASES)
