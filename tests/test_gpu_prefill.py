@@ -154,3 +154,25 @@ def test_prefill_bf16_full_size_sampled(lib):
     assert_parity(v[0], Vref, torch.bfloat16, "values")
     assert_parity(out[0, rows], Orows, torch.bfloat16, "sampled rows")
     assert torch.isfinite(out.float()).all()
+
+
+def test_prefill_long_sequence_sampled(lib):
+    """32,768 tokens (4x the measured workload's length: 171 causal query tiles of
+    the attention kernel, 512 value tiles for the last ones), d_model 256, 4 query
+    heads on 2 value groups: 40 sampled rows, the first and the last included,
+    against the oracle, and all of V."""
+    N, d, H, G, dk = 32768, 256, 4, 2, 128
+    say(f"prefill long sequence N={N} d={d} H={H} G={G} dk={dk}")
+    x = synth.normal((1, N, d), 61, 1)
+    W_Q = synth.normal((d, H * dk), 61, 2, d ** -0.5)
+    W_R = synth.normal((H, dk, dk), 61, 3, dk ** -0.5)
+    W_V = synth.normal((d, G * dk), 61, 4, d ** -0.5)
+    packed = kb.keyless_pack_weights(W_Q.to(DEV), W_R.to(DEV), W_V.to(DEV), H, G)
+    out, qr, v = kb.keyless_prefill_packed(x.to(DEV), packed, H, G, return_qv=True)
+    torch.cuda.synchronize()
+    rows = sorted(set([0, 1, N - 1] + synth.uniform_int(37, 2, N - 2, 61, 50).tolist()))
+    Wt_ref = K.fold_routing(to64(W_Q), to64(W_R), H, dk)
+    Orows, Vref = K.keyless_prefill_rows(to64(x), Wt_ref, to64(W_V), rows, H, G, dk)
+    assert_parity(v[0], Vref, torch.bfloat16, "values")
+    assert_parity(out[0, rows], Orows, torch.bfloat16, "sampled rows")
+    assert torch.isfinite(out.float()).all()
