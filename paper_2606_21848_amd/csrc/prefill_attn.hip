@@ -147,17 +147,15 @@ __global__ __launch_bounds__(kThreads, QB == 2 ? 3 : 2) void attn_bf16_kernel(At
     }
   };
 
-  // Per-lane LDS byte offsets inside a tile. The swizzle of a row depends only
-  // on the lane here, so the block, step and stage offsets are immediates.
-  int offS[KS];  // score operand: row fr, chunk 4 ks + grp (+ 16 kb rows)
-#pragma unroll
-  for (int ks = 0; ks < KS; ++ks) offS[ks] = T::off(fr, ks * 4 + grp);
-  int offT[DB];  // transposed operand: row 4 grp + fr / 4, columns 16 db + 4 (fr % 4)
-#pragma unroll
-  for (int db = 0; db < DB; ++db) {
-    const int col = db * 16 + (fr & 3) * 4;
-    offT[db] = T::off(grp * 4 + (fr >> 2), col >> 3) + (col & 7) * 2;
-  }
+  // Per-lane LDS byte offsets inside a tile, formed at each use from two
+  // registers per read kind (score operand: row fr, chunk 4 ks + grp, + 16 kb
+  // rows; transposed operand: row 4 grp + fr / 4, columns 16 db + 4 (fr % 4)).
+  // The swizzle of a row depends only on the lane here, so the block, step and
+  // stage offsets are immediates. As a table of KS + DB registers they pushed
+  // the kernel past its register budget, and the spilled entry's reload inside
+  // the tile loop came with a wait for every load in flight, the next tiles'
+  // copies included.
+  const FragOffsets<D> fo(fr, grp);
 
   const int last_row = p.causal ? min(qt * BQ + BQ, p.Nk) : p.Nk;
   const int ntiles = (last_row + BKV - 1) / BKV;
@@ -199,6 +197,9 @@ __global__ __launch_bounds__(kThreads, QB == 2 ? 3 : 2) void attn_bf16_kernel(At
     // compiler otherwise issues each read just before its use and waits for it.
     f32x4_t sc[4][QB];
     {
+      int offS[KS];
+#pragma unroll
+      for (int ks = 0; ks < KS; ++ks) offS[ks] = fo.s(ks);
       bf16x8_t sa[2][KS];
 #pragma unroll
       for (int ks = 0; ks < KS; ++ks)
@@ -303,7 +304,7 @@ __global__ __launch_bounds__(kThreads, QB == 2 ? 3 : 2) void attn_bf16_kernel(At
       bf16x8_t av[DB];
 #pragma unroll
       for (int db = 0; db < DB; ++db) {
-        const lds_u8* src = tile + offT[db] + ks * 32 * T::ROW;
+        const lds_u8* src = tile + fo.t(db) + ks * 32 * T::ROW;
         const s16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
             (__attribute__((address_space(3))) s16x4*)(src));
         const s16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
