@@ -458,7 +458,7 @@ def extra_measurements(torch, kb, configs, dev):
     def pstep(i):
         kb.keyless_prefill_packed(x, packed, H, G, out=outs[0], q_routed_out=outs[1],
                                   v_out=outs[2])
-    ms = timed_steps(pstep, 10, 3, torch)
+    ms = timed_steps(pstep, 20, 20, torch)
     flops = 2 * N * dm * (H + G) * dk + 2 * H * dk * N * (N + 1)
     res["prefill_bf16"] = {"workload": "batch 1, 8192 tokens, d_model 4096, 32 heads x 128, causal",
                            "ms": round(ms, 3), "tflops": round(flops / (ms * 1e-3) / 1e12, 2),
@@ -474,7 +474,7 @@ def extra_measurements(torch, kb, configs, dev):
     def cstep(i):
         kb.keyless_cross_attention_packed(c["xa"], c["xb"], packed, H, G, out=outs[0],
                                           q_routed_out=outs[1], v_out=outs[2])
-    ms = timed_steps(cstep, 10, 3, torch)
+    ms = timed_steps(cstep, 20, 20, torch)
     flops = 2 * B * dm * dk * (Na * H + Nb * G) + 4 * B * H * Na * Nb * dk
     res["cross_bf16"] = {"workload": "batch 4, 1024 attending x 4096 attended tokens, d_model "
                                      "4096, 32 heads x 128, no mask",

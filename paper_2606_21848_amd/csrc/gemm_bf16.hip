@@ -18,6 +18,8 @@
 // Workgroup ids are remapped so each XCD owns a band of tile rows walked
 // column-major, which keeps concurrently running tiles in that XCD's L2.
 
+#include <type_traits>
+
 #include "kl_device.h"
 #include "kl_internal.h"
 
@@ -171,27 +173,34 @@ void gemm_bf16_kernel(GemmParams2 p) {
   }
 
   // Lane holds C[row 16 i + 4 grp + r][col 16 j + fr] of the wave's 128 x 64 block.
+  // A tile whose rows all exist stores without a per-element row check.
+  auto store = [&](auto check_rows) {
+    constexpr bool CHECK = decltype(check_rows)::value;
 #pragma unroll
-  for (int j = 0; j < 4; ++j) {
-    const int col = n0 + wn * 64 + j * 16 + fr;
-    if (col >= p.N) continue;
-    uint16_t* dst;
-    long ldc;
-    if (col < p.n_split) {
-      dst = p.C0 + col;
-      ldc = p.ldc0;
-    } else {
-      dst = p.C1 + (col - p.n_split);
-      ldc = p.ldc1;
-    }
-#pragma unroll
-    for (int i = 0; i < 8; ++i)
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int row = m0 + wm * 128 + i * 16 + grp * 4 + r;
-        if (row < p.M) dst[(size_t)row * ldc] = __builtin_bit_cast(uint16_t, (__bf16)acc[i][j][r]);
+    for (int j = 0; j < 4; ++j) {
+      const int col = n0 + wn * 64 + j * 16 + fr;
+      if (col >= p.N) continue;
+      uint16_t* dst;
+      long ldc;
+      if (col < p.n_split) {
+        dst = p.C0 + col;
+        ldc = p.ldc0;
+      } else {
+        dst = p.C1 + (col - p.n_split);
+        ldc = p.ldc1;
       }
-  }
+#pragma unroll
+      for (int i = 0; i < 8; ++i)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int row = m0 + wm * 128 + i * 16 + grp * 4 + r;
+          if (!CHECK || row < p.M)
+            dst[(size_t)row * ldc] = __builtin_bit_cast(uint16_t, (__bf16)acc[i][j][r]);
+        }
+    }
+  };
+  if (m0 + BM <= p.M) store(std::false_type{});
+  else store(std::true_type{});
 }
 
 // Packing: Wp[n][k] = W~^Q[k][n] for n < H d (W~^Q = W^Q W^R per head, or W^Q
