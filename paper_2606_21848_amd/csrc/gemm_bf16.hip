@@ -154,22 +154,18 @@ void gemm_bf16_kernel(GemmParams2 p) {
   auto stageW = [&](int st) { return base + st * 2 * TILE_BYTES + TILE_BYTES; };
   const int nk = p.K / BK;
   issue(stageA(0), stageW(0), 0);
-  // Each wave issues 8 copies per tile; waiting until at most 8 are outstanding
-  // means the current tile has landed while the next one is still in flight.
+  // One barrier per k-tile. Before it, each wave waits for its copies of tile
+  // kt (the only ones in flight) and for its own LDS reads of tile kt - 1 (the
+  // barrier does not wait for those); after it, both hold for every wave, so
+  // the copies of tile kt + 1 may refill the stage of tile kt - 1 while tile kt
+  // is multiplied.
   for (int kt = 0; kt < nk; ++kt) {
     const int cur = kt & 1;
-    if (kt + 1 < nk) {
-      issue(stageA(cur ^ 1), stageW(cur ^ 1), (kt + 1) * BK);
-      KL_WAIT_VMCNT(8);
-    } else {
-      KL_WAIT_VMCNT(0);
-    }
-    __syncthreads();
-    compute(stageA(cur), stageW(cur));
-    // The next iteration's copies refill this stage: every wave's LDS reads of
-    // it must have returned first (the barrier does not wait for them).
+    KL_WAIT_VMCNT(0);
     asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
     __syncthreads();
+    if (kt + 1 < nk) issue(stageA(cur ^ 1), stageW(cur ^ 1), (kt + 1) * BK);
+    compute(stageA(cur), stageW(cur));
   }
 
   // Lane holds C[row 16 i + 4 grp + r][col 16 j + fr] of the wave's 128 x 64 block.
