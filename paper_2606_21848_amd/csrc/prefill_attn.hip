@@ -121,7 +121,7 @@ __global__ __launch_bounds__(kThreads, QB == 2 ? 3 : 2) void attn_bf16_kernel(At
   constexpr int ROWS_PER_COPY = 1024 / T::ROW;
   // The copy's source is a wave-uniform base (first row of the group, clamped)
   // plus a per-lane offset (row within the group, clamped, and chunk).
-  uint32_t col_off[T::COPIES];  // bytes: group g's columns plus the logical chunk
+  uint32_t col_off[T::COPIES];  // bytes: group g's columns plus the logical chunk (+ the lane's row below)
 #pragma unroll
   for (int c = 0; c < T::COPIES; ++c) {
     const int r = (c * 4 + wave) * ROWS_PER_COPY + lane / T::CHUNKS;
@@ -135,15 +135,28 @@ __global__ __launch_bounds__(kThreads, QB == 2 ? 3 : 2) void attn_bf16_kernel(At
   }
   const uint32_t lds0 = (uint32_t)(uintptr_t)(lds_u8*)smem;
   const size_t row_bytes = (size_t)p.v_stride * 2;
-  auto issue = [&](int jt, const int stage) {
+  const uint32_t lane_row = (uint32_t)(lane / T::CHUNKS) * (uint32_t)row_bytes;
 #pragma unroll
-    for (int c = 0; c < T::COPIES; ++c) {
-      const int r0 = jt * BKV + (c * 4 + wave) * ROWS_PER_COPY;  // uniform
-      const int r0c = min(r0, p.Nk - 1);
-      const int rl = min(r0 + lane / T::CHUNKS, p.Nk - 1) - r0c;  // 0 .. ROWS_PER_COPY - 1
-      const unsigned char* base = gV + ((size_t)b * p.Nk + r0c) * row_bytes;
-      copy_to_lds(base, (uint32_t)(rl * row_bytes) + col_off[c],
-                  lds0 + stage * T::BYTES + (c * 4 + wave) * 1024);
+  for (int c = 0; c < T::COPIES; ++c) col_off[c] += lane_row;  // now the whole per-lane offset
+  auto issue = [&](int jt, const int stage) {
+    const int j0 = jt * BKV;
+    if (j0 + BKV <= p.Nk) {
+      // Every row of the tile exists: one base per tile, per-copy steps uniform.
+      const unsigned char* tb = gV + ((size_t)b * p.Nk + j0) * row_bytes;
+#pragma unroll
+      for (int c = 0; c < T::COPIES; ++c)
+        copy_to_lds(tb + (size_t)((c * 4 + wave) * ROWS_PER_COPY) * row_bytes, col_off[c],
+                    lds0 + stage * T::BYTES + (c * 4 + wave) * 1024);
+    } else {
+#pragma unroll
+      for (int c = 0; c < T::COPIES; ++c) {
+        const int r0 = j0 + (c * 4 + wave) * ROWS_PER_COPY;  // uniform
+        const int r0c = min(r0, p.Nk - 1);
+        const int rl = min(r0 + lane / T::CHUNKS, p.Nk - 1) - r0c;  // 0 .. ROWS_PER_COPY - 1
+        const unsigned char* base = gV + ((size_t)b * p.Nk + r0c) * row_bytes;
+        copy_to_lds(base, (uint32_t)(rl * row_bytes) + col_off[c] - lane_row,
+                    lds0 + stage * T::BYTES + (c * 4 + wave) * 1024);
+      }
     }
   };
 
@@ -155,7 +168,9 @@ __global__ __launch_bounds__(kThreads, QB == 2 ? 3 : 2) void attn_bf16_kernel(At
   // the kernel past its register budget, and the spilled entry's reload inside
   // the tile loop came with a wait for every load in flight, the next tiles'
   // copies included.
-  const FragOffsets<D> fo(fr, grp);
+  FragOffsets<D> fo(fr, grp);
+  fo.sbase += (int)lds0;  // absolute LDS addresses: the tile's own offset is an immediate
+  fo.tbase += (int)lds0;
 
   const int last_row = p.causal ? min(qt * BQ + BQ, p.Nk) : p.Nk;
   const int ntiles = (last_row + BKV - 1) / BKV;
@@ -185,7 +200,9 @@ __global__ __launch_bounds__(kThreads, QB == 2 ? 3 : 2) void attn_bf16_kernel(At
     // and every tile for a wave whose rows all lie past the end (a ragged last
     // query tile): such a wave still copies and meets the barriers.
     if (q0 >= p.N || (!FIRST && p.causal && j0 > q0 + WQ - 1)) return;
-    const lds_u8* tile = (const lds_u8*)smem + STAGE * T::BYTES;
+    // fo gives absolute LDS addresses in stage 0; this stage's offset is an immediate.
+    constexpr uint32_t tile = STAGE * T::BYTES;
+    auto at = [](uint32_t a) { return (const lds_u8*)(uintptr_t)a; };
 
     // S^T[kv][q] - m[q] for kv blocks kb (16 rows) and query blocks qb.
     f32x4_t init[QB];
@@ -203,14 +220,14 @@ __global__ __launch_bounds__(kThreads, QB == 2 ? 3 : 2) void attn_bf16_kernel(At
       bf16x8_t sa[2][KS];
 #pragma unroll
       for (int ks = 0; ks < KS; ++ks)
-        sa[0][ks] = *reinterpret_cast<const __attribute__((address_space(3))) bf16x8_t*>(tile + offS[ks]);
+        sa[0][ks] = *reinterpret_cast<const __attribute__((address_space(3))) bf16x8_t*>(at(tile + offS[ks]));
 #pragma unroll
       for (int kb = 0; kb < 4; ++kb) {
         if (kb + 1 < 4) {
 #pragma unroll
           for (int ks = 0; ks < KS; ++ks)
             sa[(kb + 1) & 1][ks] = *reinterpret_cast<const __attribute__((address_space(3))) bf16x8_t*>(
-                tile + offS[ks] + (kb + 1) * 16 * T::ROW);
+                at(tile + offS[ks] + (kb + 1) * 16 * T::ROW));
         }
 #pragma unroll
         for (int ks = 0; ks < KS; ++ks)
@@ -300,11 +317,12 @@ __global__ __launch_bounds__(kThreads, QB == 2 ? 3 : 2) void attn_bf16_kernel(At
     // the 4 rows of column 16 db + fr (rows 32 ks + 4 grp .., and 16 further
     // for the high half); the all-ones operand adds the weight sums. All reads
     // of the k-step are issued ahead of its products.
+    int offT[DB];
     auto pv = [&](const int ks) {
       bf16x8_t av[DB];
 #pragma unroll
       for (int db = 0; db < DB; ++db) {
-        const lds_u8* src = tile + fo.t(db) + ks * 32 * T::ROW;
+        const lds_u8* src = at(tile + offT[db] + ks * 32 * T::ROW);
         const s16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
             (__attribute__((address_space(3))) s16x4*)(src));
         const s16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
@@ -322,6 +340,8 @@ __global__ __launch_bounds__(kThreads, QB == 2 ? 3 : 2) void attn_bf16_kernel(At
     };
     weights(0);
     weights(1);
+#pragma unroll
+    for (int db = 0; db < DB; ++db) offT[db] = fo.t(db);
     pv(0);
     pv(1);
   };
