@@ -206,9 +206,14 @@ __global__ __launch_bounds__(kThreads, 2) void bwd_dq_kernel(BwdParams p) {
       asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
       __syncthreads();
     }
+    // The first tiles' copy addresses are formed here, per sweep: hoisted out
+    // of the sweep loop by the compiler, they were spilled, and each reload
+    // came with a wait for every copy already in flight.
+    int t0 = 0;
+    asm volatile("" : "+s"(t0));
 #pragma unroll
     for (int s = 0; s < NSTAGE - 1; ++s)
-      if (s < ntiles) issue(s, s);
+      if (s < ntiles) issue(t0 + s, s);
     float dsum[QBD];
 #pragma unroll
     for (int qb = 0; qb < QBD; ++qb) dsum[qb] = 0.f;
