@@ -21,10 +21,12 @@ def _weights(d, H, G, dk, seed, dtype=torch.bfloat16):
     return W_Q, W_R, W_V
 
 
-# N_a below, at and above one 192-row query tile; N_b with ragged value tiles,
-# a single value row, and more query rows than value rows.
+# N_a below, at and above one query tile (unmasked calls take 128-row tiles,
+# causal ones 192) and ragged past several; N_b with ragged value tiles, a
+# single value row, and more query rows than value rows.
 CASES = [(2, 100, 300, 128, 4, 2, 64), (1, 257, 64, 256, 2, 2, 128), (2, 1, 1000, 128, 4, 1, 128),
-         (3, 700, 33, 256, 8, 2, 64), (2, 192, 1, 128, 2, 1, 128), (1, 385, 4097, 64 * 3, 4, 4, 128)]
+         (3, 700, 33, 256, 8, 2, 64), (2, 192, 1, 128, 2, 1, 128), (1, 385, 4097, 64 * 3, 4, 4, 128),
+         (1, 128, 200, 128, 2, 2, 128)]
 
 
 @pytest.mark.parametrize("dtype", [torch.float32, torch.bfloat16])
