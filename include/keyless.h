@@ -137,8 +137,10 @@ int keyless_fold_routing(const void* W_Q, const void* W_R, int d_model, int H, i
  * There is no key projection. bf16 uses MFMA with fp32 accumulation; the
  * routed queries and values are rounded to bf16 once, as they would be cached.
  * For bf16 the weights are folded and packed into the workspace on every call
- * (d_model must be a multiple of 64); callers that keep weights resident
- * should pack once with keyless_pack_weights and call keyless_prefill_packed.
+ * (d_model must be a multiple of 64; x, the weights, out, q_routed_out, v_out
+ * and ws 16-byte aligned, else KL_ERR_INVALID_ARG before any launch); callers
+ * that keep weights resident should pack once with keyless_pack_weights and
+ * call keyless_prefill_packed.
  */
 int keyless_prefill(const void* x, const void* W_Q, const void* W_R, const void* W_V, int B,
                     int N, int d_model, int H, int G, int d_head, int causal, float scale,
@@ -157,9 +159,12 @@ size_t keyless_prefill_workspace_size(int B, int N, int d_model, int H, int G, i
  *   W~^Q = W^Q W^R (per head; W^Q itself when W_R is NULL), row H*d_head + n
  *   is column n of W^V,
  * i.e. the projection weights transposed so that d_model is contiguous, the
- * layout the MFMA projection reads. fp32 accumulation for the fold, one
- * rounding to bf16. packed holds keyless_packed_weights_size(...) bytes.
- * bf16 only (KL_ERR_UNSUPPORTED otherwise).
+ * layout the MFMA projection reads. fp32 accumulation for the fold (a matrix
+ * core product per head), one rounding to bf16; the W^V rows (and the W^Q rows
+ * when W_R is NULL) are copied bit for bit. packed holds
+ * keyless_packed_weights_size(...) bytes. bf16 and d_head 64 or 128 only
+ * (KL_ERR_UNSUPPORTED otherwise); every pointer 16-byte aligned
+ * (KL_ERR_INVALID_ARG otherwise).
  */
 size_t keyless_packed_weights_size(int d_model, int H, int G, int d_head, kl_dtype dtype);
 int keyless_pack_weights(const void* W_Q, const void* W_R, const void* W_V, int d_model, int H,
@@ -167,7 +172,8 @@ int keyless_pack_weights(const void* W_Q, const void* W_R, const void* W_V, int 
 
 /*
  * keyless_prefill_packed - keyless_prefill with weights prepared by
- * keyless_pack_weights (bf16 only; d_model a multiple of 64). The workspace is
+ * keyless_pack_weights (bf16 only; d_model a multiple of 64; every pointer
+ * 16-byte aligned, else KL_ERR_INVALID_ARG before any launch). The workspace is
  * needed only for q_routed / v when those outputs are NULL:
  * B*N*H*d_head*2 and B*N*G*d_head*2 bytes, each rounded up to 256.
  */

@@ -127,12 +127,14 @@ def keyless_prefill(x, W_Q, W_R, W_V, H: int, G: int, d_head: int,
 
 
 def keyless_prefill_rows(x, Wt_Q, W_V, rows, H: int, G: int, d_head: int,
-                         causal: bool = True, scale: float | None = None):
+                         causal: bool = True, scale: float | None = None,
+                         return_routed: bool = False):
     """Output rows ``rows`` of Eq. 2 for batch 0 only, given the folded W~^Q.
 
     Used where the whole N x N problem is too large for the CPU: V is formed for
     all tokens the requested rows can see, Q~ only for the requested rows.
-    Returns (O [len(rows), H, d_k], V [n_seen, G, d_k]).
+    Returns (O [len(rows), H, d_k], V [n_seen, G, d_k]), and the routed queries
+    of those rows, Q~ [len(rows), H, d_k], as a third item with return_routed.
     """
     X = _f64(x)[0]
     Wt_Q = _f64(Wt_Q)
@@ -152,7 +154,7 @@ def keyless_prefill_rows(x, Wt_Q, W_V, rows, H: int, G: int, d_head: int,
             s = tau * (V_g @ Qt[k, h])
             p = softmax_rows(s[None, :])[0]
             O[k, h] = p @ V_g
-    return O, V
+    return (O, V, Qt) if return_routed else (O, V)
 
 
 # ---------------------------------------------------------------------------

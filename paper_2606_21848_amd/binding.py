@@ -264,7 +264,7 @@ def set_kernel_timer(start: "torch.cuda.Event | None", stop: "torch.cuda.Event |
 
 
 def keyless_pack_weights(W_Q: torch.Tensor, W_R: torch.Tensor | None, W_V: torch.Tensor, H: int,
-                         G: int) -> torch.Tensor:
+                         G: int, out: torch.Tensor | None = None) -> torch.Tensor:
     """Packed [(H+G)*d, d_model] bf16 weights: (W^Q W^R)^T over W^V^T, d_model contiguous."""
     load()
     d_model = W_Q.shape[0]
@@ -272,7 +272,10 @@ def keyless_pack_weights(W_Q: torch.Tensor, W_R: torch.Tensor | None, W_V: torch
     n = int(_lib.keyless_packed_weights_size(d_model, H, G, dk, _dt(W_Q)))
     if n == 0:
         raise KeylessError(KL_ERR_UNSUPPORTED, "packed weights are bf16 only")
-    packed = torch.empty(((H + G) * dk, d_model), dtype=W_Q.dtype, device=W_Q.device)
+    packed = out if out is not None else torch.empty(((H + G) * dk, d_model), dtype=W_Q.dtype,
+                                                     device=W_Q.device)
+    if packed.shape != ((H + G) * dk, d_model) or packed.dtype != W_Q.dtype:
+        raise ValueError("out must be [(H + G) * d_head, d_model] in the weights' dtype")
     _check(_lib.keyless_pack_weights(_ptr(W_Q), _ptr(W_R), _ptr(W_V), d_model, H, G, dk, _dt(W_Q),
                                      _ptr(packed), _stream(W_Q)))
     return packed

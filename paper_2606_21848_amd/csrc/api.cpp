@@ -409,6 +409,10 @@ int keyless_pack_weights(const void* W_Q, const void* W_R, const void* W_V, int 
   if (d_model <= 0 || H <= 0 || G <= 0 || d_head <= 0 || H % G != 0)
     return fail(KL_ERR_INVALID_ARG, "%s: bad sizes d_model=%d H=%d G=%d d_head=%d", who, d_model,
                 H, G, d_head);
+  if (d_head != 64 && d_head != 128)
+    return fail(KL_ERR_UNSUPPORTED, "%s: d_head %d not supported (64 or 128)", who, d_head);
+  if (!aligned16(W_Q) || !aligned16(W_V) || !aligned16(W_R) || !aligned16(packed))
+    return fail(KL_ERR_INVALID_ARG, "%s: W_Q, W_R, W_V and packed must be 16-byte aligned", who);
   kl::PackParams pp{};
   pp.W_Q = W_Q;
   pp.W_R = W_R;
@@ -520,6 +524,24 @@ QV carve_qv(char* w, int B, int N_a, int N_b, int H, int G, int d_head, size_t e
   return r;
 }
 
+// Checks of the bf16 matrix-core path, made before anything is launched: the
+// projection GEMM must handle the shape, and every operand must be 16-byte
+// aligned (the GEMM and attention kernels move 16-byte chunks of each).
+int check_bf16_path(const char* who, const void* xa, const void* xb, int B, int N_a, int N_b,
+                    int d_model, int H, int G, int d_head, const void* out,
+                    const void* q_routed_out, const void* v_out, const void* ws) {
+  const int NQ = H * d_head, NV = G * d_head;
+  const int M = std::max(std::max(B * N_a, B * N_b), 1);
+  if (const char* why = kl::gemm_bf16_unsupported(M, NQ + NV, d_model, d_model, NQ, NV))
+    return fail(KL_ERR_UNSUPPORTED, "%s: %s (d_model=%d)", who, why, d_model);
+  if (!aligned16(xa) || (N_b > 0 && !aligned16(xb)) || !aligned16(out) ||
+      !aligned16(q_routed_out) || !aligned16(v_out) || !aligned16(ws))
+    return fail(KL_ERR_INVALID_ARG,
+                "%s: x, xb, out, q_routed_out, v_out and the workspace must be 16-byte aligned",
+                who);
+  return KL_OK;
+}
+
 // bf16 projections and attention against packed weights, queries from xa
 // [B, N_a, d_model], values from xb [B, N_b, d_model]. Self-attention (xa == xb,
 // N_a == N_b) projects both in one GEMM launch; cross-attention takes two, the
@@ -529,9 +551,6 @@ int attend_packed_core(const char* who, const void* xa, const void* xb, const vo
                        float scale, void* out, void* qr, void* vv, hipStream_t st) {
   const int NQ = H * d_head, NV = G * d_head;
   const int Ma = B * N_a, Mb = B * N_b;
-  if (!kl::gemm_bf16_supported(std::max(std::max(Ma, Mb), 1), NQ + NV, d_model, d_model, NQ, NV))
-    return fail(KL_ERR_UNSUPPORTED, "%s: d_model=%d must be a multiple of 64 for bf16", who,
-                d_model);
   int s = KL_OK;
   if (xa == xb && N_a == N_b) {
     if (Ma > 0)
@@ -560,6 +579,8 @@ int attend_packed_entry(const char* who, const void* xa, const void* xb, const v
                         float scale, kl_dtype dtype, void* out, void* q_routed_out, void* v_out,
                         void* ws, size_t ws_bytes, hipStream_t st) {
   if (dtype != KL_BF16) return fail(KL_ERR_UNSUPPORTED, "%s: packed weights are bf16 only", who);
+  if (!aligned16(packed))
+    return fail(KL_ERR_INVALID_ARG, "%s: the packed weights must be 16-byte aligned", who);
   const size_t e = 2;
   const size_t qbytes = q_routed_out ? 0 : align256((size_t)B * N_a * H * d_head * e);
   const size_t vbytes = v_out ? 0 : align256((size_t)B * N_b * G * d_head * e);
@@ -567,6 +588,9 @@ int attend_packed_entry(const char* who, const void* xa, const void* xb, const v
     return fail(KL_ERR_WORKSPACE, "%s: workspace of %zu bytes needed, %zu given", who,
                 qbytes + vbytes, ws_bytes);
   if (B == 0 || (N_a == 0 && N_b == 0)) return KL_OK;
+  int s = check_bf16_path(who, xa, xb, B, N_a, N_b, d_model, H, G, d_head, out, q_routed_out,
+                          v_out, ws);
+  if (s != KL_OK) return s;
   const QV qv = carve_qv(static_cast<char*>(ws), B, N_a, N_b, H, G, d_head, e, q_routed_out, v_out);
   return attend_packed_core(who, xa, xb, packed, B, N_a, N_b, d_model, H, G, d_head, causal, scale,
                             out, qv.qr, qv.vv, st);
@@ -589,9 +613,9 @@ int attend_entry(const char* who, const void* xa, const void* xb, const void* W_
   char* w = static_cast<char*>(ws);
   int s;
   if (dtype == KL_BF16) {
-    if (d_model % 64 != 0)
-      return fail(KL_ERR_UNSUPPORTED, "%s: d_model=%d must be a multiple of 64 for bf16", who,
-                  d_model);
+    s = check_bf16_path(who, xa, xb, B, N_a, N_b, d_model, H, G, d_head, out, q_routed_out,
+                        v_out, ws);
+    if (s != KL_OK) return s;
     void* packed = w;
     w += keyless_packed_weights_size(d_model, H, G, d_head, dtype);
     s = keyless_pack_weights(W_Q, W_R, W_V, d_model, H, G, d_head, dtype, packed, st);

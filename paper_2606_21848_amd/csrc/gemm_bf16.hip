@@ -199,58 +199,17 @@ void gemm_bf16_kernel(GemmParams2 p) {
   else store(std::true_type{});
 }
 
-// Packing: Wp[n][k] = W~^Q[k][n] for n < H d (W~^Q = W^Q W^R per head, or W^Q
-// itself), Wp[H d + n][k] = W^V[k][n]. One thread per output element of a
-// 64 x 64 tile, through LDS so both the reads and the writes are coalesced.
-template <bool FOLD>
-__global__ __launch_bounds__(256) void pack_weights_kernel(PackParams p) {
-  __shared__ float tile[64][65];
-  const int n_tile = blockIdx.x, k_tile = blockIdx.y;  // 64 x 64 output tile of Wp
-  const int NQ = p.H * p.d_head;
-  const int n0 = n_tile * 64, k0 = k_tile * 64;
-  const uint16_t* Wq = reinterpret_cast<const uint16_t*>(p.W_Q);
-  const uint16_t* Wr = reinterpret_cast<const uint16_t*>(p.W_R);
-  const uint16_t* Wv = reinterpret_cast<const uint16_t*>(p.W_V);
-  // Phase 1: tile[kk][nn] = source value at (k0 + kk, n0 + nn), fp32.
-  for (int e = threadIdx.x; e < 64 * 64; e += 256) {
-    const int kk = e / 64, nn = e % 64;
-    const int k = k0 + kk, n = n0 + nn;
-    float v = 0.f;
-    if (k < p.d_model && n < p.N) {
-      if (n < NQ) {
-        if (FOLD) {
-          const int h = n / p.d_head, j = n % p.d_head;
-          const uint16_t* qrow = Wq + (size_t)k * NQ + (size_t)h * p.d_head;
-          const uint16_t* rcol = Wr + (size_t)h * p.d_head * p.d_head + j;
-          for (int i = 0; i < p.d_head; ++i)
-            v = fmaf(__uint_as_float((uint32_t)qrow[i] << 16),
-                     __uint_as_float((uint32_t)rcol[(size_t)i * p.d_head] << 16), v);
-        } else {
-          v = __uint_as_float((uint32_t)Wq[(size_t)k * NQ + n] << 16);
-        }
-      } else {
-        v = __uint_as_float((uint32_t)Wv[(size_t)k * (p.N - NQ) + (n - NQ)] << 16);
-      }
-    }
-    tile[kk][nn] = v;
-  }
-  __syncthreads();
-  uint16_t* out = reinterpret_cast<uint16_t*>(p.packed);
-  for (int e = threadIdx.x; e < 64 * 64; e += 256) {
-    const int nn = e / 64, kk = e % 64;
-    const int k = k0 + kk, n = n0 + nn;
-    if (k < p.d_model && n < p.N)
-      out[(size_t)n * p.d_model + k] = __builtin_bit_cast(uint16_t, (__bf16)tile[kk][nn]);
-  }
-}
-
 }  // namespace
 
-bool gemm_bf16_supported(int M, int N, int K, long lda, long ldc0, long ldc1) {
+const char* gemm_bf16_unsupported(int M, int N, int K, long lda, long ldc0, long ldc1) {
+  if (M <= 0 || N <= 0) return "empty product";
+  if (K < BK || K % BK != 0) return "d_model must be a positive multiple of 64 for bf16";
+  if (lda % 8 != 0 || lda < K) return "the row stride of x must be a multiple of 8 and >= d_model";
+  if (ldc0 <= 0 || ldc1 <= 0) return "output row strides must be positive";
   // Operand offsets are 32-bit byte offsets.
-  const bool fits = (size_t)M * lda * 2 < (1ull << 32) && (size_t)N * K * 2 < (1ull << 32);
-  return M > 0 && N > 0 && K >= BK && K % BK == 0 && lda % 8 == 0 && lda >= K && ldc0 > 0 &&
-         ldc1 > 0 && fits;
+  if ((size_t)M * lda * 2 >= (1ull << 32) || (size_t)N * K * 2 >= (1ull << 32))
+    return "x or the packed weights exceed 4 GiB (32-bit operand offsets)";
+  return nullptr;
 }
 
 constexpr size_t kGemmLds = 4 * TILE_BYTES;
@@ -277,15 +236,6 @@ hipError_t launch_gemm_bf16_packed(const void* A, int M, int K, long lda, const 
   p.ldc1 = ldc1;
   const int tiles = ((M + BM - 1) / BM) * ((N + BN - 1) / BN);
   hipLaunchKernelGGL(gemm_bf16_kernel, dim3(tiles), dim3(kThreads), kGemmLds, st, p);
-  return hipGetLastError();
-}
-
-hipError_t launch_pack_weights(const PackParams& p, hipStream_t st) {
-  dim3 grid((p.N + 63) / 64, (p.d_model + 63) / 64);
-  if (p.W_R)
-    hipLaunchKernelGGL(pack_weights_kernel<true>, grid, dim3(256), 0, st, p);
-  else
-    hipLaunchKernelGGL(pack_weights_kernel<false>, grid, dim3(256), 0, st, p);
   return hipGetLastError();
 }
 

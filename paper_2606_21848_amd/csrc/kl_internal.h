@@ -111,7 +111,8 @@ hipError_t launch_gemm_simple(const GemmParams& p, hipStream_t stream);
 
 // bf16 MFMA GEMM against packed weights: C = A (M x K, row-major) * Wp^T with
 // Wp [N, K] (K contiguous). Columns < n_split go to C0, the rest to C1.
-bool gemm_bf16_supported(int M, int N, int K, long lda, long ldc0, long ldc1);
+// nullptr when the bf16 GEMM handles the shape, else the reason it does not.
+const char* gemm_bf16_unsupported(int M, int N, int K, long lda, long ldc0, long ldc1);
 hipError_t launch_gemm_bf16_packed(const void* A, int M, int K, long lda, const void* Wp, int N,
                                    int n_split, void* C0, long ldc0, void* C1, long ldc1,
                                    hipStream_t stream);

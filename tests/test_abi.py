@@ -198,3 +198,42 @@ def test_latent_decode_workspace_and_rejects(lib):
     expect(lib, lat(ws_bytes=100), kb.KL_ERR_WORKSPACE, "workspace")
     expect(lib, lat(w=ctypes.c_void_p(0x100008)), kb.KL_ERR_INVALID_ARG, "aligned")
     assert lat(B=0, ws_bytes=0) == kb.KL_OK
+
+
+def test_bf16_prefill_rejects_misaligned_operands(lib):
+    """The matrix-core prefill moves 16-byte chunks of every operand: a pointer
+    off that alignment is refused host-side, before the pack or any launch."""
+    odd = ctypes.c_void_p(0x100008)
+    r256 = 1 << 30
+
+    def packed(x=FAKE, out=FAKE, qr=None, v=None, ws=FAKE, d=64):
+        return lib.keyless_prefill_packed(x, FAKE, 1, 16, d, 4, 4, 64, 1, 0.0, kb.KL_BF16, out, qr,
+                                          v, ws, r256, None)
+
+    def raw(x=FAKE, wq=FAKE, out=FAKE, ws=FAKE):
+        return lib.keyless_prefill(x, wq, FAKE, FAKE, 1, 16, 64, 4, 4, 64, 1, 0.0, kb.KL_BF16, out,
+                                   None, None, ws, r256, None)
+    expect(lib, packed(x=odd), kb.KL_ERR_INVALID_ARG, "aligned")
+    expect(lib, packed(out=odd), kb.KL_ERR_INVALID_ARG, "aligned")
+    expect(lib, packed(qr=odd, v=FAKE), kb.KL_ERR_INVALID_ARG, "aligned")
+    expect(lib, packed(v=odd, qr=FAKE), kb.KL_ERR_INVALID_ARG, "aligned")
+    expect(lib, packed(ws=odd), kb.KL_ERR_INVALID_ARG, "aligned")
+    expect(lib, packed(d=96), kb.KL_ERR_UNSUPPORTED, "multiple of 64")
+    expect(lib, raw(x=odd), kb.KL_ERR_INVALID_ARG, "aligned")
+    expect(lib, raw(ws=odd), kb.KL_ERR_INVALID_ARG, "aligned")
+    expect(lib, raw(wq=odd), kb.KL_ERR_INVALID_ARG, "aligned")
+    st = lib.keyless_cross_attention_packed(FAKE, odd, FAKE, 1, 16, 40, 64, 4, 2, 64, 0.0,
+                                            kb.KL_BF16, FAKE, None, None, FAKE, r256, None)
+    expect(lib, st, kb.KL_ERR_INVALID_ARG, "aligned")
+
+
+def test_pack_weights_rejects(lib):
+    def pack(wq=FAKE, wr=FAKE, wv=FAKE, out=FAKE, d=256, H=4, G=2, dk=64, dt=kb.KL_BF16):
+        return lib.keyless_pack_weights(wq, wr, wv, d, H, G, dk, dt, out, None)
+    odd = ctypes.c_void_p(0x100008)
+    expect(lib, pack(dk=96), kb.KL_ERR_UNSUPPORTED, "d_head 96")
+    expect(lib, pack(dt=kb.KL_F32), kb.KL_ERR_UNSUPPORTED, "bf16")
+    expect(lib, pack(G=3), kb.KL_ERR_INVALID_ARG, "bad sizes")
+    expect(lib, pack(wv=None), kb.KL_ERR_INVALID_ARG, "non-NULL")
+    for kw in ("wq", "wr", "wv", "out"):
+        expect(lib, pack(**{kw: odd}), kb.KL_ERR_INVALID_ARG, "aligned")

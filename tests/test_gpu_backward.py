@@ -8,7 +8,7 @@ import torch
 
 from oracle import keyless as K
 from paper_2606_21848_amd import binding as kb
-from tests.parity import assert_parity, say, to64
+from tests.parity import assert_parity, rowwise_rel, say, to64
 from workloads import configs, synth
 
 pytestmark = pytest.mark.gpu
@@ -107,19 +107,22 @@ def test_layer_backward_matches_oracle(lib, dtype, B, N, d, H, G, dk):
     grads = kb.keyless_weight_gradients(xs, wq, wr, wv, dq, dv, H, G)
     torch.cuda.synchronize()
     ref = K.keyless_backward(to64(x), to64(W_Q), to64(W_R), to64(W_V), to64(dO), H, G, dk)
-    if dtype == torch.float32:
-        ref_dq, ref_dv = ref["dQr"], ref["dV"]
-    else:
-        # The bf16 path stores the folded weights, the routed queries and the
-        # values in bf16 (one rounding each); that rounding alone moves dQ~ by
-        # about the bar, so dQ~ and dV are checked against the oracle's attention
-        # backward on the oracle's projections rounded the same way.
-        bf = lambda a: to64(torch.from_numpy(a).to(torch.bfloat16))
-        Wt = bf(K.fold_routing(to64(W_Q), to64(W_R), H, dk))
-        _, Qr, Vp = K.keyless_prefill(to64(x), Wt, None, to64(W_V), H, G, dk)
-        ref_dq, ref_dv = K.keyless_attention_backward(bf(Qr), bf(Vp), to64(dO), H, G, dk)
+    # The attention backward against the oracle's, on the routed queries and
+    # values the GPU's attention consumed (the same bits, copied back).
+    ref_dq, ref_dv = K.keyless_attention_backward(to64(qr), to64(v), to64(dO), H, G, dk)
     assert_parity(dq, ref_dq, dtype, "dQ~", FLOOR)
     assert_parity(dv, ref_dv, dtype, "dV", FLOOR)
+    # End to end against the float64 oracle of the whole layer: the fp32 path
+    # meets its bar; the bf16 path also rounds the folded weights, the routed
+    # queries and the values once each, which moves dQ~ by about the bf16 bar
+    # (the softmax backward's dP - rowsum subtraction amplifies it), so there the
+    # figure is reported, not asserted.
+    e2e_dq = rowwise_rel(dq, ref["dQr"], FLOOR)
+    e2e_dv = rowwise_rel(dv, ref["dV"], FLOOR)
+    say(f"  end to end against the float64 layer oracle: dQ~ {e2e_dq:.3e}, dV {e2e_dv:.3e}")
+    if dtype == torch.float32:
+        assert_parity(dq, ref["dQr"], dtype, "dQ~ end to end", FLOOR)
+        assert_parity(dv, ref["dV"], dtype, "dV end to end", FLOOR)
     assert_parity(grads["dW_R"], ref["dW_R"], dtype, "dW^R (Eq. 5)", FLOOR)
     assert_parity(grads["dW_V"].T, ref["dW_V"].T, dtype, "dW^V (Eq. 6)", FLOOR)
     assert_parity(grads["dW_Q"].T, ref["dW_Q"].T, dtype, "dW^Q", FLOOR)

@@ -333,18 +333,29 @@ def test_decode_append_matches_oracle(lib, dtype, d, H, G, paged):
 
 
 def test_decode_append_full_size(lib):
-    """The decode_bf16 workload as one fused step per sequence: equal to the
-    unfused append + decode within the bar, the cache bit-equal afterwards."""
+    """The decode_bf16 workload as one fused step per sequence, in the launch the
+    benchmark times (one workgroup per pair, the new row taken from registers):
+    all 256 (sequence, head) outputs against the oracle's decode over the cache
+    with the new row appended (the oracle's own append), the cache afterwards
+    bit-equal to that, and equal to the unfused append + decode within the bar."""
     say("decode_append full size")
     c = configs.decode_bf16(device=DEV)
-    base = c["V"].clone()
+    B, H, L = c["B"], c["H"], c["L"]
     before = c["lengths_before"]
+    # Poison the row the step appends, so the fused launch must write it.
+    c["V"][:, :, L - 1] = float("nan")
+    cache_before = c["V"].cpu()
+    base = c["V"].clone()
     vnew = c["v_new"][:, 0].contiguous()  # [B, G, d]
     a = kb.keyless_decode_append(c["q"], vnew, kb.ValueCache(c["V"]), before)
     kb.value_cache_append(kb.ValueCache(base), c["v_new"], before)
     b = kb.keyless_decode(c["q"], kb.ValueCache(base), before + 1)
     torch.cuda.synchronize()
+    ref_cache = K.value_cache_append(to64(cache_before), to64(c["v_new"]), before.cpu().numpy())
+    np.testing.assert_array_equal(to64(c["V"]), ref_cache)
     assert torch.equal(c["V"], base)
+    ref = K.keyless_decode(to64(c["q"]), ref_cache, (before + 1).cpu().numpy(), H, H)
+    assert_parity(a, ref, torch.bfloat16, "fused step against the oracle")
     assert_parity(a, to64(b), torch.bfloat16, "fused vs unfused")
 
 

@@ -27,11 +27,14 @@ def test_fold_routing(lib, dtype):
 
 
 @pytest.mark.parametrize("with_wr", [True, False])
-def test_pack_weights(lib, with_wr):
+@pytest.mark.parametrize("d,H,G,dk", [(320, 4, 2, 64), (200, 2, 1, 128), (100, 2, 2, 64),
+                                      (1024, 8, 2, 128)])
+def test_pack_weights(lib, with_wr, d, H, G, dk):
     """Packed rows: (W^Q W^R)^T per head over W^V^T, d_model contiguous. Without a
-    routing matrix the pack is a pure transpose and must be bit-exact."""
-    d, H, G, dk = 320, 4, 2, 64
-    say(f"pack weights with_wr={with_wr}")
+    routing matrix the pack is a pure transpose and must be bit-exact. d_model
+    spans whole and ragged 128-row tiles, and rows that are not 16-byte
+    aligned (d_model = 100)."""
+    say(f"pack weights with_wr={with_wr} d={d} H={H} G={G} dk={dk}")
     W_Q = synth.normal((d, H * dk), 23, 1, d ** -0.5)
     W_R = synth.normal((H, dk, dk), 23, 2, dk ** -0.5)
     W_V = synth.normal((d, G * dk), 23, 3, d ** -0.5)
@@ -150,10 +153,32 @@ def test_prefill_bf16_full_size_sampled(lib):
     torch.cuda.synchronize()
     rows = sorted(set([0, 8191] + synth.uniform_int(510, 1, 8190, 2, 50).tolist()))
     Wt_ref = K.fold_routing(to64(c["W_Q"]), to64(c["W_R"]), 32, 128)
-    Orows, Vref = K.keyless_prefill_rows(to64(c["x"]), Wt_ref, to64(c["W_V"]), rows, 32, 32, 128)
+    Orows, Vref, Qrows = K.keyless_prefill_rows(to64(c["x"]), Wt_ref, to64(c["W_V"]), rows, 32, 32,
+                                                128, return_routed=True)
     assert_parity(v[0], Vref, torch.bfloat16, "values")
+    assert_parity(qr[0, rows], Qrows, torch.bfloat16, "sampled routed queries")
     assert_parity(out[0, rows], Orows, torch.bfloat16, "sampled rows")
     assert torch.isfinite(out.float()).all()
+
+
+def test_prefill_raw_weights_full_size_sampled(lib):
+    """The same workload through keyless_prefill with the raw W^Q, W^R, W^V
+    (folded and packed into the workspace on the call): bit-equal to the packed
+    call, and its routed queries on 64 sampled rows against the oracle."""
+    say("prefill_bf16 full size, raw weights")
+    c = configs.prefill_bf16(device=DEV)
+    packed = kb.keyless_pack_weights(c["W_Q"], c["W_R"], c["W_V"], 32, 32)
+    ref = kb.keyless_prefill_packed(c["x"], packed, 32, 32, return_qv=True)
+    got = kb.keyless_prefill(c["x"], c["W_Q"], c["W_R"], c["W_V"], 32, 32, return_qv=True)
+    torch.cuda.synchronize()
+    for a, b, what in zip(got, ref, ("out", "q_routed", "v")):
+        assert torch.equal(a, b), what
+    rows = sorted(set([0, 8191] + synth.uniform_int(62, 1, 8190, 2, 51).tolist()))
+    # (x W^Q_h) W^R_h and x W^V_g of those tokens, unfolded, in float64.
+    Qrows, Vrows = K.decode_step_projections(to64(c["x"][0, rows]), to64(c["W_Q"]),
+                                             to64(c["W_R"]), to64(c["W_V"]), 32, 32, 128)
+    assert_parity(got[1][0, rows], Qrows, torch.bfloat16, "sampled routed queries")
+    assert_parity(got[2][0, rows], Vrows, torch.bfloat16, "sampled values")
 
 
 def test_prefill_long_sequence_sampled(lib):

@@ -157,15 +157,18 @@ def cross_bf16(device="cpu", seed=6, B=4, N_a=1024, N_b=4096, d_model=4096, H=32
     )
 
 
-def latent_bf16(device="cpu", seed=7, B=32, H=32, G=1, r=128, d_head=128, L=16384):
+def latent_bf16(device="cpu", seed=7, B=32, H=32, G=1, r=128, d_head=128, L=16384, copies=1):
     """Decode over a latent value-only cache (Eq. 15) at the head-to-head shape:
     one r = 128 latent shared by all 32 heads (G = 1), 16384 cached rows per
     sequence, so the cache is 1/32 of the value-only cache of that shape.
     Latent rows and routed queries ~ N(0,1); expansion matrices W_post
-    [H, r, d_head] ~ N(0, 1/d_head), which keeps the absorbed query ~ N(0,1)."""
+    [H, r, d_head] ~ N(0, 1/d_head), which keeps the absorbed query ~ N(0,1).
+    ``copies`` > 1 draws extra independent caches (streams S_V + 100*c) for a
+    timing loop that rotates over more than the last-level cache holds."""
     f = torch.bfloat16
+    caches = [normal((B, G, L, r), seed, S_V + 100 * c, 1.0, f, device) for c in range(copies)]
     return dict(
-        cache=normal((B, G, L, r), seed, S_V, 1.0, f, device),
+        cache=caches[0], caches=caches,
         q=normal((B, H, d_head), seed, S_Q, 1.0, f, device),
         W_post=normal((H, r, d_head), seed, S_WPOST, 1.0 / math.sqrt(d_head), f, device),
         lengths=torch.full((B,), L, dtype=torch.int32, device=device),
@@ -186,14 +189,16 @@ def backward_bf16(device="cpu", seed=8, B=1, N=8192, H=32, G=32, d_head=128):
     )
 
 
-def decode_b1_bf16(device="cpu", seed=9, L=2048, H=32, d_head=128):
+def decode_b1_bf16(device="cpu", seed=9, L=2048, H=32, d_head=128, copies=1):
     """Batch-1 decode at one context length (the setting of the paper's decode
     throughput measurement: batch 1, contexts 512, 2048 and 8192): a contiguous
     value-only cache [1, H, L, d_head] and routed queries [1, H, d_head] ~ N(0,1),
-    bf16; the step's new row is the cache's last row."""
+    bf16; the step's new row is the cache's last row. ``copies`` > 1 adds
+    independent caches (streams S_V + 100*c) for a rotating timing loop."""
     f = torch.bfloat16
-    V = normal((1, H, L, d_head), seed, S_V, 1.0, f, device)
-    return dict(V=V, q=normal((1, H, d_head), seed, S_Q, 1.0, f, device),
+    caches = [normal((1, H, L, d_head), seed, S_V + 100 * c, 1.0, f, device) for c in range(copies)]
+    V = caches[0]
+    return dict(V=V, caches=caches, q=normal((1, H, d_head), seed, S_Q, 1.0, f, device),
                 v_new=V[:, :, L - 1].contiguous(),
                 lengths_before=torch.full((1,), L - 1, dtype=torch.int32, device=device),
                 H=H, L=L, d_head=d_head)
