@@ -470,6 +470,16 @@ def profile_decode_side(torch, kb, configs, dev):
         kb.keyless_decode(g["q"], vc, g["lengths"], out=out, workspace=ws)
     torch.cuda.synchronize()
     del g, vc, ws, out
+    # The same shape at d_head 64, whose grouped heads take the vector-ALU
+    # consumer (decode_partial_kernel), for the counters beside the matrix cores'.
+    g = configs.paged_gqa_bf16(device=dev, d_head=64)
+    vc = kb.ValueCache(g["data"], g["block_table"])
+    ws = torch.zeros(kb.decode_workspace_bytes(vc, g["B"], g["H"]), dtype=torch.uint8, device=dev)
+    out = torch.empty_like(g["q"])
+    for _ in range(4):
+        kb.keyless_decode(g["q"], vc, g["lengths"], out=out, workspace=ws)
+    torch.cuda.synchronize()
+    del g, vc, ws, out
     st = configs.decode_step_bf16(device=dev)
     packed = kb.keyless_pack_weights(st["W_Q"], st["W_R"], st["W_V"], st["H"], st["G"])
     q_out = torch.empty((st["B"], st["H"], st["d_head"]), dtype=torch.bfloat16, device=dev)
