@@ -357,6 +357,25 @@ int keyless_decode_append(const void* q_routed, const void* v_new, const kl_valu
                           const int32_t* lengths_before, int B, int H, float scale, void* out,
                           void* ws, size_t ws_bytes, void* stream);
 
+/*
+ * keyless_decode_noalloc - keyless_decode for callers that cannot allocate
+ * device memory (code under HIP graph capture, tight serving loops, harnesses
+ * that forbid allocation): the same result, kernels and work split, with the
+ * workspace taken from a fixed scratch array of 16 MiB that the library holds
+ * on each GPU it runs on (resolved once per device, kept until the process
+ * ends). The caller passes only inputs and outputs; nothing is allocated,
+ * freed or synchronised. A decode whose workspace
+ * (keyless_decode_workspace_size with chunk_rows 0) exceeds 16 MiB returns
+ * KL_ERR_UNSUPPORTED before any launch. All calls on one GPU share its scratch
+ * array, so calls that overlap on one GPU (other streams, other host threads)
+ * race and must be ordered by the caller; the scratch needs no clearing, as
+ * every call writes each workspace entry before reading it. Other arguments and
+ * errors as for keyless_decode.
+ */
+int keyless_decode_noalloc(const void* q_routed, const kl_value_cache* cache,
+                           const int32_t* lengths, int B, int H, float scale, void* out,
+                           void* stream);
+
 /* As keyless_decode, with the cache length split into chunks of chunk_rows
  * rows fixed by the caller (a multiple of 64; 0 selects the built-in choice):
  * one workgroup per (b, group, chunk), then a merge of the chunks of each

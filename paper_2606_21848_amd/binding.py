@@ -30,7 +30,7 @@ EXPORTS = (
     "keyless_attention_backward_workspace_size", "keyless_weight_gradients",
     "keyless_weight_gradients_workspace_size",
     "keyless_decode_project", "keyless_decode", "keyless_decode_chunked", "keyless_decode_workspace_size",
-    "keyless_decode_append",
+    "keyless_decode_append", "keyless_decode_noalloc",
     "value_cache_append", "standard_decode", "standard_decode_chunked",
     "keyless_set_kernel_timer", "keyless_last_error", "keyless_version",
 )
@@ -82,6 +82,7 @@ def load(path: str = LIB_PATH):
         "keyless_decode": (i, [vp, cp, vp, i, i, f, vp, vp, sz, vp]),
         "keyless_decode_chunked": (i, [vp, cp, vp, i, i, f, vp, vp, sz, i, vp]),
         "keyless_decode_append": (i, [vp, vp, cp, vp, i, i, f, vp, vp, sz, vp]),
+        "keyless_decode_noalloc": (i, [vp, cp, vp, i, i, f, vp, vp]),
         "keyless_decode_workspace_size": (sz, [cp, i, i, i]),
         "keyless_latent_decode": (i, [vp, vp, cp, vp, i, i, i, f, vp, vp, sz, vp]),
         "keyless_latent_decode_workspace_size": (sz, [cp, i, i, i]),
@@ -498,4 +499,19 @@ def keyless_decode_append(q_routed: torch.Tensor, v_new: torch.Tensor, cache: Va
     _check(_lib.keyless_decode_append(_ptr(q_routed), _ptr(v_new), cache.ref, _ptr(lengths_before), B,
                                       H, scale, _ptr(out), _ptr(workspace), workspace.numel(),
                                       _stream(q_routed)))
+    return out
+
+
+def keyless_decode_noalloc(q_routed: torch.Tensor, cache: ValueCache, lengths: torch.Tensor,
+                           scale: float = 0.0, out: torch.Tensor | None = None) -> torch.Tensor:
+    """keyless_decode with the library's fixed scratch as its workspace (the
+    call allocates no device memory; ``out`` may be passed in too)."""
+    load()
+    B, H, _ = q_routed.shape
+    if lengths.dtype != torch.int32:
+        raise TypeError("lengths must be int32")
+    if out is None:
+        out = torch.empty_like(q_routed)
+    _check(_lib.keyless_decode_noalloc(_ptr(q_routed), cache.ref, _ptr(lengths), B, H, scale,
+                                       _ptr(out), _stream(q_routed)))
     return out

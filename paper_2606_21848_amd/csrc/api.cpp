@@ -272,6 +272,28 @@ int keyless_decode_append(const void* q_routed, const void* v_new, const kl_valu
                        stream, who, v_new);
 }
 
+int keyless_decode_noalloc(const void* q_routed, const kl_value_cache* cache,
+                           const int32_t* lengths, int B, int H, float scale, void* out,
+                           void* stream) {
+  const char* who = "keyless_decode_noalloc";
+  int st = check_cache(cache, who);
+  if (st != KL_OK) return st;
+  if (B < 0 || H <= 0) return fail(KL_ERR_INVALID_ARG, "%s: bad B=%d or H=%d", who, B, H);
+  const size_t need = keyless_decode_workspace_size(cache, B, H, 0);
+  if (need > kl::kScratchBytes)
+    return fail(KL_ERR_UNSUPPORTED,
+                "%s: this decode needs %zu bytes of scratch, more than the %zu bytes the "
+                "entry point holds; call keyless_decode with a workspace",
+                who, need, kl::kScratchBytes);
+  void* ws = nullptr;
+  if (need > 0 && B > 0) {
+    int s = hip_status(kl::scratch_address(&ws), who);
+    if (s != KL_OK) return s;
+  }
+  return decode_common(q_routed, nullptr, cache, lengths, B, H, scale, out, ws,
+                       ws ? kl::kScratchBytes : 0, 0, stream, who);
+}
+
 int keyless_decode_chunked(const void* q_routed, const kl_value_cache* cache,
                            const int32_t* lengths, int B, int H, float scale, void* out, void* ws,
                            size_t ws_bytes, int chunk_rows, void* stream) {

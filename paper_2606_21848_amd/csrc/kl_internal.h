@@ -12,6 +12,11 @@ namespace kl {
 
 constexpr int kMaxSplits = 1024;
 
+// The fixed scratch of keyless_decode_noalloc: its size, and its device address
+// on the current device (looked up once per device, then cached).
+constexpr size_t kScratchBytes = size_t(16) << 20;
+hipError_t scratch_address(void** out);
+
 // Raise a kernel's dynamic-LDS limit to `bytes`, once per device (devices
 // 0..31 are remembered in `done`; others set it on every call).
 inline hipError_t set_max_lds(const void* fn, int bytes, std::atomic<uint32_t>& done) {

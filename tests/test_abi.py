@@ -237,3 +237,17 @@ def test_pack_weights_rejects(lib):
     expect(lib, pack(wv=None), kb.KL_ERR_INVALID_ARG, "non-NULL")
     for kw in ("wq", "wr", "wv", "out"):
         expect(lib, pack(**{kw: odd}), kb.KL_ERR_INVALID_ARG, "aligned")
+
+
+def test_decode_noalloc_rejects_oversized_workspace(lib):
+    """The scratch of the no-allocation decode holds 16 MiB: a decode needing
+    more is refused before anything touches the device."""
+    big = cache(G=8, layout=kb.KL_PAGED, mb=2048)
+    need = lib.keyless_decode_workspace_size(ctypes.byref(big), 4096, 32, 0)
+    assert need > 16 << 20
+    st = lib.keyless_decode_noalloc(FAKE, ctypes.byref(big), FAKE, 4096, 32, 0.0, FAKE, None)
+    expect(lib, st, kb.KL_ERR_UNSUPPORTED, "16777216")
+    expect(lib, lib.keyless_decode_noalloc(FAKE, None, FAKE, 1, 1, 0.0, FAKE, None),
+           kb.KL_ERR_INVALID_ARG, "NULL")
+    assert lib.keyless_decode_noalloc(FAKE, ctypes.byref(cache()), FAKE, 0, 8, 0.0, FAKE, None) == \
+        kb.KL_OK
