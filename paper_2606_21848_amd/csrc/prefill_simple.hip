@@ -29,18 +29,18 @@ __device__ __forceinline__ void st<uint16_t>(uint16_t* p, size_t i, float v) {
   p[i] = (uint16_t)f32_to_bf16(v);
 }
 
-constexpr int GT = 64;  // output tile (64 x 64, 4 x 4 per thread)
 constexpr int GK = 64;  // k per step: few steps, so few exposed load latencies on small products
 
-// The 16 A and 16 B elements one thread stages per k-step: A is GT rows x GK
-// columns (consecutive threads take consecutive k), B is GK rows x GT columns
-// (consecutive threads take consecutive n), zero outside the matrices.
-template <typename T>
+// One k-step of the GT x GT output tile: the thread's share of the A tile
+// (GT rows x GK columns; consecutive threads take consecutive k) and of the B
+// tile (GK rows x GT columns; consecutive threads take consecutive n), zero
+// outside the matrices.
+template <typename T, int GT>
 __device__ __forceinline__ void gemm_load(const GemmParams& p, const T* A, const T* Bm, int m0,
-                                          int n0, int k0, size_t acs, size_t bcs, float (&ra)[16],
-                                          float (&rb)[16]) {
+                                          int n0, int k0, size_t acs, size_t bcs,
+                                          float (&ra)[GT * GK / 256], float (&rb)[GT * GK / 256]) {
 #pragma unroll
-  for (int r = 0; r < 16; ++r) {
+  for (int r = 0; r < GT * GK / 256; ++r) {
     const int i = threadIdx.x + 256 * r;
     const int kk = i % GK, mm = i / GK;
     const int gm = m0 + mm, gk = k0 + kk;
@@ -51,8 +51,12 @@ __device__ __forceinline__ void gemm_load(const GemmParams& p, const T* A, const
   }
 }
 
-template <typename T>
+// GT x GT output tile per workgroup of 256 threads (16 x 16 threads, each
+// GT / 16 x GT / 16 outputs): 64 for large products, 32 where 64-wide tiles
+// would leave most of the chip idle.
+template <typename T, int GT>
 __global__ __launch_bounds__(256) void gemm_simple_kernel(GemmParams p) {
+  constexpr int R = GT / 16, NL = GT * GK / 256;
   const T* A = reinterpret_cast<const T*>(p.A) + (size_t)blockIdx.z * p.strideA;
   const T* Bm = reinterpret_cast<const T*>(p.Bm) + (size_t)blockIdx.z * p.strideB;
   T* C = reinterpret_cast<T*>(p.C) + (size_t)blockIdx.z * p.strideC;
@@ -60,39 +64,39 @@ __global__ __launch_bounds__(256) void gemm_simple_kernel(GemmParams p) {
   __shared__ float sB[GK][GT + 1];
   const int tx = threadIdx.x % 16, ty = threadIdx.x / 16;
   const int m0 = blockIdx.y * GT, n0 = blockIdx.x * GT;
-  float c[4][4] = {};
+  float c[R][R] = {};
   const size_t acs = p.a_cs ? p.a_cs : 1, bcs = p.b_cs ? p.b_cs : 1;
   // The next k-step's elements are loaded into registers while the current
   // one is multiplied out of LDS.
-  float ra[16], rb[16];
-  gemm_load<T>(p, A, Bm, m0, n0, 0, acs, bcs, ra, rb);
+  float ra[NL], rb[NL];
+  gemm_load<T, GT>(p, A, Bm, m0, n0, 0, acs, bcs, ra, rb);
   for (int k0 = 0; k0 < p.K; k0 += GK) {
 #pragma unroll
-    for (int r = 0; r < 16; ++r) {
+    for (int r = 0; r < NL; ++r) {
       const int i = threadIdx.x + 256 * r;
       sA[i % GK][i / GK] = ra[r];
       sB[i / GT][i % GT] = rb[r];
     }
     __syncthreads();
-    if (k0 + GK < p.K) gemm_load<T>(p, A, Bm, m0, n0, k0 + GK, acs, bcs, ra, rb);
+    if (k0 + GK < p.K) gemm_load<T, GT>(p, A, Bm, m0, n0, k0 + GK, acs, bcs, ra, rb);
 #pragma unroll 16
     for (int kk = 0; kk < GK; ++kk) {
-      float a[4], bv[4];
+      float a[R], bv[R];
 #pragma unroll
-      for (int i = 0; i < 4; ++i) a[i] = sA[kk][ty + 16 * i];
+      for (int i = 0; i < R; ++i) a[i] = sA[kk][ty + 16 * i];
 #pragma unroll
-      for (int j = 0; j < 4; ++j) bv[j] = sB[kk][tx + 16 * j];
+      for (int j = 0; j < R; ++j) bv[j] = sB[kk][tx + 16 * j];
 #pragma unroll
-      for (int i = 0; i < 4; ++i)
+      for (int i = 0; i < R; ++i)
 #pragma unroll
-        for (int j = 0; j < 4; ++j) c[i][j] = fmaf(a[i], bv[j], c[i][j]);
+        for (int j = 0; j < R; ++j) c[i][j] = fmaf(a[i], bv[j], c[i][j]);
     }
     __syncthreads();
   }
 #pragma unroll
-  for (int i = 0; i < 4; ++i)
+  for (int i = 0; i < R; ++i)
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
+    for (int j = 0; j < R; ++j) {
       const int gm = m0 + ty + 16 * i, gn = n0 + tx + 16 * j;
       if (gm < p.M && gn < p.N) {
         const size_t at = (size_t)gm * p.ldc + gn;
@@ -143,20 +147,39 @@ __global__ __launch_bounds__(256) void attn_simple_kernel(AttnParams p) {
       sV[jj][cc] = (j < p.Nk) ? ld(V, ((size_t)b * p.Nk + j) * p.v_stride + (size_t)g * D + cc) : 0.f;
     }
     __syncthreads();
+    // Four value rows per update: four independent score chains, one rescale.
+    // Rows past what this group sees (or past the tile's end) get no weight,
+    // and their values are replaced by zeros so that nothing non-finite in them
+    // can reach the sum.
     const int jn = min(SV_ROWS, jend - j0);
-    for (int jj = 0; jj < jn; ++jj) {
-      const f32xE v = *reinterpret_cast<const f32xE*>(&sV[jj][c * E]);
-      float s = 0.f;
+    for (int jj = 0; jj < jn; jj += 4) {
+      f32xE v[4];
+      float s[4];
 #pragma unroll
-      for (int e = 0; e < E; ++e) s = fmaf(q[e], v[e], s);
-      s = group_sum<16>(s);
-      if (j0 + jj >= seen) s = -INFINITY;
-      const float mn = fmaxf(m, s);
+      for (int u = 0; u < 4; ++u) {
+        v[u] = *reinterpret_cast<const f32xE*>(&sV[jj + u][c * E]);
+        s[u] = 0.f;
+#pragma unroll
+        for (int e = 0; e < E; ++e) s[u] = fmaf(q[e], v[u][e], s[u]);
+      }
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        s[u] = group_sum<16>(s[u]);
+        if (j0 + jj + u >= seen || jj + u >= jn) {
+          s[u] = -INFINITY;
+          v[u] = f32xE{};
+        }
+      }
+      const float mn = fmaxf(fmaxf(m, fmaxf(s[0], s[1])), fmaxf(s[2], s[3]));
       const float ms = mn == -INFINITY ? 0.f : mn;  // nothing seen yet: no shift
-      const float alpha = fast_exp2(m - ms), w = fast_exp2(s - ms);
-      l = fmaf(l, alpha, w);
+      const float alpha = fast_exp2(m - ms);
+      float w[4];
 #pragma unroll
-      for (int e = 0; e < E; ++e) acc[e] = fmaf(w, v[e], acc[e] * alpha);
+      for (int u = 0; u < 4; ++u) w[u] = fast_exp2(s[u] - ms);
+      l = fmaf(l, alpha, (w[0] + w[1]) + (w[2] + w[3]));
+#pragma unroll
+      for (int e = 0; e < E; ++e)
+        acc[e] = fmaf(w[3], v[3][e], fmaf(w[2], v[2][e], fmaf(w[1], v[1][e], fmaf(w[0], v[0][e], acc[e] * alpha))));
       m = mn;
     }
   }
@@ -179,14 +202,20 @@ __global__ __launch_bounds__(256) void attn_simple_kernel(AttnParams p) {
 
 }  // namespace
 
-hipError_t launch_gemm_simple(const GemmParams& p, hipStream_t st) {
-  if (p.M == 0 || p.N == 0 || p.batch == 0) return hipSuccess;
+template <int GT>
+hipError_t launch_gemm_gt(const GemmParams& p, hipStream_t st) {
   dim3 grid((p.N + GT - 1) / GT, (p.M + GT - 1) / GT, p.batch);
   if (p.dtype == KL_BF16)
-    hipLaunchKernelGGL(gemm_simple_kernel<uint16_t>, grid, dim3(256), 0, st, p);
+    hipLaunchKernelGGL((gemm_simple_kernel<uint16_t, GT>), grid, dim3(256), 0, st, p);
   else
-    hipLaunchKernelGGL(gemm_simple_kernel<float>, grid, dim3(256), 0, st, p);
+    hipLaunchKernelGGL((gemm_simple_kernel<float, GT>), grid, dim3(256), 0, st, p);
   return hipGetLastError();
+}
+
+hipError_t launch_gemm_simple(const GemmParams& p, hipStream_t st) {
+  if (p.M == 0 || p.N == 0 || p.batch == 0) return hipSuccess;
+  const long tiles64 = (long)((p.N + 63) / 64) * ((p.M + 63) / 64) * p.batch;
+  return tiles64 < 256 ? launch_gemm_gt<32>(p, st) : launch_gemm_gt<64>(p, st);
 }
 
 hipError_t launch_prefill_attention_simple(const AttnParams& p, hipStream_t st) {
