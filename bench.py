@@ -721,7 +721,16 @@ def extra_measurements(torch, kb, configs, dev):
                            q_routed_out=outs[1], v_out=outs[2], workspace=pws)
     st = call_stats(pstep, STAT_CALLS, 20, torch)
     st_raw = call_stats(pstep_raw, STAT_CALLS, 5, torch)
+    # The attention kernel alone, on the call's own routed queries and values
+    # (keyless_attention_forward launches the same kernel); the projection GEMM
+    # is the rest of the call.
+    aout = torch.empty_like(outs[0])
+    st_att = call_stats(lambda i: kb.keyless_attention_forward(outs[1], outs[2], out=aout),
+                        STAT_CALLS, 10, torch)
     flops = 2 * N * dm * (H + G) * dk + 2 * H * dk * N * (N + 1)
+    att_flops = 2 * H * dk * N * (N + 1)
+    gemm_flops = 2 * N * dm * (H + G) * dk
+    gemm_ms = st["median_ms"] - st_att["median_ms"]
     rows = sorted(set([0, N - 1] + synth.uniform_int(510, 1, N - 2, 2, 50).tolist()))
     xh, wqh, wrh, wvh = np64(x), np64(p["W_Q"]), np64(p["W_R"]), np64(p["W_V"])
     Wt = K.fold_routing(wqh, wrh, H, dk)  # one-time, outside the timed sample
@@ -737,6 +746,16 @@ def extra_measurements(torch, kb, configs, dev):
         "ms": round(st["median_ms"], 4), "stats": st,
         "tflops": rate(st, flops, 1e-12),
         "frac_of_bf16_mfma_peak": round(rate(st, flops, 1e-12) / BF16_MFMA_PEAK_TFLOPS, 4),
+        "attention": dict(st_att, tflops=rate(st_att, att_flops, 1e-12),
+                          frac_of_bf16_mfma_peak=round(rate(st_att, att_flops, 1e-12) /
+                                                       BF16_MFMA_PEAK_TFLOPS, 4),
+                          note="attn_bf16_kernel alone (keyless_attention_forward on the call's "
+                               "routed queries and values), 2 H d_k N (N + 1) FLOP"),
+        "projection_gemm": {"ms": round(gemm_ms, 4),
+                            "tflops": round(gemm_flops / (gemm_ms * 1e-3) * 1e-12, 2),
+                            "frac_of_bf16_mfma_peak": round(gemm_flops / (gemm_ms * 1e-3) * 1e-12 /
+                                                            BF16_MFMA_PEAK_TFLOPS, 4),
+                            "note": "median call minus median attention; 2 N d (H + G) d_k FLOP"},
         "raw_weights": dict(st_raw, note="keyless_prefill with W^Q, W^R, W^V as given: the fold "
                                          "and pack run inside every call"),
         "pack_weights": dict(st_pack, note="keyless_pack_weights alone: fold of W^R into W^Q "
@@ -745,7 +764,7 @@ def extra_measurements(torch, kb, configs, dev):
                                   f"a sample: the full V projection and the {len(rows)} sampled "
                                   f"output rows (their routed queries and attention), "
                                   f"{sample_flop / 1e9:.1f} GFLOP in {el:.1f} s")}
-    del p, packed, x, outs, pws, xh, wqh, wrh, wvh, Wt
+    del p, packed, x, outs, pws, xh, wqh, wrh, wvh, Wt, aout
 
     # Cross-attention (Eq. 14): 1024 attending tokens against 4096 attended ones.
     c = configs.cross_bf16(device=dev)

@@ -82,27 +82,6 @@ __global__ __launch_bounds__(kThreads, 2) void attn_bf16_kernel(AttnParams p) {
 
   const uint16_t* __restrict__ Q = reinterpret_cast<const uint16_t*>(p.q);
 
-  // Routed-query fragments (B operand of S^T): query row q0 + 16 qb + fr,
-  // columns 32 ks + 8 grp .. + 7, multiplied by c = scale * log2(e) and rounded
-  // to bf16 once, so the products come out in exponent (log2) units. Rows past
-  // the end are clamped (never stored).
-  const float c = p.scale_log2;
-  bf16x8_t qf[QB][KS];
-#pragma unroll
-  for (int qb = 0; qb < QB; ++qb) {
-    const int qq = min(q0 + qb * 16 + fr, p.N - 1);
-    const uint16_t* src = Q + ((size_t)b * p.N + qq) * p.q_stride + (size_t)h * D + grp * 8;
-#pragma unroll
-    for (int ks = 0; ks < KS; ++ks) {
-      const u32x4 raw = *reinterpret_cast<const u32x4*>(src + ks * 32);
-      u32x4 w;
-#pragma unroll
-      for (int j = 0; j < 4; ++j)
-        w[j] = pack2(__uint_as_float(raw[j] << 16) * c, __uint_as_float(raw[j] & 0xFFFF0000u) * c);
-      qf[qb][ks] = __builtin_bit_cast(bf16x8_t, w);
-    }
-  }
-
   f32x4_t o[DB][QB];
 #pragma unroll
   for (int i = 0; i < DB; ++i)
@@ -182,6 +161,30 @@ __global__ __launch_bounds__(kThreads, 2) void attn_bf16_kernel(AttnParams p) {
 #pragma unroll
   for (int s = 0; s < NSTAGE - 1; ++s)
     if (s < ntiles) issue(s, s);
+
+  // Routed-query fragments (B operand of S^T), loaded after the first value
+  // tiles are requested so that the two latencies overlap (light causal tiles,
+  // which run last, are dominated by them): query row q0 + 16 qb + fr,
+  // columns 32 ks + 8 grp .. + 7, multiplied by c = scale * log2(e) and rounded
+  // to bf16 once, so the products come out in exponent (log2) units. Rows past
+  // the end are clamped (never stored).
+  const float c = p.scale_log2;
+  bf16x8_t qf[QB][KS];
+#pragma unroll
+  for (int qb = 0; qb < QB; ++qb) {
+    const int qq = min(q0 + qb * 16 + fr, p.N - 1);
+    const uint16_t* src = Q + ((size_t)b * p.N + qq) * p.q_stride + (size_t)h * D + grp * 8;
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) {
+      const u32x4 raw = *reinterpret_cast<const u32x4*>(src + ks * 32);
+      u32x4 w;
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+        w[j] = pack2(__uint_as_float(raw[j] << 16) * c, __uint_as_float(raw[j] & 0xFFFF0000u) * c);
+      qf[qb][ks] = __builtin_bit_cast(bf16x8_t, w);
+    }
+  }
+
 
   // One value tile. Scores come out of the MFMA already shifted by the
   // reference: the accumulation starts from -m (in log2 units, as q carries c).
