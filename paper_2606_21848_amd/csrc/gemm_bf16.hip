@@ -7,8 +7,9 @@
 // n_split go to C0 (the routed queries), the rest to C1 (the values).
 // fp32 accumulation in v_mfma_f32_16x16x32_bf16, one rounding to bf16 on store.
 //
-// Tile 256 x 256 x 64, 8 waves (2 x 4), each wave 128 x 64 of C (128 fp32
-// accumulators per lane, two waves per SIMD). Each operand tile is 256 rows of
+// Tile 256 x 256 x 64, 16 waves (4 x 4), each wave 64 x 64 of C (64 fp32
+// accumulators per lane, four waves per SIMD: while some waves restart a k-tile
+// with their LDS reads after the barrier, others keep the matrix pipe busy). Each operand tile is 256 rows of
 // 128 bytes in LDS with the 16-byte chunks of row r XOR-swizzled by
 // (r >> 1) & 7, so the fragment reads (16 rows per access) are free of bank
 // conflicts. Tiles move from memory straight into LDS (global_load_lds, 16
@@ -31,12 +32,9 @@ typedef __attribute__((__vector_size__(4 * sizeof(float)))) float f32x4_t;
 typedef __attribute__((address_space(3))) unsigned char lds_u8;
 
 constexpr int BM = 256, BN = 256, BK = 64;
-constexpr int kThreads = 512;
+constexpr int kThreads = 1024;
 constexpr int TILE_BYTES = 256 * BK * 2;  // one operand tile, 32 KiB
 static_assert(BK == 64, "the fragment schedule assumes two 32-wide k-steps per tile");
-// Instruction classes of __builtin_amdgcn_sched_group_barrier.
-constexpr int kSchedMfma = 0x008;
-constexpr int kSchedDsRead = 0x100;
 
 struct GemmParams2 {
   const uint16_t* A;   // [M, K]
@@ -53,9 +51,9 @@ __device__ __forceinline__ int swz(int row, int chunk) {
   return row * (BK * 2) + ((chunk ^ ((row >> 1) & 7)) << 4);
 }
 
-// Two waves per SIMD (the 128 KiB of LDS allow one workgroup per CU): the
-// register budget is 256, enough to hold all fragments of a k-step.
-__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2)))
+// Four waves per SIMD (the 128 KiB of LDS allow one workgroup per CU): the
+// register budget is 128, the accumulators and one k-step's fragments.
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(4, 4)))
 void gemm_bf16_kernel(GemmParams2 p) {
   const int tilesM = (p.M + BM - 1) / BM, tilesN = (p.N + BN - 1) / BN;
   const int ntiles = tilesM * tilesN;
@@ -75,17 +73,17 @@ void gemm_bf16_kernel(GemmParams2 p) {
 
   const int t = threadIdx.x, lane = t & 63;
   const int wave = __builtin_amdgcn_readfirstlane(t >> 6);
-  const int wm = wave >> 2, wn = wave & 3;  // wave tile: rows 128 wm.., columns 64 wn..
+  const int wm = wave >> 2, wn = wave & 3;  // wave tile: rows 64 wm.., columns 64 wn..
 
   // Direct-to-LDS copies: one wave instruction fills 8 rows (1 KiB) of a tile,
   // lane L landing at byte 16 L, i.e. row L / 8, physical chunk L % 8, which
-  // holds logical chunk (L % 8) ^ ((row >> 1) & 7). Each wave fills 4 row groups
+  // holds logical chunk (L % 8) ^ ((row >> 1) & 7). Each wave fills 2 row groups
   // of each operand. Rows past the end are clamped: they only feed output rows
   // or columns that are never stored.
-  uint32_t offA[4], offW[4];
+  uint32_t offA[2], offW[2];
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const int r = (i * 8 + wave) * 8 + (lane >> 3);
+  for (int i = 0; i < 2; ++i) {
+    const int r = (i * 16 + wave) * 8 + (lane >> 3);
     const int lc = (lane & 7) ^ ((r >> 1) & 7);
     const int ra = min(m0 + r, p.M - 1), rw = min(n0 + r, p.N - 1);
     offA[i] = (uint32_t)(((size_t)ra * p.lda + lc * 8) * 2);
@@ -97,56 +95,41 @@ void gemm_bf16_kernel(GemmParams2 p) {
     const unsigned char* ga = gA + (size_t)k0 * 2;
     const unsigned char* gw = gW + (size_t)k0 * 2;
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const uint32_t grp_off = (uint32_t)((i * 8 + wave) * 1024);
+    for (int i = 0; i < 2; ++i) {
+      const uint32_t grp_off = (uint32_t)((i * 16 + wave) * 1024);
       copy_to_lds(ga, offA[i], (uint32_t)(uintptr_t)sa + grp_off);
       copy_to_lds(gw, offW[i], (uint32_t)(uintptr_t)sw + grp_off);
     }
   };
 
-  f32x4_t acc[8][4];
+  f32x4_t acc[4][4];
 #pragma unroll
-  for (int i = 0; i < 8; ++i)
+  for (int i = 0; i < 4; ++i)
 #pragma unroll
     for (int j = 0; j < 4; ++j) acc[i][j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 
   const int fr = lane & 15, grp = lane >> 4;
-  // Both k-steps of a tile: every fragment read is issued up front (in order of
-  // first use), and the schedule pins the second k-step's reads between the
-  // first k-step's products, so no product waits on a read issued just before
-  // it (the compiler otherwise interleaves them one by one).
+  // Per 32-wide k-step: the wave's 4 A and 4 W fragments, then its 16 products
+  // (one fragment set; the other three waves on the SIMD cover the read latency).
   auto compute = [&](const lds_u8* a, const lds_u8* w) {
-    bf16x8_t af[2][8], bf[2][4];
 #pragma unroll
     for (int ks = 0; ks < BK / 32; ++ks) {
       const int chunk = ks * 4 + grp;
-      af[ks][0] = *reinterpret_cast<const __attribute__((address_space(3))) bf16x8_t*>(
-          a + swz(wm * 128 + fr, chunk));
+      bf16x8_t af[4], bf[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+        af[i] = *reinterpret_cast<const __attribute__((address_space(3))) bf16x8_t*>(
+            a + swz(wm * 64 + i * 16 + fr, chunk));
 #pragma unroll
       for (int j = 0; j < 4; ++j)
-        bf[ks][j] = *reinterpret_cast<const __attribute__((address_space(3))) bf16x8_t*>(
+        bf[j] = *reinterpret_cast<const __attribute__((address_space(3))) bf16x8_t*>(
             w + swz(wn * 64 + j * 16 + fr, chunk));
 #pragma unroll
-      for (int i = 1; i < 8; ++i)
-        af[ks][i] = *reinterpret_cast<const __attribute__((address_space(3))) bf16x8_t*>(
-            a + swz(wm * 128 + i * 16 + fr, chunk));
-    }
-#pragma unroll
-    for (int ks = 0; ks < BK / 32; ++ks)
-#pragma unroll
-      for (int i = 0; i < 8; ++i)
+      for (int i = 0; i < 4; ++i)
 #pragma unroll
         for (int j = 0; j < 4; ++j)
-          acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[ks][i], bf[ks][j], acc[i][j], 0, 0, 0);
-    // Groups in order: 12 reads (k-step 0), then 4 x (8 products of k-step 0,
-    // 3 reads of k-step 1), then the 32 products of k-step 1.
-    __builtin_amdgcn_sched_group_barrier(kSchedDsRead, 12, 0);
-#pragma unroll
-    for (int c = 0; c < 4; ++c) {
-      __builtin_amdgcn_sched_group_barrier(kSchedMfma, 8, 0);
-      __builtin_amdgcn_sched_group_barrier(kSchedDsRead, 3, 0);
+          acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[i], bf[j], acc[i][j], 0, 0, 0);
     }
-    __builtin_amdgcn_sched_group_barrier(kSchedMfma, 32, 0);
   };
 
   lds_u8* const base = (lds_u8*)smem;
@@ -168,7 +151,7 @@ void gemm_bf16_kernel(GemmParams2 p) {
     compute(stageA(cur), stageW(cur));
   }
 
-  // Lane holds C[row 16 i + 4 grp + r][col 16 j + fr] of the wave's 128 x 64 block.
+  // Lane holds C[row 16 i + 4 grp + r][col 16 j + fr] of the wave's 64 x 64 block.
   // A tile whose rows all exist stores without a per-element row check.
   auto store = [&](auto check_rows) {
     constexpr bool CHECK = decltype(check_rows)::value;
@@ -186,10 +169,10 @@ void gemm_bf16_kernel(GemmParams2 p) {
         ldc = p.ldc1;
       }
 #pragma unroll
-      for (int i = 0; i < 8; ++i)
+      for (int i = 0; i < 4; ++i)
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
-          const int row = m0 + wm * 128 + i * 16 + grp * 4 + r;
+          const int row = m0 + wm * 64 + i * 16 + grp * 4 + r;
           if (!CHECK || row < p.M)
             dst[(size_t)row * ldc] = __builtin_bit_cast(uint16_t, (__bf16)acc[i][j][r]);
         }
@@ -240,3 +223,4 @@ hipError_t launch_gemm_bf16_packed(const void* A, int M, int K, long lda, const 
 }
 
 }  // namespace kl
+
