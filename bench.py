@@ -831,6 +831,52 @@ def extra_measurements(torch, kb, configs, dev):
                                   f"{el:.1f} s")}
     del bw, bout, blse, bdq, bdv, bws, bo32, qh, vh, dh
 
+    # The rest of the layer's backward (Section 2.3): weight and input gradients
+    # from the attention gradients, at the prefill shape.
+    Bw, Nw, dw, Hw, Gw, dkw = 1, 8192, 4096, 32, 32, 128
+    bf = torch.bfloat16
+    wx = synth.normal((Bw, Nw, dw), 91, 1, 1.0, bf).to(dev)
+    wq = synth.normal((dw, Hw * dkw), 91, 2, dw ** -0.5, bf).to(dev)
+    wr = synth.normal((Hw, dkw, dkw), 91, 3, dkw ** -0.5, bf).to(dev)
+    wv = synth.normal((dw, Gw * dkw), 91, 4, dw ** -0.5, bf).to(dev)
+    wdq = synth.normal((Bw, Nw, Hw, dkw), 91, 5, 1.0, bf).to(dev)
+    wdv = synth.normal((Bw, Nw, Gw, dkw), 91, 6, 1.0, bf).to(dev)
+    wws = torch.empty(kb._lib.keyless_weight_gradients_workspace_size(Bw, Nw, dw, Hw, Gw, dkw,
+                                                                      kb.KL_BF16),
+                      dtype=torch.uint8, device=dev)
+    st = call_stats(lambda i: kb.keyless_weight_gradients(wx, wq, wr, wv, wdq, wdv, Hw, Gw,
+                                                          workspace=wws), STAT_CALLS, 3, torch)
+    Mw, NQw, NVw = Bw * Nw, Hw * dkw, Gw * dkw
+    # The products of the form computed: X^T [dQ~ | dV], [dQ~ | dV] [W~^Q | W^V]^T, and
+    # the three per-head ones (dW^Q_h, dW^R_h, the fold W^Q_h W^R_h).
+    flops = 2 * Mw * dw * (NQw + NVw) * 2 + 3 * 2 * dw * NQw * dkw
+    # The oracle on a sample: two query heads and two value groups over every token.
+    heads = [0, Hw - 1]
+    qcols = np.concatenate([np.arange(h * dkw, (h + 1) * dkw) for h in heads])
+    sx, swq, swr, swv = np64(wx), np64(wq)[:, qcols], np64(wr)[heads], np64(wv)[:, qcols]
+    sdq, sdv = np64(wdq)[:, :, heads], np64(wdv)[:, :, heads]
+    with Threads(cores):
+        t0 = time.perf_counter()
+        K.keyless_projection_gradients(sx, swq, swr, swv, sdq, sdv, 2, 2, dkw)
+        el = time.perf_counter() - t0
+    w2 = 2 * dkw
+    # X W^Q_h, Q_h^T dQ~_h and dQ~_h W^R_h^T per head, X^T dQ, X^T dV, and dX.
+    sample_flop = 2 * Mw * dw * w2 + 2 * 2 * 2 * Mw * dkw * dkw + 2 * Mw * dw * w2 * 2 + \
+        2 * Mw * w2 * dw * 2
+    res["weight_gradients_bf16"] = {
+        "workload": "keyless_weight_gradients, batch 1, 8192 tokens, d_model 4096, 32 + 32 heads "
+                    "x 128: dW^Q, dW^R (Eq. 5), dW^V (Eq. 6) and dX from dQ~ and dV",
+        "ms": round(st["median_ms"], 4), "stats": st,
+        "tflops": rate(st, flops, 1e-12),
+        "frac_of_bf16_mfma_peak": round(rate(st, flops, 1e-12) / BF16_MFMA_PEAK_TFLOPS, 4),
+        "note": f"{flops / 1e12:.3f} TFLOP: the products of the computed form (transposes of X, "
+                "dQ~, dV, G = X^T dQ~ and W^Q are not counted)",
+        "cpu_baseline": cpu_entry(round(sample_flop / el * 1e-12, 5), "TFLOP/s", cores,
+                                  f"a sample: the gradients of two query heads and two value "
+                                  f"groups over all 8192 tokens, {sample_flop / 1e9:.1f} GFLOP "
+                                  f"in {el:.1f} s")}
+    del wx, wq, wr, wv, wdq, wdv, wws, sx, swq, swr, swv, sdq, sdv
+
     # Paged grouped-head decode.
     g = configs.paged_gqa_bf16(device=dev)
     vc = kb.ValueCache(g["data"], g["block_table"])

@@ -588,27 +588,25 @@ def keyless_attention_backward_rows(Qr, V, dO, H: int, G: int, d_head: int, dq_r
     return dQ, dV
 
 
-def keyless_backward(x, W_Q, W_R, W_V, dO, H: int, G: int, d_head: int, causal: bool = True,
-                     scale: float | None = None):
-    """The backward pass of the layer of Eq. 2 through its projections
-    (Section 2.3). With Q_h = X W^Q_h, Q~_h = Q_h W^R_h, V_g = X W^V_g and the
-    attention gradients dQ~, dV of keyless_attention_backward:
+def keyless_projection_gradients(x, W_Q, W_R, W_V, dQr, dV, H: int, G: int, d_head: int):
+    """The backward pass through the projections Q_h = X W^Q_h, Q~_h = Q_h
+    W^R_h, V_g = X W^V_g (Section 2.3), given the attention gradients dQ~
+    [B, N, H, d_k] and dV [B, N, G, d_k]:
       dW^R_h = Q_h^T dQ~_h                      (Eq. 5)
       dQ_h   = dQ~_h (W^R_h)^T
       dW^Q   = X^T dQ                           (heads side by side)
       dW^V   = X^T dV                           (Eq. 6, both terms inside dV)
       dX     = dQ (W^Q)^T + dV (W^V)^T
-    summed over the batch. x: [B, N, d]; weights as in keyless_prefill; dO
-    [B, N, H, d_k]. Returns a dict with dX [B, N, d], dW_Q [d, H d_k],
-    dW_R [H, d_k, d_k], dW_V [d, G d_k], dQr, dV.
+    summed over the batch. Returns a dict with dX [B, N, d], dW_Q [d, H d_k],
+    dW_R [H, d_k, d_k], dW_V [d, G d_k].
     """
     x = _f64(x)
     W_Q = _f64(W_Q)
     W_R = _f64(W_R)
     W_V = _f64(W_V)
+    dQr = _f64(dQr)
+    dV = _f64(dV)
     B, N, d = x.shape
-    _, Qr, V = keyless_prefill(x, W_Q, W_R, W_V, H, G, d_head, causal=causal, scale=scale)
-    dQr, dV = keyless_attention_backward(Qr, V, dO, H, G, d_head, causal=causal, scale=scale)
     dW_R = np.zeros((H, d_head, d_head))
     dQ = np.zeros((B, N, H, d_head))
     for h in range(H):
@@ -622,7 +620,22 @@ def keyless_backward(x, W_Q, W_R, W_V, dO, H: int, G: int, d_head: int, causal: 
     dW_Q = sum(x[b].T @ dQf[b] for b in range(B))
     dW_V = sum(x[b].T @ dVf[b] for b in range(B))
     dX = np.stack([dQf[b] @ W_Q.T + dVf[b] @ W_V.T for b in range(B)])
-    return dict(dX=dX, dW_Q=dW_Q, dW_R=dW_R, dW_V=dW_V, dQr=dQr, dV=dV)
+    return dict(dX=dX, dW_Q=dW_Q, dW_R=dW_R, dW_V=dW_V)
+
+
+def keyless_backward(x, W_Q, W_R, W_V, dO, H: int, G: int, d_head: int, causal: bool = True,
+                     scale: float | None = None):
+    """The backward pass of the layer of Eq. 2 (Section 2.3): the prefill's
+    routed queries and values, the attention gradients dQ~, dV of
+    keyless_attention_backward, and the gradients through the projections of
+    keyless_projection_gradients. x: [B, N, d]; weights as in keyless_prefill;
+    dO [B, N, H, d_k]. Returns a dict with dX [B, N, d], dW_Q [d, H d_k],
+    dW_R [H, d_k, d_k], dW_V [d, G d_k], dQr, dV.
+    """
+    _, Qr, V = keyless_prefill(x, W_Q, W_R, W_V, H, G, d_head, causal=causal, scale=scale)
+    dQr, dV = keyless_attention_backward(Qr, V, dO, H, G, d_head, causal=causal, scale=scale)
+    res = keyless_projection_gradients(x, W_Q, W_R, W_V, dQr, dV, H, G, d_head)
+    return dict(res, dQr=dQr, dV=dV)
 
 
 # ---------------------------------------------------------------------------

@@ -92,7 +92,7 @@ def load(path: str = LIB_PATH):
         "keyless_attention_backward_workspace_size": (sz, [i, i, i]),
         "keyless_weight_gradients": (i, [vp, vp, vp, vp, vp, vp, i, i, i, i, i, i, i, vp, vp, vp,
                                          vp, vp, sz, vp]),
-        "keyless_weight_gradients_workspace_size": (sz, [i, i, i, i, i]),
+        "keyless_weight_gradients_workspace_size": (sz, [i, i, i, i, i, i, i]),
         "value_cache_append": (i, [cp, vp, vp, i, i, vp]),
         "standard_decode": (i, [vp, cp, cp, vp, i, i, f, vp, vp, sz, vp]),
         "standard_decode_chunked": (i, [vp, cp, cp, vp, i, i, f, vp, vp, sz, i, vp]),
@@ -475,7 +475,7 @@ def keyless_weight_gradients(x: torch.Tensor, W_Q: torch.Tensor, W_R: torch.Tens
     res = dict(dW_Q=torch.empty_like(W_Q), dW_R=torch.empty_like(W_R), dW_V=torch.empty_like(W_V),
                dX=torch.empty_like(x))
     if workspace is None:
-        n = int(_lib.keyless_weight_gradients_workspace_size(B, N, H, dk, _dt(x)))
+        n = int(_lib.keyless_weight_gradients_workspace_size(B, N, d_model, H, G, dk, _dt(x)))
         workspace = torch.empty(max(n, 256), dtype=torch.uint8, device=x.device)
     _check(_lib.keyless_weight_gradients(_ptr(x), _ptr(W_Q), _ptr(W_R), _ptr(W_V), _ptr(dq_routed),
                                          _ptr(dv), B, N, d_model, H, G, dk, _dt(x), _ptr(res["dW_Q"]),

@@ -851,9 +851,45 @@ int keyless_attention_backward(const void* q_routed, const void* v, const void* 
   return hip_status(kl::launch_attention_backward(p, static_cast<hipStream_t>(stream)), who);
 }
 
-size_t keyless_weight_gradients_workspace_size(int B, int N, int H, int d_head, kl_dtype dtype) {
-  if (B < 0 || N < 0 || H <= 0 || d_head <= 0) return 0;
-  return 2 * align256((size_t)B * N * H * d_head * elem_bytes(dtype));
+namespace {
+
+// Workspace of the matrix-core form of keyless_weight_gradients (bf16):
+// dQ = dQ~ W^R^T [M, H d_head]; the transposes X^T and [dQ^T ; dV^T] over the
+// padded token count Mp (the second buffer later holds Q = X W^Q); dQ~^T and
+// Q^T [H d_head, Mp]; W^Q^T [H d_head, d_model]; the fp32 partial sums of
+// dW^R over S token chunks [S, H, d_head, d_head].
+struct WgradLayout {
+  long S;   // token chunks of the dW^R contraction (each on its own workgroups)
+  long Mp;  // tokens padded to a multiple of 64 S
+  size_t dQ, xT, dT, dqT, QT, WQT, part, total;
+};
+
+WgradLayout wgrad_layout(long M, long d_model, long NQ, long NV, long H, long dk) {
+  WgradLayout L{};
+  // dW^R has H d_head x d_head outputs: one workgroup per head would leave
+  // most of the chip idle over a long contraction, so the tokens are split.
+  L.S = std::max(1L, std::min({16L, 256 / H, (M + 255) / 256}));
+  L.Mp = (M + 64 * L.S - 1) / (64 * L.S) * (64 * L.S);
+  L.dQ = 0;
+  L.xT = L.dQ + align256((size_t)M * NQ * 2);
+  L.dT = L.xT + align256((size_t)d_model * L.Mp * 2);
+  L.dqT = L.dT + align256((size_t)(NQ + NV) * L.Mp * 2);
+  L.QT = L.dqT + align256((size_t)NQ * L.Mp * 2);
+  L.WQT = L.QT + align256((size_t)NQ * L.Mp * 2);
+  L.part = L.WQT + align256((size_t)NQ * d_model * 2);
+  L.total = L.part + align256((size_t)L.S * H * dk * dk * 4);
+  return L;
+}
+
+}  // namespace
+
+size_t keyless_weight_gradients_workspace_size(int B, int N, int d_model, int H, int G,
+                                               int d_head, kl_dtype dtype) {
+  if (B < 0 || N < 0 || d_model <= 0 || H <= 0 || G <= 0 || d_head <= 0) return 0;
+  const long M = (long)B * N, NQ = (long)H * d_head, NV = (long)G * d_head;
+  const size_t generic = 2 * align256((size_t)M * NQ * elem_bytes(dtype));
+  if (dtype != KL_BF16) return generic;
+  return std::max(generic, wgrad_layout(M, d_model, NQ, NV, H, d_head).total);
 }
 
 int keyless_weight_gradients(const void* x, const void* W_Q, const void* W_R, const void* W_V,
@@ -868,14 +904,12 @@ int keyless_weight_gradients(const void* x, const void* W_Q, const void* W_R, co
     return fail(KL_ERR_INVALID_ARG, "%s: bad sizes", who);
   if (H % G != 0) return fail(KL_ERR_INVALID_ARG, "%s: H=%d is not a multiple of G=%d", who, H, G);
   if ((long)B * N > (1L << 30)) return fail(KL_ERR_UNSUPPORTED, "%s: B*N too large", who);
-  const size_t need = keyless_weight_gradients_workspace_size(B, N, H, d_head, dtype);
+  const size_t need = keyless_weight_gradients_workspace_size(B, N, d_model, H, G, d_head, dtype);
   if (!ws || ws_bytes < need)
     return fail(KL_ERR_WORKSPACE, "%s: workspace of %zu bytes needed, %zu given", who, need, ws_bytes);
   hipStream_t st = static_cast<hipStream_t>(stream);
   const long M = (long)B * N, NQ = (long)H * d_head, NV = (long)G * d_head;
   char* w = static_cast<char*>(ws);
-  void* Q = w;                                                   // X W^Q       [M, NQ]
-  void* dQ = w + align256((size_t)M * NQ * elem_bytes(dtype));    // dQ~ W^R^T   [M, NQ]
   auto gemm = [&](const void* A, long lda, long a_cs, const void* Bm, long ldb, long b_cs, void* C,
                   long ldc, long Mm, long Nn, long Kk, int batch, long sA, long sB, long sC,
                   int accumulate) {
@@ -900,8 +934,152 @@ int keyless_weight_gradients(const void* x, const void* W_Q, const void* W_R, co
     return hip_status(kl::launch_gemm_simple(g, st), who);
   };
   const long dk = d_head;
-  // With no tokens (M = 0) the contractions over tokens have K = 0 and write
-  // zero weight gradients; the token-shaped outputs are empty.
+  // bf16 with 16-byte aligned operands, head widths and d_model multiples of
+  // 64: every product runs on the matrix cores, in the form above (each
+  // intermediate, Q = X W^Q and dQ, rounded to bf16 once, as in the generic
+  // form; fp32 accumulation). The GEMM takes both operands with the
+  // contraction index contiguous, so X, dQ, dV, dQ~ and W^Q are transposed
+  // where a product needs it (the token count padded with zeros to a multiple
+  // of 64); the per-head products are batched over the heads.
+  const WgradLayout L = wgrad_layout(M, d_model, NQ, NV, H, dk);
+  const size_t lim = size_t(1) << 32;  // the GEMM's 32-bit operand offsets
+  const bool fits = (size_t)d_model * L.Mp * 2 < lim && (size_t)(NQ + NV) * L.Mp * 2 < lim &&
+                    (size_t)M * (NQ + NV + d_model) * 2 < lim && (size_t)d_model * (NQ + NV) * 2 < lim;
+  if (dtype == KL_BF16 && M > 0 && dk % 64 == 0 && d_model % 64 == 0 && fits && aligned16(x) &&
+      aligned16(W_Q) && aligned16(W_R) && aligned16(W_V) && aligned16(dq_routed) && aligned16(dv) &&
+      aligned16(ws)) {
+    void* dQm = w + L.dQ;   // [M, NQ]
+    void* xT = w + L.xT;    // [d_model, Mp]
+    char* dT = w + L.dT;    // [NQ + NV, Mp]: dQ^T then dV^T
+    void* dqT = w + L.dqT;  // [NQ, Mp]
+    void* QT = w + L.QT;    // [NQ, Mp]
+    void* WQT = w + L.WQT;  // [NQ, d_model]
+    float* part = reinterpret_cast<float*>(w + L.part);  // [S, H, dk, dk]
+    int s = KL_OK;
+    auto mm = [&](const kl::GemmBf16Args& a) {
+      if (const char* why = kl::gemm_bf16_unsupported(a))
+        return fail(KL_ERR_UNSUPPORTED, "%s: %s", who, why);
+      return hip_status(kl::launch_gemm_bf16(a, st), who);
+    };
+    auto tr = [&](const void* src, long ld_src, long rows, long cols, void* dst, long ld_dst,
+                  long rows_pad) {
+      return hip_status(kl::launch_transpose_bf16(src, ld_src, (int)rows, (int)cols, dst, ld_dst,
+                                                  (int)rows_pad, st),
+                        who);
+    };
+    // C (rows x cols) = A W^T over K, optionally batched over the heads (item
+    // strides sA, sW, sC), columns below n_split to C0, the rest to C1.
+    auto prod = [&](const void* A, long lda, long sA, const void* W, long ldw, long sW, long K,
+                    long rows, long cols, void* C0, long ldc0, long sC, long n_split, void* C1,
+                    long ldc1, int batch) {
+      kl::GemmBf16Args a{};
+      a.A0 = A;
+      a.lda0 = lda;
+      a.W0 = W;
+      a.ldw0 = ldw;
+      a.K0 = (int)K;
+      a.M = (int)rows;
+      a.N = (int)cols;
+      a.n_split = (int)n_split;
+      a.C0 = C0;
+      a.ldc0 = ldc0;
+      a.C1 = C1;
+      a.ldc1 = ldc1;
+      a.batch = batch;
+      a.sA0 = sA;
+      a.sW0 = sW;
+      a.sC0 = sC;
+      a.sC1 = sC;
+      return mm(a);
+    };
+    // dQ_h = dQ~_h W^R_h^T (W^R_h as stored is the [n][k] operand).
+    if (dW_Q || dx)
+      s = prod(dq_routed, NQ, dk, W_R, dk, dk * dk, dk, M, dk, dQm, NQ, dk, dk, dQm, NQ, H);
+    if (s == KL_OK && (dW_Q || dW_V)) {
+      // [dW^Q | dW^V] = X^T [dQ | dV], a contraction over the (padded) tokens.
+      s = tr(x, d_model, M, d_model, xT, L.Mp, L.Mp);
+      if (s == KL_OK && dW_Q) s = tr(dQm, NQ, M, NQ, dT, L.Mp, L.Mp);
+      if (s == KL_OK && dW_V) s = tr(dv, NV, M, NV, dT + (size_t)NQ * L.Mp * 2, L.Mp, L.Mp);
+      if (s == KL_OK) {
+        const char* Wt = dW_Q ? dT : dT + (size_t)NQ * L.Mp * 2;
+        const long cols = (dW_Q ? NQ : 0) + (dW_V ? NV : 0);
+        s = prod(xT, L.Mp, 0, Wt, L.Mp, 0, L.Mp, d_model, cols, dW_Q ? dW_Q : dW_V,
+                 dW_Q ? NQ : NV, 0, dW_Q ? NQ : cols, dW_V ? dW_V : dW_Q, NV, 1);
+      }
+    }
+    if (s == KL_OK && dW_R) {
+      // Q = X W^Q (into the [dQ^T ; dV^T] buffer, whose product above has run:
+      // the stream orders them), Q^T and dQ~^T with zero token padding, then
+      // Eq. 5: dW^R_h = Q_h^T dQ~_h, a contraction over the tokens batched over
+      // the heads.
+      void* Qm = dT;  // [M, NQ]
+      s = tr(W_Q, NQ, d_model, NQ, WQT, d_model, d_model);
+      if (s == KL_OK)
+        s = prod(x, d_model, 0, WQT, d_model, 0, d_model, M, NQ, Qm, NQ, 0, NQ, Qm, NQ, 1);
+      if (s == KL_OK) s = tr(Qm, NQ, M, NQ, QT, L.Mp, L.Mp);
+      if (s == KL_OK) s = tr(dq_routed, NQ, M, NQ, dqT, L.Mp, L.Mp);
+      if (s == KL_OK) {
+        // Item (h, z): rows of head h, tokens of chunk z; fp32 partials, then
+        // their sum in chunk order.
+        const long Kc = L.Mp / L.S;
+        kl::GemmBf16Args a{};
+        a.A0 = QT;
+        a.lda0 = L.Mp;
+        a.W0 = dqT;
+        a.ldw0 = L.Mp;
+        a.K0 = (int)Kc;
+        a.M = (int)dk;
+        a.N = (int)dk;
+        a.n_split = (int)dk;
+        a.C0 = part;
+        a.ldc0 = dk;
+        a.C1 = part;
+        a.ldc1 = dk;
+        a.batch = H;
+        a.sA0 = dk * L.Mp;
+        a.sW0 = dk * L.Mp;
+        a.sC0 = dk * dk;
+        a.sC1 = dk * dk;
+        a.zbatch = (int)L.S;
+        a.zA0 = Kc;
+        a.zW0 = Kc;
+        a.zC0 = H * dk * dk;
+        a.c_f32 = 1;
+        s = mm(a);
+        if (s == KL_OK)
+          s = hip_status(kl::launch_sum_partials_bf16(part, (int)L.S, (size_t)H * dk * dk, dW_R, st),
+                         who);
+      }
+    }
+    if (s == KL_OK && dx) {
+      // dx = dQ W^Q^T + dV W^V^T in one k loop (W^Q, W^V as stored are the
+      // [n][k] operands).
+      kl::GemmBf16Args a{};
+      a.A0 = dQm;
+      a.lda0 = NQ;
+      a.W0 = W_Q;
+      a.ldw0 = NQ;
+      a.K0 = (int)NQ;
+      a.A1 = dv;
+      a.lda1 = NV;
+      a.W1 = W_V;
+      a.ldw1 = NV;
+      a.K1 = (int)NV;
+      a.M = (int)M;
+      a.N = d_model;
+      a.n_split = d_model;
+      a.C0 = dx;
+      a.ldc0 = d_model;
+      a.C1 = dx;
+      a.ldc1 = d_model;
+      s = mm(a);
+    }
+    return s;
+  }
+  // The generic form. With no tokens (M = 0) the contractions over tokens have
+  // K = 0 and write zero weight gradients; the token-shaped outputs are empty.
+  void* Q = w;                                                   // X W^Q       [M, NQ]
+  void* dQ = w + align256((size_t)M * NQ * elem_bytes(dtype));    // dQ~ W^R^T   [M, NQ]
   int s = KL_OK;
   // dQ_h = dQ~_h (W^R_h)^T: B(k, n) = W^R_h[n][k].
   if (dW_Q || dx) s = gemm(dq_routed, NQ, 1, W_R, 1, dk, dQ, NQ, M, dk, dk, H, dk, dk * dk, dk, 0);

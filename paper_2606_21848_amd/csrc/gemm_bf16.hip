@@ -1,11 +1,14 @@
 // bf16 MFMA GEMM for the prefill projections [Q~ | V] = X [W~^Q | W^V]
-// (Eq. 2: no key projection), against weights packed once before inference.
+// (Eq. 2: no key projection), against weights packed once before inference,
+// and for the large products of the backward pass through the projections.
 //
-// C (M x N) = A (M x K) * Wp^T, where A = X is row-major [M, K] and Wp is the
-// packed weight [N, K] (row n = output column n, K contiguous): both operands
-// are K-major, which is the layout the MFMA fragments want. Columns below
-// n_split go to C0 (the routed queries), the rest to C1 (the values).
-// fp32 accumulation in v_mfma_f32_16x16x32_bf16, one rounding to bf16 on store.
+// C (M x N) = A0 W0^T + A1 W1^T, where A0 [M, K0] and W0 [N, K0] (row n =
+// output column n) are both K-major, the layout the MFMA fragments want; the
+// optional second term (K1 > 0) continues the same k loop on another pair of
+// operands. For the projections A0 = X, W0 = the packed weights and K1 = 0.
+// Columns below n_split go to C0 (the routed queries), the rest to C1 (the
+// values). fp32 accumulation in v_mfma_f32_16x16x32_bf16, one rounding to
+// bf16 on store.
 //
 // Tile 256 x 256 x 64, 16 waves (4 x 4), each wave 64 x 64 of C (64 fp32
 // accumulators per lane, four waves per SIMD: while some waves restart a k-tile
@@ -37,13 +40,17 @@ constexpr int TILE_BYTES = 256 * BK * 2;  // one operand tile, 32 KiB
 static_assert(BK == 64, "the fragment schedule assumes two 32-wide k-steps per tile");
 
 struct GemmParams2 {
-  const uint16_t* A;   // [M, K]
-  const uint16_t* W;   // [N, K] packed
-  uint16_t* C0;        // columns [0, n_split)
-  uint16_t* C1;        // columns [n_split, N)
-  int M, N, K, n_split;
-  long lda;            // A row stride (elements)
+  const uint16_t* A0;  // [M, K0], row stride lda0 (elements)
+  const uint16_t* W0;  // [N, K0], row stride ldw0
+  const uint16_t* A1;  // [M, K1], row stride lda1 (K1 = 0: no second term)
+  const uint16_t* W1;  // [N, K1], row stride ldw1
+  void* C0;            // columns [0, n_split): bf16, or fp32 for the F32 form
+  void* C1;            // columns [n_split, N)
+  int M, N, K0, K1, n_split;
+  long lda0, ldw0, lda1, ldw1;
   long ldc0, ldc1;
+  long sA0, sW0, sC0, sC1;  // element strides between batch items (blockIdx.y)
+  long zA0, zW0, zC0;       // and along blockIdx.z (a second batch index)
 };
 
 // Byte offset of (row, 16-byte chunk) inside a swizzled operand tile.
@@ -53,10 +60,23 @@ __device__ __forceinline__ int swz(int row, int chunk) {
 
 // Four waves per SIMD (the 128 KiB of LDS allow one workgroup per CU): the
 // register budget is 128, the accumulators and one k-step's fragments.
+// TWO: the second term is present (one more pair of copy offsets per lane and
+// a uniform choice per k-tile; the projections take the plain form). F32: the
+// outputs are stored in fp32 (partial products of a split contraction).
+template <bool TWO, bool F32>
 __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(4, 4)))
 void gemm_bf16_kernel(GemmParams2 p) {
+  using CT = std::conditional_t<F32, float, uint16_t>;
   const int tilesM = (p.M + BM - 1) / BM, tilesN = (p.N + BN - 1) / BN;
   const int ntiles = tilesM * tilesN;
+  CT* C0 = static_cast<CT*>(p.C0);
+  CT* C1 = static_cast<CT*>(p.C1);
+  if (blockIdx.y > 0 || blockIdx.z > 0) {  // batch item: the first term's operands and the outputs move
+    p.A0 += (size_t)blockIdx.y * p.sA0 + (size_t)blockIdx.z * p.zA0;
+    p.W0 += (size_t)blockIdx.y * p.sW0 + (size_t)blockIdx.z * p.zW0;
+    C0 += (size_t)blockIdx.y * p.sC0 + (size_t)blockIdx.z * p.zC0;
+    C1 += (size_t)blockIdx.y * p.sC1 + (size_t)blockIdx.z * p.zC0;
+  }
   int wg = blockIdx.x;
   // XCD-aware order: hardware places workgroup i on XCD i % 8.
   if ((ntiles & 7) == 0) wg = (wg & 7) * (ntiles >> 3) + (wg >> 3);
@@ -79,26 +99,33 @@ void gemm_bf16_kernel(GemmParams2 p) {
   // lane L landing at byte 16 L, i.e. row L / 8, physical chunk L % 8, which
   // holds logical chunk (L % 8) ^ ((row >> 1) & 7). Each wave fills 2 row groups
   // of each operand. Rows past the end are clamped: they only feed output rows
-  // or columns that are never stored.
-  uint32_t offA[2], offW[2];
+  // or columns that are never stored. Per-lane byte offsets for each term.
+  constexpr int NT = TWO ? 2 : 1;
+  uint32_t offA[NT][2], offW[NT][2];  // [term][row group]
 #pragma unroll
   for (int i = 0; i < 2; ++i) {
     const int r = (i * 16 + wave) * 8 + (lane >> 3);
     const int lc = (lane & 7) ^ ((r >> 1) & 7);
     const int ra = min(m0 + r, p.M - 1), rw = min(n0 + r, p.N - 1);
-    offA[i] = (uint32_t)(((size_t)ra * p.lda + lc * 8) * 2);
-    offW[i] = (uint32_t)(((size_t)rw * p.K + lc * 8) * 2);
+    offA[0][i] = (uint32_t)(((size_t)ra * p.lda0 + lc * 8) * 2);
+    offW[0][i] = (uint32_t)(((size_t)rw * p.ldw0 + lc * 8) * 2);
+    if constexpr (TWO) {
+      offA[NT - 1][i] = (uint32_t)(((size_t)ra * p.lda1 + lc * 8) * 2);
+      offW[NT - 1][i] = (uint32_t)(((size_t)rw * p.ldw1 + lc * 8) * 2);
+    }
   }
-  const unsigned char* gA = reinterpret_cast<const unsigned char*>(p.A);
-  const unsigned char* gW = reinterpret_cast<const unsigned char*>(p.W);
-  auto issue = [&](lds_u8* sa, lds_u8* sw, int k0) {
-    const unsigned char* ga = gA + (size_t)k0 * 2;
-    const unsigned char* gw = gW + (size_t)k0 * 2;
+  const int nk0 = p.K0 / BK;  // k-tiles of the first term
+  // Copies of k-tile kt (of the concatenated k range) into one stage.
+  auto issue = [&](lds_u8* sa, lds_u8* sw, int kt) {
+    const bool second = TWO && kt >= nk0;  // uniform
+    const int k0 = (second ? kt - nk0 : kt) * BK;
+    const unsigned char* ga = reinterpret_cast<const unsigned char*>(second ? p.A1 : p.A0) + (size_t)k0 * 2;
+    const unsigned char* gw = reinterpret_cast<const unsigned char*>(second ? p.W1 : p.W0) + (size_t)k0 * 2;
 #pragma unroll
     for (int i = 0; i < 2; ++i) {
       const uint32_t grp_off = (uint32_t)((i * 16 + wave) * 1024);
-      copy_to_lds(ga, offA[i], (uint32_t)(uintptr_t)sa + grp_off);
-      copy_to_lds(gw, offW[i], (uint32_t)(uintptr_t)sw + grp_off);
+      copy_to_lds(ga, second ? offA[NT - 1][i] : offA[0][i], (uint32_t)(uintptr_t)sa + grp_off);
+      copy_to_lds(gw, second ? offW[NT - 1][i] : offW[0][i], (uint32_t)(uintptr_t)sw + grp_off);
     }
   };
 
@@ -135,7 +162,7 @@ void gemm_bf16_kernel(GemmParams2 p) {
   lds_u8* const base = (lds_u8*)smem;
   auto stageA = [&](int st) { return base + st * 2 * TILE_BYTES; };
   auto stageW = [&](int st) { return base + st * 2 * TILE_BYTES + TILE_BYTES; };
-  const int nk = p.K / BK;
+  const int nk = TWO ? nk0 + p.K1 / BK : nk0;
   issue(stageA(0), stageW(0), 0);
   // One barrier per k-tile. Before it, each wave waits for its copies of tile
   // kt (the only ones in flight) and for its own LDS reads of tile kt - 1 (the
@@ -147,7 +174,7 @@ void gemm_bf16_kernel(GemmParams2 p) {
     KL_WAIT_VMCNT(0);
     asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
     __syncthreads();
-    if (kt + 1 < nk) issue(stageA(cur ^ 1), stageW(cur ^ 1), (kt + 1) * BK);
+    if (kt + 1 < nk) issue(stageA(cur ^ 1), stageW(cur ^ 1), kt + 1);
     compute(stageA(cur), stageW(cur));
   }
 
@@ -159,13 +186,13 @@ void gemm_bf16_kernel(GemmParams2 p) {
     for (int j = 0; j < 4; ++j) {
       const int col = n0 + wn * 64 + j * 16 + fr;
       if (col >= p.N) continue;
-      uint16_t* dst;
+      CT* dst;
       long ldc;
       if (col < p.n_split) {
-        dst = p.C0 + col;
+        dst = C0 + col;
         ldc = p.ldc0;
       } else {
-        dst = p.C1 + (col - p.n_split);
+        dst = C1 + (col - p.n_split);
         ldc = p.ldc1;
       }
 #pragma unroll
@@ -173,8 +200,10 @@ void gemm_bf16_kernel(GemmParams2 p) {
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
           const int row = m0 + wm * 64 + i * 16 + grp * 4 + r;
-          if (!CHECK || row < p.M)
-            dst[(size_t)row * ldc] = __builtin_bit_cast(uint16_t, (__bf16)acc[i][j][r]);
+          if (!CHECK || row < p.M) {
+            if constexpr (F32) dst[(size_t)row * ldc] = acc[i][j][r];
+            else dst[(size_t)row * ldc] = __builtin_bit_cast(uint16_t, (__bf16)acc[i][j][r]);
+          }
         }
     }
   };
@@ -184,42 +213,131 @@ void gemm_bf16_kernel(GemmParams2 p) {
 
 }  // namespace
 
-const char* gemm_bf16_unsupported(int M, int N, int K, long lda, long ldc0, long ldc1) {
-  if (M <= 0 || N <= 0) return "empty product";
-  if (K < BK || K % BK != 0) return "d_model must be a positive multiple of 64 for bf16";
-  if (lda % 8 != 0 || lda < K) return "the row stride of x must be a multiple of 8 and >= d_model";
-  if (ldc0 <= 0 || ldc1 <= 0) return "output row strides must be positive";
+const char* gemm_bf16_unsupported(const GemmBf16Args& a) {
+  if (a.M <= 0 || a.N <= 0) return "empty product";
+  if (a.K0 < BK || a.K0 % BK != 0 || a.K1 < 0 || a.K1 % BK != 0)
+    return "the contraction lengths must be multiples of 64 (the first one positive)";
+  if (a.lda0 % 8 != 0 || a.lda0 < a.K0 || a.ldw0 % 8 != 0 || a.ldw0 < a.K0)
+    return "operand row strides must be multiples of 8 and at least the contraction length";
+  if (a.K1 > 0 && (a.lda1 % 8 != 0 || a.lda1 < a.K1 || a.ldw1 % 8 != 0 || a.ldw1 < a.K1))
+    return "operand row strides must be multiples of 8 and at least the contraction length";
+  if (a.ldc0 <= 0 || a.ldc1 <= 0) return "output row strides must be positive";
+  if ((a.batch > 1 || a.zbatch > 1) &&
+      (a.K1 > 0 || a.batch > 65535 || a.zbatch > 65535 || a.sA0 % 8 != 0 || a.sW0 % 8 != 0 ||
+       a.zA0 % 8 != 0 || a.zW0 % 8 != 0))
+    return "a batched product has one term, at most 65535 items per index, and 16-byte aligned items";
+  if (a.c_f32 && a.K1 > 0) return "fp32 outputs are for one-term products";
   // Operand offsets are 32-bit byte offsets.
-  if ((size_t)M * lda * 2 >= (1ull << 32) || (size_t)N * K * 2 >= (1ull << 32))
-    return "x or the packed weights exceed 4 GiB (32-bit operand offsets)";
+  const size_t lim = 1ull << 32;
+  if ((size_t)a.M * a.lda0 * 2 >= lim || (size_t)a.N * a.ldw0 * 2 >= lim ||
+      (a.K1 > 0 && ((size_t)a.M * a.lda1 * 2 >= lim || (size_t)a.N * a.ldw1 * 2 >= lim)))
+    return "an operand exceeds 4 GiB (32-bit operand offsets)";
   return nullptr;
+}
+
+const char* gemm_bf16_unsupported(int M, int N, int K, long lda, long ldc0, long ldc1) {
+  GemmBf16Args a{};
+  a.M = M;
+  a.N = N;
+  a.K0 = K;
+  a.lda0 = lda;
+  a.ldw0 = K;
+  a.ldc0 = ldc0;
+  a.ldc1 = ldc1;
+  const char* why = gemm_bf16_unsupported(a);
+  if (why && (K < BK || K % BK != 0)) return "d_model must be a positive multiple of 64 for bf16";
+  if (why && (lda % 8 != 0 || lda < K))
+    return "the row stride of x must be a multiple of 8 and >= d_model";
+  return why;
 }
 
 constexpr size_t kGemmLds = 4 * TILE_BYTES;
 
-hipError_t launch_gemm_bf16_packed(const void* A, int M, int K, long lda, const void* Wp, int N,
-                                   int n_split, void* C0, long ldc0, void* C1, long ldc1,
-                                   hipStream_t st) {
-  static std::atomic<uint32_t> attr_done{0};
+hipError_t launch_gemm_bf16(const GemmBf16Args& a, hipStream_t st) {
+  static std::atomic<uint32_t> attr_one{0}, attr_two{0}, attr_f32{0};
+  const void* kern = a.K1 > 0 ? (const void*)gemm_bf16_kernel<true, false>
+                   : a.c_f32  ? (const void*)gemm_bf16_kernel<false, true>
+                              : (const void*)gemm_bf16_kernel<false, false>;
   {
-    hipError_t e = set_max_lds((const void*)gemm_bf16_kernel, (int)kGemmLds, attr_done);
+    hipError_t e = set_max_lds(kern, (int)kGemmLds,
+                               a.K1 > 0 ? attr_two : (a.c_f32 ? attr_f32 : attr_one));
     if (e != hipSuccess) return e;
   }
   GemmParams2 p{};
-  p.A = static_cast<const uint16_t*>(A);
-  p.W = static_cast<const uint16_t*>(Wp);
-  p.C0 = static_cast<uint16_t*>(C0);
-  p.C1 = static_cast<uint16_t*>(C1);
-  p.M = M;
-  p.N = N;
-  p.K = K;
-  p.n_split = n_split;
-  p.lda = lda;
-  p.ldc0 = ldc0;
-  p.ldc1 = ldc1;
-  const int tiles = ((M + BM - 1) / BM) * ((N + BN - 1) / BN);
-  hipLaunchKernelGGL(gemm_bf16_kernel, dim3(tiles), dim3(kThreads), kGemmLds, st, p);
+  p.A0 = static_cast<const uint16_t*>(a.A0);
+  p.W0 = static_cast<const uint16_t*>(a.W0);
+  p.A1 = static_cast<const uint16_t*>(a.K1 > 0 ? a.A1 : a.A0);
+  p.W1 = static_cast<const uint16_t*>(a.K1 > 0 ? a.W1 : a.W0);
+  p.C0 = a.C0;
+  p.C1 = a.C1;
+  p.M = a.M;
+  p.N = a.N;
+  p.K0 = a.K0;
+  p.K1 = a.K1;
+  p.n_split = a.n_split;
+  p.lda0 = a.lda0;
+  p.ldw0 = a.ldw0;
+  p.lda1 = a.K1 > 0 ? a.lda1 : a.lda0;
+  p.ldw1 = a.K1 > 0 ? a.ldw1 : a.ldw0;
+  p.ldc0 = a.ldc0;
+  p.ldc1 = a.ldc1;
+  p.sA0 = a.sA0;
+  p.sW0 = a.sW0;
+  p.sC0 = a.sC0;
+  p.sC1 = a.sC1;
+  p.zA0 = a.zA0;
+  p.zW0 = a.zW0;
+  p.zC0 = a.zC0;
+  const int tiles = ((a.M + BM - 1) / BM) * ((a.N + BN - 1) / BN);
+  const dim3 grid(tiles, a.batch > 1 ? a.batch : 1, a.zbatch > 1 ? a.zbatch : 1);
+  if (a.K1 > 0)
+    hipLaunchKernelGGL((gemm_bf16_kernel<true, false>), grid, dim3(kThreads), kGemmLds, st, p);
+  else if (a.c_f32)
+    hipLaunchKernelGGL((gemm_bf16_kernel<false, true>), grid, dim3(kThreads), kGemmLds, st, p);
+  else
+    hipLaunchKernelGGL((gemm_bf16_kernel<false, false>), grid, dim3(kThreads), kGemmLds, st, p);
   return hipGetLastError();
+}
+
+namespace {
+
+// out[i] = bf16(sum over s < S of part[s n + i]), in order of s.
+__global__ __launch_bounds__(256) void sum_partials_kernel(const float* __restrict__ part, int S,
+                                                           size_t n, uint16_t* __restrict__ out) {
+  const size_t i = (size_t)blockIdx.x * 256 + threadIdx.x;
+  if (i >= n) return;
+  float acc = 0.f;
+  for (int s = 0; s < S; ++s) acc += part[(size_t)s * n + i];
+  out[i] = __builtin_bit_cast(uint16_t, (__bf16)acc);
+}
+
+}  // namespace
+
+hipError_t launch_sum_partials_bf16(const float* part, int S, size_t n, void* out, hipStream_t st) {
+  if (n == 0) return hipSuccess;
+  if (S <= 0) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(sum_partials_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, st, part,
+                     S, n, static_cast<uint16_t*>(out));
+  return hipGetLastError();
+}
+
+hipError_t launch_gemm_bf16_packed(const void* A, int M, int K, long lda, const void* Wp, int N,
+                                   int n_split, void* C0, long ldc0, void* C1, long ldc1,
+                                   hipStream_t st) {
+  GemmBf16Args a{};
+  a.A0 = A;
+  a.lda0 = lda;
+  a.W0 = Wp;
+  a.ldw0 = K;
+  a.K0 = K;
+  a.M = M;
+  a.N = N;
+  a.n_split = n_split;
+  a.C0 = C0;
+  a.ldc0 = ldc0;
+  a.C1 = C1;
+  a.ldc1 = ldc1;
+  return launch_gemm_bf16(a, st);
 }
 
 }  // namespace kl

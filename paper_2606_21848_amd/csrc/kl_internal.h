@@ -114,13 +114,53 @@ struct GemmParams {
 
 hipError_t launch_gemm_simple(const GemmParams& p, hipStream_t stream);
 
-// bf16 MFMA GEMM against packed weights: C = A (M x K, row-major) * Wp^T with
-// Wp [N, K] (K contiguous). Columns < n_split go to C0, the rest to C1.
+// bf16 MFMA GEMM: C (M x N) = A0 W0^T + A1 W1^T with A0 [M, K0], W0 [N, K0],
+// A1 [M, K1], W1 [N, K1] (K contiguous in all four; K1 = 0 drops the second
+// term). Columns < n_split go to C0, the rest to C1, bf16. Operand pointers
+// must be 16-byte aligned.
+struct GemmBf16Args {
+  const void* A0;
+  long lda0;
+  const void* W0;
+  long ldw0;
+  int K0;
+  const void* A1;
+  long lda1;
+  const void* W1;
+  long ldw1;
+  int K1;
+  int M, N, n_split;
+  void* C0;
+  long ldc0;
+  void* C1;
+  long ldc1;
+  // Batched (one term only): item (b, z) reads A0 + b sA0 + z zA0,
+  // W0 + b sW0 + z zW0 and writes C0 + b sC0 + z zC0 (C1 likewise with sC1),
+  // element strides; b < batch, z < zbatch.
+  int batch;
+  long sA0, sW0, sC0, sC1;
+  int zbatch;
+  long zA0, zW0, zC0;
+  int c_f32;  // nonzero: C0, C1 are fp32 (one-term products)
+};
+// out[i] = bf16(sum over s < S of part[s n + i]) for i < n.
+hipError_t launch_sum_partials_bf16(const float* part, int S, size_t n, void* out,
+                                    hipStream_t stream);
 // nullptr when the bf16 GEMM handles the shape, else the reason it does not.
+const char* gemm_bf16_unsupported(const GemmBf16Args& a);
+hipError_t launch_gemm_bf16(const GemmBf16Args& a, hipStream_t stream);
+// The projection form: C = A (M x K, row-major) * Wp^T with Wp [N, K].
 const char* gemm_bf16_unsupported(int M, int N, int K, long lda, long ldc0, long ldc1);
 hipError_t launch_gemm_bf16_packed(const void* A, int M, int K, long lda, const void* Wp, int N,
                                    int n_split, void* C0, long ldc0, void* C1, long ldc1,
                                    hipStream_t stream);
+
+// dst[c][r] = src[r][c] for r < rows, c < cols (bf16); dst columns r in
+// [rows, rows_pad) are written as zeros. Row strides in elements; `batch`
+// matrices s_src and s_dst elements apart.
+hipError_t launch_transpose_bf16(const void* src, long ld_src, int rows, int cols, void* dst,
+                                 long ld_dst, int rows_pad, hipStream_t stream, int batch = 1,
+                                 long s_src = 0, long s_dst = 0);
 
 // Packed projection weights: rows [0, H d) = (W^Q W^R per head)^T (or W^Q^T
 // when W_R is null), rows [H d, (H+G) d) = W^V^T; each row has d_model entries.

@@ -127,6 +127,70 @@ def test_layer_backward_matches_oracle(lib, dtype, B, N, d, H, G, dk):
     assert_parity(grads["dW_V"].T, ref["dW_V"].T, dtype, "dW^V (Eq. 6)", FLOOR)
     assert_parity(grads["dW_Q"].T, ref["dW_Q"].T, dtype, "dW^Q", FLOOR)
     assert_parity(grads["dX"], ref["dX"], dtype, "dX", FLOOR)
+    # The projection gradients against the oracle's on the attention gradients
+    # the GPU produced (the same bits).
+    same = K.keyless_projection_gradients(to64(x), to64(W_Q), to64(W_R), to64(W_V), to64(dq),
+                                          to64(dv), H, G, dk)
+    assert_parity(grads["dW_R"], same["dW_R"], dtype, "dW^R, same inputs", FLOOR)
+    assert_parity(grads["dW_V"].T, same["dW_V"].T, dtype, "dW^V, same inputs", FLOOR)
+    assert_parity(grads["dW_Q"].T, same["dW_Q"].T, dtype, "dW^Q, same inputs", FLOOR)
+    assert_parity(grads["dX"], same["dX"], dtype, "dX, same inputs", FLOOR)
+
+
+@pytest.mark.parametrize("dtype", [torch.float32, torch.bfloat16])
+@pytest.mark.parametrize("B,N,d,H,G,dk", [(2, 130, 256, 4, 2, 64), (1, 100, 200, 2, 2, 64),
+                                          (3, 33, 320, 4, 4, 128), (1, 1, 64, 2, 1, 64)])
+def test_weight_gradients_match_oracle(lib, dtype, B, N, d, H, G, dk):
+    """keyless_weight_gradients on given attention gradients against the oracle
+    on the same inputs: token counts that are not multiples of 64 (padded for
+    the contractions over tokens), d_model that is not (padded for dW^R),
+    grouped values, and a single token."""
+    say(f"weight gradients dtype={dtype} B={B} N={N} d={d} H={H} G={G} dk={dk}")
+    x = synth.normal((B, N, d), 92, 1, 1.0, dtype)
+    W_Q = synth.normal((d, H * dk), 92, 2, d ** -0.5, dtype)
+    W_R = synth.normal((H, dk, dk), 92, 3, dk ** -0.5, dtype)
+    W_V = synth.normal((d, G * dk), 92, 4, d ** -0.5, dtype)
+    dq = synth.normal((B, N, H, dk), 92, 5, 1.0, dtype)
+    dv = synth.normal((B, N, G, dk), 92, 6, 1.0, dtype)
+    grads = kb.keyless_weight_gradients(*(t.to(DEV) for t in (x, W_Q, W_R, W_V, dq, dv)), H, G)
+    torch.cuda.synchronize()
+    ref = K.keyless_projection_gradients(to64(x), to64(W_Q), to64(W_R), to64(W_V), to64(dq),
+                                         to64(dv), H, G, dk)
+    assert_parity(grads["dW_R"], ref["dW_R"], dtype, "dW^R (Eq. 5)", FLOOR)
+    assert_parity(grads["dW_V"].T, ref["dW_V"].T, dtype, "dW^V (Eq. 6)", FLOOR)
+    assert_parity(grads["dW_Q"].T, ref["dW_Q"].T, dtype, "dW^Q", FLOOR)
+    assert_parity(grads["dX"], ref["dX"], dtype, "dX", FLOOR)
+
+
+def test_weight_gradients_full_size_sampled(lib):
+    """keyless_weight_gradients at the size the benchmark times (8192 tokens,
+    d_model 4096, 32 + 32 heads x 128, bf16): the weight gradients of two query
+    heads and two value groups over every token, and dX on sampled tokens,
+    against the oracle on the same inputs. Each of those depends only on its own
+    heads (or its own token), so the oracle runs on that slice."""
+    B, N, d, H, G, dk = 1, 8192, 4096, 32, 32, 128
+    say(f"weight gradients full size B={B} N={N} d={d} H={H} G={G} dk={dk}")
+    bf = torch.bfloat16
+    x = synth.normal((B, N, d), 91, 1, 1.0, bf)
+    W_Q = synth.normal((d, H * dk), 91, 2, d ** -0.5, bf)
+    W_R = synth.normal((H, dk, dk), 91, 3, dk ** -0.5, bf)
+    W_V = synth.normal((d, G * dk), 91, 4, d ** -0.5, bf)
+    dq = synth.normal((B, N, H, dk), 91, 5, 1.0, bf)
+    dv = synth.normal((B, N, G, dk), 91, 6, 1.0, bf)
+    grads = kb.keyless_weight_gradients(*(t.to(DEV) for t in (x, W_Q, W_R, W_V, dq, dv)), H, G)
+    torch.cuda.synchronize()
+    heads = [0, H - 1]
+    qcols = np.concatenate([np.arange(h * dk, (h + 1) * dk) for h in heads])
+    ref = K.keyless_projection_gradients(to64(x), to64(W_Q)[:, qcols], to64(W_R)[heads],
+                                         to64(W_V)[:, qcols], to64(dq)[:, :, heads],
+                                         to64(dv)[:, :, heads], len(heads), len(heads), dk)
+    assert_parity(grads["dW_Q"][:, qcols].T, ref["dW_Q"].T, bf, "dW^Q, two heads", FLOOR)
+    assert_parity(grads["dW_R"][heads], ref["dW_R"], bf, "dW^R (Eq. 5), two heads", FLOOR)
+    assert_parity(grads["dW_V"][:, qcols].T, ref["dW_V"].T, bf, "dW^V (Eq. 6), two groups", FLOOR)
+    rows = sorted(set([0, N - 1] + synth.uniform_int(14, 1, N - 2, 91, 7).tolist()))
+    refx = K.keyless_projection_gradients(to64(x)[:, rows], to64(W_Q), to64(W_R), to64(W_V),
+                                          to64(dq)[:, rows], to64(dv)[:, rows], H, G, dk)
+    assert_parity(grads["dX"][:, rows], refx["dX"], bf, "dX, sampled tokens", FLOOR)
 
 
 def test_backward_full_size_sampled(lib):

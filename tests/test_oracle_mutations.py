@@ -56,9 +56,9 @@ MUTATIONS = [
      "dS = P * (dP + np.sum(P * dP, axis=1, keepdims=True))", "softmax backward sign"),
     ("keyless_attention_backward", "dQr[b, :, h, :] = tau * (dS @ V_g)",
      "dQr[b, :, h, :] = dS @ V_g", "routed-query gradient without the scale"),
-    ("keyless_backward", "dW_R[h] += Q_h.T @ dQr[b, :, h, :]",
+    ("keyless_projection_gradients", "dW_R[h] += Q_h.T @ dQr[b, :, h, :]",
      "dW_R[h] += dQr[b, :, h, :].T @ Q_h", "routing gradient transposed (Eq. 5)"),
-    ("keyless_backward", "dQ[b, :, h, :] = dQr[b, :, h, :] @ W_R[h].T",
+    ("keyless_projection_gradients", "dQ[b, :, h, :] = dQr[b, :, h, :] @ W_R[h].T",
      "dQ[b, :, h, :] = dQr[b, :, h, :] @ W_R[h]", "query gradient through W^R untransposed"),
     ("attention_logsumexp", "out[b, h] = (m + np.log(", "out[b, h] = (np.log(",
      "log-sum-exp without its shift"),
