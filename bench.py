@@ -847,34 +847,25 @@ def extra_measurements(torch, kb, configs, dev):
     st = call_stats(lambda i: kb.keyless_weight_gradients(wx, wq, wr, wv, wdq, wdv, Hw, Gw,
                                                           workspace=wws), STAT_CALLS, 3, torch)
     Mw, NQw, NVw = Bw * Nw, Hw * dkw, Gw * dkw
-    # The products of the form computed: X^T [dQ~ | dV], [dQ~ | dV] [W~^Q | W^V]^T, and
-    # the three per-head ones (dW^Q_h, dW^R_h, the fold W^Q_h W^R_h).
-    flops = 2 * Mw * dw * (NQw + NVw) * 2 + 3 * 2 * dw * NQw * dkw
-    # The oracle on a sample: two query heads and two value groups over every token.
-    heads = [0, Hw - 1]
-    qcols = np.concatenate([np.arange(h * dkw, (h + 1) * dkw) for h in heads])
-    sx, swq, swr, swv = np64(wx), np64(wq)[:, qcols], np64(wr)[heads], np64(wv)[:, qcols]
-    sdq, sdv = np64(wdq)[:, :, heads], np64(wdv)[:, :, heads]
+    # The definition's products (Section 2.3): Q = X W^Q, dQ = dQ~ W^R^T, dW^R = Q^T dQ~,
+    # dW^Q = X^T dQ, dW^V = X^T dV, dX = dQ W^Q^T + dV W^V^T.
+    flops = 2 * Mw * dw * NQw + 2 * 2 * Mw * NQw * dkw + 2 * 2 * Mw * dw * (NQw + NVw)
+    # The oracle on the whole workload (its contractions are BLAS products).
+    sx, swq, swr, swv, sdq, sdv = (np64(t) for t in (wx, wq, wr, wv, wdq, wdv))
     with Threads(cores):
         t0 = time.perf_counter()
-        K.keyless_projection_gradients(sx, swq, swr, swv, sdq, sdv, 2, 2, dkw)
+        K.keyless_projection_gradients(sx, swq, swr, swv, sdq, sdv, Hw, Gw, dkw)
         el = time.perf_counter() - t0
-    w2 = 2 * dkw
-    # X W^Q_h, Q_h^T dQ~_h and dQ~_h W^R_h^T per head, X^T dQ, X^T dV, and dX.
-    sample_flop = 2 * Mw * dw * w2 + 2 * 2 * 2 * Mw * dkw * dkw + 2 * Mw * dw * w2 * 2 + \
-        2 * Mw * w2 * dw * 2
     res["weight_gradients_bf16"] = {
         "workload": "keyless_weight_gradients, batch 1, 8192 tokens, d_model 4096, 32 + 32 heads "
                     "x 128: dW^Q, dW^R (Eq. 5), dW^V (Eq. 6) and dX from dQ~ and dV",
         "ms": round(st["median_ms"], 4), "stats": st,
         "tflops": rate(st, flops, 1e-12),
         "frac_of_bf16_mfma_peak": round(rate(st, flops, 1e-12) / BF16_MFMA_PEAK_TFLOPS, 4),
-        "note": f"{flops / 1e12:.3f} TFLOP: the products of the computed form (transposes of X, "
-                "dQ~, dV, G = X^T dQ~ and W^Q are not counted)",
-        "cpu_baseline": cpu_entry(round(sample_flop / el * 1e-12, 5), "TFLOP/s", cores,
-                                  f"a sample: the gradients of two query heads and two value "
-                                  f"groups over all 8192 tokens, {sample_flop / 1e9:.1f} GFLOP "
-                                  f"in {el:.1f} s")}
+        "note": f"{flops / 1e12:.3f} TFLOP: the products of the definition (the transposes the "
+                "matrix-core form adds are not counted)",
+        "cpu_baseline": cpu_entry(round(flops / el * 1e-12, 5), "TFLOP/s", cores,
+                                  f"the whole workload in float64, {el:.1f} s")}
     del wx, wq, wr, wv, wdq, wdv, wws, sx, swq, swr, swv, sdq, sdv
 
     # Paged grouped-head decode.
