@@ -296,6 +296,15 @@ def _grid(row):
         int(row.get("Grid_Size_Z", 1)))
 
 
+def _grid_label(row):
+    """The grid in work-items; X x Y x Z when the grid has more than one
+    dimension (batched launches of the same kernel and size then stay apart)."""
+    y, z = int(row.get("Grid_Size_Y", 1) or 1), int(row.get("Grid_Size_Z", 1) or 1)
+    if y == 1 and z == 1:
+        return _grid(row)
+    return f"{row.get('Grid_Size_X')} x {y} x {z}"
+
+
 def _short(name):
     short = name.replace("void ", "").replace("(anonymous namespace)::", "")
     return short[:short.rfind("(")] if "(" in short else short
@@ -394,7 +403,7 @@ def summarize_trace(trace_dir, steps, warmup, json_out=None):
         if "kl::" not in name:  # this library's kernels only (not the input generation)
             continue
         dur = (int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3
-        groups.setdefault((_short(name), _grid(r)), []).append(dur)
+        groups.setdefault((_short(name), _grid_label(r)), []).append(dur)
     print("| kernel | grid (work-items) | launches | avg us | median us | min us | max us |")
     print("|---|---|---|---|---|---|---|")
     for (name, grid), d in sorted(groups.items(), key=lambda kv: -sum(kv[1])):
