@@ -162,6 +162,37 @@ def test_weight_gradients_match_oracle(lib, dtype, B, N, d, H, G, dk):
     assert_parity(grads["dX"], ref["dX"], dtype, "dX", FLOOR)
 
 
+@pytest.mark.parametrize("wanted", [("dW_Q",), ("dW_V",), ("dW_R",), ("dX",), ("dW_Q", "dX"),
+                                    ("dW_R", "dW_V")])
+def test_weight_gradients_subsets(lib, wanted):
+    """Any of the four outputs may be skipped (NULL): each requested subset is
+    bit-equal to the same outputs of the full call, and skipped ones are not
+    written."""
+    B, N, d, H, G, dk = 1, 192, 256, 4, 2, 64
+    say(f"weight gradients subset {wanted}")
+    bf = torch.bfloat16
+    x, W_Q, W_R, W_V = (synth.normal(sh, 93, i + 1, sc, bf).to(DEV) for i, (sh, sc) in enumerate(
+        [((B, N, d), 1.0), ((d, H * dk), d ** -0.5), ((H, dk, dk), dk ** -0.5),
+         ((d, G * dk), d ** -0.5)]))
+    dq = synth.normal((B, N, H, dk), 93, 5, 1.0, bf).to(DEV)
+    dv = synth.normal((B, N, G, dk), 93, 6, 1.0, bf).to(DEV)
+    full = kb.keyless_weight_gradients(x, W_Q, W_R, W_V, dq, dv, H, G)
+    outs = {k: torch.full_like(v, 7.0) for k, v in full.items()}
+    ws = torch.empty(kb._lib.keyless_weight_gradients_workspace_size(B, N, d, H, G, dk, kb.KL_BF16),
+                     dtype=torch.uint8, device=DEV)
+    ptr = lambda k: kb._ptr(outs[k]) if k in wanted else None
+    kb._check(kb._lib.keyless_weight_gradients(
+        kb._ptr(x), kb._ptr(W_Q), kb._ptr(W_R), kb._ptr(W_V), kb._ptr(dq), kb._ptr(dv), B, N, d, H,
+        G, dk, kb.KL_BF16, ptr("dW_Q"), ptr("dW_R"), ptr("dW_V"), ptr("dX"), kb._ptr(ws),
+        ws.numel(), kb._stream(x)))
+    torch.cuda.synchronize()
+    for k in full:
+        if k in wanted:
+            assert torch.equal(outs[k], full[k]), f"{k} differs from the full call"
+        else:
+            assert bool((outs[k] == 7.0).all()), f"{k} was written although not requested"
+
+
 def test_weight_gradients_full_size_sampled(lib):
     """keyless_weight_gradients at the size the benchmark times (8192 tokens,
     d_model 4096, 32 + 32 heads x 128, bf16): the weight gradients of two query
