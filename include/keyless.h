@@ -280,14 +280,11 @@ size_t keyless_attention_backward_workspace_size(int B, int N, int H);
  * keyless_attention_backward. Outputs dW_Q, dW_R, dW_V (the weights' shapes) and
  * dx [B, N, d_model]; any of them may be NULL to skip it. ws, ws_bytes:
  * keyless_weight_gradients_workspace_size(...) bytes, 16-byte aligned.
- * bf16 with 16-byte aligned operands and d_head a multiple of 64 runs the
- * large products on the matrix cores (fp32 accumulation, bf16 rounding of the
- * intermediates X^T dq_routed and W_Q W_R): [X^T dq_routed | dW_V] in one
- * product over the tokens (after transposing x, dq_routed and dv), and
- * dx = dq_routed (W_Q W_R)^T + dv W_V^T in another; the per-head products with
- * a d_head-long side (dW_Q, dW_R, the fold) and every other case run on the
- * generic fp32-arithmetic kernel. Returns KL_ERR_WORKSPACE when the workspace
- * is too small.
+ * bf16 with 16-byte aligned inputs and workspace, and d_head and d_model
+ * multiples of 64, runs every product above on the matrix cores (fp32
+ * accumulation; X W^Q and dQ rounded to bf16 once, as stored intermediates);
+ * other cases run the same products on the generic fp32-arithmetic kernel.
+ * Returns KL_ERR_WORKSPACE when the workspace is too small.
  */
 int keyless_weight_gradients(const void* x, const void* W_Q, const void* W_R, const void* W_V,
                              const void* dq_routed, const void* dv, int B, int N, int d_model,
