@@ -98,7 +98,7 @@ int cache_capacity(const kl_value_cache* c) {
 //    Used while the tile count fits comfortably in 32 bits; beyond that the
 //    cache is split into chunks of 8192 rows.
 struct DecodePlan {
-  int chunk, S, waves;
+  int chunk, S;
   bool balanced;
 };
 
@@ -111,7 +111,6 @@ DecodePlan plan_decode(const kl_value_cache* c, int B, int chunk_rows) {
   const int cap = cache_capacity(c);
   const long pairs = (long)B * c->G;
   DecodePlan pl{};
-  pl.waves = 4;
   if (chunk_rows > 0) {
     pl.chunk = chunk_rows;
   } else if (c->layout == KL_CONTIGUOUS && pairs >= kComputeUnits) {
@@ -134,10 +133,6 @@ DecodePlan plan_decode(const kl_value_cache* c, int B, int chunk_rows) {
     pl.chunk = 8192;
   }
   pl.S = cap > 0 ? (cap + pl.chunk - 1) / pl.chunk : 1;
-  if (const char* w = getenv("KL_DECODE_WAVES")) {
-    const int v = atoi(w);
-    if (v == 4 || v == 8) pl.waves = v;
-  }
   return pl;
 }
 
@@ -229,7 +224,6 @@ int decode_common(const void* q, const kl_value_cache* k_cache, const kl_value_c
   p.max_blocks = v_cache->max_blocks_per_seq;
   p.chunk = pl.chunk;
   p.S = pl.S;
-  p.waves = pl.waves;
   p.scale_log2 = scale_or_default(scale, p.D) * kLog2e;
   p.ev_start = g_timer_start;
   p.ev_stop = g_timer_stop;

@@ -9,10 +9,11 @@
 // the lane group with DPP) and for the weighted sum acc += exp(s - m) v of the
 // online softmax. Nothing is re-read, so a value row crosses HBM once.
 //
-// With one split per sequence (enough (b, g) pairs to fill the chip) a wide
-// workgroup of 8 waves walks the whole cache of its pair and writes the output
-// directly. Otherwise each split emits (acc[D], m, l) in fp32 to the workspace
-// and decode_combine merges the splits of each (b, h) in split order.
+// With one split per sequence (enough (b, g) pairs to fill the chip) the
+// workgroup walks the whole cache of its pair and writes the output directly
+// (four waves: eight ran 3% slower on the batch-8 step). Otherwise each split
+// emits (acc[D], m, l) in fp32 to the workspace and decode_combine merges the
+// splits of each (b, h) in split order.
 
 #include "kl_device.h"
 #include "kl_internal.h"
@@ -917,26 +918,13 @@ hipError_t launch_t(const DecodeParams& p, hipStream_t st) {
   return e;
 }
 
-template <typename T, int D, int R, bool PAGED, bool KEYS>
-hipError_t pick_waves(const DecodeParams& p, hipStream_t st) {
-  switch (p.waves) {
-    case 4: return launch_t<T, D, R, PAGED, KEYS, 4>(p, st);
-    case 8:
-      // Fall back to 4 waves where an 8-wave ring, or the merge rows of 16 or
-      // more heads per group, would not fit in LDS.
-      if constexpr (Ring<T, D, KEYS, 8>::BYTES > 98304 || R >= 16)
-        return launch_t<T, D, R, PAGED, KEYS, 4>(p, st);
-      else return launch_t<T, D, R, PAGED, KEYS, 8>(p, st);
-    default: return hipErrorInvalidValue;
-  }
-}
-
 template <typename T, int D, int R>
 hipError_t pick_layout(const DecodeParams& p, hipStream_t st) {
+  constexpr int NW = 4;  // waves per workgroup
   const bool keys = p.kdata != nullptr;
   if (p.paged)
-    return keys ? pick_waves<T, D, R, true, true>(p, st) : pick_waves<T, D, R, true, false>(p, st);
-  return keys ? pick_waves<T, D, R, false, true>(p, st) : pick_waves<T, D, R, false, false>(p, st);
+    return keys ? launch_t<T, D, R, true, true, NW>(p, st) : launch_t<T, D, R, true, false, NW>(p, st);
+  return keys ? launch_t<T, D, R, false, true, NW>(p, st) : launch_t<T, D, R, false, false, NW>(p, st);
 }
 
 template <typename T, int D>

@@ -52,7 +52,6 @@ struct DecodeParams {
   int num_blocks, max_blocks;
   int chunk;              // rows per split (multiple of 64)
   int S;                  // splits per sequence (at most kMaxSplits)
-  int waves;              // waves per workgroup of the split kernel: 4 or 8
   bool balanced;          // balanced mode: nwg workgroups share the tiles of all pairs evenly
   int nwg;                // workgroups in balanced mode (at most kMaxSplits)
   float scale_log2;       // scale * log2(e)
