@@ -168,7 +168,7 @@ def rate(stats, work, unit_scale):
 
 
 # ---------------------------------------------------------------------------
-# CPU oracle baselines (the oracle as it stands, on the GPU machine's host cores)
+# CPU oracle baselines (the oracle as it stands, on the host's cores)
 # ---------------------------------------------------------------------------
 
 def host_cores():
