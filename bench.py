@@ -653,11 +653,20 @@ def main():
     print(json.dumps(result), flush=True)
 
 
+class _Results(dict):
+    """The extra measurements by workload; each one, once measured, is named on
+    stderr so that a long run shows its progress."""
+
+    def __setitem__(self, key, value):
+        super().__setitem__(key, value)
+        print(f"measured {key}", file=sys.stderr, flush=True)
+
+
 def extra_measurements(torch, kb, configs, dev):
     import numpy as np
     from oracle import keyless as K
     from workloads import synth
-    res = {}
+    res = _Results()
     cores = host_cores()
 
     def cpu_time(fn, secs=2.0, threads=None):
@@ -1004,6 +1013,61 @@ def extra_measurements(torch, kb, configs, dev):
     res["decode_b1_bf16"] = {"workload": "batch 1, 32 heads x 128, contiguous cache of 512 / 2048 "
                                          "/ 8192 rows: one fused decode step (the attention part of "
                                          "a layer's step)", "by_context": b1}
+
+    # The attention of the paper's decode testbed: 28 layers, 12 query heads over
+    # 2 value heads of 128, batch 1 (six heads per group, the matrix-core consumer),
+    # at its three contexts. A step is one token: 28 launches of the fused append +
+    # decode, each on its own layer's cache; the standard K+V decode over the same
+    # shape beside it. Each context rotates over enough copies of the 28 layers'
+    # caches to fill 512 MB of values, and the steps of one rotation are replayed
+    # from one captured HIP graph (eager, the host's 28 launches pace the step).
+    tb = {}
+    for L in (512, 2048, 8192):
+        per_step = 28 * 2 * L * 128 * 2
+        copies = max(1, -(-(512 << 20) // per_step))
+        t = configs.testbed_gqa_bf16(device=dev, L=L, copies=copies)
+        vcs = [kb.ValueCache(t["V"][i]) for i in range(28 * copies)]
+        kcs = [kb.ValueCache(t["K"][i]) for i in range(28 * copies)]
+        ws_t = torch.zeros(max(kb.decode_workspace_bytes(vcs[0], 1, 12), 256), dtype=torch.uint8,
+                           device=dev)
+        o_t = torch.empty_like(t["q"])
+
+        def kstep(i, t=t, vcs=vcs, ws_t=ws_t, o_t=o_t, copies=copies):
+            c = (i % copies) * 28
+            for layer in range(28):
+                kb.keyless_decode_append(t["q"][layer], t["v_new"][c + layer], vcs[c + layer],
+                                         t["lengths_before"], out=o_t[layer], workspace=ws_t)
+
+        def sstep(i, t=t, vcs=vcs, kcs=kcs, ws_t=ws_t, o_t=o_t, copies=copies):
+            c = (i % copies) * 28
+            for layer in range(28):
+                kb.standard_decode(t["q"][layer], kcs[c + layer], vcs[c + layer], t["lengths"],
+                                   out=o_t[layer], workspace=ws_t)
+        st_e = call_stats(kstep, 20, 3, torch)
+        st_k = graph_stats(kstep, 20, torch, per_graph=copies)
+        st_s = graph_stats(sstep, 20, torch, per_graph=copies)
+        qh_t = np64(t["q"][0])
+        vh_t = np64(t["V"][0])
+        cs, cn = cpu_time(lambda: K.keyless_decode(qh_t, vh_t, np.array([L]), 12, 2), 1.0)
+        tb[str(L)] = {
+            "keyless_step_us": round(st_k["median_ms"] * 1e3, 2), "keyless_stats": st_k,
+            "keyless_tokens_per_s": rate(st_k, 1, 1.0),
+            "keyless_cache_gbps": rate(st_k, per_step, 1e-9),
+            "standard_step_us": round(st_s["median_ms"] * 1e3, 2), "standard_stats": st_s,
+            "standard_tokens_per_s": rate(st_s, 1, 1.0),
+            "standard_cache_gbps": rate(st_s, 2 * per_step, 1e-9),
+            "keyless_eager_step_us": round(st_e["median_ms"] * 1e3, 2),
+            "cache_bytes_per_step": per_step, "step_copies_rotated": copies,
+            "cpu_baseline": cpu_entry(round(1.0 / (28 * cs), 2), "tokens/s", cores,
+                                      f"the decode of one layer (12 heads over {L} rows) x 28, "
+                                      f"median of {cn} runs")}
+        del t, vcs, kcs, ws_t, o_t, vh_t
+    res["testbed_gqa_bf16"] = {
+        "workload": "the paper's decode testbed attention: batch 1, 28 layers of 12 query heads "
+                    "over 2 value heads x 128 (6 heads per group), contiguous caches of 512 / "
+                    "2048 / 8192 rows; one token = 28 fused append + decode launches (standard: "
+                    "28 K+V decodes), replayed from a HIP graph",
+        "by_context": tb}
 
     # Head-to-head: keyless value-only vs standard K+V, same structure.
     hh = configs.head_to_head_bf16(device=dev)

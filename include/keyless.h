@@ -26,7 +26,8 @@
  *    to [0, capacity], treat block ids outside [0, num_blocks) as empty rows,
  *    and drop appended rows that fall beyond capacity, so bad device data can
  *    give wrong results but never an out-of-bounds access.
- *  - Supported: d_head in {64, 128}; H / G in {1, 2, 4, 8}; element type bf16
+ *  - Supported: d_head in {64, 128}; H / G any value for prefill, 1 to 8 for
+ *    decode (also 16 or 32 for a bf16 cache with d_head 128); element type bf16
  *    (stored as raw 16-bit words) or fp32; arithmetic is fp32 in both cases.
  */
 #ifndef KEYLESS_H_
@@ -322,8 +323,8 @@ int keyless_decode_project(const void* x, const void* packed, int B, int d_model
  * keyless_decode - one decode step over a value-only cache (Section 3):
  *   out[b,h] = sum_{i < lengths[b]} alpha_i v_i,
  *   alpha_i = exp(scale <q_routed[b,h], v_i>) / sum_j exp(scale <q_routed[b,h], v_j>)
- * with v_i the rows of group h / (H / G) of sequence b. H / G is 1, 2, 4 or 8,
- * and also 16 or 32 for a bf16 cache with d_head 128 (KL_ERR_UNSUPPORTED otherwise).
+ * with v_i the rows of group h / (H / G) of sequence b. H / G is 1 to 8, and
+ * also 16 or 32 for a bf16 cache with d_head 128 (KL_ERR_UNSUPPORTED otherwise).
  *   q_routed [B, H, d_head]  routed queries x W~^Q of the current tokens (cache dtype)
  *   cache    value-only cache descriptor (host pointer)
  *   lengths  [B] int32, device: rows per sequence, the current token's value

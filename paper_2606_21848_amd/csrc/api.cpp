@@ -150,10 +150,9 @@ size_t partials_bytes(const DecodePlan& pl, int B, int H, int G, int d_head) {
 // Query heads per cached group the decode kernels handle.
 int check_group_ratio(const char* who, const kl_value_cache* c, int R) {
   const bool wide_groups = c->dtype == KL_BF16 && c->d_head == 128;
-  if (R != 1 && R != 2 && R != 4 && R != 8 && !((R == 16 || R == 32) && wide_groups))
+  if (!(R >= 1 && R <= 8) && !((R == 16 || R == 32) && wide_groups))
     return fail(KL_ERR_UNSUPPORTED,
-                "%s: H/G=%d not supported (1, 2, 4 or 8; also 16 or 32 for bf16 with d_head 128)",
-                who, R);
+                "%s: H/G=%d not supported (1 to 8; also 16 or 32 for bf16 with d_head 128)", who, R);
   return KL_OK;
 }
 

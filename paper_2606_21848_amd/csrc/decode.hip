@@ -932,7 +932,11 @@ hipError_t pick_r(const DecodeParams& p, hipStream_t st) {
   switch (p.R) {
     case 1: return pick_layout<T, D, 1>(p, st);
     case 2: return pick_layout<T, D, 2>(p, st);
+    case 3: return pick_layout<T, D, 3>(p, st);
     case 4: return pick_layout<T, D, 4>(p, st);
+    case 5: return pick_layout<T, D, 5>(p, st);
+    case 6: return pick_layout<T, D, 6>(p, st);
+    case 7: return pick_layout<T, D, 7>(p, st);
     case 8: return pick_layout<T, D, 8>(p, st);
     case 16:
     case 32:

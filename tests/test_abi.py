@@ -74,6 +74,8 @@ def test_decode_rejects_bad_arguments(lib):
     expect(lib, decode(lib, cache(G=1), H=64), kb.KL_ERR_UNSUPPORTED, "H/G=64")
     expect(lib, decode(lib, cache(G=1, dtype=kb.KL_F32), H=16), kb.KL_ERR_UNSUPPORTED, "H/G=16")
     expect(lib, decode(lib, cache(G=1, d=64), H=32), kb.KL_ERR_UNSUPPORTED, "H/G=32")
+    expect(lib, decode(lib, cache(G=1), H=12), kb.KL_ERR_UNSUPPORTED, "H/G=12")
+    expect(lib, decode(lib, cache(G=1, dtype=kb.KL_F32), H=9), kb.KL_ERR_UNSUPPORTED, "H/G=9")
     expect(lib, decode(lib, cache(), ws_bytes=1000), kb.KL_ERR_WORKSPACE, "workspace")
     expect(lib, decode(lib, cache(), chunk=100), kb.KL_ERR_INVALID_ARG, "multiple of 64")
     expect(lib, decode(lib, cache(L_max=1 << 20), chunk=64), kb.KL_ERR_UNSUPPORTED, "splits")

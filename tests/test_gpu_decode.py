@@ -60,6 +60,14 @@ CASES = [
     (torch.float32, 64, 4, 4),
     (torch.float32, 128, 4, 2),
     (torch.float32, 64, 8, 1),
+    # Ratios that are not powers of two: 12 query heads over 2 value heads (the
+    # 1.5B model's attention shape), 3, 5 and 7 heads per group on both consumers.
+    (torch.bfloat16, 128, 12, 2),
+    (torch.bfloat16, 128, 21, 3),
+    (torch.bfloat16, 128, 5, 1),
+    (torch.bfloat16, 64, 6, 2),
+    (torch.float32, 128, 10, 2),
+    (torch.float32, 64, 7, 1),
 ]
 
 
@@ -122,7 +130,8 @@ def test_grouped_equals_mha_over_repeated_values(lib):
 
 
 @pytest.mark.parametrize("H,G,d,dtype", [(4, 2, 128, torch.bfloat16), (2, 2, 128, torch.bfloat16),
-                                         (4, 4, 64, torch.float32), (32, 1, 128, torch.bfloat16)])
+                                         (4, 4, 64, torch.float32), (32, 1, 128, torch.bfloat16),
+                                         (12, 2, 128, torch.bfloat16)])
 def test_balanced_mode_ragged_and_empty(lib, H, G, d, dtype):
     """Balanced mode (paged cache, library choice): the workgroups' equal tile
     shares cut pairs at arbitrary tiles, one long pair spans ~150 workgroups,
@@ -200,7 +209,7 @@ def test_append_past_capacity_is_dropped(lib, paged):
 
 
 @pytest.mark.parametrize("dtype,d,H,G", [(torch.bfloat16, 128, 8, 8), (torch.bfloat16, 128, 8, 2),
-                                         (torch.float32, 64, 4, 4)])
+                                         (torch.float32, 64, 4, 4), (torch.bfloat16, 128, 12, 2)])
 def test_standard_decode_matches_oracle(lib, dtype, d, H, G):
     B, L = 6, 700
     say(f"standard dtype={dtype} d={d} H={H} G={G}")
@@ -282,7 +291,8 @@ def test_head_to_head_full_size_sampled(lib):
 
 
 APPEND_CASES = [(torch.bfloat16, 128, 8, 8), (torch.bfloat16, 128, 8, 2), (torch.bfloat16, 128, 32, 1),
-                (torch.bfloat16, 64, 4, 4), (torch.float32, 64, 4, 4), (torch.float32, 128, 4, 2)]
+                (torch.bfloat16, 64, 4, 4), (torch.float32, 64, 4, 4), (torch.float32, 128, 4, 2),
+                (torch.bfloat16, 128, 12, 2), (torch.float32, 64, 6, 2)]
 
 
 @pytest.mark.parametrize("dtype,d,H,G", APPEND_CASES)
@@ -359,8 +369,33 @@ def test_decode_append_full_size(lib):
     assert_parity(a, to64(b), torch.bfloat16, "fused vs unfused")
 
 
+@pytest.mark.parametrize("L", [512, 2048, 8192])
+def test_testbed_layers_full_size(lib, L):
+    """The paper's decode testbed attention at its contexts (batch 1, 12 query
+    heads over 2 value heads of 128) in the launch the benchmark replays: three of
+    the 28 layers' fused steps, each on its own cache, with the row the step
+    appends poisoned beforehand; every output against the oracle's append then
+    decode, and each cache bit-equal to the oracle's append afterwards."""
+    say(f"testbed layers L={L}")
+    t = configs.testbed_gqa_bf16(device=DEV, L=L, layers=3)
+    t["V"][:, :, :, L - 1] = float("nan")
+    cache_before = t["V"].cpu()
+    ws = torch.full((max(kb.decode_workspace_bytes(kb.ValueCache(t["V"][0]), 1, 12), 256),), 0xFF,
+                    dtype=torch.uint8, device=DEV)
+    outs = [kb.keyless_decode_append(t["q"][i], t["v_new"][i], kb.ValueCache(t["V"][i]),
+                                     t["lengths_before"], workspace=ws) for i in range(3)]
+    torch.cuda.synchronize()
+    before = t["lengths_before"].cpu().numpy()
+    for i in range(3):
+        ref_cache = K.value_cache_append(to64(cache_before[i]), to64(t["v_new"][i][:, None]),
+                                         before)
+        np.testing.assert_array_equal(to64(t["V"][i]), ref_cache)
+        ref = K.keyless_decode(to64(t["q"][i]), ref_cache, before + 1, 12, 2)
+        assert_parity(outs[i], ref, torch.bfloat16, f"layer {i}")
+
+
 @pytest.mark.parametrize("H,G,d,dtype", [(8, 8, 128, torch.bfloat16), (32, 1, 128, torch.bfloat16),
-                                         (4, 2, 64, torch.float32)])
+                                         (4, 2, 64, torch.float32), (12, 2, 128, torch.bfloat16)])
 @pytest.mark.parametrize("paged", [False, True])
 def test_small_batch_split_ragged(lib, H, G, d, dtype, paged):
     """At most four sequences take fixed splits sized from the capacity (the

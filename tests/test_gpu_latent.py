@@ -23,6 +23,8 @@ CASES = [
     (torch.bfloat16, 128, 64, 8, 8),     # per-head latent, r narrower than d_head
     (torch.float32, 128, 64, 8, 2),
     (torch.float32, 64, 128, 4, 4),
+    (torch.bfloat16, 128, 128, 12, 2),   # 6 heads per latent group
+    (torch.float32, 64, 64, 6, 2),       # 3 heads per latent group
 ]
 
 

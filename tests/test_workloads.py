@@ -66,3 +66,14 @@ def test_decode_config_new_value_is_last_row():
     c = configs.decode_bf16(B=2, H=3, L=10, d_head=8)
     assert torch.equal(c["v_new"][:, 0], c["V"][:, :, 9, :])
     assert np.all(c["lengths_before"].numpy() == 9)
+
+
+def test_testbed_config_layers_copies_and_new_rows():
+    c = configs.testbed_gqa_bf16(L=20, layers=3, copies=2, d_head=8)
+    assert c["V"].shape == (6, 1, 2, 20, 8) and c["K"].shape == c["V"].shape
+    assert c["q"].shape == (3, 1, 12, 8)
+    assert torch.equal(c["v_new"], c["V"][:, :, :, 19, :])
+    # Copies are independent draws; the first copy does not depend on how many follow.
+    assert not torch.equal(c["V"][:3], c["V"][3:])
+    assert torch.equal(c["V"][:3], configs.testbed_gqa_bf16(L=20, layers=3, d_head=8)["V"])
+    assert int(c["lengths"][0]) == 20 and int(c["lengths_before"][0]) == 19

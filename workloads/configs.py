@@ -15,7 +15,8 @@ import torch
 from .synth import normal, permutation, uniform_int
 
 NAMES = ("tiny_fp32", "decode_bf16", "prefill_bf16", "paged_gqa_bf16", "head_to_head_bf16",
-         "decode_step_bf16", "cross_bf16", "latent_bf16", "backward_bf16", "decode_b1_bf16")
+         "decode_step_bf16", "cross_bf16", "latent_bf16", "backward_bf16", "decode_b1_bf16",
+         "testbed_gqa_bf16")
 
 # Stream ids (one per drawn tensor).
 S_X, S_WQ, S_WR, S_WV, S_XNEXT, S_V, S_Q, S_K, S_LEN, S_PERM, S_VNEW, S_XB, S_WPOST, S_DO = range(14)
@@ -202,3 +203,27 @@ def decode_b1_bf16(device="cpu", seed=9, L=2048, H=32, d_head=128, copies=1):
                 v_new=V[:, :, L - 1].contiguous(),
                 lengths_before=torch.full((1,), L - 1, dtype=torch.int32, device=device),
                 H=H, L=L, d_head=d_head)
+
+
+def testbed_gqa_bf16(device="cpu", seed=10, L=8192, layers=28, H=12, G=2, d_head=128, copies=1,
+                     with_keys=True):
+    """The attention of the paper's decode-throughput testbed (a 1.5B model with
+    28 layers, 12 query heads over 2 value heads of 128, batch 1, contexts 512,
+    2048 and 8192): per layer a contiguous value-only cache [1, G, L, d_head]
+    and routed queries [1, H, d_head] ~ N(0,1), bf16, and for the standard
+    comparison a key cache of the same shape. The caches of all layers (and of
+    ``copies`` independent steps, streams S_V + 100*c and S_K + 100*c) sit in
+    one tensor [copies * layers, 1, G, L, d_head]; the step's new value row of a
+    layer is its cache's last row."""
+    f = torch.bfloat16
+
+    def stack(stream):
+        return torch.cat([normal((layers, 1, G, L, d_head), seed, stream + 100 * c, 1.0, f, device)
+                          for c in range(copies)])
+    V = stack(S_V)
+    K = stack(S_K) if with_keys else None
+    q = normal((layers, 1, H, d_head), seed, S_Q, 1.0, f, device)
+    return dict(V=V, K=K, q=q, v_new=V[:, :, :, L - 1].contiguous(),
+                lengths=torch.full((1,), L, dtype=torch.int32, device=device),
+                lengths_before=torch.full((1,), L - 1, dtype=torch.int32, device=device),
+                layers=layers, copies=copies, H=H, G=G, L=L, d_head=d_head)
