@@ -67,6 +67,31 @@ def test_workspace_sizes(lib):
     assert n == 256 * 256 * 4 + 128 * 256 * 4 * 2
 
 
+def _split_bytes(B, H, S, d=128):
+    part = B * H * S * (d + 2) * 4
+    return (part + 255) // 256 * 256
+
+
+def test_small_batch_split_plan(lib):
+    """The built-in split of a few sequences, seen through the workspace size
+    (fp32 partial rows per head and split): about 512 splits over the capacity
+    of all (b, g) pairs, at least 256 rows each; a capacity of at most 1024 rows
+    is one split and needs no workspace."""
+    def size(B, G, H, L):
+        return lib.keyless_decode_workspace_size(ctypes.byref(cache(G=G, L_max=L)), B, H, 0)
+    # The paper's decode testbed shape (12 query heads over 2 value heads, batch 1).
+    assert size(1, 2, 12, 512) == 0
+    assert size(1, 2, 12, 2048) == _split_bytes(1, 12, 8)      # 256-row splits
+    assert size(1, 2, 12, 8192) == _split_bytes(1, 12, 32)
+    assert size(1, 32, 32, 8192) == _split_bytes(1, 32, 16)    # 512 rows, 512 workgroups
+    assert size(4, 8, 32, 32768) == _split_bytes(4, 32, 16)    # 2048 rows
+    assert size(1, 1, 1, 524288) == _split_bytes(1, 1, 512)    # 1024 rows
+    assert size(1, 1, 8, 64) == 0
+    # Paged: the capacity (blocks per sequence x block size) sets the split.
+    p = cache(G=2, layout=kb.KL_PAGED, bs=16, mb=128)          # 2048 rows
+    assert lib.keyless_decode_workspace_size(ctypes.byref(p), 1, 12, 0) == _split_bytes(1, 12, 8)
+
+
 def test_decode_rejects_bad_arguments(lib):
     expect(lib, decode(lib, cache(), q=None), kb.KL_ERR_INVALID_ARG, "non-NULL")
     expect(lib, decode(lib, cache(d=96)), kb.KL_ERR_UNSUPPORTED, "d_head 96")

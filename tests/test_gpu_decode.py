@@ -394,6 +394,45 @@ def test_testbed_layers_full_size(lib, L):
         assert_parity(outs[i], ref, torch.bfloat16, f"layer {i}")
 
 
+def test_fused_step_graph_replays(lib):
+    """The fused append + decode at the paper's testbed shape (batch 1, 12 query
+    heads over 2 value heads, 2048 rows: 8 splits and the merge kernel) captured
+    once and replayed four times, with eager calls on another workspace and a
+    restored cache between replays: every replay equals the eager step, and the
+    first matches the oracle."""
+    L = 2048
+    say("fused step graph replays")
+    t = configs.testbed_gqa_bf16(device=DEV, L=L, layers=1, with_keys=False)
+    V, q, vnew, before = t["V"][0], t["q"][0], t["v_new"][0], t["lengths_before"]
+    base = V.clone()
+    vc = kb.ValueCache(V)
+    out = torch.empty_like(q)
+    ws = torch.empty(kb.decode_workspace_bytes(vc, 1, 12), dtype=torch.uint8, device=DEV)
+    assert ws.numel() > 0
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        kb.keyless_decode_append(q, vnew, vc, before, out=out, workspace=ws)
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        kb.keyless_decode_append(q, vnew, vc, before, out=out, workspace=ws)
+    ref_cache = K.value_cache_append(to64(base), to64(vnew[:, None]), before.cpu().numpy())
+    ref = K.keyless_decode(to64(q), ref_cache, before.cpu().numpy() + 1, 12, 2)
+    for rep in range(4):
+        if rep:
+            q.copy_(synth.normal((1, 12, 128), 26, rep).to(DEV))
+        V.copy_(base)
+        eager = kb.keyless_decode_append(q, vnew, kb.ValueCache(base.clone()), before)
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        assert torch.equal(out, eager), f"replay {rep}"
+        if rep == 0:
+            assert_parity(out, ref, torch.bfloat16, "first replay against the oracle")
+
+
 @pytest.mark.parametrize("H,G,d,dtype", [(8, 8, 128, torch.bfloat16), (32, 1, 128, torch.bfloat16),
                                          (4, 2, 64, torch.float32), (12, 2, 128, torch.bfloat16)])
 @pytest.mark.parametrize("paged", [False, True])
