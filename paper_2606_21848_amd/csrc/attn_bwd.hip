@@ -135,7 +135,9 @@ struct TileCopier {
 // dQ~ for 128 query rows of one head. Mirrors the forward kernel: S^T = V Q~^T
 // and dP^T = V dO^T share each value-row fragment read; dS^T feeds
 // dQ~^T += V^T dS^T as the B operand.
-template <int D>
+// SWEEP0: Dd is formed here in a first sweep (no fp32 output); else it comes
+// from bwd_prep_kernel and one sweep does.
+template <int D, bool SWEEP0>
 __global__ __launch_bounds__(kThreads, 2) void bwd_dq_kernel(BwdParams p) {
   using TL = AttnTile<D, kTileRows>;
   constexpr int KS = D / 32, DB = D / 16;
@@ -157,6 +159,11 @@ __global__ __launch_bounds__(kThreads, 2) void bwd_dq_kernel(BwdParams p) {
   // B operands: query row q0 + 16 qb + fr, columns 32 ks + 8 grp .. + 7; the
   // routed query multiplied by c and rounded to bf16 as in the forward.
   bf16x8_t qf[QBD][KS], df[QBD][KS];
+  // One sweep: the score and dP accumulators start from -lse (log2 units) and
+  // -Dd, both per query (one per lane column), so P = 2^S and dS = P dP come
+  // straight out of the products. The two-sweep form, at its register limit,
+  // subtracts them (lse2, dd) instead.
+  f32x4_t nlse[QBD], ndd[QBD];
   float lse2[QBD], dd[QBD];
 #pragma unroll
   for (int qb = 0; qb < QBD; ++qb) {
@@ -173,8 +180,15 @@ __global__ __launch_bounds__(kThreads, 2) void bwd_dq_kernel(BwdParams p) {
       qf[qb][ks] = __builtin_bit_cast(bf16x8_t, w);
       df[qb][ks] = __builtin_bit_cast(bf16x8_t, *reinterpret_cast<const u32x4*>(sd + ks * 32));
     }
-    lse2[qb] = p.lse[((size_t)b * p.H + h) * p.N + qq] * kLog2e;
-    dd[qb] = p.out_f32 ? p.Dd[((size_t)b * p.H + h) * p.N + qq] : 0.f;  // else the first sweep
+    const float l2 = p.lse[((size_t)b * p.H + h) * p.N + qq] * kLog2e;
+    if constexpr (SWEEP0) {
+      lse2[qb] = l2;
+      dd[qb] = 0.f;  // from the first sweep
+    } else {
+      const float d0 = p.Dd[((size_t)b * p.H + h) * p.N + qq];
+      nlse[qb] = f32x4_t{-l2, -l2, -l2, -l2};
+      ndd[qb] = f32x4_t{-d0, -d0, -d0, -d0};
+    }
   }
   f32x4_t acc[DB][QBD];
 #pragma unroll
@@ -200,7 +214,7 @@ __global__ __launch_bounds__(kThreads, 2) void bwd_dq_kernel(BwdParams p) {
   // dV kernel; the second forms dS and accumulates dQ~.
   // With the forward's fp32 output, Dd comes from bwd_prep_kernel and one sweep does.
 #pragma unroll 1
-  for (int sweep = p.out_f32 ? 1 : 0; sweep < 2; ++sweep) {
+  for (int sweep = SWEEP0 ? 0 : 1; sweep < 2; ++sweep) {
     if (sweep == 1) {
       // Every wave's reads of the first sweep's last stages have returned.
       asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
@@ -228,8 +242,16 @@ __global__ __launch_bounds__(kThreads, 2) void bwd_dq_kernel(BwdParams p) {
       const int j0 = jt * kTileRows;
       // Above this wave's diagonal, or rows all past the end (a ragged last tile).
       if (q0 >= p.N || (p.causal && j0 > q0 + 16 * QBD - 1)) continue;
-      const lds_u8* tile = (const lds_u8*)smem + stage * TL::BYTES;
+      // Fragment offsets from this tile's stage: one v_xad_u32 forms a read's
+      // whole address (the row blocks are immediate offsets). The two-sweep
+      // form, at its register limit, keeps them relative and adds the stage.
+      const uint32_t sbase = lds0 + stage * TL::BYTES;
+      const FragOffsets<D> fi = SWEEP0 ? fo : fo.at(sbase);
+      const uint32_t sadd = SWEEP0 ? sbase : 0u;
+      auto lds_at = [&](int a) { return (const lds_u8*)(size_t)((uint32_t)a + sadd); };
 
+      // Tiles on this wave's diagonal or past the sequence's end mask weights
+      // (one uniform test per block of weights).
       const bool edge = (p.causal && j0 + kTileRows - 1 > q0) || (j0 + kTileRows > p.N);
       // One 32-row k-step at a time (value blocks kb = 2 ks, 2 ks + 1), which
       // keeps half of the tile's scores live.
@@ -240,8 +262,13 @@ __global__ __launch_bounds__(kThreads, 2) void bwd_dq_kernel(BwdParams p) {
         for (int hh = 0; hh < 2; ++hh)
 #pragma unroll
           for (int qb = 0; qb < QBD; ++qb) {
-            sc[hh][qb] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-            dp[hh][qb] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+            if constexpr (SWEEP0) {
+              sc[hh][qb] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+              dp[hh][qb] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+            } else {
+              sc[hh][qb] = nlse[qb];
+              dp[hh][qb] = ndd[qb];
+            }
           }
         // Both blocks' value fragments are read up front; the schedule puts the
         // second block's reads between the first block's products.
@@ -251,7 +278,7 @@ __global__ __launch_bounds__(kThreads, 2) void bwd_dq_kernel(BwdParams p) {
 #pragma unroll
           for (int kd = 0; kd < KS; ++kd)
             va[hh][kd] = *reinterpret_cast<const __attribute__((address_space(3))) bf16x8_t*>(
-                tile + fo.s(kd) + (2 * ks + hh) * 16 * TL::ROW);
+                lds_at(fi.s(kd)) + (2 * ks + hh) * 16 * TL::ROW);
 #pragma unroll
         for (int hh = 0; hh < 2; ++hh)
 #pragma unroll
@@ -269,41 +296,53 @@ __global__ __launch_bounds__(kThreads, 2) void bwd_dq_kernel(BwdParams p) {
         }
         __builtin_amdgcn_sched_group_barrier(kSchedMfma, 2 * QBD * KS, 0);
         // Lane: rows j0 + 16 (2 ks + hh) + 4 grp + r of query q0 + 16 qb + fr.
-        auto weight = [&](int hh, int qb, int r) {
-          float pr = fast_exp2(sc[hh][qb][r] - lse2[qb]);
-          if (edge) {
-            const int kv = j0 + (2 * ks + hh) * 16 + grp * 4 + r;
-            if (kv >= p.N || (p.causal && kv > q0 + qb * 16 + fr)) pr = 0.f;
-          }
-          return pr;
-        };
-        if (sweep == 0) {
+        // The weights, masked on tiles at this wave's diagonal or past the
+        // sequence's end; the test is uniform, taken once per k-step.
+        auto weights = [&](auto masked_tag, auto use) {
+          constexpr bool MASKED = decltype(masked_tag)::value;
 #pragma unroll
           for (int qb = 0; qb < QBD; ++qb)
 #pragma unroll
             for (int hh = 0; hh < 2; ++hh)
 #pragma unroll
-              for (int r = 0; r < 4; ++r) dsum[qb] = fmaf(weight(hh, qb, r), dp[hh][qb][r], dsum[qb]);
+              for (int r = 0; r < 4; ++r) {
+                float pr = fast_exp2(SWEEP0 ? sc[hh][qb][r] - lse2[qb] : sc[hh][qb][r]);
+                if constexpr (MASKED) {
+                  const int kv = j0 + (2 * ks + hh) * 16 + grp * 4 + r;
+                  pr = (kv >= p.N || (p.causal && kv > q0 + qb * 16 + fr)) ? 0.f : pr;
+                }
+                use(qb, hh, r, pr);
+              }
+        };
+        if (sweep == 0) {
+          auto acc_dd = [&](int qb, int hh, int r, float pr) {
+            dsum[qb] = fmaf(pr, dp[hh][qb][r], dsum[qb]);
+          };
+          if (edge) weights(std::true_type{}, acc_dd);
+          else weights(std::false_type{}, acc_dd);
           continue;
         }
         // dS^T fragments of the k-step (rows 32 ks + {4 grp .., 16 + 4 grp ..}).
+        float dsv[QBD][2][4];
+        auto keep_ds = [&](int qb, int hh, int r, float pr) {
+          dsv[qb][hh][r] = pr * (SWEEP0 ? dp[hh][qb][r] - dd[qb] : dp[hh][qb][r]);
+        };
+        if (edge) weights(std::true_type{}, keep_ds);
+        else weights(std::false_type{}, keep_ds);
         bf16x8_t pf[QBD];
 #pragma unroll
         for (int qb = 0; qb < QBD; ++qb) {
           u32x4 w;
 #pragma unroll
           for (int hh = 0; hh < 2; ++hh) {
-            float ds[4];
-#pragma unroll
-            for (int r = 0; r < 4; ++r) ds[r] = weight(hh, qb, r) * (dp[hh][qb][r] - dd[qb]);
-            w[2 * hh] = pack2(ds[0], ds[1]);
-            w[2 * hh + 1] = pack2(ds[2], ds[3]);
+            w[2 * hh] = pack2(dsv[qb][hh][0], dsv[qb][hh][1]);
+            w[2 * hh + 1] = pack2(dsv[qb][hh][2], dsv[qb][hh][3]);
           }
           pf[qb] = __builtin_bit_cast(bf16x8_t, w);
         }
 #pragma unroll
         for (int db = 0; db < DB; ++db) {
-          const lds_u8* src = tile + fo.t(db) + ks * 32 * TL::ROW;
+          const lds_u8* src = lds_at(fi.t(db)) + ks * 32 * TL::ROW;
           const s16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
               (__attribute__((address_space(3))) s16x4*)(src));
           const s16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
@@ -407,21 +446,43 @@ __global__ __launch_bounds__(kThreads, 2) void bwd_dv_kernel(BwdParams p) {
   // moved into working registers at the top of the item, right after the wait
   // that covers both. Loaded where they are used, they would make the compiler
   // wait for every load in flight, which includes the next item's tile copies
-  // (issued as inline assembly, which it does not count).
+  // (issued as inline assembly, which it does not count). Rows 16 qb + 4 grp ..
+  // + 3 are consecutive: one 16-byte load per block and array when the tile
+  // lies inside the sequence and N keeps the rows 16-byte aligned.
   float lsen[4][4], ddn[4][4];
+  const bool vec_rows = (p.N & 3) == 0;
   auto prefetch = [&](int it) {
     const int h = g * R + it / per_head, qt = qt0 + it % per_head;
-    const float* lse = p.lse + ((size_t)b * p.H + h) * p.N;
-    const float* ddv = p.Dd + ((size_t)b * p.H + h) * p.N;
+    const size_t row0 = ((size_t)b * p.H + h) * p.N;
+    const float* lse = p.lse + row0;
+    const float* ddv = p.Dd + row0;
+    const int q0 = qt * kTileRows;
+    if (vec_rows && q0 + kTileRows <= p.N) {
 #pragma unroll
-    for (int qb = 0; qb < 4; ++qb)
+      for (int qb = 0; qb < 4; ++qb) {
+        const f32x4_t x = *reinterpret_cast<const f32x4_t*>(lse + q0 + qb * 16 + grp * 4);
+        const f32x4_t y = *reinterpret_cast<const f32x4_t*>(ddv + q0 + qb * 16 + grp * 4);
 #pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int q = min(qt * kTileRows + qb * 16 + grp * 4 + r, p.N - 1);
-        lsen[qb][r] = lse[q];
-        ddn[qb][r] = ddv[q];
+        for (int r = 0; r < 4; ++r) {
+          lsen[qb][r] = x[r];
+          ddn[qb][r] = y[r];
+        }
       }
+    } else {
+      // Rows past the sequence's end (their tile rows repeat row N - 1) take
+      // lse = +inf, so their weights and dS are exactly zero with no mask.
+#pragma unroll
+      for (int qb = 0; qb < 4; ++qb)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int q = q0 + qb * 16 + grp * 4 + r;
+          const int qc = min(q, p.N - 1);
+          lsen[qb][r] = q < p.N ? lse[qc] : INFINITY;
+          ddn[qb][r] = ddv[qc];
+        }
+    }
   };
+  auto lds_at = [](int a) { return (const lds_u8*)(size_t)(uint32_t)a; };
   if (items > 0) {
     issue(0);
     prefetch(0);
@@ -436,7 +497,7 @@ __global__ __launch_bounds__(kThreads, 2) void bwd_dv_kernel(BwdParams p) {
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
         asm volatile("v_mul_f32 %0, %1, %2" : "=v"(l2c[qb][r]) : "v"(kLog2e), "v"(lsen[qb][r]));
-        asm volatile("v_mov_b32 %0, %1" : "=v"(ddc[qb][r]) : "v"(ddn[qb][r]));
+        asm volatile("v_mul_f32 %0, %1, %2" : "=v"(ddc[qb][r]) : "v"(p.scale), "v"(ddn[qb][r]));
       }
     if (it + 1 < items) {
       issue(it + 1);
@@ -445,9 +506,12 @@ __global__ __launch_bounds__(kThreads, 2) void bwd_dv_kernel(BwdParams p) {
     const int qt = qt0 + it % per_head;
     const int q0 = qt * kTileRows;
     if (p.causal && q0 + kTileRows - 1 < kv0) continue;  // every row of the tile is before ours
-    const lds_u8* tq = (const lds_u8*)smem + (it & 1) * 2 * TL::BYTES;
-    const lds_u8* td = tq + TL::BYTES;
-    const bool edge = (p.causal && q0 < kv0 + 16 * KVB - 1) || (q0 + kTileRows > p.N);
+    // Fragment offsets from this item's stage: one v_xad_u32 forms a read's
+    // whole address (the dO tile and the row blocks are immediate offsets).
+    const FragOffsets<D> fi = fo.at(lds0 + (it & 1) * 2 * TL::BYTES);
+    // Tiles that reach this wave's value rows on the diagonal mask the weights
+    // of later value rows (one uniform test per block of weights).
+    const bool diag = p.causal && q0 < kv0 + 16 * KVB - 1;
     // Two 32-row query steps; each is one K = 32 step of the dV products.
 #pragma unroll
     for (int qs = 0; qs < 2; ++qs) {
@@ -467,10 +531,9 @@ __global__ __launch_bounds__(kThreads, 2) void bwd_dv_kernel(BwdParams p) {
         bf16x8_t aq[KS], ad[KS];
 #pragma unroll
         for (int ks = 0; ks < KS; ++ks) {
-          aq[ks] = *reinterpret_cast<const __attribute__((address_space(3))) bf16x8_t*>(
-              tq + fo.s(ks) + qb * 16 * TL::ROW);
-          ad[ks] = *reinterpret_cast<const __attribute__((address_space(3))) bf16x8_t*>(
-              td + fo.s(ks) + qb * 16 * TL::ROW);
+          const lds_u8* a = lds_at(fi.s(ks)) + qb * 16 * TL::ROW;
+          aq[ks] = *reinterpret_cast<const __attribute__((address_space(3))) bf16x8_t*>(a);
+          ad[ks] = *reinterpret_cast<const __attribute__((address_space(3))) bf16x8_t*>(a + TL::BYTES);
         }
 #pragma unroll
         for (int ks = 0; ks < KS; ++ks)
@@ -490,21 +553,26 @@ __global__ __launch_bounds__(kThreads, 2) void bwd_dv_kernel(BwdParams p) {
         // Lane: query rows q0 + 16 qb + 4 grp + r against value row kv0 + 16 kb + fr.
         const float* l2 = l2c[qb];
         const float* dq = ddc[qb];
+        float pr[KVB][4];
+#pragma unroll
+        for (int kb = 0; kb < KVB; ++kb)
+#pragma unroll
+          for (int r = 0; r < 4; ++r) pr[kb][r] = fast_exp2(sc[kb][r] * c - l2[r]);
+        if (diag) {
+#pragma unroll
+          for (int kb = 0; kb < KVB; ++kb)
+#pragma unroll
+            for (int r = 0; r < 4; ++r)
+              if (kv0 + kb * 16 + fr > q0 + qb * 16 + grp * 4 + r) pr[kb][r] = 0.f;
+        }
 #pragma unroll
         for (int kb = 0; kb < KVB; ++kb) {
-          const int kv = kv0 + kb * 16 + fr;
-          float pr[4], ds[4];
+          float ds[4];
+          // tau dS = P (tau dP - tau Dd)
 #pragma unroll
-          for (int r = 0; r < 4; ++r) {
-            pr[r] = fast_exp2(sc[kb][r] * c - l2[r]);
-            if (edge) {
-              const int q = q0 + qb * 16 + grp * 4 + r;
-              if (q >= p.N || (p.causal && kv > q)) pr[r] = 0.f;
-            }
-            ds[r] = pr[r] * (dp[kb][r] - dq[r]) * p.scale;
-          }
-          wp[kb][2 * hh] = pack2(pr[0], pr[1]);
-          wp[kb][2 * hh + 1] = pack2(pr[2], pr[3]);
+          for (int r = 0; r < 4; ++r) ds[r] = pr[kb][r] * fmaf(dp[kb][r], p.scale, -dq[r]);
+          wp[kb][2 * hh] = pack2(pr[kb][0], pr[kb][1]);
+          wp[kb][2 * hh + 1] = pack2(pr[kb][2], pr[kb][3]);
           wsv[kb][2 * hh] = pack2(ds[0], ds[1]);
           wsv[kb][2 * hh + 1] = pack2(ds[2], ds[3]);
         }
@@ -517,11 +585,12 @@ __global__ __launch_bounds__(kThreads, 2) void bwd_dv_kernel(BwdParams p) {
       // dV^T[d][kv] += dO^T P + Q~^T (tau dS) over query rows 32 qs + {4 grp .., 16 + 4 grp ..}.
       // Transposed reads run two column blocks ahead of the products.
       auto rd = [&](const int db, bf16x8_t& ad, bf16x8_t& aq) {
-        const int o = fo.t(db) + qs * 32 * TL::ROW;
-        const s16x4 dlo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) s16x4*)(td + o));
-        const s16x4 dhi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) s16x4*)(td + o + 16 * TL::ROW));
-        const s16x4 qlo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) s16x4*)(tq + o));
-        const s16x4 qhi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) s16x4*)(tq + o + 16 * TL::ROW));
+        const lds_u8* a = lds_at(fi.t(db)) + qs * 32 * TL::ROW;
+        typedef __attribute__((address_space(3))) s16x4 lds_s16x4;
+        const s16x4 dlo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)(a + TL::BYTES));
+        const s16x4 dhi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)(a + TL::BYTES + 16 * TL::ROW));
+        const s16x4 qlo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)a);
+        const s16x4 qhi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)(a + 16 * TL::ROW));
         ad = __builtin_bit_cast(bf16x8_t, __builtin_shufflevector(dlo, dhi, 0, 1, 2, 3, 4, 5, 6, 7));
         aq = __builtin_bit_cast(bf16x8_t, __builtin_shufflevector(qlo, qhi, 0, 1, 2, 3, 4, 5, 6, 7));
       };
@@ -693,8 +762,12 @@ hipError_t launch_simple(const BwdParams& p, hipStream_t st) {
 template <int D>
 hipError_t launch_mfma(const BwdParams& p, hipStream_t st) {
   using TL = AttnTile<D, kTileRows>;
-  hipLaunchKernelGGL(bwd_dq_kernel<D>, dim3(p.H, (p.N + BQD - 1) / BQD, p.B), dim3(kThreads),
-                     NSTAGE * TL::BYTES, st, p);
+  if (p.out_f32)
+    hipLaunchKernelGGL((bwd_dq_kernel<D, false>), dim3(p.H, (p.N + BQD - 1) / BQD, p.B),
+                       dim3(kThreads), NSTAGE * TL::BYTES, st, p);
+  else
+    hipLaunchKernelGGL((bwd_dq_kernel<D, true>), dim3(p.H, (p.N + BQD - 1) / BQD, p.B),
+                       dim3(kThreads), NSTAGE * TL::BYTES, st, p);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(bwd_dv_kernel<D>, dim3(p.G, (p.N + BKVD - 1) / BKVD, p.B), dim3(kThreads),

@@ -57,6 +57,14 @@ struct FragOffsets {
   }
   __device__ __forceinline__ int s(int ks) const { return xad(skey, ks << 6, sbase); }
   __device__ __forceinline__ int t(int db) const { return xad(tkey, db << 5, tbase); }
+  // The same offsets relative to `base` (a tile's LDS address), so that a read
+  // needs only the one v_xad_u32 for its whole address.
+  __device__ __forceinline__ FragOffsets at(uint32_t base) const {
+    FragOffsets f = *this;
+    f.sbase += (int)base;
+    f.tbase += (int)base;
+    return f;
+  }
 };
 
 // Two floats rounded to bf16 (nearest even) and packed low, high.
