@@ -67,6 +67,10 @@ def parse():
     ap.add_argument("--profile-prefill", action="store_true",
                     help="run the prefill workload (weights packed once, then 3 calls) and "
                          "print nothing else: the program for the prefill counter passes")
+    ap.add_argument("--profile-backward", action="store_true",
+                    help="run the backward workload (one forward keeping its fp32 output, then "
+                         "4 backward calls) and print nothing else: the program for the "
+                         "backward counter passes")
     ap.add_argument("--profile-decode-side", action="store_true",
                     help="run the counter calibration, then a few launches of the paged "
                          "grouped-head decode, the decode-step projection and the latent "
@@ -548,6 +552,19 @@ def main():
                                       q_routed_out=outs[1], v_out=outs[2])
         torch.cuda.synchronize()
         print("profile prefill done", flush=True)
+        return
+    if args.profile_backward:
+        bw = configs.backward_bf16(device=dev)
+        bo32 = torch.empty(bw["q"].shape, dtype=torch.float32, device=dev)
+        bout, blse = kb.keyless_attention_forward(bw["q"], bw["v"], out_f32=bo32)
+        bdq, bdv = torch.empty_like(bw["q"]), torch.empty_like(bw["v"])
+        bws = torch.empty(max(kb.attention_backward_workspace_bytes(bw["B"], bw["N"], bw["H"]),
+                              256), dtype=torch.uint8, device=dev)
+        for _ in range(4):
+            kb.keyless_attention_backward(bw["q"], bw["v"], bout, bw["dout"], blse, dq=bdq,
+                                          dv=bdv, workspace=bws, out_f32=bo32)
+        torch.cuda.synchronize()
+        print("profile backward done", flush=True)
         return
     if args.profile_decode_side:
         profile_decode_side(torch, kb, configs, dev)
@@ -1038,13 +1055,31 @@ def extra_measurements(torch, kb, configs, dev):
                 kb.keyless_decode_append(t["q"][layer], t["v_new"][c + layer], vcs[c + layer],
                                          t["lengths_before"], out=o_t[layer], workspace=ws_t)
 
-        def sstep(i, t=t, vcs=vcs, kcs=kcs, ws_t=ws_t, o_t=o_t, copies=copies):
+        def kdec(i, t=t, vcs=vcs, ws_t=ws_t, o_t=o_t, copies=copies):
+            c = (i % copies) * 28
+            for layer in range(28):
+                kb.keyless_decode(t["q"][layer], vcs[c + layer], t["lengths"], out=o_t[layer],
+                                  workspace=ws_t)
+
+        def sdec(i, t=t, vcs=vcs, kcs=kcs, ws_t=ws_t, o_t=o_t, copies=copies):
             c = (i % copies) * 28
             for layer in range(28):
                 kb.standard_decode(t["q"][layer], kcs[c + layer], vcs[c + layer], t["lengths"],
                                    out=o_t[layer], workspace=ws_t)
+        k_new = t["K"][:, :, :, L - 1].unsqueeze(1).contiguous()  # [28 copies, 1, 1, G, d]
+        v_new4 = t["v_new"].unsqueeze(1)
+
+        def sstep(i, t=t, vcs=vcs, kcs=kcs, ws_t=ws_t, o_t=o_t, copies=copies):
+            c = (i % copies) * 28
+            for layer in range(28):
+                kb.value_cache_append(kcs[c + layer], k_new[c + layer], t["lengths_before"])
+                kb.value_cache_append(vcs[c + layer], v_new4[c + layer], t["lengths_before"])
+                kb.standard_decode(t["q"][layer], kcs[c + layer], vcs[c + layer], t["lengths"],
+                                   out=o_t[layer], workspace=ws_t)
         st_e = call_stats(kstep, 20, 3, torch)
         st_k = graph_stats(kstep, 20, torch, per_graph=copies)
+        st_kd = graph_stats(kdec, 20, torch, per_graph=copies)
+        st_sd = graph_stats(sdec, 20, torch, per_graph=copies)
         st_s = graph_stats(sstep, 20, torch, per_graph=copies)
         qh_t = np64(t["q"][0])
         vh_t = np64(t["V"][0])
@@ -1052,21 +1087,25 @@ def extra_measurements(torch, kb, configs, dev):
         tb[str(L)] = {
             "keyless_step_us": round(st_k["median_ms"] * 1e3, 2), "keyless_stats": st_k,
             "keyless_tokens_per_s": rate(st_k, 1, 1.0),
-            "keyless_cache_gbps": rate(st_k, per_step, 1e-9),
             "standard_step_us": round(st_s["median_ms"] * 1e3, 2), "standard_stats": st_s,
             "standard_tokens_per_s": rate(st_s, 1, 1.0),
-            "standard_cache_gbps": rate(st_s, 2 * per_step, 1e-9),
+            "keyless_decode_us": round(st_kd["median_ms"] * 1e3, 2),
+            "keyless_decode_stats": st_kd, "keyless_decode_cache_gbps": rate(st_kd, per_step, 1e-9),
+            "standard_decode_us": round(st_sd["median_ms"] * 1e3, 2),
+            "standard_decode_stats": st_sd,
+            "standard_decode_cache_gbps": rate(st_sd, 2 * per_step, 1e-9),
             "keyless_eager_step_us": round(st_e["median_ms"] * 1e3, 2),
             "cache_bytes_per_step": per_step, "step_copies_rotated": copies,
             "cpu_baseline": cpu_entry(round(1.0 / (28 * cs), 2), "tokens/s", cores,
                                       f"the decode of one layer (12 heads over {L} rows) x 28, "
                                       f"median of {cn} runs")}
-        del t, vcs, kcs, ws_t, o_t, vh_t
+        del t, vcs, kcs, ws_t, o_t, vh_t, k_new, v_new4
     res["testbed_gqa_bf16"] = {
         "workload": "the paper's decode testbed attention: batch 1, 28 layers of 12 query heads "
                     "over 2 value heads x 128 (6 heads per group), contiguous caches of 512 / "
-                    "2048 / 8192 rows; one token = 28 fused append + decode launches (standard: "
-                    "28 K+V decodes), replayed from a HIP graph",
+                    "2048 / 8192 rows, replayed from a HIP graph. keyless step: 28 fused append "
+                    "+ decode launches; standard step: per layer the key and value rows "
+                    "appended, then the K+V decode (3 launches); *_decode: the decodes alone",
         "by_context": tb}
 
     # Head-to-head: keyless value-only vs standard K+V, same structure.
