@@ -13,7 +13,7 @@
 // tiles stream through LDS as in the forward, queries and dO stay in
 // registers; a first sweep forms Dd as rowsum(P * dP) in fp32, since
 // rowsum(dO * O) over the bf16-rounded output would put that rounding into
-// every dP - Dd) and then bwd_dv_kernel (one workgroup per 128-row value tile
+// every dP - Dd) and then bwd_dv_kernel (one workgroup per 192-row value tile
 // and value group; query and dO tiles of every head of the group stream
 // through LDS, the values stay in registers). fp32: bwd_prep_kernel (Dd from
 // the fp32 output) and two vector-ALU kernels. No atomics: every output
@@ -93,7 +93,7 @@ __global__ __launch_bounds__(256) void bwd_prep_kernel(BwdParams p) {
 constexpr int QBD = 2;                 // 16-row query blocks per wave (dQ~ kernel)
 constexpr int BQD = 4 * 16 * QBD;      // query rows per workgroup
 constexpr int NSTAGE = 3;              // value tiles in flight (dQ~ kernel)
-constexpr int KVB = 2;                 // 16-row value blocks per wave (dV kernel)
+constexpr int KVB = 3;                 // 16-row value blocks per wave (dV kernel)
 constexpr int BKVD = 4 * 16 * KVB;     // value rows per workgroup
 
 // Direct-to-LDS copy of rows [row0, row0 + 64) (clamped to n_rows - 1) of a
@@ -383,9 +383,9 @@ __global__ __launch_bounds__(kThreads, 2) void bwd_dq_kernel(BwdParams p) {
   }
 }
 
-// dV for 128 value rows of one group: every head of the group and every query
+// dV for 192 value rows of one group: every head of the group and every query
 // tile that can see these rows stream through LDS (routed queries and dO, two
-// stages); the wave's 32 value rows stay in registers as the B operand of
+// stages); the wave's 48 value rows stay in registers as the B operand of
 // S = Q~ V^T and dP = dO V^T, whose results (one value row per lane) are the B
 // operands of dV^T += dO^T P + tau Q~^T dS.
 template <int D>
@@ -421,7 +421,7 @@ __global__ __launch_bounds__(kThreads, 2) void bwd_dv_kernel(BwdParams p) {
     for (int kb = 0; kb < KVB; ++kb) acc[i][kb] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 
   // Work items: (head of the group, query tile) pairs, query tiles from the
-  // first one that can see row kvt * 128.
+  // first one that can see row kvt * BKVD.
   const int ntq = (p.N + kTileRows - 1) / kTileRows;
   const int qt0 = p.causal ? (kvt * BKVD) / kTileRows : 0;
   const int per_head = ntq - qt0;
@@ -431,6 +431,10 @@ __global__ __launch_bounds__(kThreads, 2) void bwd_dv_kernel(BwdParams p) {
   const unsigned char* gD = reinterpret_cast<const unsigned char*>(p.dout);
   const size_t qrow = (size_t)p.q_stride * 2, drow = (size_t)p.o_stride * 2;
   const uint32_t lds0 = (uint32_t)(uintptr_t)(lds_u8*)smem;
+  // The log-sum-exp and Dd of an item's 64 query rows travel with its tiles:
+  // wave 0 copies them (one word per lane, rows past the end clamped) into the
+  // stage's row area, 256 bytes each, behind the four tiles of the two stages.
+  const uint32_t rows0 = lds0 + 4 * TL::BYTES;
   auto issue = [&](int it) {
     const int h = g * R + it / per_head, qt = qt0 + it % per_head;
     const uint32_t st = lds0 + (it & 1) * 2 * TL::BYTES;
@@ -438,77 +442,30 @@ __global__ __launch_bounds__(kThreads, 2) void bwd_dv_kernel(BwdParams p) {
              lane, st);
     cp.issue(gD + (size_t)b * p.N * drow, drow, (uint32_t)(h * D * 2), qt * kTileRows, p.N, wave,
              lane, st + TL::BYTES);
+    if (wave == 0) {
+      const size_t row0 = ((size_t)b * p.H + h) * p.N;
+      const uint32_t off = (uint32_t)min(qt * kTileRows + lane, p.N - 1) * 4;
+      copy_dword_to_lds(p.lse + row0, off, rows0 + (it & 1) * 512);
+      copy_dword_to_lds(p.Dd + row0, off, rows0 + (it & 1) * 512 + 256);
+    }
   };
   const FragOffsets<D> fo(fr, grp);
 
-  // The log-sum-exp and Dd of an item's query rows (lane: rows 16 qb + 4 grp + r
-  // of the tile) are loaded one item ahead, after that item's tile copies, and
-  // moved into working registers at the top of the item, right after the wait
-  // that covers both. Loaded where they are used, they would make the compiler
-  // wait for every load in flight, which includes the next item's tile copies
-  // (issued as inline assembly, which it does not count). Rows 16 qb + 4 grp ..
-  // + 3 are consecutive: one 16-byte load per block and array when the tile
-  // lies inside the sequence and N keeps the rows 16-byte aligned.
-  float lsen[4][4], ddn[4][4];
-  const bool vec_rows = (p.N & 3) == 0;
-  auto prefetch = [&](int it) {
-    const int h = g * R + it / per_head, qt = qt0 + it % per_head;
-    const size_t row0 = ((size_t)b * p.H + h) * p.N;
-    const float* lse = p.lse + row0;
-    const float* ddv = p.Dd + row0;
-    const int q0 = qt * kTileRows;
-    if (vec_rows && q0 + kTileRows <= p.N) {
-#pragma unroll
-      for (int qb = 0; qb < 4; ++qb) {
-        const f32x4_t x = *reinterpret_cast<const f32x4_t*>(lse + q0 + qb * 16 + grp * 4);
-        const f32x4_t y = *reinterpret_cast<const f32x4_t*>(ddv + q0 + qb * 16 + grp * 4);
-#pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          lsen[qb][r] = x[r];
-          ddn[qb][r] = y[r];
-        }
-      }
-    } else {
-      // Rows past the sequence's end (their tile rows repeat row N - 1) take
-      // lse = +inf, so their weights and dS are exactly zero with no mask.
-#pragma unroll
-      for (int qb = 0; qb < 4; ++qb)
-#pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          const int q = q0 + qb * 16 + grp * 4 + r;
-          const int qc = min(q, p.N - 1);
-          lsen[qb][r] = q < p.N ? lse[qc] : INFINITY;
-          ddn[qb][r] = ddv[qc];
-        }
-    }
-  };
   auto lds_at = [](int a) { return (const lds_u8*)(size_t)(uint32_t)a; };
-  if (items > 0) {
-    issue(0);
-    prefetch(0);
-  }
+  if (items > 0) issue(0);
   for (int it = 0; it < items; ++it) {
     KL_WAIT_VMCNT(0);
     asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
     __syncthreads();
-    float l2c[4][4], ddc[4][4];
-#pragma unroll
-    for (int qb = 0; qb < 4; ++qb)
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        asm volatile("v_mul_f32 %0, %1, %2" : "=v"(l2c[qb][r]) : "v"(kLog2e), "v"(lsen[qb][r]));
-        asm volatile("v_mul_f32 %0, %1, %2" : "=v"(ddc[qb][r]) : "v"(p.scale), "v"(ddn[qb][r]));
-      }
-    if (it + 1 < items) {
-      issue(it + 1);
-      prefetch(it + 1);
-    }
+    if (it + 1 < items) issue(it + 1);
     const int qt = qt0 + it % per_head;
     const int q0 = qt * kTileRows;
     if (p.causal && q0 + kTileRows - 1 < kv0) continue;  // every row of the tile is before ours
     // Fragment offsets from this item's stage: one v_xad_u32 forms a read's
     // whole address (the dO tile and the row blocks are immediate offsets).
     const FragOffsets<D> fi = fo.at(lds0 + (it & 1) * 2 * TL::BYTES);
+    const int rows_it = rows0 + (it & 1) * 512;
+    const bool tail = q0 + kTileRows > p.N;
     // Tiles that reach this wave's value rows on the diagonal mask the weights
     // of later value rows (one uniform test per block of weights).
     const bool diag = p.causal && q0 < kv0 + 16 * KVB - 1;
@@ -551,8 +508,20 @@ __global__ __launch_bounds__(kThreads, 2) void bwd_dv_kernel(BwdParams p) {
         __builtin_amdgcn_sched_group_barrier(kSchedMfma, 4 * KVB, 0);
         __builtin_amdgcn_sched_barrier(0);
         // Lane: query rows q0 + 16 qb + 4 grp + r against value row kv0 + 16 kb + fr.
-        const float* l2 = l2c[qb];
-        const float* dq = ddc[qb];
+        // This block's rows 16 qb + 4 grp .. + 3: lse in log2 units (rows past the
+        // sequence's end, copies of row N - 1 in the tile, get +inf, so their
+        // weights and dS are exactly zero) and tau Dd.
+        const f32x4_t lv = *reinterpret_cast<const __attribute__((address_space(3))) f32x4_t*>(
+            lds_at(rows_it) + (qb * 16 + grp * 4) * 4);
+        const f32x4_t dv4 = *reinterpret_cast<const __attribute__((address_space(3))) f32x4_t*>(
+            lds_at(rows_it) + 256 + (qb * 16 + grp * 4) * 4);
+        float l2[4], dq[4];
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          l2[r] = lv[r] * kLog2e;
+          if (tail) l2[r] = (q0 + qb * 16 + grp * 4 + r < p.N) ? l2[r] : INFINITY;
+          dq[r] = dv4[r] * p.scale;
+        }
         float pr[KVB][4];
 #pragma unroll
         for (int kb = 0; kb < KVB; ++kb)
@@ -770,8 +739,14 @@ hipError_t launch_mfma(const BwdParams& p, hipStream_t st) {
                        dim3(kThreads), NSTAGE * TL::BYTES, st, p);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
+  constexpr int dv_lds = 4 * TL::BYTES + 1024;  // two stages of Q~ and dO tiles, lse and Dd rows
+  if (dv_lds > 65536) {
+    static std::atomic<uint32_t> done{0};
+    e = set_max_lds(reinterpret_cast<const void*>(bwd_dv_kernel<D>), dv_lds, done);
+    if (e != hipSuccess) return e;
+  }
   hipLaunchKernelGGL(bwd_dv_kernel<D>, dim3(p.G, (p.N + BKVD - 1) / BKVD, p.B), dim3(kThreads),
-                     4 * TL::BYTES, st, p);
+                     dv_lds, st, p);
   return hipGetLastError();
 }
 
