@@ -48,6 +48,16 @@ constexpr int kSchedMfma = 0x008;
 constexpr int kSchedDsRead = 0x100;
 constexpr float kLog2e = 1.4426950408889634f;
 
+// One 4-byte-per-lane copy from global memory straight into LDS
+// (global_load_lds_dword): lane L's word lands at lds + 4 L; otherwise as
+// copy_to_lds (counted by vmcnt, not by the compiler).
+__device__ __forceinline__ void copy_dword_to_lds(const void* gbase, uint32_t voff, uint32_t lds) {
+  asm volatile("s_mov_b32 m0, %2\n\ts_nop 0\n\tglobal_load_lds_dword %0, %1"
+               :
+               : "v"(voff), "s"(gbase), "s"(lds)
+               : "memory", "m0");
+}
+
 template <typename T>
 __device__ __forceinline__ float ldx(const T* p, size_t i) {
   if constexpr (sizeof(T) == 2) return __uint_as_float((uint32_t)p[i] << 16);

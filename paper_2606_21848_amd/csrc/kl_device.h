@@ -74,15 +74,6 @@ __device__ __forceinline__ void copy_to_lds_nt(const void* gbase, uint32_t voff,
                : "memory", "m0");
 }
 
-// One 4-byte-per-lane copy from global memory straight into LDS
-// (global_load_lds_dword): lane L's word lands at lds + 4 L. As copy_to_lds.
-__device__ __forceinline__ void copy_dword_to_lds(const void* gbase, uint32_t voff, uint32_t lds) {
-  asm volatile("s_mov_b32 m0, %2\n\ts_nop 0\n\tglobal_load_lds_dword %0, %1"
-               :
-               : "v"(voff), "s"(gbase), "s"(lds)
-               : "memory", "m0");
-}
-
 // s_waitcnt with only the vector-memory counter constrained (0..63).
 #define KL_WAIT_VMCNT(n) \
   __builtin_amdgcn_s_waitcnt((((n) & 15) | (((n) >> 4) << 14)) | (0x7 << 4) | (0xF << 8))
