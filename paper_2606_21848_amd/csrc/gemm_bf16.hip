@@ -151,11 +151,13 @@ void gemm_bf16_kernel(GemmParams2 p) {
       for (int j = 0; j < 4; ++j)
         bf[j] = *reinterpret_cast<const __attribute__((address_space(3))) bf16x8_t*>(
             w + swz(wn * 64 + j * 16 + fr, chunk));
+      // W as the A operand: the result block is C^T, so a lane holds four
+      // consecutive output columns of one row (one 8-byte store in bf16).
 #pragma unroll
       for (int i = 0; i < 4; ++i)
 #pragma unroll
         for (int j = 0; j < 4; ++j)
-          acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[i], bf[j], acc[i][j], 0, 0, 0);
+          acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(bf[j], af[i], acc[i][j], 0, 0, 0);
     }
   };
 
@@ -178,33 +180,47 @@ void gemm_bf16_kernel(GemmParams2 p) {
     compute(stageA(cur), stageW(cur));
   }
 
-  // Lane holds C[row 16 i + 4 grp + r][col 16 j + fr] of the wave's 64 x 64 block.
-  // A tile whose rows all exist stores without a per-element row check.
+  // Lane holds C[row 16 i + fr][col 16 j + 4 grp + r] of the wave's 64 x 64 block:
+  // four consecutive columns, stored as one 8-byte (bf16) or 16-byte (fp32)
+  // store when they lie on one side of n_split, inside N, and the outputs' row
+  // strides and bases keep them aligned (uniform); otherwise element by element.
+  // A tile whose rows all exist stores without a per-row check.
+  constexpr int VB = 4 * (int)sizeof(CT);  // bytes of four outputs
+  const bool vec = p.ldc0 % 4 == 0 && p.ldc1 % 4 == 0 && p.n_split % 4 == 0 &&
+                   reinterpret_cast<uintptr_t>(C0) % VB == 0 &&
+                   reinterpret_cast<uintptr_t>(C1) % VB == 0;
   auto store = [&](auto check_rows) {
     constexpr bool CHECK = decltype(check_rows)::value;
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const int col = n0 + wn * 64 + j * 16 + fr;
-      if (col >= p.N) continue;
-      CT* dst;
-      long ldc;
-      if (col < p.n_split) {
-        dst = C0 + col;
-        ldc = p.ldc0;
-      } else {
-        dst = C1 + (col - p.n_split);
-        ldc = p.ldc1;
-      }
+    for (int i = 0; i < 4; ++i) {
+      const int row = m0 + wm * 64 + i * 16 + fr;
+      if (CHECK && row >= p.M) continue;
 #pragma unroll
-      for (int i = 0; i < 4; ++i)
+      for (int j = 0; j < 4; ++j) {
+        const int col = n0 + wn * 64 + j * 16 + grp * 4;
+        if (vec && col + 4 <= p.N && (col + 4 <= p.n_split || col >= p.n_split)) {
+          CT* dst = col < p.n_split ? C0 + (size_t)row * p.ldc0 + col
+                                    : C1 + (size_t)row * p.ldc1 + (col - p.n_split);
+          if constexpr (F32) {
+            *reinterpret_cast<f32x4_t*>(dst) = acc[i][j];
+          } else {
+            typedef __attribute__((__vector_size__(4 * sizeof(__bf16)))) __bf16 bf16x4_t;
+            const bf16x4_t v = {(__bf16)acc[i][j][0], (__bf16)acc[i][j][1], (__bf16)acc[i][j][2],
+                                (__bf16)acc[i][j][3]};
+            *reinterpret_cast<bf16x4_t*>(dst) = v;
+          }
+        } else {
 #pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          const int row = m0 + wm * 64 + i * 16 + grp * 4 + r;
-          if (!CHECK || row < p.M) {
-            if constexpr (F32) dst[(size_t)row * ldc] = acc[i][j][r];
-            else dst[(size_t)row * ldc] = __builtin_bit_cast(uint16_t, (__bf16)acc[i][j][r]);
+          for (int r = 0; r < 4; ++r) {
+            const int c = col + r;
+            if (c >= p.N) continue;
+            CT* dst = c < p.n_split ? C0 + (size_t)row * p.ldc0 + c
+                                    : C1 + (size_t)row * p.ldc1 + (c - p.n_split);
+            if constexpr (F32) *dst = acc[i][j][r];
+            else *dst = __builtin_bit_cast(uint16_t, (__bf16)acc[i][j][r]);
           }
         }
+      }
     }
   };
   if (m0 + BM <= p.M) store(std::false_type{});
