@@ -11,9 +11,10 @@
 //
 // bf16: bwd_dq_kernel (one workgroup per 128-row query tile and head; value
 // tiles stream through LDS as in the forward, queries and dO stay in
-// registers; a first sweep forms Dd as rowsum(P * dP) in fp32, since
-// rowsum(dO * O) over the bf16-rounded output would put that rounding into
-// every dP - Dd) and then bwd_dv_kernel (one workgroup per 192-row value tile
+// registers; Dd = rowsum(dO * O) from the forward's fp32 output when the
+// caller kept it, formed in the kernel's prologue, else a first sweep forms
+// it as rowsum(P * dP) in fp32, since rowsum(dO * O) over the bf16-rounded
+// output would put that rounding into every dP - Dd) and then bwd_dv_kernel (one workgroup per 192-row value tile
 // and value group; query and dO tiles of every head of the group stream
 // through LDS, the values stay in registers). fp32: bwd_prep_kernel (Dd from
 // the fp32 output) and two vector-ALU kernels. No atomics: every output
@@ -195,7 +196,27 @@ __global__ __launch_bounds__(kThreads, 2) void bwd_dq_kernel(BwdParams p) {
       lse2[qb] = l2;
       dd[qb] = 0.f;  // from the first sweep
     } else {
-      const float d0 = p.Dd[((size_t)b * p.H + h) * p.N + qq];
+      // Dd = rowsum(dO * O) from the forward's fp32 output: this lane's 32
+      // columns of the row (where its dO fragments are), then the 4 lane groups;
+      // published for the dV kernel.
+      const float* o = p.out_f32 + (((size_t)b * p.N + qq) * p.H + h) * D + grp * 8;
+      float d0 = 0.f;
+#pragma unroll
+      for (int ks = 0; ks < KS; ++ks) {
+        const f32x4_t o0 = *reinterpret_cast<const f32x4_t*>(o + ks * 32);
+        const f32x4_t o1 = *reinterpret_cast<const f32x4_t*>(o + ks * 32 + 4);
+        const u32x4 g = __builtin_bit_cast(u32x4, df[qb][ks]);
+#pragma unroll
+        for (int j = 0; j < 2; ++j) {
+          d0 = fmaf(__uint_as_float(g[j] << 16), o0[2 * j], d0);
+          d0 = fmaf(__uint_as_float(g[j] & 0xFFFF0000u), o0[2 * j + 1], d0);
+          d0 = fmaf(__uint_as_float(g[j + 2] << 16), o1[2 * j], d0);
+          d0 = fmaf(__uint_as_float(g[j + 2] & 0xFFFF0000u), o1[2 * j + 1], d0);
+        }
+      }
+      d0 += __shfl_xor(d0, 16);
+      d0 += __shfl_xor(d0, 32);
+      if (grp == 0 && q0 + qb * 16 + fr < p.N) p.Dd[((size_t)b * p.H + h) * p.N + qq] = d0;
       nlse[qb] = f32x4_t{-l2, -l2, -l2, -l2};
       ndd[qb] = f32x4_t{-d0, -d0, -d0, -d0};
     }
@@ -785,10 +806,12 @@ bool attn_bwd_mfma_supported(const BwdParams& p) {
 hipError_t launch_attention_backward(const BwdParams& p, hipStream_t st) {
   if (p.B == 0 || p.N == 0) return hipSuccess;
   if (p.D != 64 && p.D != 128) return hipErrorInvalidValue;
-  // Dd: from the fp32 output when there is one (the prep kernel), else, on the
-  // matrix cores, from P and dP in the dQ~ kernel's first sweep.
+  // Dd: on the matrix cores from the fp32 output when there is one (in the dQ~
+  // kernel's prologue, which publishes it for the dV kernel), else from P and
+  // dP in the dQ~ kernel's first sweep; on the vector ALU from the output (the
+  // prep kernel).
   const bool mfma = attn_bwd_mfma_supported(p);
-  if (!mfma || p.out_f32) {
+  if (!mfma) {
     hipError_t e = p.dtype == KL_BF16 ? launch_prep<uint16_t>(p, st) : launch_prep<float>(p, st);
     if (e != hipSuccess) return e;
   }
