@@ -256,9 +256,7 @@ int keyless_attention_forward(const void* q_routed, const void* v, int B, int N,
  *   output would carry its rounding into every dP - rowsum);
  *   dq_routed [B, N, H, d_head], dv [B, N, G, d_head]; all 16-byte aligned.
  *   ws, ws_bytes  keyless_attention_backward_workspace_size(B, N, H) bytes (the
- *                 per-row rowsum(dO * O), B*H*N floats), or
- *                 keyless_attention_backward_stored_workspace_size(B, N, H,
- *                 causal) bytes for the stored-dS form (below)
+ *                 per-row rowsum(dO * O), B*H*N floats)
  * Self-attention only (the value rows are the query rows). bf16 with d_head 64
  * or 128 runs on MFMA (P and dS rounded to bf16 for the products, fp32
  * accumulation); fp32 on the vector ALU. Every output element is written once
@@ -270,20 +268,6 @@ int keyless_attention_backward(const void* q_routed, const void* v, const void* 
                                int d_head, int causal, float scale, kl_dtype dtype, void* dq_routed,
                                void* dv, void* ws, size_t ws_bytes, void* stream);
 size_t keyless_attention_backward_workspace_size(int B, int N, int H);
-
-/*
- * keyless_attention_backward_stored_workspace_size - a workspace for
- * keyless_attention_backward that also holds tau dS: given at least this many
- * bytes, bf16 with d_head 64 or 128 and out_f32 given runs the stored-dS form,
- * in which the dV kernel writes tau dS (bf16, 64 x 64 tiles; with `causal` only
- * those on or below the diagonal) and dq_routed = tau dS V is read back from it
- * rather than forming S and dP a second time. Same results up to the order of
- * the fp32 sums. B*H*ceil(N/64)*(ceil(N/64)+1)/2 (causal) or
- * B*H*ceil(N/64)^2 tiles of 8 KiB and 1 KiB of scratch beyond
- * keyless_attention_backward_workspace_size (the tiles rounded up to 256 bytes);
- * returns 0 for B < 0, N < 0 or H <= 0.
- */
-size_t keyless_attention_backward_stored_workspace_size(int B, int N, int H, int causal);
 
 /*
  * keyless_weight_gradients - the rest of the backward pass through the

@@ -27,8 +27,7 @@ EXPORTS = (
     "keyless_cross_attention_packed",
     "keyless_latent_decode", "keyless_latent_decode_workspace_size",
     "keyless_attention_forward", "keyless_attention_backward",
-    "keyless_attention_backward_workspace_size",
-    "keyless_attention_backward_stored_workspace_size", "keyless_weight_gradients",
+    "keyless_attention_backward_workspace_size", "keyless_weight_gradients",
     "keyless_weight_gradients_workspace_size",
     "keyless_decode_project", "keyless_decode", "keyless_decode_chunked", "keyless_decode_workspace_size",
     "keyless_decode_append", "keyless_decode_noalloc",
@@ -91,7 +90,6 @@ def load(path: str = LIB_PATH):
         "keyless_attention_backward": (i, [vp, vp, vp, vp, vp, vp, i, i, i, i, i, i, f, i, vp,
                                            vp, vp, sz, vp]),
         "keyless_attention_backward_workspace_size": (sz, [i, i, i]),
-        "keyless_attention_backward_stored_workspace_size": (sz, [i, i, i, i]),
         "keyless_weight_gradients": (i, [vp, vp, vp, vp, vp, vp, i, i, i, i, i, i, i, vp, vp, vp,
                                          vp, vp, sz, vp]),
         "keyless_weight_gradients_workspace_size": (sz, [i, i, i, i, i, i, i]),
@@ -439,23 +437,16 @@ def keyless_attention_forward(q_routed: torch.Tensor, v: torch.Tensor, causal: b
     return out, lse
 
 
-def attention_backward_workspace_bytes(B: int, N: int, H: int, stored_ds: bool = False,
-                                       causal: bool = True) -> int:
-    """Workspace of keyless_attention_backward: the row sums only, or with
-    `stored_ds` also room for tau dS (the faster bf16 form, with out_f32)."""
+def attention_backward_workspace_bytes(B: int, N: int, H: int) -> int:
     load()
-    if stored_ds:
-        return int(_lib.keyless_attention_backward_stored_workspace_size(B, N, H, int(causal)))
     return int(_lib.keyless_attention_backward_workspace_size(B, N, H))
 
 
 def keyless_attention_backward(q_routed: torch.Tensor, v: torch.Tensor, out: torch.Tensor,
                                dout: torch.Tensor, lse: torch.Tensor, causal: bool = True,
-                               scale: float = 0.0, dq=None, dv=None, workspace=None, out_f32=None,
-                               stored_ds: bool = False):
+                               scale: float = 0.0, dq=None, dv=None, workspace=None, out_f32=None):
     """(dq_routed, dv) of the keyless attention from dout and the forward's out, lse
-    (and its fp32 output, when kept). Without a workspace, one is allocated: with
-    `stored_ds`, large enough for the stored-dS form."""
+    (and its fp32 output, when kept)."""
     load()
     B, N, H, dk = q_routed.shape
     G = v.shape[2]
@@ -464,7 +455,7 @@ def keyless_attention_backward(q_routed: torch.Tensor, v: torch.Tensor, out: tor
     if dv is None:
         dv = torch.empty_like(v)
     if workspace is None:
-        n = attention_backward_workspace_bytes(B, N, H, stored_ds, causal)
+        n = int(_lib.keyless_attention_backward_workspace_size(B, N, H))
         workspace = torch.empty(max(n, 256), dtype=torch.uint8, device=q_routed.device)
     _check(_lib.keyless_attention_backward(_ptr(q_routed), _ptr(v), _ptr(out), _ptr(out_f32),
                                            _ptr(dout), _ptr(lse),

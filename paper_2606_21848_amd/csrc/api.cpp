@@ -803,22 +803,6 @@ size_t keyless_attention_backward_workspace_size(int B, int N, int H) {
   return align256((size_t)B * H * N * sizeof(float));
 }
 
-namespace {
-// 64 x 64 tiles of tau dS per (batch, head): those on or below the diagonal
-// (causal), else all.
-size_t bwd_ds_tiles(int N, int causal) {
-  const size_t ntq = ((size_t)N + 63) / 64;
-  return causal ? ntq * (ntq + 1) / 2 : ntq * ntq;
-}
-}  // namespace
-
-size_t keyless_attention_backward_stored_workspace_size(int B, int N, int H, int causal) {
-  if (B < 0 || N < 0 || H <= 0) return 0;
-  // The tiles, then 1 KiB that stores with nothing to store write to.
-  return keyless_attention_backward_workspace_size(B, N, H) +
-         align256((size_t)B * H * bwd_ds_tiles(N, causal) * 64 * 64 * 2) + 1024;
-}
-
 int keyless_attention_backward(const void* q_routed, const void* v, const void* out,
                                const float* out_f32, const void* dout, const float* lse, int B,
                                int N, int H, int G,
@@ -844,13 +828,6 @@ int keyless_attention_backward(const void* q_routed, const void* v, const void* 
   p.dout = dout;
   p.lse = lse;
   p.Dd = static_cast<float*>(ws);
-  // The stored-dS form: bf16 on the matrix cores with the fp32 output, given
-  // the larger workspace.
-  if (out_f32 && dtype == KL_BF16 &&
-      ws_bytes >= keyless_attention_backward_stored_workspace_size(B, N, H, causal)) {
-    p.ds = reinterpret_cast<uint16_t*>(static_cast<char*>(ws) + need);
-    p.ds_tiles = (long)bwd_ds_tiles(N, causal);
-  }
   p.dq = dq_routed;
   p.dv = dv;
   p.q_stride = p.o_stride = p.dq_stride = (long)H * d_head;

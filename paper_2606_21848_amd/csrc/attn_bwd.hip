@@ -414,32 +414,12 @@ __global__ __launch_bounds__(kThreads, 2) void bwd_dq_kernel(BwdParams p) {
   }
 }
 
-// Layout of a stored 64 x 64 tile of tau dS (value rows kv, query rows q of
-// the tile): 1 KiB units of 16 value rows x 32 query rows, (kv / 16, q / 32)
-// in row-major order; in a unit, 16 bytes per (value row, lane group grp) at
-// (kv % 16 + 16 grp) 16 bytes, holding the query rows 4 grp .. + 3 and
-// 16 + 4 grp .. + 3 of the unit's 32 (the order in which the dV kernel's lanes
-// hold them). Element offset of the unit entry (kv, qs = q / 32, grp):
-__device__ __forceinline__ int ds_unit(int kv, int qs, int grp) {
-  return ((kv >> 4) * 2 + qs) * 512 + ((kv & 15) + 16 * grp) * 8;
-}
-// Its inverse for the dQ~ kernel, which reads each 16-byte entry as one
-// 8-column chunk of an AttnTile<64, 64> row (column 8 (4 qs + grp) + e): the
-// query row of column j of the tile.
-__device__ __forceinline__ int ds_query_of_column(int j) {
-  const int c = j >> 3, e = j & 7;
-  return (c >> 2) * 32 + (c & 3) * 4 + (e < 4 ? e : 12 + e);
-}
-
 // dV for 192 value rows of one group: every head of the group and every query
 // tile that can see these rows stream through LDS (routed queries and dO, two
 // stages); the wave's 48 value rows stay in registers as the B operand of
 // S = Q~ V^T and dP = dO V^T, whose results (one value row per lane) are the B
 // operands of dV^T += dO^T P + tau Q~^T dS.
-// STORE: also writes its tau dS to p.ds (bf16, the tiles that the dQ~ kernel
-// reads: value rows past the end as zeros, none above the causal diagonal), so
-// that dQ~ = tau dS V needs no second pass over S and dP.
-template <int D, bool STORE>
+template <int D>
 __global__ __launch_bounds__(kThreads, 2) void bwd_dv_kernel(BwdParams p) {
   using TL = AttnTile<D, kTileRows>;
   constexpr int KS = D / 32, DB = D / 16;
@@ -465,10 +445,6 @@ __global__ __launch_bounds__(kThreads, 2) void bwd_dv_kernel(BwdParams p) {
     for (int ks = 0; ks < KS; ++ks)
       vf[kb][ks] = __builtin_bit_cast(bf16x8_t, *reinterpret_cast<const u32x4*>(sv + ks * 32));
   }
-  // Wait for them here: the item loop's own waits (one of which leaves the dS
-  // stores in flight) do not tell the compiler that these loads are done, and it
-  // would wait before each first use inside the loop, with the stores counted.
-  if constexpr (STORE) KL_WAIT_VMCNT(0);
   f32x4_t acc[DB][KVB];
 #pragma unroll
   for (int i = 0; i < DB; ++i)
@@ -505,47 +481,17 @@ __global__ __launch_bounds__(kThreads, 2) void bwd_dv_kernel(BwdParams p) {
     }
   };
   const FragOffsets<D> fo(fr, grp);
-  // dS stores: lane (fr, grp) holds, for value row kv0 + 16 kb + fr, the query
-  // rows 32 qs + 4 grp .. + 3 and 32 qs + 16 + 4 grp .. + 3 of each step, and
-  // stores them as they are (16 bytes), so that one store writes the wave's
-  // whole 16 x 32 block, 1 KiB in a row (the tile layout at ds_unit). Its
-  // element offset in the (b, h) block without the query tile's base:
-  int ds_off[KVB];
-#pragma unroll
-  for (int kb = 0; kb < KVB; ++kb) {
-    const int kv = kv0 + kb * 16 + fr;
-    ds_off[kb] = (kv >> 6) * 4096 + ds_unit(kv & 63, 0, grp);
-  }
-
-  // Lanes with nothing to store (above the diagonal, past the last tile) write
-  // to a scratch slot behind the tiles instead, so that every item that is not
-  // skipped issues exactly DS_STORES stores, after the next item's copies.
-  // Vector memory operations complete in issue order, so the wait for those
-  // copies can leave the item's stores in flight (it waits for the earlier
-  // items' stores, long done by then).
-  constexpr int DS_STORES = 2 * KVB;
-  uint16_t* ds_trash = nullptr;
-  if constexpr (STORE) ds_trash = p.ds + (size_t)p.B * p.H * p.ds_tiles * 4096;
-  bool stored_last = false;  // uniform: the previous item issued its stores
 
   auto lds_at = [](int a) { return (const lds_u8*)(size_t)(uint32_t)a; };
   if (items > 0) issue(0);
   for (int it = 0; it < items; ++it) {
-    if (STORE && stored_last) KL_WAIT_VMCNT(DS_STORES);
-    else KL_WAIT_VMCNT(0);
-    stored_last = false;
+    KL_WAIT_VMCNT(0);
     asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
     __syncthreads();
     if (it + 1 < items) issue(it + 1);
     const int qt = qt0 + it % per_head;
     const int q0 = qt * kTileRows;
     if (p.causal && q0 + kTileRows - 1 < kv0) continue;  // every row of the tile is before ours
-    uint16_t* ds_tile = nullptr;
-    if constexpr (STORE) {
-      const int hd = g * R + it / per_head;
-      ds_tile = p.ds + ((size_t)(b * p.H + hd) * p.ds_tiles +
-                        (p.causal ? (size_t)qt * (qt + 1) / 2 : (size_t)qt * ntq)) * 4096;
-    }
     // Fragment offsets from this item's stage: one v_xad_u32 forms a read's
     // whole address (the dO tile and the row blocks are immediate offsets).
     const FragOffsets<D> fi = fo.at(lds0 + (it & 1) * 2 * TL::BYTES);
@@ -636,21 +582,6 @@ __global__ __launch_bounds__(kThreads, 2) void bwd_dv_kernel(BwdParams p) {
         pp[kb] = __builtin_bit_cast(bf16x8_t, wp[kb]);
         ps[kb] = __builtin_bit_cast(bf16x8_t, wsv[kb]);
       }
-      if constexpr (STORE) {
-        // Rows of value tiles that the dQ~ kernel reads: kt <= qt (causal) or
-        // any of the ntq tiles; rows past the end hold zeros there.
-#pragma unroll
-        for (int kb = 0; kb < KVB; ++kb) {
-          const int kv = kv0 + kb * 16 + fr;
-          const int kt = kv >> 6;
-          const bool keep = p.causal ? kt <= qt : kt < ntq;  // uniform over the block
-          const bool live = kv < p.N;
-          uint16_t* d = keep ? ds_tile + ds_off[kb] + qs * 512 : ds_trash + lane * 8;
-          // Streaming stores: the tiles are read back only by the next kernel.
-          __builtin_nontemporal_store(live ? wsv[kb] : u32x4{0u, 0u, 0u, 0u}, reinterpret_cast<u32x4*>(d));
-        }
-        stored_last = true;
-      }
       // dV^T[d][kv] += dO^T P + Q~^T (tau dS) over query rows 32 qs + {4 grp .., 16 + 4 grp ..}.
       // Transposed reads run two column blocks ahead of the products.
       auto rd = [&](const int db, bf16x8_t& ad, bf16x8_t& aq) {
@@ -700,164 +631,6 @@ __global__ __launch_bounds__(kThreads, 2) void bwd_dv_kernel(BwdParams p) {
     for (int db = 0; db < DB; ++db) {
       const u32x2 w{pack2(acc[db][kb][0], acc[db][kb][1]), pack2(acc[db][kb][2], acc[db][kb][3])};
       *reinterpret_cast<u32x2*>(dst + db * 16) = w;
-    }
-  }
-}
-
-// dQ~ = tau dS V for 256 query rows (four stored 64-row tiles) of one head from
-// the stored tau dS: a plain product over the value rows that the causal mask
-// leaves, with the four dS tiles and the value tile of each 64-row step
-// streaming through LDS together (the value tile serves all 256 rows). Both
-// operands come from transposing reads of their row-major tiles ([value
-// row][query column], [value row][d]; the dS tile's columns in the stored
-// order, mapped back to query rows at the end); the result holds dQ~^T, four
-// consecutive columns of one query row per lane. Eight waves: wave w owns the
-// 64 rows of tile w / 2 and half w % 2 of the columns.
-constexpr int DQS_WAVES = 8;
-constexpr int DQS_TILES = 4;    // 64-row query tiles per workgroup
-constexpr int DQS_STAGES = 3;
-
-template <int D>
-__global__ __launch_bounds__(DQS_WAVES * 64, 1) void bwd_dq_stored_kernel(BwdParams p) {
-  using TV = AttnTile<D, kTileRows>;
-  using TS = AttnTile<64, kTileRows>;
-  constexpr int DBH = D / 32;                              // 16-column blocks per wave
-  constexpr int NV = TV::BYTES / 1024;                     // 1 KiB copies of a value tile
-  constexpr int NCOPY = NV + DQS_TILES * TS::BYTES / 1024;  // copies per stage
-  static_assert(NCOPY % DQS_WAVES == 0, "copies split evenly over the waves");
-  constexpr int K = NCOPY / DQS_WAVES;                     // copies per wave per stage
-  constexpr int STAGE = DQS_TILES * TS::BYTES + TV::BYTES;
-  constexpr int CHV = D / 8, RPC = 1024 / TV::ROW;         // value rows: chunks, rows per copy
-  extern __shared__ __attribute__((aligned(1024))) unsigned char smem[];
-  const int ntq = (p.N + kTileRows - 1) / kTileRows;
-  const int nQ = (ntq + DQS_TILES - 1) / DQS_TILES;
-  // One-dimensional grid. Workgroup i runs on XCD i % 8; with B H a multiple
-  // of 8, XCD x takes the heads x, x + 8, ... one after another, so the head's
-  // values stay in that XCD's L2 while its tiles stream. Heaviest causal
-  // workgroups first.
-  const int L = blockIdx.x, HB = p.B * p.H;
-  int hb, qi;
-  if (HB % 8 == 0) {
-    const int x = L % 8, sl = L / 8;
-    hb = (sl / nQ) * 8 + x;
-    qi = sl % nQ;
-  } else {
-    hb = L % HB;
-    qi = L / HB;
-  }
-  const int Q = p.causal ? (nQ - 1 - qi) : qi;
-  const int h = hb % p.H, b = hb / p.H;
-  const int g = h / (p.H / p.G);
-  const int t = threadIdx.x, lane = t & 63;
-  const int wave = __builtin_amdgcn_readfirstlane(t >> 6);
-  const int fr = lane & 15, grp = lane >> 4;
-  const int sub = wave >> 1, half = wave & 1;
-  const int qt_w = Q * DQS_TILES + sub;  // this wave's query tile
-
-  f32x4_t acc[DBH][4];
-#pragma unroll
-  for (int i = 0; i < DBH; ++i)
-#pragma unroll
-    for (int qb = 0; qb < 4; ++qb) acc[i][qb] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-
-  // Copy k of this wave, item wave K + k of the stage: value-tile rows
-  // RPC item .. (items below NV), else rows 8 (c % 8) .. of dS tile c / 8
-  // (c = item - NV). Lane L fills physical chunk L % chunks of its row with the
-  // logical chunk the swizzle puts there (the swizzles are XORs with a row key).
-  uint32_t src[K];
-#pragma unroll
-  for (int k = 0; k < K; ++k) {
-    const int item = wave * K + k;
-    if (item < NV) {
-      const int r = item * RPC + lane / CHV;
-      const int key = D == 128 ? (((r & 7) << 1) | ((r >> 3) & 1)) : ((r >> 1) & 7);
-      src[k] = (uint32_t)(g * D * 2) + (uint32_t)(((lane % CHV) ^ key) * 16);
-    } else {
-      const int r = ((item - NV) % 8) * 8 + lane / 8;
-      const int lc = (lane % 8) ^ ((r >> 1) & 7);
-      src[k] = (uint32_t)ds_unit(r, lc >> 2, lc & 3) * 2;
-    }
-  }
-  const unsigned char* gV = reinterpret_cast<const unsigned char*>(p.v) + (size_t)b * p.N * p.v_stride * 2;
-  const unsigned char* gS = reinterpret_cast<const unsigned char*>(p.ds + (size_t)(b * p.H + h) * p.ds_tiles * 4096);
-  const uint32_t lds0 = (uint32_t)(uintptr_t)(lds_u8*)smem;
-  auto issue = [&](int kt, int stage) {
-    const uint32_t st = lds0 + stage * STAGE;
-#pragma unroll
-    for (int k = 0; k < K; ++k) {
-      const int item = wave * K + k;  // uniform
-      if (item < NV) {
-        // Rows past the end copy row N - 1 (their dS rows are zero).
-        const int r0 = kt * kTileRows + item * RPC;
-        const int r0c = min(r0, p.N - 1);
-        const int rl = min(r0 + lane / CHV, p.N - 1) - r0c;
-        copy_to_lds(gV + (size_t)r0c * p.v_stride * 2, src[k] + (uint32_t)rl * (uint32_t)(p.v_stride * 2),
-                    st + DQS_TILES * TS::BYTES + item * 1024);
-      } else {
-        const int c = item - NV, s4 = c / 8;
-        // A tile that this step does not use (past the causal diagonal or the
-        // last query tile) is replaced by a stored one; its products are skipped.
-        const int qs_c = min(Q * DQS_TILES + s4, ntq - 1);
-        const int kt_c = p.causal ? min(kt, qs_c) : kt;
-        const size_t tile = (p.causal ? (size_t)qs_c * (qs_c + 1) / 2 : (size_t)qs_c * ntq) + kt_c;
-        copy_to_lds(gS + tile * TS::BYTES, src[k], st + s4 * TS::BYTES + (c % 8) * 1024);
-      }
-    }
-  };
-  const FragOffsets<64> fs(fr, grp);
-  const FragOffsets<D> fv(fr, grp);
-  const int last_tile = min(Q * DQS_TILES + DQS_TILES - 1, ntq - 1);
-  const int ntiles = p.causal ? last_tile + 1 : ntq;
-#pragma unroll
-  for (int s = 0; s < DQS_STAGES - 1; ++s)
-    if (s < ntiles) issue(s, s);
-  for (int kt = 0; kt < ntiles; ++kt) {
-    const int stage = kt % DQS_STAGES;
-    if (kt + 1 < ntiles) KL_WAIT_VMCNT(K);
-    else KL_WAIT_VMCNT(0);
-    asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
-    __syncthreads();
-    if (kt + DQS_STAGES - 1 < ntiles) issue(kt + DQS_STAGES - 1, (kt + DQS_STAGES - 1) % DQS_STAGES);
-    if (qt_w >= ntq || (p.causal && kt > qt_w)) continue;  // uniform per wave
-    const uint32_t st = lds0 + stage * STAGE;
-    const FragOffsets<64> fsi = fs.at(st + sub * TS::BYTES);
-    const FragOffsets<D> fvi = fv.at(st + DQS_TILES * TS::BYTES);
-    // Transposing reads of 32 value rows (32 ks + {4 grp .., 16 + 4 grp ..}) of
-    // one 16-column block: the same row order in both operands.
-    auto tr = [](int a, int ks, int row) {
-      typedef __attribute__((address_space(3))) s16x4 lds_s16x4;
-      const lds_u8* src = (const lds_u8*)(size_t)(uint32_t)a + ks * 32 * row;
-      const s16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)src);
-      const s16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)(src + 16 * row));
-      return __builtin_bit_cast(bf16x8_t, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
-    };
-#pragma unroll
-    for (int ks = 0; ks < 2; ++ks) {
-      bf16x8_t av[DBH], bs[4];
-#pragma unroll
-      for (int i = 0; i < DBH; ++i) av[i] = tr(fvi.t(half * DBH + i), ks, TV::ROW);
-#pragma unroll
-      for (int qb = 0; qb < 4; ++qb) bs[qb] = tr(fsi.t(qb), ks, TS::ROW);
-#pragma unroll
-      for (int i = 0; i < DBH; ++i)
-#pragma unroll
-        for (int qb = 0; qb < 4; ++qb)
-          acc[i][qb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av[i], bs[qb], acc[i][qb], 0, 0, 0);
-    }
-  }
-
-  // Lane holds dQ~^T[16 (DBH half + i) + 4 grp + r][query of column 16 qb + fr].
-  if (qt_w >= ntq) return;
-  uint16_t* __restrict__ out = reinterpret_cast<uint16_t*>(p.dq);
-#pragma unroll
-  for (int qb = 0; qb < 4; ++qb) {
-    const int q = qt_w * kTileRows + ds_query_of_column(qb * 16 + fr);
-    if (q >= p.N) continue;
-    uint16_t* dst = out + ((size_t)b * p.N + q) * p.dq_stride + (size_t)h * D + grp * 4;
-#pragma unroll
-    for (int i = 0; i < DBH; ++i) {
-      const u32x2 w{pack2(acc[i][qb][0], acc[i][qb][1]), pack2(acc[i][qb][2], acc[i][qb][3])};
-      *reinterpret_cast<u32x2*>(dst + (half * DBH + i) * 16) = w;
     }
   }
 }
@@ -1000,41 +773,11 @@ hipError_t launch_mfma(const BwdParams& p, hipStream_t st) {
   constexpr int dv_lds = 4 * TL::BYTES + 1024;  // two stages of Q~ and dO tiles, lse and Dd rows
   if (dv_lds > 65536) {
     static std::atomic<uint32_t> done{0};
-    e = set_max_lds(reinterpret_cast<const void*>(bwd_dv_kernel<D, false>), dv_lds, done);
+    e = set_max_lds(reinterpret_cast<const void*>(bwd_dv_kernel<D>), dv_lds, done);
     if (e != hipSuccess) return e;
   }
-  hipLaunchKernelGGL((bwd_dv_kernel<D, false>), dim3(p.G, (p.N + BKVD - 1) / BKVD, p.B),
-                     dim3(kThreads), dv_lds, st, p);
-  return hipGetLastError();
-}
-
-// The stored-dS form (Dd already in p.Dd): the dV kernel writes tau dS, then
-// dQ~ = tau dS V reads it back.
-template <int D>
-hipError_t launch_mfma_stored(const BwdParams& p, hipStream_t st) {
-  using TL = AttnTile<D, kTileRows>;
-  constexpr int dv_lds = 4 * TL::BYTES + 1024;
-  hipError_t e = hipSuccess;
-  if (dv_lds > 65536) {
-    static std::atomic<uint32_t> done{0};
-    e = set_max_lds(reinterpret_cast<const void*>(bwd_dv_kernel<D, true>), dv_lds, done);
-    if (e != hipSuccess) return e;
-  }
-  hipLaunchKernelGGL((bwd_dv_kernel<D, true>), dim3(p.G, (p.N + BKVD - 1) / BKVD, p.B),
-                     dim3(kThreads), dv_lds, st, p);
-  e = hipGetLastError();
-  if (e != hipSuccess) return e;
-  constexpr int dq_lds = DQS_STAGES * (DQS_TILES * AttnTile<64, kTileRows>::BYTES + TL::BYTES);
-  if (dq_lds > 65536) {
-    static std::atomic<uint32_t> done{0};
-    e = set_max_lds(reinterpret_cast<const void*>(bwd_dq_stored_kernel<D>), dq_lds, done);
-    if (e != hipSuccess) return e;
-  }
-  const long ntq = (p.N + kTileRows - 1) / kTileRows;
-  const long wgs = (long)p.B * p.H * ((ntq + DQS_TILES - 1) / DQS_TILES);
-  if (wgs > INT32_MAX) return hipErrorInvalidConfiguration;
-  hipLaunchKernelGGL(bwd_dq_stored_kernel<D>, dim3((unsigned)wgs), dim3(DQS_WAVES * 64), dq_lds, st,
-                     p);
+  hipLaunchKernelGGL(bwd_dv_kernel<D>, dim3(p.G, (p.N + BKVD - 1) / BKVD, p.B), dim3(kThreads),
+                     dv_lds, st, p);
   return hipGetLastError();
 }
 
@@ -1068,12 +811,6 @@ hipError_t launch_attention_backward(const BwdParams& p, hipStream_t st) {
   // dP in the dQ~ kernel's first sweep; on the vector ALU from the output (the
   // prep kernel).
   const bool mfma = attn_bwd_mfma_supported(p);
-  if (mfma && p.ds && p.out_f32) {
-    // Stored dS: Dd from the fp32 output first, since the dV kernel runs first.
-    hipError_t e = launch_prep<uint16_t>(p, st);
-    if (e != hipSuccess) return e;
-    return p.D == 128 ? launch_mfma_stored<128>(p, st) : launch_mfma_stored<64>(p, st);
-  }
   if (!mfma) {
     hipError_t e = p.dtype == KL_BF16 ? launch_prep<uint16_t>(p, st) : launch_prep<float>(p, st);
     if (e != hipSuccess) return e;

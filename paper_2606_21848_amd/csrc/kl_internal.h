@@ -212,12 +212,6 @@ struct BwdParams {
   const float* out_f32;  // [B, N, H, D] the forward's fp32 output, or null (then Dd is formed
                          // from P and dP in a first sweep of the dQ~ kernel)
   float* Dd;
-  // tau dS in bf16, 64 x 64 tiles [value row][query row] per (batch, head):
-  // ds_tiles of them, tile (query tile qt, value tile kt) at qt (qt + 1) / 2 + kt
-  // (causal, kt <= qt) or qt * ceil(N / 64) + kt; null when the dQ~ kernel forms
-  // S and dP itself.
-  uint16_t* ds;
-  long ds_tiles;
   void* dq;
   void* dv;
   long q_stride, v_stride, o_stride, dq_stride, dv_stride;

@@ -54,23 +54,20 @@ def test_attention_forward_lse(lib, dtype, causal, B, N, H, G, dk):
     assert err <= (1e-4 if dtype == torch.float32 else 2e-2), f"lse error {err:.3e}"
 
 
-@pytest.mark.parametrize("mode", ["sweep", "f32", "stored"])
+@pytest.mark.parametrize("keep_f32", [False, True])
 @pytest.mark.parametrize("dtype", [torch.float32, torch.bfloat16])
 @pytest.mark.parametrize("causal", [True, False])
 @pytest.mark.parametrize("B,N,H,G,dk", SHAPES)
-def test_attention_backward_matches_oracle(lib, dtype, causal, B, N, H, G, dk, mode):
+def test_attention_backward_matches_oracle(lib, dtype, causal, B, N, H, G, dk, keep_f32):
     """Both ways of forming rowsum(P * dP): from the forward's fp32 output
-    (f32, stored) and, without it, from P and dP in the dQ~ kernel (sweep); and
-    both ways of forming dQ~: from S and dP formed again, or (stored, bf16) from
-    the tau dS that the dV kernel stored."""
+    (keep_f32) and, without it, from P and dP in the dQ~ kernel."""
     say(f"attention backward dtype={dtype} causal={causal} B={B} N={N} H={H} G={G} dk={dk} "
-        f"mode={mode}")
+        f"keep_f32={keep_f32}")
     Qr, V, dO = _qvd(B, N, H, G, dk, 72, dtype)
     q, v, g = Qr.to(DEV), V.to(DEV), dO.to(DEV)
-    o32 = torch.empty((B, N, H, dk), dtype=torch.float32, device=DEV) if mode != "sweep" else None
+    o32 = torch.empty((B, N, H, dk), dtype=torch.float32, device=DEV) if keep_f32 else None
     out, lse = kb.keyless_attention_forward(q, v, causal=causal, out_f32=o32)
-    dq, dv = kb.keyless_attention_backward(q, v, out, g, lse, causal=causal, out_f32=o32,
-                                           stored_ds=mode == "stored")
+    dq, dv = kb.keyless_attention_backward(q, v, out, g, lse, causal=causal, out_f32=o32)
     torch.cuda.synchronize()
     ref_dq, ref_dv = K.keyless_attention_backward(to64(Qr), to64(V), to64(dO), H, G, dk,
                                                   causal=causal)
@@ -80,47 +77,16 @@ def test_attention_backward_matches_oracle(lib, dtype, causal, B, N, H, G, dk, m
     assert_parity(dv, ref_dv, dtype, "dV", FLOOR, scale)
 
 
-@pytest.mark.parametrize("stored", [False, True])
-def test_attention_backward_is_deterministic(lib, stored):
+def test_attention_backward_is_deterministic(lib):
     B, N, H, G, dk = 1, 700, 8, 2, 128
-    say(f"attention backward determinism stored={stored}")
+    say("attention backward determinism")
     Qr, V, dO = (t.to(DEV) for t in _qvd(B, N, H, G, dk, 73, torch.bfloat16))
-    o32 = torch.empty((B, N, H, dk), dtype=torch.float32, device=DEV) if stored else None
-    out, lse = kb.keyless_attention_forward(Qr, V, out_f32=o32)
-    first = kb.keyless_attention_backward(Qr, V, out, dO, lse, out_f32=o32, stored_ds=stored)
+    out, lse = kb.keyless_attention_forward(Qr, V)
+    first = kb.keyless_attention_backward(Qr, V, out, dO, lse)
     for _ in range(2):
-        again = kb.keyless_attention_backward(Qr, V, out, dO, lse, out_f32=o32, stored_ds=stored)
+        again = kb.keyless_attention_backward(Qr, V, out, dO, lse)
         torch.cuda.synchronize()
         assert torch.equal(first[0], again[0]) and torch.equal(first[1], again[1])
-
-
-@pytest.mark.parametrize("causal", [True, False])
-def test_stored_form_follows_the_workspace(lib, causal):
-    """The stored-dS form runs exactly when the workspace holds its tiles: one
-    byte short, the call gives the other form's results bit for bit. Run twice
-    over a workspace full of NaN first, so that no tile may be read unwritten."""
-    B, N, H, G, dk = 2, 333, 4, 2, 128
-    say(f"stored-dS selection causal={causal}")
-    Qr, V, dO = (t.to(DEV) for t in _qvd(B, N, H, G, dk, 74, torch.bfloat16))
-    o32 = torch.empty((B, N, H, dk), dtype=torch.float32, device=DEV)
-    out, lse = kb.keyless_attention_forward(Qr, V, causal=causal, out_f32=o32)
-    small = kb.attention_backward_workspace_bytes(B, N, H)
-    big = kb.attention_backward_workspace_bytes(B, N, H, stored_ds=True, causal=causal)
-    ntq = -(-N // 64)
-    tiles = ntq * (ntq + 1) // 2 if causal else ntq * ntq
-    assert big == small + -(-(B * H * tiles * 8192) // 256) * 256 + 1024
-    ws = torch.full((big // 4,), float("nan"), dtype=torch.float32, device=DEV).view(torch.uint8)
-    ref = kb.keyless_attention_backward(Qr, V, out, dO, lse, causal=causal, out_f32=o32)
-    short = kb.keyless_attention_backward(Qr, V, out, dO, lse, causal=causal, out_f32=o32,
-                                          workspace=ws[:big - 1])
-    stored = [kb.keyless_attention_backward(Qr, V, out, dO, lse, causal=causal, out_f32=o32,
-                                            workspace=ws) for _ in range(2)]
-    torch.cuda.synchronize()
-    assert torch.equal(short[0], ref[0]) and torch.equal(short[1], ref[1])
-    assert torch.equal(stored[0][0], stored[1][0]) and torch.equal(stored[0][1], stored[1][1])
-    dq, dv = stored[0]
-    assert_parity(dq, to64(ref[0]), torch.bfloat16, "dQ~ stored vs formed", FLOOR)
-    assert_parity(dv, to64(ref[1]), torch.bfloat16, "dV stored vs formed", FLOOR)
 
 
 @pytest.mark.parametrize("dtype", [torch.float32, torch.bfloat16])
@@ -258,18 +224,15 @@ def test_weight_gradients_full_size_sampled(lib):
     assert_parity(grads["dX"][:, rows], refx["dX"], bf, "dX, sampled tokens", FLOOR)
 
 
-@pytest.mark.parametrize("stored", [True, False])
-def test_backward_full_size_sampled(lib, stored):
+def test_backward_full_size_sampled(lib):
     """The measured backward workload (8192 tokens, 32 heads x 128, causal, the
-    routed queries and values of the prefill workload's layer), in the stored-dS
-    form that is timed and in the other: 24 sampled dQ~ rows anywhere and the dV
-    rows of the last 48 positions against the oracle."""
-    say(f"backward full size stored={stored}")
+    routed queries and values of the prefill workload's layer): 24 sampled dQ~
+    rows anywhere and the dV rows of the last 48 positions against the oracle."""
+    say("backward full size")
     c = configs.backward_bf16(device=DEV)
     o32 = torch.empty(c["q"].shape, dtype=torch.float32, device=DEV)
     out, lse = kb.keyless_attention_forward(c["q"], c["v"], out_f32=o32)
-    dq, dv = kb.keyless_attention_backward(c["q"], c["v"], out, c["dout"], lse, out_f32=o32,
-                                           stored_ds=stored)
+    dq, dv = kb.keyless_attention_backward(c["q"], c["v"], out, c["dout"], lse, out_f32=o32)
     torch.cuda.synchronize()
     assert torch.isfinite(dq.float()).all() and torch.isfinite(dv.float()).all()
     N = c["N"]
