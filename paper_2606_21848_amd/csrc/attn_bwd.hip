@@ -14,11 +14,12 @@
 // registers; Dd = rowsum(dO * O) from the forward's fp32 output when the
 // caller kept it, formed in the kernel's prologue, else a first sweep forms
 // it as rowsum(P * dP) in fp32, since rowsum(dO * O) over the bf16-rounded
-// output would put that rounding into every dP - Dd) and then bwd_dv_kernel (one workgroup per 192-row value tile
-// and value group; query and dO tiles of every head of the group stream
-// through LDS, the values stay in registers). fp32: bwd_prep_kernel (Dd from
-// the fp32 output) and two vector-ALU kernels. No atomics: every output
-// element is written once, by one lane.
+// output would put that rounding into every dP - Dd) and then bwd_dv_kernel
+// (one workgroup per 192-row value tile and value group; query and dO tiles of
+// every head of the group stream through LDS, the values stay in registers).
+// fp32 (and shapes the matrix-core kernels do not take): bwd_prep_kernel (Dd
+// from the fp32 output, else from the output) and two vector-ALU kernels. No
+// atomics: every output element is written once, by one lane.
 //
 // bf16 runs on v_mfma_f32_16x16x32_bf16 with the forward's operand layouts:
 // scores come out with one query per lane (S^T = V Q~^T) in the dQ~ kernel and
@@ -70,8 +71,9 @@ __device__ __forceinline__ void stx(T* p, size_t i, float v) {
   else p[i] = v;
 }
 
-// Dd[b, h, q] = sum_d dO[b, q, h, d] O[b, q, h, d]; 16 lanes per row. O is the
-// forward's fp32 output when given (TO = float, row stride H D), else `out`.
+// Dd[b, h, q] = sum_d dO[b, q, h, d] O[b, q, h, d] for the vector-ALU kernels;
+// 16 lanes per row. O is the forward's fp32 output when given (TO = float, row
+// stride H D), else `out`.
 template <typename TO, typename T, int D>
 __global__ __launch_bounds__(256) void bwd_prep_kernel(BwdParams p) {
   const long rows = (long)p.B * p.N * p.H;
@@ -146,8 +148,9 @@ struct TileCopier {
 // dQ~ for 128 query rows of one head. Mirrors the forward kernel: S^T = V Q~^T
 // and dP^T = V dO^T share each value-row fragment read; dS^T feeds
 // dQ~^T += V^T dS^T as the B operand.
-// SWEEP0: Dd is formed here in a first sweep (no fp32 output); else it comes
-// from bwd_prep_kernel and one sweep does.
+// SWEEP0: Dd is formed here in a first sweep (no fp32 output); else the
+// prologue forms it from the fp32 output and one sweep does. Either way it is
+// written for the dV kernel.
 template <int D, bool SWEEP0>
 __global__ __launch_bounds__(kThreads, 2) void bwd_dq_kernel(BwdParams p) {
   using TL = AttnTile<D, kTileRows>;
@@ -243,7 +246,7 @@ __global__ __launch_bounds__(kThreads, 2) void bwd_dq_kernel(BwdParams p) {
   // fp32 (the definition, rather than rowsum(dO * O) from the rounded output,
   // whose rounding the subtraction dP - Dd would amplify) and writes it for the
   // dV kernel; the second forms dS and accumulates dQ~.
-  // With the forward's fp32 output, Dd comes from bwd_prep_kernel and one sweep does.
+  // With the forward's fp32 output, the prologue formed Dd and one sweep does.
 #pragma unroll 1
   for (int sweep = SWEEP0 ? 0 : 1; sweep < 2; ++sweep) {
     if (sweep == 1) {
