@@ -106,6 +106,7 @@ __global__ __launch_bounds__(256) void bwd_prep_kernel(BwdParams p) {
 constexpr int QBD = 2;                 // 16-row query blocks per wave (dQ~ kernel)
 constexpr int BQD = 4 * 16 * QBD;      // query rows per workgroup
 constexpr int NSTAGE = 3;              // value tiles in flight (dQ~ kernel)
+static_assert(NSTAGE >= 2, "the dQ~ kernel's ring needs two stages");
 constexpr int KVB = 3;                 // 16-row value blocks per wave (dV kernel)
 constexpr int BKVD = 4 * 16 * KVB;     // value rows per workgroup
 
@@ -268,7 +269,8 @@ __global__ __launch_bounds__(kThreads, 2) void bwd_dq_kernel(BwdParams p) {
 
     for (int jt = 0; jt < ntiles; ++jt) {
       const int stage = jt % NSTAGE;
-      if (jt + 1 < ntiles) KL_WAIT_VMCNT(TL::COPIES);
+      // Tiles jt + 1 .. jt + NSTAGE - 2 may stay in flight (the last tile waits for all).
+      if (jt + 1 < ntiles) KL_WAIT_VMCNT((NSTAGE - 2) * TL::COPIES);
       else KL_WAIT_VMCNT(0);
       asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
       __syncthreads();

@@ -44,6 +44,7 @@ typedef __attribute__((address_space(3))) unsigned char lds_u8;
 
 constexpr int BKV = 64;     // value rows per tile
 constexpr int NSTAGE = 3;   // value tiles in flight (the tile loop is unrolled by 3)
+static_assert(NSTAGE == 3, "the tile loop below calls process once per stage, three per pass");
 constexpr int kThreads = 256;
 // Instruction classes of __builtin_amdgcn_sched_group_barrier.
 constexpr int kSchedMfma = 0x008;
@@ -194,8 +195,9 @@ __global__ __launch_bounds__(kThreads, 2) void attn_bf16_kernel(AttnParams p) {
   auto process = [&](const int jt, auto stage_tag, auto first_tag) {
     constexpr int STAGE = decltype(stage_tag)::value;
     constexpr bool FIRST = decltype(first_tag)::value;
-    // Tile jt has landed once at most the copies of the later issued tile remain.
-    if (jt + 1 < ntiles) KL_WAIT_VMCNT(T::COPIES);
+    // Tile jt has landed once at most the copies of the later issued tiles
+    // (jt + 1 .. jt + NSTAGE - 2) remain.
+    if (jt + 1 < ntiles) KL_WAIT_VMCNT((NSTAGE - 2) * T::COPIES);
     else KL_WAIT_VMCNT(0);
     // The copies issued below refill the stage of tile jt - 1: every wave's LDS
     // reads of it must have returned before the barrier (the barrier itself does
