@@ -75,6 +75,10 @@ def parse():
                     help="run the counter calibration, then a few launches of the paged "
                          "grouped-head decode, the decode-step projection and the latent "
                          "decode: the program for their counter passes")
+    ap.add_argument("--profile-keys", action="store_true",
+                    help="run the counter calibration, then a few launches each of the keyless "
+                         "decode and the standard K+V decode on one shape (batch 32, 32 heads x "
+                         "128, 4096 cached rows): the program for their counter passes")
     ap.add_argument("--reduce-mfma", nargs="+", metavar="PMC_DIR",
                     help="summarise rocprofv3 --pmc runs of --profile-prefill (MfmaUtil, "
                          "MfmaFlopsBF16, ...) per prefill kernel as markdown")
@@ -513,6 +517,26 @@ def profile_decode_side(torch, kb, configs, dev):
     print("profile decode side done", flush=True)
 
 
+def profile_keys(torch, kb, configs, dev):
+    """The byte comparison of Section 3 under the counters: after the calibration
+    copy, 4 launches of the keyless decode over a value-only cache and 4 of the
+    standard decode over keys and values of the same shape (batch 32, 32 heads x
+    128, 4096 rows: 1 GiB of values, and as much again of keys)."""
+    calibration_copy(torch, dev)
+    hh = configs.head_to_head_bf16(device=dev, L=4096)
+    vcache, kcache = kb.ValueCache(hh["V"]), kb.ValueCache(hh["K"])
+    ws = torch.zeros(max(kb.decode_workspace_bytes(vcache, hh["B"], hh["H"]), 256),
+                     dtype=torch.uint8, device=dev)
+    out = torch.empty_like(hh["q"])
+    for _ in range(4):
+        kb.keyless_decode(hh["q"], vcache, hh["lengths"], out=out, workspace=ws)
+    torch.cuda.synchronize()
+    for _ in range(4):
+        kb.standard_decode(hh["q"], kcache, vcache, hh["lengths"], out=out, workspace=ws)
+    torch.cuda.synchronize()
+    print("profile keys done", flush=True)
+
+
 # ---------------------------------------------------------------------------
 # The run
 # ---------------------------------------------------------------------------
@@ -568,6 +592,9 @@ def main():
         return
     if args.profile_decode_side:
         profile_decode_side(torch, kb, configs, dev)
+        return
+    if args.profile_keys:
+        profile_keys(torch, kb, configs, dev)
         return
     if args.profile_pass:
         calibration_copy(torch, dev)
