@@ -323,6 +323,26 @@ __device__ __forceinline__ void append_and_stage(const DecodeParams& p, int b, i
 // otherwise each workgroup on it stores a partial at index pair + w, which is
 // unique (along the tile sequence both the pair and the workgroup index are
 // non-decreasing and at least one grows from one segment to the next).
+// Balanced mode over at most kWavePlanMax sequences runs no plan kernel: a
+// wave derives the plan from the lengths, one sequence per lane. n = the
+// lane's tiles (zero past B), pre = the exclusive prefix sum of n over the
+// sequences before it, sum = the tiles of all sequences (uniform).
+constexpr int kWavePlanMax = 64;
+struct LanePlan {
+  int n, pre, sum;
+};
+__device__ __forceinline__ LanePlan lane_plan(const DecodeParams& p, int cap) {
+  const int lane = threadIdx.x & 63;
+  const int n = lane < p.B ? (decode_rows(p, lane, cap) + kTile - 1) / kTile : 0;
+  int incl = n;
+#pragma unroll
+  for (int off = 1; off < 64; off <<= 1) {
+    const int v = __shfl_up(incl, off, 64);
+    if (lane >= off) incl += v;
+  }
+  return {n, incl - n, __builtin_amdgcn_readlane(incl, 63)};
+}
+
 template <typename T, int D, int R, bool PAGED, int NW, class Seg>
 __device__ __forceinline__ void for_each_segment(const DecodeParams& p, Seg seg) {
   if (!p.balanced) {
@@ -342,23 +362,46 @@ __device__ __forceinline__ void for_each_segment(const DecodeParams& p, Seg seg)
     return;
   }
   const __attribute__((address_space(4))) int* plan = (const __attribute__((address_space(4))) int*)p.plan;
-  const int total = plan[0], per = plan[1];
   const __attribute__((address_space(4))) int* pre = plan + 2;  // exclusive prefix sums of tiles, [B + 1]
+  const bool wave_planned = p.B <= kWavePlanMax;  // uniform
+  const int cap = PAGED ? (p.max_blocks << p.block_shift) : p.L_max;
+  int total, per;
+  LanePlan lp{};
+  if (wave_planned) {
+    lp = lane_plan(p, cap);
+    total = p.G * lp.sum;
+    per = total > 0 ? (total + p.nwg - 1) / p.nwg : 1;
+  } else {
+    total = plan[0];
+    per = plan[1];
+  }
   const int w = blockIdx.x;
   int t = w * per;
   const int t_end = min(total, t + per);
   if (t >= t_end) return;
   // Sequence holding tile t: the last b with G * pre[b] <= t (empty sequences
-  // share their start with the next one and are skipped by taking the last).
-  int lo = 0, hi = p.B - 1;
-  while (lo < hi) {
-    const int mid = (lo + hi + 1) >> 1;
-    if (p.G * pre[mid] <= t) lo = mid; else hi = mid - 1;
+  // share their start with the next one and are skipped by taking the last),
+  // and pre[b], carried along as the walk moves to later sequences.
+  int b, preb;
+  if (wave_planned) {
+    const unsigned long long below = __ballot((int)(threadIdx.x & 63) < p.B && p.G * lp.pre <= t);
+    b = 63 - __clzll((long long)below);  // tile 0 lies in sequence 0 or later: below != 0
+    preb = __builtin_amdgcn_readlane(lp.pre, b);
+  } else {
+    int lo = 0, hi = p.B - 1;
+    while (lo < hi) {
+      const int mid = (lo + hi + 1) >> 1;
+      if (p.G * pre[mid] <= t) lo = mid; else hi = mid - 1;
+    }
+    b = lo;
+    preb = pre[b];
   }
-  int b = lo;
+  auto tiles_of = [&](int bb) {  // tiles per pair of sequence bb
+    return wave_planned ? (seq_len<PAGED>(p, bb) + kTile - 1) / kTile : pre[bb + 1] - pre[bb];
+  };
   while (t < t_end) {
-    const int n = pre[b + 1] - pre[b];  // tiles per pair of sequence b (> 0 here)
-    const int base = p.G * pre[b];
+    const int n = tiles_of(b);  // > 0 here
+    const int base = p.G * preb;
     const int g = (t - base) / n;
     const int tp = base + g * n;  // first tile of pair (b, g)
     const int seg_end = min(t_end, tp + n);
@@ -370,8 +413,9 @@ __device__ __forceinline__ void for_each_segment(const DecodeParams& p, Seg seg)
     seg(b, g, (t - tp) * kTile, min((seg_end - tp) * kTile, len), o);
     t = seg_end;
     if (t >= base + p.G * n) {  // past the last pair of b: next non-empty sequence
+      preb += n;
       ++b;
-      while (b < p.B && pre[b + 1] == pre[b]) ++b;
+      while (b < p.B && tiles_of(b) == 0) ++b;
     }
   }
 }
@@ -770,7 +814,7 @@ __global__ __launch_bounds__(NW * 64) void decode_mfma_kernel(DecodeParams p) {
 // Balanced-mode plan: tiles per sequence n_b = ceil(len_b / 16), their
 // exclusive prefix sums pre[0..B], the total T = G pre[B] over all pairs and
 // the tiles per workgroup ceil(T / nwg). One workgroup scans the sequences in
-// blocks of 1024.
+// blocks of 1024. It runs for more than kWavePlanMax sequences only.
 __global__ __launch_bounds__(1024) void decode_plan_kernel(DecodeParams p) {
   __shared__ int s_scan[1024];
   __shared__ int s_carry;
@@ -826,11 +870,21 @@ __global__ __launch_bounds__(256) void decode_combine_kernel(DecodeParams p) {
   } else {
     // The workgroups that covered pair (b, g) wrote partials pair + w for w in
     // [first, last]; a pair inside one workgroup was stored directly.
-    const int* pre = p.plan + 2;
-    const int per = p.plan[1];
-    const int n = pre[b + 1] - pre[b];
+    int per, preb, n;
+    if (p.B <= kWavePlanMax) {  // no plan kernel ran: the same plan from the lengths
+      const LanePlan lp = lane_plan(p, cap);
+      const int total = p.G * lp.sum;
+      per = total > 0 ? (total + p.nwg - 1) / p.nwg : 1;
+      preb = __builtin_amdgcn_readlane(lp.pre, b);
+      n = __builtin_amdgcn_readlane(lp.n, b);
+    } else {
+      const int* pre = p.plan + 2;
+      per = p.plan[1];
+      preb = pre[b];
+      n = pre[b + 1] - pre[b];
+    }
     const int h = bh % p.H, g = h / p.R, r = h % p.R;
-    const int tp = p.G * pre[b] + g * n;
+    const int tp = p.G * preb + g * n;
     const int first = n > 0 ? tp / per : 0;
     const int last = n > 0 ? (tp + n - 1) / per : -1;
     if (n > 0 && first == last) return;
@@ -877,7 +931,7 @@ __global__ __launch_bounds__(256) void decode_combine_kernel(DecodeParams p) {
 template <typename T, int D, int R, bool PAGED, bool KEYS, int NW>
 hipError_t launch_t(const DecodeParams& p, hipStream_t st) {
   const dim3 grid = p.balanced ? dim3(p.nwg) : dim3(p.S, p.G, p.B);
-  if (p.balanced) {
+  if (p.balanced && p.B > kWavePlanMax) {
     hipLaunchKernelGGL(decode_plan_kernel, dim3(1), dim3(1024), 0, st, p);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
