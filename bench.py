@@ -703,12 +703,58 @@ def main():
                      "trace": trace_from_profile()},
     }
     del caches
+    if not args.only_headline:
+        ceil = read_ceiling(torch, kb, dev, step_bytes, len(c["caches"]))
+        ceil["decode_frac_of_it"] = round(achieved / ceil["gbps"], 4)
+        result["roofline"]["practical_read_ceiling"] = ceil
     if not (args.quick or args.only_headline):
         result["extra"] = extra_measurements(torch, kb, configs, dev)
     if not args.only_headline:
         result["cpu_baseline"] = cpu_decode_bf16(c, args.cpu_seconds)
     del c
     print(json.dumps(result), flush=True)
+
+
+def read_ceiling(torch, kb, dev, nbytes, copies):
+    """The practical read ceiling beside the 8 TB/s peak: the library's streaming-
+    read probe (16-byte non-temporal loads, each workgroup streaming a contiguous
+    share) over `copies` rotated
+    buffers of the step's size, the decode's working set; the best of four grid
+    sizes, each the median of STAT_CALLS calls."""
+    n = nbytes // 16 * 16
+    bufs = [torch.ones(n // 4, dtype=torch.float32, device=dev) for _ in range(copies)]
+    sink = torch.zeros(1, dtype=torch.int32, device=dev)
+    best = None
+    for wg in (1024, 2048, 4096, 8192):
+        st = call_stats(lambda i: kb.probe_read(bufs[i % copies], sink, wg), STAT_CALLS, 10, torch,
+                        batch=10)
+        if best is None or rate(st, n, 1e-9) > best[0]:
+            best = (rate(st, n, 1e-9), wg, st)
+    del bufs
+    return {"gbps": best[0], "frac_of_peak": round(best[0] / HBM_PEAK_GBPS, 4),
+            "workgroups": best[1], "median_us": round(best[2]["median_ms"] * 1e3, 2),
+            "how": f"keyless_probe_read over {copies} rotated buffers of {n:,} B, best of 1024 / "
+                   f"2048 / 4096 / 8192 workgroups, median of {STAT_CALLS} samples of 10 "
+                   f"back-to-back calls each"}
+
+
+def mfma_ceiling(torch, kb, dev):
+    """The practical matrix-core ceiling beside the 2.5 PFLOP/s peak: the
+    library's probe loop of independent bf16 16x16x32 products on constant
+    operands (about 2 TFLOP per launch), the best of 2, 4 and 8 waves per SIMD.
+    Constant operands draw less power than real data: an upper bound."""
+    sink = torch.zeros(1, dtype=torch.float32, device=dev)
+    best = None
+    for wg in (512, 1024, 2048):
+        iters = max(1, int(2.0e12 // (wg * 4 * 16 * 16384)))
+        flop = wg * 4 * iters * 16 * 16384
+        st = call_stats(lambda i: kb.probe_mfma(sink, iters, wg), 20, 3, torch)
+        if best is None or rate(st, flop, 1e-12) > best[0]:
+            best = (rate(st, flop, 1e-12), wg)
+    return {"tflops": best[0], "frac_of_peak": round(best[0] / BF16_MFMA_PEAK_TFLOPS, 4),
+            "waves_per_simd": best[1] * 4 // 1024,
+            "how": "keyless_probe_mfma, about 2 TFLOP per launch, best of 2 / 4 / 8 waves per "
+                   "SIMD, median of 20 launches each"}
 
 
 class _Results(dict):
@@ -816,6 +862,7 @@ def extra_measurements(torch, kb, configs, dev):
         el = time.perf_counter() - t0
     sample_flop = 2 * N * dm * G * dk + 2 * len(rows) * dm * H * dk + \
         sum(4 * H * dk * (i + 1) for i in rows)
+    mceil = mfma_ceiling(torch, kb, dev)
     res["prefill_bf16"] = {
         "workload": "batch 1, 8192 tokens, d_model 4096, 32 heads x 128, causal "
                     "(keyless_prefill_packed: projection GEMM + attention)",
@@ -832,6 +879,8 @@ def extra_measurements(torch, kb, configs, dev):
                             "frac_of_bf16_mfma_peak": round(gemm_flops / (gemm_ms * 1e-3) * 1e-12 /
                                                             BF16_MFMA_PEAK_TFLOPS, 4),
                             "note": "median call minus median attention; 2 N d (H + G) d_k FLOP"},
+        "practical_mfma_ceiling": mceil,
+        "frac_of_practical_mfma_ceiling": round(rate(st, flops, 1e-12) / mceil["tflops"], 4),
         "raw_weights": dict(st_raw, note="keyless_prefill with W^Q, W^R, W^V as given: the fold "
                                          "and pack run inside every call"),
         "pack_weights": dict(st_pack, note="keyless_pack_weights alone: fold of W^R into W^Q "

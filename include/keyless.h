@@ -435,6 +435,29 @@ int standard_decode_chunked(const void* q, const kl_value_cache* k_cache,
  */
 void keyless_set_kernel_timer(void* start_event, void* stop_event);
 
+/*
+ * keyless_probe_read, keyless_probe_mfma - instrumentation for benchmarks: the
+ * practical ceilings that the roofline fractions of the kernels above are read
+ * against. Neither computes anything of the method.
+ *
+ * keyless_probe_read reads the `bytes` bytes at device pointer `src` once
+ * (16-byte non-temporal loads; each of `workgroups` workgroups of 256 lanes
+ * streams a contiguous share) and writes nothing but, in a case no real input
+ * is expected to give, one word to the device word `sink`. `src` must be 16-byte aligned and `bytes`
+ * a multiple of 16; `workgroups` in [1, 2^20]. Enqueued on `stream`.
+ *
+ * keyless_probe_mfma runs, in each of `workgroups` workgroups of 4 waves,
+ * `iters` rounds of 16 independent bf16 matrix-core products of 16 x 16 x 32
+ * (workgroups x 4 x iters x 16 x 16384 FLOP in all) on constant operands, and
+ * likewise writes at most one word to the device float `sink`. `iters` >= 1,
+ * `workgroups` in [1, 2^20].
+ *
+ * Both return KL_ERR_INVALID_ARG for arguments outside these ranges.
+ */
+int keyless_probe_read(const void* src, size_t bytes, unsigned* sink, int workgroups,
+                       void* stream);
+int keyless_probe_mfma(float* sink, int iters, int workgroups, void* stream);
+
 /* Thread-local text describing the last non-OK status returned on this thread. */
 const char* keyless_last_error(void);
 

@@ -32,7 +32,8 @@ EXPORTS = (
     "keyless_decode_project", "keyless_decode", "keyless_decode_chunked", "keyless_decode_workspace_size",
     "keyless_decode_append", "keyless_decode_noalloc",
     "value_cache_append", "standard_decode", "standard_decode_chunked",
-    "keyless_set_kernel_timer", "keyless_last_error", "keyless_version",
+    "keyless_set_kernel_timer", "keyless_probe_read", "keyless_probe_mfma",
+    "keyless_last_error", "keyless_version",
 )
 
 
@@ -97,6 +98,8 @@ def load(path: str = LIB_PATH):
         "standard_decode": (i, [vp, cp, cp, vp, i, i, f, vp, vp, sz, vp]),
         "standard_decode_chunked": (i, [vp, cp, cp, vp, i, i, f, vp, vp, sz, i, vp]),
         "keyless_set_kernel_timer": (None, [vp, vp]),
+        "keyless_probe_read": (i, [vp, sz, vp, i, vp]),
+        "keyless_probe_mfma": (i, [vp, i, i, vp]),
         "keyless_last_error": (ctypes.c_char_p, []),
         "keyless_version": (ctypes.c_char_p, []),
     }
@@ -262,6 +265,20 @@ def set_kernel_timer(start: "torch.cuda.Event | None", stop: "torch.cuda.Event |
     else:
         _lib.keyless_set_kernel_timer(ctypes.c_void_p(start.cuda_event),
                                       ctypes.c_void_p(stop.cuda_event))
+
+
+def probe_read(buf: torch.Tensor, sink: torch.Tensor, workgroups: int) -> None:
+    """Stream-read every byte of ``buf`` once (the practical read ceiling)."""
+    load()
+    _check(_lib.keyless_probe_read(_ptr(buf), buf.numel() * buf.element_size(), _ptr(sink),
+                                   workgroups, _stream(buf)))
+
+
+def probe_mfma(sink: torch.Tensor, iters: int, workgroups: int) -> int:
+    """Run the matrix-core loop; returns its FLOP count."""
+    load()
+    _check(_lib.keyless_probe_mfma(_ptr(sink), iters, workgroups, _stream(sink)))
+    return workgroups * 4 * iters * 16 * 16 * 16 * 32 * 2
 
 
 def keyless_pack_weights(W_Q: torch.Tensor, W_R: torch.Tensor | None, W_V: torch.Tensor, H: int,

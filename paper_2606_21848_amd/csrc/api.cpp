@@ -237,6 +237,29 @@ const char* keyless_last_error(void) { return g_err.c_str(); }
 
 const char* keyless_version(void) { return "keyless-gfx950 0.1"; }
 
+int keyless_probe_read(const void* src, size_t bytes, unsigned* sink, int workgroups,
+                       void* stream) {
+  const char* who = "keyless_probe_read";
+  if (!src || !sink) return fail(KL_ERR_INVALID_ARG, "%s: src and sink must be non-NULL", who);
+  if (bytes % 16 != 0 || !aligned16(src))
+    return fail(KL_ERR_INVALID_ARG, "%s: src must be 16-byte aligned and bytes a multiple of 16", who);
+  if (workgroups < 1 || workgroups > (1 << 20))
+    return fail(KL_ERR_INVALID_ARG, "%s: workgroups=%d outside [1, 2^20]", who, workgroups);
+  if (bytes == 0) return KL_OK;
+  return hip_status(kl::launch_probe_read(src, bytes, sink, workgroups,
+                                          static_cast<hipStream_t>(stream)), who);
+}
+
+int keyless_probe_mfma(float* sink, int iters, int workgroups, void* stream) {
+  const char* who = "keyless_probe_mfma";
+  if (!sink) return fail(KL_ERR_INVALID_ARG, "%s: sink must be non-NULL", who);
+  if (iters < 1 || workgroups < 1 || workgroups > (1 << 20))
+    return fail(KL_ERR_INVALID_ARG, "%s: iters=%d or workgroups=%d out of range", who, iters,
+                workgroups);
+  return hip_status(kl::launch_probe_mfma(sink, iters, workgroups, static_cast<hipStream_t>(stream)),
+                    who);
+}
+
 void keyless_set_kernel_timer(void* start_event, void* stop_event) {
   const bool on = start_event && stop_event;
   g_timer_start = on ? static_cast<hipEvent_t>(start_event) : nullptr;

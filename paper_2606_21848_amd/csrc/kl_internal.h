@@ -230,4 +230,11 @@ hipError_t launch_prefill_attention(const AttnParams& p, hipStream_t stream);
 // fp32 (or fallback) VALU attention.
 hipError_t launch_prefill_attention_simple(const AttnParams& p, hipStream_t stream);
 
+// Measuring kernels (not part of the method): a streaming read of bytes (a
+// multiple of 16, src 16-byte aligned) and a loop of matrix-core products,
+// 4 waves x iters x 16 products of 16 x 16 x 32 per workgroup.
+hipError_t launch_probe_read(const void* src, size_t bytes, unsigned* sink, int workgroups,
+                             hipStream_t stream);
+hipError_t launch_probe_mfma(float* sink, int iters, int workgroups, hipStream_t stream);
+
 }  // namespace kl

@@ -278,3 +278,20 @@ def test_decode_noalloc_rejects_oversized_workspace(lib):
            kb.KL_ERR_INVALID_ARG, "NULL")
     assert lib.keyless_decode_noalloc(FAKE, ctypes.byref(cache()), FAKE, 0, 8, 0.0, FAKE, None) == \
         kb.KL_OK
+
+
+def test_probes_validate_before_launch(lib):
+    """The measuring probes refuse bad arguments on the host, before any launch."""
+    fake_sink = ctypes.c_void_p(0x200000)
+    misaligned = ctypes.c_void_p(0x100008)
+    expect(lib, lib.keyless_probe_read(None, 1024, fake_sink, 256, None), kb.KL_ERR_INVALID_ARG,
+           "non-NULL")
+    expect(lib, lib.keyless_probe_read(FAKE, 1000, fake_sink, 256, None), kb.KL_ERR_INVALID_ARG,
+           "multiple of 16")
+    expect(lib, lib.keyless_probe_read(misaligned, 1024, fake_sink, 256, None),
+           kb.KL_ERR_INVALID_ARG, "aligned")
+    expect(lib, lib.keyless_probe_read(FAKE, 1024, fake_sink, 0, None), kb.KL_ERR_INVALID_ARG,
+           "workgroups")
+    expect(lib, lib.keyless_probe_mfma(None, 10, 256, None), kb.KL_ERR_INVALID_ARG, "non-NULL")
+    expect(lib, lib.keyless_probe_mfma(fake_sink, 0, 256, None), kb.KL_ERR_INVALID_ARG, "range")
+    expect(lib, lib.keyless_probe_mfma(fake_sink, 10, 0, None), kb.KL_ERR_INVALID_ARG, "range")

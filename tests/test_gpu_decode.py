@@ -154,6 +154,41 @@ def test_balanced_mode_ragged_and_empty(lib, H, G, d, dtype):
         assert torch.all(out.cpu()[lengths == 0] == 0)
 
 
+@pytest.mark.parametrize("B", [63, 64, 65, 300, 1100])
+@pytest.mark.parametrize("H,G,d,dtype", [(4, 2, 128, torch.bfloat16), (2, 1, 64, torch.float32)])
+@pytest.mark.parametrize("paged", [True, False])
+def test_balanced_mode_sequence_counts(lib, B, H, G, d, dtype, paged):
+    """Balanced mode on both sides of the in-kernel plan's limit: with at most 64
+    sequences the decode and merge kernels derive the work split from the
+    lengths, with more the plan kernel writes it (1100 sequences also cross its
+    1024-sequence scan blocks). Ragged lengths with the edge cases, and empty
+    sequences first, inside and last. A contiguous cache takes the balanced split
+    only below one (sequence, group) pair per compute unit."""
+    if not paged and B * G >= 256:
+        pytest.skip("a contiguous cache with this many pairs takes one workgroup per pair")
+    L = 200
+    lengths = _lengths(B, L, 40 + B)
+    lengths[0] = 0
+    lengths[B // 2] = 0
+    lengths[-1] = 0
+    say(f"balanced B={B} H={H} G={G} d={d} dtype={dtype} paged={paged}")
+    cache = synth.normal((B, G, L, d), 19, B, 1.0, dtype)
+    q = synth.normal((B, H, d), 19, B + 1, 1.0, dtype)
+    if paged:
+        data, table = _paged(cache, lengths, 16, 7)
+        vc = kb.ValueCache(data.to(DEV), table.to(DEV))
+        ref = K.keyless_decode(to64(q), to64(data), lengths.numpy(), H, G,
+                               block_table=table.numpy(), block_size=16)
+    else:
+        vc = kb.ValueCache(cache.to(DEV))
+        ref = K.keyless_decode(to64(q), to64(cache), lengths.numpy(), H, G)
+    ws = torch.full((kb.decode_workspace_bytes(vc, B, H),), 0xFF, dtype=torch.uint8, device=DEV)
+    out = kb.keyless_decode(q.to(DEV), vc, lengths.to(DEV), workspace=ws)
+    torch.cuda.synchronize()
+    assert_parity(out, ref, dtype, f"balanced B={B}")
+    assert torch.all(out.cpu()[lengths == 0] == 0)
+
+
 def test_lengths_beyond_capacity_are_clamped(lib):
     B, G, H, L, d = 2, 2, 2, 100, 64
     say("length clamp")
