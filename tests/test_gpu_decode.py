@@ -189,6 +189,34 @@ def test_balanced_mode_sequence_counts(lib, B, H, G, d, dtype, paged):
     assert torch.all(out.cpu()[lengths == 0] == 0)
 
 
+@pytest.mark.parametrize("B", [64, 65, 300])
+def test_decode_append_balanced_sequence_counts(lib, B):
+    """The fused step (new row appended at lengths_before, decode over one more
+    row) in the balanced split on both sides of the in-kernel plan's limit, whose
+    tile counts include every sequence's new row; ragged positions, paged cache.
+    Outputs against the oracle's append then decode, the cache bit-equal to the
+    oracle's append afterwards."""
+    H, G, d, L, dtype = 4, 2, 128, 96, torch.bfloat16
+    say(f"decode_append balanced B={B}")
+    cache = synth.normal((B, G, L, d), 21, B, 1.0, dtype)
+    vnew = synth.normal((B, G, d), 21, B + 1, 1.0, dtype)
+    q = synth.normal((B, H, d), 21, B + 2, 1.0, dtype)
+    data, table = _paged(cache, torch.full((B,), L, dtype=torch.int32), 16, 8)
+    tab = table.numpy()
+    before = synth.uniform_int(B, 0, L - 1, 21, B + 3).to(torch.int32)
+    before[0] = 0
+    before[-1] = L - 1
+    ref_data = K.value_cache_append(to64(data), to64(vnew[:, None]), before.tolist(), tab, 16)
+    ref = K.keyless_decode(to64(q), ref_data, (before + 1).numpy(), H, G, block_table=tab,
+                           block_size=16)
+    dev_data = data.to(DEV)
+    vc = kb.ValueCache(dev_data, table.to(DEV))
+    out = kb.keyless_decode_append(q.to(DEV), vnew.to(DEV), vc, before.to(DEV))
+    torch.cuda.synchronize()
+    assert_parity(out, ref, dtype, f"fused step, balanced B={B}")
+    assert np.array_equal(to64(dev_data.cpu()), ref_data, equal_nan=True)
+
+
 def test_lengths_beyond_capacity_are_clamped(lib):
     B, G, H, L, d = 2, 2, 2, 100, 64
     say("length clamp")
